@@ -1,0 +1,177 @@
+"""Oracle for per-position sampling of the factorised proposal (Eq. 8).
+
+Each drafted position i of each sequence is one row of base logits z
+(fp32, [V]). For temperature T > 0 the proposal is q_i = softmax(z/T) over a
+support S (all V tokens, or the top_k largest logits, lower index first on
+ties), and the token is drawn by Gumbel-max: y = argmax_{v in S} (z_v/T + g_v)
+with g_v standard Gumbel noise. T = 0 is greedy: y = argmax_v z_v (lowest index
+on ties), q a point mass. The row also yields lse = log sum_{v in S} exp(z_v/T)
+and log q(y) = z_y/T - lse, which the verifier's acceptance test and residual
+(Eq. 1-2) need.
+
+The argmax is an integer decision taken from fp32 keys, so the keys are
+computed exactly as the GPU kernel does: fl(fl(z_v / T) + g_v), every step an
+IEEE fp32 operation. The noise is fully specified here:
+
+* bits: Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers:
+  as easy as 1, 2, 3", SC 2011) with key (seed, step) and counter
+  (v div 8, row, 0, 0); token v takes 32-bit half (v mod 2) of output word
+  ((v div 2) mod 4);
+* uniform: k = bits >> 9, u = (2k + 1) * 2^-24, exact in fp32, in (0, 1);
+* Gumbel: g = -log(-log(u)) with the fp32 logarithm ``logf`` below, a fixed
+  sequence of IEEE fp32 operations (no fused multiply-add): exponent split,
+  mantissa folded into [sqrt(1/2), sqrt(2)], then 2 atanh(f), f = (m-1)/(m+1),
+  by its odd power series to the f^11 term.
+
+lse and log q are computed in float64 here.
+"""
+from __future__ import annotations
+
+import numpy as np
+import scipy.special
+
+# Philox4x64 multipliers and Weyl key increments (Salmon et al., SC 2011).
+PHILOX_M0 = np.uint64(0xD2E7470EE14C6C93)
+PHILOX_M1 = np.uint64(0xCA5A826395121157)
+PHILOX_W0 = np.uint64(0x9E3779B97F4A7C15)
+PHILOX_W1 = np.uint64(0xBB67AE8584CAA73B)
+_M32 = np.uint64(0xFFFFFFFF)
+_S32 = np.uint64(32)
+
+
+def _mulhilo64(a, b):
+    """(hi, lo) 64-bit halves of the 128-bit product a*b (a array, b scalar)."""
+    a = np.asarray(a, dtype=np.uint64)
+    al, ah = a & _M32, a >> _S32
+    bl, bh = b & _M32, b >> _S32
+    p0, p1, p2, p3 = al * bl, al * bh, ah * bl, ah * bh      # each < 2^64, exact
+    mid = (p0 >> _S32) + (p1 & _M32) + (p2 & _M32)
+    hi = p3 + (p1 >> _S32) + (p2 >> _S32) + (mid >> _S32)
+    with np.errstate(over="ignore"):
+        lo = a * b                                            # wraps mod 2^64
+    return hi, lo
+
+
+def philox4x64_10(ctr, key):
+    """Philox4x64 with 10 rounds. ctr: 4 uint64 arrays, key: 2 uint64 arrays
+    (broadcastable). Returns the 4 output words."""
+    c = [np.asarray(x, dtype=np.uint64) for x in ctr]
+    k0, k1 = (np.asarray(x, dtype=np.uint64) for x in key)
+    with np.errstate(over="ignore"):
+        for rnd in range(10):
+            if rnd:
+                k0 = k0 + PHILOX_W0
+                k1 = k1 + PHILOX_W1
+            hi0, lo0 = _mulhilo64(c[0], PHILOX_M0)
+            hi1, lo1 = _mulhilo64(c[2], PHILOX_M1)
+            c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]
+    return c
+
+
+# fp32 constants of logf, as bit patterns (nearest fp32 to the exact value).
+def _f(bits):
+    return np.array(bits, dtype=np.uint32).view(np.float32)[()]
+
+
+C3, C5, C7, C9, C11 = (_f(0x3EAAAAAB), _f(0x3E4CCCCD), _f(0x3E124925), _f(0x3DE38E39),
+                       _f(0x3DBA2E8C))                          # 1/3, 1/5, 1/7, 1/9, 1/11
+LN2_HI = _f(0x3F317200)    # ln 2 to 16 bits: e * LN2_HI is exact for |e| <= 255
+LN2_LO = _f(0x35BFBE8E)    # ln 2 - LN2_HI
+SQRT2 = _f(0x3FB504F3)
+ONE, TWO, HALF = np.float32(1.0), np.float32(2.0), np.float32(0.5)
+
+
+def logf(x):
+    """Natural log of positive normal fp32 values, as a fixed sequence of
+    IEEE fp32 operations (each rounded to nearest, none fused).
+
+    x = 2^e * m, m in [1, 2); if m > sqrt(2): m /= 2, e += 1. Then
+    log x = e ln2 + 2 atanh(f), f = (m - 1) / (m + 1), |f| <= 0.1716, and
+    2 atanh(f) = 2f (1 + s/3 + s^2/5 + s^3/7 + s^4/9 + s^5/11), s = f^2
+    (truncation below 1e-10 relative)."""
+    x = np.asarray(x, dtype=np.float32)
+    bits = x.view(np.uint32)
+    e = (((bits >> np.uint32(23)) & np.uint32(0xFF)).astype(np.int32) - 127)
+    m = ((bits & np.uint32(0x7FFFFF)) | np.uint32(0x3F800000)).view(np.float32)
+    big = m > SQRT2
+    m = np.where(big, m * HALF, m)
+    e = (e + big.astype(np.int32)).astype(np.float32)
+    f = (m - ONE) / (m + ONE)
+    s = f * f
+    p = C11
+    p = p * s + C9
+    p = p * s + C7
+    p = p * s + C5
+    p = p * s + C3
+    p = p * s + ONE
+    r = (f * TWO) * p
+    return (e * LN2_HI + (e * LN2_LO + r)).astype(np.float32)
+
+
+def philox_bits(seed, step, row, v):
+    """The 32 noise bits of token v in row `row` (uint32 arrays)."""
+    v, row = np.broadcast_arrays(np.asarray(v, dtype=np.uint64),
+                                 np.asarray(row, dtype=np.uint64))
+    zero = np.zeros_like(v)
+    key = (np.uint64(seed), np.uint64(step))
+    w = philox4x64_10((v >> np.uint64(3), row, zero, zero), key)
+    w = np.stack(w, axis=0)                                    # [4][...]
+    word = np.take_along_axis(w, ((v >> np.uint64(1)) & np.uint64(3)).astype(np.int64)[None],
+                              axis=0)[0]
+    half = (v & np.uint64(1)) * np.uint64(32)
+    return ((word >> half) & _M32).astype(np.uint32)
+
+
+def uniform(bits):
+    """u = (2 (bits >> 9) + 1) 2^-24, exact in fp32, strictly inside (0, 1)."""
+    k = (np.asarray(bits, dtype=np.uint32) >> np.uint32(9)).astype(np.float32)
+    return ((k * TWO + ONE) * np.float32(2.0 ** -24)).astype(np.float32)
+
+
+def gumbel(seed, step, row, v):
+    """g = -log(-log(u)) in fp32 for token(s) v of row `row`."""
+    u = uniform(philox_bits(seed, step, row, v))
+    return -logf(-logf(u))
+
+
+def support(z, top_k):
+    """Token ids in the support: all, or the top_k largest z (lower index
+    first among equal values)."""
+    V = z.shape[0]
+    if top_k <= 0 or top_k >= V:
+        return np.arange(V)
+    return np.sort(np.argsort(-z.astype(np.float64), kind="stable")[:top_k])
+
+
+def sample(logits, temperature, top_k, seed, step, rows=None, chunk=16):
+    """Tokens (int64), lse and log q (float64) for the rows of a [n][V] fp32
+    logits array. `rows` gives each row's index in the noise counter
+    (default 0..n-1). Rows are processed `chunk` at a time."""
+    z = np.asarray(logits, dtype=np.float32)
+    n, V = z.shape
+    rows = np.arange(n) if rows is None else np.asarray(rows)
+    if temperature == 0.0:
+        y = np.argmax(z, axis=1)                                # first maximum
+        return y.astype(np.int64), z[np.arange(n), y].astype(np.float64), np.zeros(n)
+    T = np.float32(temperature)
+    ys, lses = [], []
+    for a in range(0, n, chunk):
+        zc = z[a:a + chunk]
+        inside = np.zeros(zc.shape, dtype=bool)
+        for i in range(zc.shape[0]):
+            inside[i, support(zc[i], top_k)] = True
+        key = zc / T + gumbel(seed, step, rows[a:a + chunk, None], np.arange(V)[None, :])
+        key = np.where(inside, key, -np.inf)                   # fp32 keys, support only
+        ys.append(np.argmax(key, axis=1))                      # first maximum
+        zs = np.where(inside, zc.astype(np.float64) / float(T), -np.inf)
+        lses.append(scipy.special.logsumexp(zs, axis=1))
+    y = np.concatenate(ys).astype(np.int64)
+    lse = np.concatenate(lses)
+    return y, lse, z[np.arange(n), y].astype(np.float64) / float(T) - lse
+
+
+def sample_row(z, temperature, top_k, seed, step, row):
+    """(token, lse, logq) for one row of fp32 logits z [V]."""
+    y, lse, logq = sample(np.asarray(z, dtype=np.float32)[None], temperature, top_k, seed,
+                          step, rows=[row])
+    return int(y[0]), float(lse[0]), float(logq[0])

@@ -1,0 +1,158 @@
+"""Oracle for the fixed-size context views (Sec. 2.2; App. A.2, Eq. 10-11).
+
+Per sequence the views are:
+
+* the recent K/V window: the last min(t, W) target K/V rows of every selected
+  layer, row p kept in ring slot p mod W (Sec. 2.2, App. B.1);
+* the global summary: for every layer j, query head h and summary query
+  r < R, the value m and log-normalizer eta of attention from the fixed query
+  G[j,h,r] over all t target rows of the head's K/V group (Eq. 5, Eq. 10);
+* the boundary hidden states h of the selected layers at the last ingested
+  position (Sec. 2.2, the input of the boundary fusion).
+
+All arithmetic is float64. Inputs are float64 arrays holding the values of
+the drawn tensors (bf16 values are exact in float64).
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+import scipy.special
+
+
+@dataclasses.dataclass
+class ViewState:
+    t: int            # target rows ingested so far (positions 0..t-1 cached)
+    Kw: np.ndarray    # [D][Hkv][W][d]  window keys, slot = position mod W
+    Vw: np.ndarray    # [D][Hkv][W][d]  window values
+    M: np.ndarray     # [D][Hq][R][d]   summary values m
+    eta: np.ndarray   # [D][Hq][R]      summary log-normalizers (-inf = empty)
+    h: np.ndarray     # [L_b][hidden]   boundary hidden states
+
+    def copy(self) -> "ViewState":
+        return ViewState(self.t, self.Kw.copy(), self.Vw.copy(), self.M.copy(),
+                         self.eta.copy(), self.h.copy())
+
+
+def empty(s) -> ViewState:
+    """The state before any row: t = 0, empty summary (eta = -inf, m = 0),
+    zero window and boundary. Merging anything into it gives that thing
+    (App. A.2: the merge is defined for nonempty sets; the empty set is its
+    identity)."""
+    D, Hq, Hkv, W, R, d = (s.n_layers, s.n_q_heads, s.n_kv_heads, s.window,
+                           s.summary, s.head_dim)
+    return ViewState(
+        t=0,
+        Kw=np.zeros((D, Hkv, W, d)), Vw=np.zeros((D, Hkv, W, d)),
+        M=np.zeros((D, Hq, R, d)), eta=np.full((D, Hq, R), -np.inf),
+        h=np.zeros((s.n_feat_layers, s.hidden)),
+    )
+
+
+def set_statistics(G, K, V, d):
+    """eta_N and m_N of Eq. 10 for one head: G [R][d] queries, K/V [n][d]
+    rows of the set N (n >= 1). Log-sum-exp with max subtraction (App. A.2)."""
+    s = (G @ K.T) / np.sqrt(d)                    # s_j = g^T k_j / sqrt(d)   [R][n]
+    mx = s.max(axis=1, keepdims=True)
+    w = np.exp(s - mx)
+    eta = mx[:, 0] + np.log(w.sum(axis=1))        # log sum_j exp(s_j)
+    m = np.exp(s - eta[:, None]) @ V              # sum_j exp(s_j - eta) v_j
+    return eta, m
+
+
+def merge(eta_a, m_a, eta_n, m_n):
+    """Eq. 11 with max subtraction: eta = log(e^eta_A + e^eta_N),
+    m = e^(eta_A - eta) m_A + e^(eta_N - eta) m_N. An empty A (eta_A = -inf)
+    returns N unchanged."""
+    out_eta = np.empty_like(eta_n)
+    out_m = np.empty_like(m_n)
+    empty_a = np.isneginf(eta_a)
+    out_eta[empty_a] = eta_n[empty_a]
+    out_m[empty_a] = m_n[empty_a]
+    f = ~empty_a
+    mu = np.maximum(eta_a[f], eta_n[f])
+    eta = mu + np.log(np.exp(eta_a[f] - mu) + np.exp(eta_n[f] - mu))
+    out_eta[f] = eta
+    out_m[f] = (np.exp(eta_a[f] - eta)[:, None] * m_a[f]
+                + np.exp(eta_n[f] - eta)[:, None] * m_n[f])
+    return out_eta, out_m
+
+
+def update(s, st: ViewState, G, K_new, V_new, h_new) -> ViewState:
+    """Ingest n new target rows (Sec. 2.4, Inference; App. A.2).
+
+    K_new, V_new: [n][D][Hkv][d] rows for positions t..t+n-1. h_new:
+    [L_b][hidden] boundary states at the new boundary. n = 0 returns the
+    state unchanged, h included (no row was committed, the boundary did not
+    move)."""
+    n = K_new.shape[0]
+    out = st.copy()
+    if n == 0:
+        return out
+    W, d = s.window, s.head_dim
+    rep = s.n_q_heads // s.n_kv_heads
+    for r in range(n):                              # ring write, in order
+        out.Kw[:, :, (st.t + r) % W, :] = K_new[r]
+        out.Vw[:, :, (st.t + r) % W, :] = V_new[r]
+    for j in range(s.n_layers):
+        for h in range(s.n_q_heads):
+            g = h // rep                            # the head's K/V group
+            eta_n, m_n = set_statistics(G[j, h], K_new[:, j, g, :], V_new[:, j, g, :], d)
+            out.eta[j, h], out.M[j, h] = merge(st.eta[j, h], st.M[j, h], eta_n, m_n)
+    out.h = np.array(h_new, dtype=np.float64, copy=True)
+    out.t = st.t + n
+    return out
+
+
+def brute_summary(s, G, K_all, V_all):
+    """Eq. 5 directly: M = Attn(G, K_{1:t}, V_{1:t}) and its log-normalizer,
+    for every layer and query head, over all t rows at once."""
+    t = K_all.shape[0]
+    D, Hq = s.n_layers, s.n_q_heads
+    rep = Hq // s.n_kv_heads
+    M = np.zeros((D, Hq, s.summary, s.head_dim))
+    eta = np.full((D, Hq, s.summary), -np.inf)
+    if t == 0:
+        return M, eta
+    for j in range(D):
+        for h in range(Hq):
+            K = K_all[:, j, h // rep, :]
+            V = V_all[:, j, h // rep, :]
+            sc = G[j, h] @ K.T / np.sqrt(s.head_dim)
+            M[j, h] = scipy.special.softmax(sc, axis=1) @ V
+            eta[j, h] = scipy.special.logsumexp(sc, axis=1)
+    return M, eta
+
+
+def brute_window(s, K_all, V_all):
+    """The last min(t, W) rows, each at slot position mod W, and the mask of
+    valid slots."""
+    t = K_all.shape[0]
+    W = s.window
+    Kw = np.zeros((s.n_layers, s.n_kv_heads, W, s.head_dim))
+    Vw = np.zeros_like(Kw)
+    valid = np.zeros(W, dtype=bool)
+    for p in range(max(0, t - W), t):
+        Kw[:, :, p % W, :] = K_all[p]
+        Vw[:, :, p % W, :] = V_all[p]
+        valid[p % W] = True
+    return Kw, Vw, valid
+
+
+def window_valid(s, t: int) -> np.ndarray:
+    """Slots holding a cached row after t rows: all W once t >= W, else 0..t-1."""
+    valid = np.zeros(s.window, dtype=bool)
+    valid[:min(t, s.window)] = True
+    return valid
+
+
+def state_bytes(s) -> int:
+    """Bytes of one sequence's views as stored: window K and V in the model
+    dtype, summary m and eta in fp32 per query head, boundary h in the model
+    dtype. No term depends on t (Sec. 2.4, Fixed-cost complexity)."""
+    el = 2 if s.dtype == "bf16" else 4
+    window = 2 * s.n_layers * s.window * s.n_kv_heads * s.head_dim * el
+    summary = s.n_layers * s.n_q_heads * s.summary * (s.head_dim + 1) * 4
+    boundary = s.n_feat_layers * s.hidden * el
+    return window + summary + boundary

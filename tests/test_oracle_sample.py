@@ -1,0 +1,138 @@
+"""Pins of the sampler oracle (Eq. 8): Philox4x64-10 against numpy's own
+implementation, the fp32 logarithm against numpy's log, Gumbel moments
+(closed forms), Gumbel-max frequencies against softmax(z/T) (chi-square),
+greedy against numpy argmax, top-k support against a sort, lse closed forms."""
+import math
+
+import numpy as np
+import pytest
+import scipy.stats
+
+from oracle import sample as Sm
+
+
+@pytest.mark.parametrize("ctr,key", [
+    ((0, 0, 0, 0), (0, 0)),
+    ((7, 3, 5, 9), (123, 456)),
+    ((2 ** 64 - 2, 2 ** 64 - 1, 1, 2 ** 63), (2 ** 64 - 1, 2 ** 63 + 5)),
+])
+def test_philox_matches_numpy(ctr, key):
+    # numpy's Philox bit generator increments the counter before each block
+    bg = np.random.Philox(counter=np.array(ctr, dtype=np.uint64),
+                          key=np.array(key, dtype=np.uint64))
+    ref = bg.random_raw(8)
+    as_int = sum(int(v) << (64 * i) for i, v in enumerate(ctr))
+    for blk in range(2):
+        c = (as_int + blk + 1) % 2 ** 256              # 256-bit counter increment
+        words = [np.uint64((c >> (64 * i)) & (2 ** 64 - 1)) for i in range(4)]
+        got = Sm.philox4x64_10(words, (np.uint64(key[0]), np.uint64(key[1])))
+        assert [int(g) for g in got] == [int(r) for r in ref[4 * blk:4 * blk + 4]]
+
+
+def test_logf_within_three_ulp_of_numpy():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([
+        rng.uniform(1e-7, 20.0, 400_000), np.exp(rng.uniform(-87, 88, 200_000)),
+        2.0 ** np.arange(-126, 127), [np.nextafter(1.0, 0.0), 1.0, 1.4142135, 1.4142137,
+                                      0.70710677, 5.9604645e-08, 16.635532]]).astype(np.float32)
+    got = Sm.logf(x).astype(np.float64)
+    ref = np.log(x.astype(np.float64))
+    ulp = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
+    ulp = np.maximum(ulp, np.spacing(np.float32(0)))
+    assert np.max(np.abs(got - ref) / ulp) <= 3.0
+    assert Sm.logf(np.float32([1.0]))[0] == 0.0
+
+
+def test_uniform_is_exact_and_open():
+    bits = np.array([0, 511, 512, 2 ** 31, 2 ** 32 - 1], dtype=np.uint32)
+    u = Sm.uniform(bits)
+    assert u[0] == 2.0 ** -24 and u[1] == 2.0 ** -24 and u[2] == 3 * 2.0 ** -24
+    assert u[-1] == 1 - 2.0 ** -24
+    assert np.all((u > 0) & (u < 1))
+
+
+def test_gumbel_moments():
+    g = Sm.gumbel(5, 0, np.arange(2000)[:, None], np.arange(1000)[None, :]).astype(np.float64)
+    # standard Gumbel: mean = Euler-Mascheroni gamma, variance = pi^2 / 6
+    assert abs(g.mean() - 0.5772156649) < 0.004
+    assert abs(g.var() - math.pi ** 2 / 6) < 0.01
+    assert np.isfinite(g).all() and g.max() < 16.7
+
+
+def test_noise_streams_differ_by_seed_step_and_row():
+    v = np.arange(64)
+    a = Sm.philox_bits(1, 0, 0, v)
+    assert len(set(a.tolist())) == 64
+    for other in (Sm.philox_bits(2, 0, 0, v), Sm.philox_bits(1, 1, 0, v),
+                  Sm.philox_bits(1, 0, 1, v)):
+        assert np.mean(a == other) < 0.05
+
+
+@pytest.mark.parametrize("T,top_k", [(1.0, 0), (0.7, 0), (1.3, 3)])
+def test_gumbel_max_frequencies_follow_softmax(T, top_k):
+    z = np.float32([0.3, -1.2, 1.1, 0.0, 2.0, -0.4])
+    n = 30_000
+    y, _, _ = Sm.sample(np.tile(z, (n, 1)), T, top_k, 42, 7, chunk=4096)
+    counts = np.bincount(y, minlength=6).astype(np.float64)
+    S = Sm.support(z, top_k)
+    zs = z[S].astype(np.float64) / T
+    p = np.exp(zs - zs.max())
+    p = p / p.sum()
+    assert counts.sum() == counts[S].sum()
+    chi2 = scipy.stats.chisquare(counts[S], p * n)
+    assert chi2.pvalue > 1e-3
+
+
+def test_logq_is_the_log_probability_of_the_token():
+    z = np.float32([0.5, 1.5, -0.25, 3.0])
+    T = float(np.float32(0.8))                  # the temperature is an fp32 argument
+    y, lse, logq = Sm.sample_row(z, 0.8, 0, 1, 2, 3)
+    assert lse == pytest.approx(math.log(sum(math.exp(float(v) / T) for v in z)), rel=1e-12)
+    assert logq == pytest.approx(float(z[y]) / T - lse, rel=1e-12)
+    # the empirical frequency of each token matches exp(log q)
+    n = 20_000
+    ys, _, lq = Sm.sample(np.tile(z, (n, 1)), 0.8, 0, 3, 4, chunk=4096)
+    for v in range(4):
+        sel = ys == v
+        assert abs(sel.mean() - math.exp(lq[sel][0])) < 0.015
+
+
+def test_lse_closed_forms():
+    V = 1000
+    z = np.full(V, np.float32(2.5))
+    _, lse, logq = Sm.sample_row(z, 0.5, 0, 0, 0, 0)
+    assert lse == pytest.approx(5.0 + math.log(V), rel=1e-13)
+    assert logq == pytest.approx(-math.log(V), rel=1e-12)
+    p = np.random.default_rng(1).dirichlet(np.ones(50))
+    _, lse, _ = Sm.sample_row(np.log(p).astype(np.float32), 1.0, 0, 0, 0, 0)
+    assert abs(lse) < 1e-6
+
+
+def test_greedy_is_first_argmax():
+    rng = np.random.default_rng(2)
+    z = rng.normal(size=(50, 300)).astype(np.float32)
+    z[3, [10, 200]] = 9.0                       # tie: the lower index wins
+    y, lse, logq = Sm.sample(z, 0.0, 0, 0, 0)
+    assert np.array_equal(y, np.argmax(z, axis=1))
+    assert y[3] == 10 and np.all(logq == 0.0)
+
+
+def test_top_k_support_is_the_k_largest_lower_index_first():
+    z = np.float32([1.0, 3.0, 3.0, -2.0, 3.0, 0.5, 2.0])
+    assert Sm.support(z, 2).tolist() == [1, 2]
+    assert Sm.support(z, 4).tolist() == [1, 2, 4, 6]
+    assert Sm.support(z, 0).tolist() == list(range(7))
+    rng = np.random.default_rng(3)
+    for _ in range(20):
+        zz = rng.integers(-3, 3, 40).astype(np.float32)
+        k = int(rng.integers(1, 40))
+        brute = sorted(range(40), key=lambda v: (-float(zz[v]), v))[:k]
+        assert Sm.support(zz, k).tolist() == sorted(brute)
+
+
+def test_sampled_token_is_in_the_top_k_support():
+    rng = np.random.default_rng(4)
+    z = rng.normal(size=(40, 500)).astype(np.float32)
+    y, _, _ = Sm.sample(z, 1.0, 5, 9, 1)
+    for r in range(40):
+        assert y[r] in set(Sm.support(z[r], 5).tolist())
