@@ -1,0 +1,216 @@
+/*
+ * ldr.h -- fixed-cost speculative drafting on one MI355X (gfx950).
+ *
+ * C ABI of the drafting step of "Efficient speculative decoding with a
+ * fixed-cost parallel drafter" (LongSpark): the fixed-size context views of
+ * Sec. 2.2 and their incremental maintenance (App. A.2, Eq. 10-11), the
+ * block-diffusion drafter forward (Sec. 2.3, Eq. 4 and Eq. 6, App. A.1,
+ * App. B.1) and per-position sampling of the factorised proposal (Eq. 8).
+ *
+ * Conventions shared by every entry point:
+ *  - Pointers marked "dev" are device memory owned by the caller (for
+ *    example PyTorch tensors). The library never frees them and never keeps
+ *    them beyond the call, except the arena, position and G pointers that
+ *    ldr_views_init records in the handle.
+ *  - `stream` is a hipStream_t (NULL: the legacy default stream). Every call
+ *    that takes one only enqueues work on it and returns without waiting.
+ *  - Host-side validation is synchronous: on a bad argument nothing is
+ *    enqueued and LDR_EINVAL is returned. A failed kernel launch returns
+ *    LDR_EHIP. Errors detected on the device (an out-of-range row count) set
+ *    a sticky flag read by ldr_views_status.
+ *  - Matrices are row-major in the nn.Linear [out][in] layout. "dtype" is the
+ *    configuration's element type (fp32 or bf16) of weights, window rows,
+ *    summary queries and boundary states; summary values and
+ *    log-normalizers, logits and sampler outputs are always fp32.
+ *  - All 16-byte-vector accesses need 16-byte-aligned pointers and row
+ *    lengths; the library checks this and returns LDR_EINVAL otherwise.
+ */
+#ifndef LDR_H
+#define LDR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum ldr_status {
+  LDR_OK = 0,
+  LDR_EINVAL = -1,  /* bad argument, shape or alignment (host check)        */
+  LDR_ERANGE = -2,  /* a per-sequence row count outside [0, max_new]        */
+  LDR_EHIP = -3,    /* a HIP runtime call or kernel launch failed           */
+  LDR_ENOMEM = -4   /* the small host/device bookkeeping allocation failed  */
+};
+
+enum ldr_dtype { LDR_F32 = 0, LDR_BF16 = 1 };
+
+/* Drafter shape (App. B.1: D = 5 Qwen3-style layers, W = 256, R = 16). */
+typedef struct ldr_config {
+  int32_t hidden;        /* model width                                        */
+  int32_t n_q_heads;     /* Hq                                                 */
+  int32_t n_kv_heads;    /* Hkv, divides Hq; q head h reads kv group h/(Hq/Hkv) */
+  int32_t head_dim;      /* d, 64 or 128                                       */
+  int32_t mlp;           /* SwiGLU intermediate width                          */
+  int32_t vocab;         /* V                                                  */
+  int32_t n_layers;      /* D: draft layers, each paired with one window and
+                            one summary bank (Sec. 2.3)                        */
+  int32_t n_feat_layers; /* L_b: boundary hidden states fused into c_t         */
+  int32_t block;         /* B: slots = proposals per round, 1..16              */
+  int32_t window;        /* W: recent K/V rows kept per layer                  */
+  int32_t summary;       /* R: summary queries per layer and query head        */
+  int32_t dtype;         /* enum ldr_dtype                                     */
+  float rope_theta;      /* rotary base                                        */
+  float ntk_alpha;       /* fixed NTK scaling: base = theta * alpha^(d/(d-2))  */
+  float rms_eps;         /* RMSNorm epsilon                                    */
+} ldr_config;
+
+/* Device pointers of one draft layer (Qwen3-style block, App. B.1). */
+typedef struct ldr_layer_weights {
+  const void* in_norm;   /* dev [hidden]                 pre-attention RMSNorm gain */
+  const void* wqkv;      /* dev [(Hq+2Hkv)d][hidden]     rows: q heads, k heads, v heads */
+  const void* q_norm;    /* dev [d]                      per-head q RMSNorm gain  */
+  const void* k_norm;    /* dev [d]                      per-head k RMSNorm gain  */
+  const void* wo;        /* dev [hidden][Hq d]                                     */
+  const void* post_norm; /* dev [hidden]                 pre-MLP RMSNorm gain     */
+  const void* w_gate_up; /* dev [2 mlp][hidden]          rows: gate, then up      */
+  const void* w_down;    /* dev [hidden][mlp]                                      */
+} ldr_layer_weights;
+
+/* Device pointers of the drafter (all in the configuration dtype). The
+ * embedding, final norm and vocabulary head are the target's, frozen
+ * (Sec. 2.3); embed and lm_head may be the same pointer. */
+typedef struct ldr_weights {
+  const void* embed;       /* dev [V][hidden]                                   */
+  const void* mask_emb;    /* dev [hidden]      the mask-token embedding         */
+  const void* pos_emb;     /* dev [B][hidden]   within-block positional encoding */
+  const void* fc_w;        /* dev [hidden][L_b hidden]  boundary fusion          */
+  const void* fc_norm;     /* dev [hidden]      boundary fusion RMSNorm gain     */
+  const void* final_norm;  /* dev [hidden]                                       */
+  const void* lm_head;     /* dev [V][hidden]                                    */
+  const ldr_layer_weights* layers; /* host array of n_layers entries            */
+} ldr_weights;
+
+typedef struct ldr_views ldr_views; /* opaque host handle */
+
+/* Per-sequence bytes of the fixed-size views (Sec. 2.4, Fixed-cost
+ * complexity): window K and V [D][Hkv][W][d] (dtype), summary values
+ * [D][Hq][R][d] and log-normalizers [D][Hq][R] (fp32), boundary states
+ * [L_b][hidden] (dtype), each region 256-byte aligned. No term depends on the
+ * prefix length. Returns 0 for an invalid configuration. */
+size_t ldr_views_state_bytes(const ldr_config* cfg);
+
+/* Byte stride between sequences in the arena (state bytes rounded up to 256),
+ * so an arena for `batch` sequences needs batch * stride bytes. */
+size_t ldr_views_stride_bytes(const ldr_config* cfg);
+
+/* Byte offsets, inside one sequence's slot, of the window K, window V,
+ * summary values, summary log-normalizers and boundary states (5 entries
+ * written to `offsets`). Returns LDR_OK or LDR_EINVAL. */
+int ldr_views_layout(const ldr_config* cfg, size_t offsets[5]);
+
+/* Workspace bytes ldr_draft_step needs for `batch` sequences. */
+size_t ldr_workspace_bytes(const ldr_config* cfg, int32_t batch);
+
+/* Validates a configuration: LDR_OK or LDR_EINVAL. */
+int ldr_config_check(const ldr_config* cfg);
+
+/* Creates a views handle for `batch` sequences over a caller-owned arena and
+ * enqueues its reset to the empty state (Sec. 2.2; App. A.2): every position
+ * counter 0, summary log-normalizers -inf, summary values, window and
+ * boundary states 0. Then, if max_prefix > 0, ingests a first prefix chunk
+ * exactly as ldr_views_update would (the summary is initialised over the
+ * prefix once, at prefill: Sec. 2.2, Fig. "global-summary").
+ *   arena      dev [batch][stride] bytes, 256-byte aligned (kept in the handle)
+ *   pos        dev int64 [batch]: rows ingested per sequence, t (kept)
+ *   G          dev [D][Hq][R][d] dtype: the fixed summary queries (kept)
+ *   n_prefix   dev int32 [batch] rows per sequence in the chunk, or NULL
+ *   K_prefix, V_prefix  dev [batch][max_prefix][D][Hkv][d] dtype
+ *   h_boundary dev [batch][L_b][hidden] dtype: boundary states after it
+ * The handle also owns a 256-byte device status word, freed by
+ * ldr_views_destroy. */
+int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* arena,
+                   int64_t* pos, const void* G, const int32_t* n_prefix, int32_t max_prefix,
+                   const void* K_prefix, const void* V_prefix, const void* h_boundary,
+                   void* stream);
+
+/* Ingests the target K/V rows committed by one verification pass (Sec. 2.4,
+ * Inference; App. A.2). For every sequence b with n = n_new[b] rows:
+ *  - row r (position t_b + r) is written to window slot (t_b + r) mod W for
+ *    every layer (only the last min(n, W) rows can survive, and only they
+ *    are written);
+ *  - the rows form the set N of Eq. 10 for every (layer j, query head h,
+ *    summary query r): s = G[j,h,r] . k / sqrt(d) over the head's K/V group,
+ *    eta_N and m_N by log-sum-exp with max subtraction, merged into (eta, m)
+ *    by Eq. 11;
+ *  - the boundary states become h_new[b];
+ *  - t_b += n.
+ * n = 0 leaves that sequence's views and t bit-identical (App. A.2). A count
+ * outside [0, max_new] leaves the sequence unchanged and sets the sticky
+ * LDR_ERANGE flag.
+ *   n_new       dev int32 [batch]
+ *   K_new, V_new dev [batch][max_new][D][Hkv][d] dtype (row r of sequence b at
+ *               [b][r]; rows r >= n_new[b] are ignored)
+ *   h_new       dev [batch][L_b][hidden] dtype */
+int ldr_views_update(ldr_views* v, const int32_t* n_new, int32_t max_new, const void* K_new,
+                     const void* V_new, const void* h_new, void* stream);
+
+/* Waits for `stream` and returns the sticky device status: LDR_OK,
+ * LDR_ERANGE once any update saw an out-of-range row count, else LDR_EINVAL
+ * once any draft step saw an anchor outside [0, V) (that slot then used token
+ * 0). Clears the status if `clear` is nonzero. */
+int ldr_views_status(ldr_views* v, int clear, void* stream);
+
+/* Frees the handle and its status word; the arena, pos and G stay the
+ * caller's. NULL is ignored. */
+void ldr_views_destroy(ldr_views* v);
+
+/* One block proposal (Eq. 4; Sec. 2.3; App. A.1): base logits z^(0) of the B
+ * slots of every sequence, from the views alone.
+ *  c_b = RMSNorm(W_fc [h_0; ...; h_{L_b-1}]), x_{b,i} = E[u_i] + P_i + c_b with
+ *  u_0 = anchor[b] and u_i = the mask embedding for i >= 1; slot i sits at
+ *  absolute position t_b + i. Then D pre-norm layers: per-head q/k RMSNorm and
+ *  rotary embedding on the block's q and k, attention of every query head h
+ *  over [block k; window K of layer j; G[j,h]] with values
+ *  [block v; window V; M[j,h]] under ONE softmax (Eq. 6), no mask among the
+ *  slots, window slots masked while t_b < W, summary entries masked while
+ *  t_b = 0; SwiGLU MLP. Final RMSNorm and vocabulary head.
+ *   anchor    dev int32 [batch], each in [0, V); an anchor outside it is
+ *             replaced by token 0 and recorded in the views status
+ *   logits    dev fp32 [batch][B][V] (row b*B + i proposes y_{i+1})
+ *   workspace dev, at least ldr_workspace_bytes(cfg, batch) bytes, 256-aligned;
+ *             its contents are scratch, owned by the caller. */
+int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                   float* logits, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes ldr_sample needs for `rows` rows of `vocab` logits. */
+size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
+
+/* Per-position sampling of the factorised proposal (Eq. 8), one row at a
+ * time and independently. temperature = 0: tokens[r] = argmax z (lowest index
+ * on ties), lse[r] = that maximum, logq[r] = 0. temperature T > 0: support S =
+ * all V tokens (top_k = 0) or the top_k largest logits (lower index first on
+ * ties); tokens[r] = argmax over S of fl(fl(z_v / T) + g_v) (lowest index on
+ * ties) with g_v = -log(-log(u_v)) Gumbel noise from Philox4x64-10 (key
+ * (seed, step), counter (v div 8, r, 0, 0), 32-bit half v mod 2 of word
+ * (v div 2) mod 4, u = (2 (bits >> 9) + 1) 2^-24) and a fixed-operation fp32
+ * logarithm, so the tokens are reproducible bit for bit on any IEEE machine;
+ * lse[r] = log sum_{v in S} exp(z_v / T); logq[r] = z_y / T - lse[r].
+ *   logits dev fp32 [rows][vocab]; tokens dev int32 [rows]; lse, logq dev fp32 [rows]
+ *   workspace dev, ldr_sample_workspace_bytes(rows, vocab) bytes. */
+int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperature,
+               int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
+               float* logq, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Writes the Gumbel noise ldr_sample uses: out[r][v] = g_v of row r, for
+ * rows [0, rows) and tokens [0, vocab). out dev fp32 [rows][vocab]. */
+int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t rows, int32_t vocab, float* out,
+                    void* stream);
+
+/* A static string naming a status code. */
+const char* ldr_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LDR_H */

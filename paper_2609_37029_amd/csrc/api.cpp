@@ -1,0 +1,325 @@
+// Host side of the C ABI: configuration checks, the per-sequence arena
+// layout, the workspace plan of one draft step, argument validation and the
+// launch sequence. Every step of the drafting computation runs in the HIP
+// kernels of views.hip, gemm.hip, draft.hip and sample.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+
+#include "ldr_internal.h"
+
+namespace ldr {
+int views_dims_per_thread(const Shape& s);
+
+bool make_shape(const ldr_config* c, Shape* s) {
+  if (!c) return false;
+  if (c->hidden <= 0 || c->hidden % 64) return false;
+  if (c->n_q_heads <= 0 || c->n_kv_heads <= 0 || c->n_q_heads % c->n_kv_heads) return false;
+  if (c->head_dim != 64 && c->head_dim != 128) return false;
+  if (c->mlp <= 0 || c->mlp % 64) return false;
+  if (c->vocab <= 0) return false;
+  if (c->n_layers <= 0 || c->n_feat_layers <= 0) return false;
+  if (c->block < 1 || c->block > 16) return false;
+  if (c->window < 1 || c->summary < 1) return false;
+  if (c->dtype != LDR_F32 && c->dtype != LDR_BF16) return false;
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f) || !(c->ntk_alpha > 0.f)) return false;
+  s->hidden = c->hidden; s->hq = c->n_q_heads; s->hkv = c->n_kv_heads; s->d = c->head_dim;
+  s->mlp = c->mlp; s->vocab = c->vocab; s->D = c->n_layers; s->Lb = c->n_feat_layers;
+  s->B = c->block; s->W = c->window; s->R = c->summary; s->dtype = c->dtype;
+  s->rep = s->hq / s->hkv;
+  s->qkv_out = (s->hq + 2 * s->hkv) * s->d;
+  s->eps = c->rms_eps;
+  s->rope_base = (double)c->rope_theta *
+                 std::pow((double)c->ntk_alpha, (double)s->d / (double)(s->d - 2));
+  s->el = c->dtype == LDR_BF16 ? 2 : 4;
+  if (views_dims_per_thread(*s) == 0) return false;
+  return true;
+}
+
+Layout make_layout(const Shape& s) {
+  Layout L;
+  const size_t win = (size_t)s.D * s.hkv * s.W * s.d * s.el;
+  L.kw = 0;
+  L.vw = align_up(L.kw + win);
+  L.m = align_up(L.vw + win);
+  L.eta = align_up(L.m + (size_t)s.D * s.hq * s.R * s.d * 4);
+  L.h = align_up(L.eta + (size_t)s.D * s.hq * s.R * 4);
+  L.bytes = L.h + (size_t)s.Lb * s.hidden * s.el;
+  L.stride = align_up(L.bytes);
+  return L;
+}
+
+// Workspace regions of one draft step for `batch` sequences.
+struct WsPlan {
+  size_t part, x, nrm, o, act, rope, bytes;
+  GemmPlan fc, qkv, wo, gu, down, lm;
+};
+
+static WsPlan plan_ws(const Shape& s, int batch) {
+  WsPlan w;
+  const int M = batch * s.B;
+  w.fc = plan_gemm(s.dtype, batch, s.hidden, s.Lb * s.hidden, true);
+  w.qkv = plan_gemm(s.dtype, M, s.qkv_out, s.hidden, true);
+  w.wo = plan_gemm(s.dtype, M, s.hidden, s.hq * s.d, true);
+  w.gu = plan_gemm(s.dtype, M, 2 * s.mlp, s.hidden, false);   // SwiGLU epilogue: no split
+  w.down = plan_gemm(s.dtype, M, s.hidden, s.mlp, true);
+  w.lm = plan_gemm(s.dtype, M, s.vocab, s.hidden, false);     // writes the logits directly
+  size_t part = (size_t)w.fc.splits * batch * s.hidden;
+  part = part > (size_t)w.qkv.splits * M * s.qkv_out ? part : (size_t)w.qkv.splits * M * s.qkv_out;
+  part = part > (size_t)w.wo.splits * M * s.hidden ? part : (size_t)w.wo.splits * M * s.hidden;
+  part = part > (size_t)w.down.splits * M * s.hidden ? part : (size_t)w.down.splits * M * s.hidden;
+  size_t off = 0;
+  w.part = off; off = align_up(off + part * 4);
+  w.x = off; off = align_up(off + (size_t)M * s.hidden * 4);
+  w.nrm = off; off = align_up(off + (size_t)M * s.hidden * s.el);
+  w.o = off; off = align_up(off + (size_t)M * s.hq * s.d * s.el);
+  w.act = off; off = align_up(off + (size_t)M * s.mlp * s.el);
+  w.rope = off; off = align_up(off + (size_t)2 * M * (s.d / 2) * 4);
+  w.bytes = off;
+  return w;
+}
+
+static bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+}  // namespace ldr
+
+using namespace ldr;
+
+struct ldr_views {
+  ldr_config cfg;
+  Shape s;
+  Layout L;
+  int batch;
+  uint8_t* arena;
+  int64_t* pos;
+  const void* G;
+  int32_t* status;  // device, 256 bytes
+};
+
+extern "C" {
+
+int ldr_config_check(const ldr_config* cfg) {
+  Shape s;
+  return make_shape(cfg, &s) ? LDR_OK : LDR_EINVAL;
+}
+
+size_t ldr_views_state_bytes(const ldr_config* cfg) {
+  Shape s;
+  if (!make_shape(cfg, &s)) return 0;
+  return make_layout(s).bytes;
+}
+
+size_t ldr_views_stride_bytes(const ldr_config* cfg) {
+  Shape s;
+  if (!make_shape(cfg, &s)) return 0;
+  return make_layout(s).stride;
+}
+
+int ldr_views_layout(const ldr_config* cfg, size_t offsets[5]) {
+  Shape s;
+  if (!offsets || !make_shape(cfg, &s)) return LDR_EINVAL;
+  const Layout L = make_layout(s);
+  offsets[0] = L.kw; offsets[1] = L.vw; offsets[2] = L.m; offsets[3] = L.eta; offsets[4] = L.h;
+  return LDR_OK;
+}
+
+size_t ldr_workspace_bytes(const ldr_config* cfg, int32_t batch) {
+  Shape s;
+  if (batch <= 0 || !make_shape(cfg, &s)) return 0;
+  return plan_ws(s, batch).bytes;
+}
+
+const char* ldr_strerror(int status) {
+  switch (status) {
+    case LDR_OK: return "ok";
+    case LDR_EINVAL: return "invalid argument";
+    case LDR_ERANGE: return "row count out of range";
+    case LDR_EHIP: return "HIP runtime error";
+    case LDR_ENOMEM: return "out of memory";
+    default: return "unknown status";
+  }
+}
+
+static int views_update_impl(ldr_views* v, const int32_t* n_new, int32_t max_new,
+                             const void* K_new, const void* V_new, const void* h_new,
+                             hipStream_t st) {
+  if (!v || !n_new || max_new < 0) return LDR_EINVAL;
+  if (max_new > 0 && (!K_new || !V_new || !aligned(K_new, 16) || !aligned(V_new, 16)))
+    return LDR_EINVAL;
+  if (!h_new || !aligned(h_new, 16)) return LDR_EINVAL;
+  if (max_new > 0) {
+    if (launch_views_update(v->s, v->L, v->batch, v->arena, v->pos, v->G, n_new, max_new, K_new,
+                            V_new, h_new, st) != hipSuccess)
+      return LDR_EHIP;
+  }
+  if (launch_views_commit(v->batch, v->pos, n_new, max_new, v->status, st) != hipSuccess)
+    return LDR_EHIP;
+  return LDR_OK;
+}
+
+int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* arena,
+                   int64_t* pos, const void* G, const int32_t* n_prefix, int32_t max_prefix,
+                   const void* K_prefix, const void* V_prefix, const void* h_boundary,
+                   void* stream) {
+  if (!out) return LDR_EINVAL;
+  *out = nullptr;
+  Shape s;
+  if (!make_shape(cfg, &s) || batch <= 0 || !arena || !pos || !G) return LDR_EINVAL;
+  if (!aligned(arena, kAlign) || !aligned(G, 16) || !aligned(pos, 8)) return LDR_EINVAL;
+  if (max_prefix < 0 || (max_prefix > 0 && !n_prefix)) return LDR_EINVAL;
+  ldr_views* v = new (std::nothrow) ldr_views;
+  if (!v) return LDR_ENOMEM;
+  v->cfg = *cfg; v->s = s; v->L = make_layout(s); v->batch = batch;
+  v->arena = static_cast<uint8_t*>(arena); v->pos = pos; v->G = G; v->status = nullptr;
+  if (hipMalloc(reinterpret_cast<void**>(&v->status), 256) != hipSuccess) {
+    delete v;
+    return LDR_ENOMEM;
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipMemsetAsync(v->status, 0, 256, st) != hipSuccess ||
+      launch_views_reset(s, v->L, batch, arena, pos, st) != hipSuccess) {
+    ldr_views_destroy(v);
+    return LDR_EHIP;
+  }
+  if (max_prefix > 0) {
+    const int rc = views_update_impl(v, n_prefix, max_prefix, K_prefix, V_prefix, h_boundary, st);
+    if (rc != LDR_OK) {
+      hipStreamSynchronize(st);
+      ldr_views_destroy(v);
+      return rc;
+    }
+  }
+  *out = v;
+  return LDR_OK;
+}
+
+int ldr_views_update(ldr_views* v, const int32_t* n_new, int32_t max_new, const void* K_new,
+                     const void* V_new, const void* h_new, void* stream) {
+  return views_update_impl(v, n_new, max_new, K_new, V_new, h_new,
+                           static_cast<hipStream_t>(stream));
+}
+
+int ldr_views_status(ldr_views* v, int clear, void* stream) {
+  if (!v) return LDR_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t flag = 0;
+  if (hipMemcpyAsync(&flag, v->status, sizeof(flag), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return LDR_EHIP;
+  if (clear && flag) {
+    if (hipMemsetAsync(v->status, 0, sizeof(int32_t), st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      return LDR_EHIP;
+  }
+  if (flag & kFlagRange) return LDR_ERANGE;
+  return flag ? LDR_EINVAL : LDR_OK;
+}
+
+void ldr_views_destroy(ldr_views* v) {
+  if (!v) return;
+  if (v->status) hipFree(v->status);
+  delete v;
+}
+
+static bool weights_ok(const Shape& s, const ldr_weights* w) {
+  if (!w || !w->layers) return false;
+  const void* top[] = {w->embed, w->mask_emb, w->pos_emb, w->fc_w, w->fc_norm, w->final_norm,
+                       w->lm_head};
+  for (const void* p : top)
+    if (!p || !aligned(p, 16)) return false;
+  for (int j = 0; j < s.D; ++j) {
+    const ldr_layer_weights& L = w->layers[j];
+    const void* ps[] = {L.in_norm, L.wqkv, L.q_norm, L.k_norm, L.wo, L.post_norm, L.w_gate_up,
+                        L.w_down};
+    for (const void* p : ps)
+      if (!p || !aligned(p, 16)) return false;
+  }
+  return true;
+}
+
+int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                   float* logits, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!v || !anchor || !logits || !workspace) return LDR_EINVAL;
+  const Shape& s = v->s;
+  if (!weights_ok(s, w) || !aligned(workspace, kAlign) || !aligned(logits, 16)) return LDR_EINVAL;
+  const int batch = v->batch, M = batch * s.B;
+  const WsPlan ws = plan_ws(s, batch);
+  if (workspace_bytes < ws.bytes) return LDR_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint8_t* base = static_cast<uint8_t*>(workspace);
+  DraftPtrs p;
+  p.arena = v->arena; p.pos = v->pos; p.G = v->G; p.status = v->status;
+  p.part = reinterpret_cast<float*>(base + ws.part);
+  p.x = reinterpret_cast<float*>(base + ws.x);
+  p.nrm = base + ws.nrm; p.o = base + ws.o; p.act = base + ws.act;
+  p.rope = reinterpret_cast<float*>(base + ws.rope);
+
+#define LDR_TRY(x) do { if ((x) != hipSuccess) return LDR_EHIP; } while (0)
+  // boundary fusion: W_fc over the stored boundary states (rows of the arena)
+  GemmArgs g;
+  g.A = v->arena + v->L.h; g.lda = (long)(v->L.stride / s.el);
+  g.W = w->fc_w; g.ldw = (long)s.Lb * s.hidden; g.out = p.part; g.ldo = s.hidden;
+  g.split_stride = (long)batch * s.hidden; g.M = batch; g.N = s.hidden; g.K = s.Lb * s.hidden;
+  g.splits = ws.fc.splits; g.mlp = 0;
+  LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.fc, g, st));
+  LDR_TRY(launch_slot_init(s, batch, p, ws.fc.splits, w, anchor, st));
+  for (int j = 0; j < s.D; ++j) {
+    const ldr_layer_weights& L = w->layers[j];
+    g.A = p.nrm; g.lda = s.hidden; g.W = L.wqkv; g.ldw = s.hidden; g.out = p.part;
+    g.ldo = s.qkv_out; g.split_stride = (long)M * s.qkv_out; g.M = M; g.N = s.qkv_out;
+    g.K = s.hidden; g.splits = ws.qkv.splits;
+    LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.qkv, g, st));
+    LDR_TRY(launch_attention(s, v->L, batch, p, ws.qkv.splits, j, &L, st));
+    g.A = p.o; g.lda = (long)s.hq * s.d; g.W = L.wo; g.ldw = (long)s.hq * s.d; g.out = p.part;
+    g.ldo = s.hidden; g.split_stride = (long)M * s.hidden; g.N = s.hidden; g.K = s.hq * s.d;
+    g.splits = ws.wo.splits;
+    LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.wo, g, st));
+    LDR_TRY(launch_resid_norm(s, M, p, ws.wo.splits, L.post_norm, st));
+    g.A = p.nrm; g.lda = s.hidden; g.W = L.w_gate_up; g.ldw = s.hidden; g.out = p.act;
+    g.ldo = s.mlp; g.split_stride = 0; g.N = 2 * s.mlp; g.K = s.hidden; g.splits = 1;
+    g.mlp = s.mlp;
+    LDR_TRY(launch_gemm(s.dtype, EPI_SWIGLU, ws.gu, g, st));
+    g.A = p.act; g.lda = s.mlp; g.W = L.w_down; g.ldw = s.mlp; g.out = p.part; g.ldo = s.hidden;
+    g.split_stride = (long)M * s.hidden; g.N = s.hidden; g.K = s.mlp; g.splits = ws.down.splits;
+    g.mlp = 0;
+    LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.down, g, st));
+    const void* next = j + 1 < s.D ? w->layers[j + 1].in_norm : w->final_norm;
+    LDR_TRY(launch_resid_norm(s, M, p, ws.down.splits, next, st));
+  }
+  g.A = p.nrm; g.lda = s.hidden; g.W = w->lm_head; g.ldw = s.hidden; g.out = logits;
+  g.ldo = s.vocab; g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden; g.splits = 1;
+  LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.lm, g, st));
+#undef LDR_TRY
+  return LDR_OK;
+}
+
+size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab) {
+  if (rows <= 0 || vocab <= 0) return 0;
+  return align_up((size_t)rows * sample_splits(rows, vocab) * 16);
+}
+
+int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperature,
+               int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
+               float* logq, void* workspace, size_t workspace_bytes, void* stream) {
+  if (!logits || !tokens || !lse || !logq || !workspace) return LDR_EINVAL;
+  if (rows <= 0 || vocab <= 0 || !(temperature >= 0.f) || std::isinf(temperature))
+    return LDR_EINVAL;
+  if (top_k != 0) return LDR_EINVAL;
+  if (workspace_bytes < ldr_sample_workspace_bytes(rows, vocab) || !aligned(workspace, 16))
+    return LDR_EINVAL;
+  return launch_sample(logits, rows, vocab, temperature, top_k, seed, step, tokens, lse, logq,
+                       workspace, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? LDR_OK : LDR_EHIP;
+}
+
+int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t rows, int32_t vocab, float* out,
+                    void* stream) {
+  if (!out || rows <= 0 || vocab <= 0) return LDR_EINVAL;
+  return launch_gumbel_fill(seed, step, rows, vocab, out, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess ? LDR_OK : LDR_EHIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,122 @@
+// Internal declarations of the drafting-step library: derived shapes, the
+// per-sequence arena layout, bf16 helpers and the kernel launchers that the
+// host API (api.cpp) calls. Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/ldr.h"
+
+namespace ldr {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a; }
+
+// Byte offsets of the views inside one sequence's arena slot.
+struct Layout {
+  size_t kw, vw, m, eta, h;  // region offsets
+  size_t bytes;              // sum of the (aligned) regions
+  size_t stride;             // per-sequence stride, bytes rounded up to kAlign
+};
+
+struct Shape {
+  int hidden, hq, hkv, d, mlp, vocab, D, Lb, B, W, R, dtype;
+  int rep;       // hq / hkv
+  int qkv_out;   // (hq + 2 hkv) d
+  float eps;
+  double rope_base;
+  size_t el;     // bytes per element of the configuration dtype
+};
+
+bool make_shape(const ldr_config* c, Shape* s);
+Layout make_layout(const Shape& s);
+
+// ---- bf16 helpers (round to nearest even, as torch does) ------------------
+__host__ __device__ inline float bf16_to_f32(uint16_t h) {
+  union { uint32_t u; float f; } v;
+  v.u = (uint32_t)h << 16;
+  return v.f;
+}
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+  union { uint32_t u; float f; } v;
+  v.f = f;
+  if ((v.u & 0x7f800000u) == 0x7f800000u && (v.u & 0x007fffffu))  // NaN stays NaN
+    return (uint16_t)((v.u >> 16) | 0x40);
+  uint32_t r = v.u + 0x7fffu + ((v.u >> 16) & 1u);
+  return (uint16_t)(r >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+  __device__ static float load(const float* p) { return *p; }
+  __device__ static void store(float* p, float v) { *p = v; }
+};
+template <> struct Elem<uint16_t> {
+  __device__ static float load(const uint16_t* p) { return bf16_to_f32(*p); }
+  __device__ static void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+// ---- kernel launchers -------------------------------------------------------
+// Views (views.hip)
+hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* arena,
+                              int64_t* pos, hipStream_t st);
+hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void* arena,
+                               const int64_t* pos, const void* G, const int32_t* n_new,
+                               int max_new, const void* K_new, const void* V_new,
+                               const void* h_new, hipStream_t st);
+hipError_t launch_views_commit(int batch, int64_t* pos, const int32_t* n_new, int max_new,
+                               int32_t* status, hipStream_t st);
+
+// GEMM (gemm.hip): C = A[M][K] . W[N][K]^T, fp32 accumulation.
+enum GemmEpi {
+  EPI_STORE = 0,   // out fp32 [split][M][N] (split-K partials; split 0 only if S = 1)
+  EPI_SWIGLU = 1,  // W rows are [gate; up] (N = 2 mlp): act[M][mlp] = silu(g) * u
+};
+struct GemmArgs {
+  const void* A; long lda;     // [M][K] activations (dtype), row stride in elements
+  const void* W; long ldw;     // [N][K] weights (dtype)
+  void* out;                   // EPI_STORE: float*; EPI_SWIGLU: dtype*
+  long ldo;                    // output row stride (elements)
+  long split_stride;           // EPI_STORE: elements between split partials
+  int M, N, K, splits;
+  int mlp;                     // EPI_SWIGLU: N / 2
+};
+struct GemmPlan { int cfg, splits; int grid_x, grid_y; };
+// Tile configuration and split-K factor; splits = 1 unless allow_split.
+GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split);
+hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
+
+// Draft step pieces (draft.hip)
+struct DraftPtrs {
+  const uint8_t* arena; const int64_t* pos; const void* G;
+  float* part;     // split-K partials
+  float* x;        // residual stream fp32 [M][hidden]
+  void* nrm;       // normalised activations (dtype) [M][hidden]
+  void* o;         // attention output (dtype) [M][hq d]
+  void* act;       // SwiGLU output (dtype) [M][mlp]
+  float* rope;     // cos/sin [batch][B][d/2] x 2
+  int32_t* status; // sticky flags of the views handle
+};
+
+// Bits of the sticky device status word.
+constexpr int kFlagRange = 1;   // an update saw a row count outside [0, max_new]
+constexpr int kFlagAnchor = 2;  // a draft step saw an anchor outside [0, V)
+hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
+                            const ldr_weights* w, const int32_t* anchor, hipStream_t st);
+hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
+                             const void* gain, hipStream_t st);
+hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
+                            int qkv_splits, int layer, const ldr_layer_weights* lw,
+                            hipStream_t st);
+
+// Sampler (sample.hip)
+int sample_splits(int rows, int vocab);
+hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
+                         int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
+                         float* logq, void* ws, hipStream_t st);
+hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
+                              hipStream_t st);
+
+}  // namespace ldr

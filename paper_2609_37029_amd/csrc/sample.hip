@@ -1,0 +1,230 @@
+// Per-position sampling of the factorised proposal (Eq. 8).
+//
+// Each row of fp32 logits is split into vocabulary chunks. One workgroup per
+// (chunk, row) streams its logits once and keeps, per thread, the best
+// Gumbel-max key with its token and the running max / sum of exp(z/T) for the
+// log-normaliser; a block reduction writes one partial per chunk. A merge
+// kernel combines the chunks of a row in vocabulary order (lower token wins
+// ties) and writes the token, lse and log q(y).
+//
+// The noise is a pure function of (seed, step, row, token): Philox4x64-10
+// (Salmon et al., SC 2011; key (seed, step), counter (v/8, row, 0, 0)); one
+// Philox block serves 8 consecutive tokens, 32 bits each. The uniform
+// u = (2 (bits >> 9) + 1) 2^-24 is exact, and g = -log(-log u) uses a log
+// made of IEEE fp32 operations only (no contraction, correctly rounded
+// division), so the keys fl(fl(z/T) + g) are reproducible bit for bit.
+#include "ldr_internal.h"
+
+namespace ldr {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kGroup = 8;  // tokens per Philox block
+
+constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
+constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
+
+__device__ inline void philox4x64_10(uint64_t c[4], uint64_t k0, uint64_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    if (r) { k0 += kW0; k1 += kW1; }
+    const uint64_t hi0 = __umul64hi(kM0, c[0]), lo0 = kM0 * c[0];
+    const uint64_t hi1 = __umul64hi(kM1, c[2]), lo1 = kM1 * c[2];
+    const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
+    c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+  }
+}
+
+// Natural log of a positive normal float: x = 2^e m, m folded into
+// (sqrt(1/2), sqrt(2)], log x = e ln2 + 2 atanh(f), f = (m-1)/(m+1), with the
+// odd series of atanh to f^11. Each operation is one IEEE fp32 rounding.
+__device__ inline float fixed_logf(float x) {
+#pragma clang fp contract(off)
+  const float kC3 = __uint_as_float(0x3EAAAAABu), kC5 = __uint_as_float(0x3E4CCCCDu);
+  const float kC7 = __uint_as_float(0x3E124925u), kC9 = __uint_as_float(0x3DE38E39u);
+  const float kC11 = __uint_as_float(0x3DBA2E8Cu);
+  const float kLn2Hi = __uint_as_float(0x3F317200u), kLn2Lo = __uint_as_float(0x35BFBE8Eu);
+  const float kSqrt2 = __uint_as_float(0x3FB504F3u);
+  const uint32_t bits = __float_as_uint(x);
+  int e = (int)((bits >> 23) & 0xffu) - 127;
+  float m = __uint_as_float((bits & 0x7fffffu) | 0x3f800000u);
+  if (m > kSqrt2) { m = m * 0.5f; e += 1; }
+  const float ef = (float)e;
+  const float f = (m - 1.0f) / (m + 1.0f);
+  const float s = f * f;
+  float p = kC11;
+  p = p * s + kC9;
+  p = p * s + kC7;
+  p = p * s + kC5;
+  p = p * s + kC3;
+  p = p * s + 1.0f;
+  const float r = (f * 2.0f) * p;
+  const float lo = ef * kLn2Lo + r;
+  return ef * kLn2Hi + lo;
+}
+
+__device__ inline float gumbel_from_bits(uint32_t bits) {
+#pragma clang fp contract(off)
+  const float u = ((float)(bits >> 9) * 2.0f + 1.0f) * 5.9604644775390625e-08f;  // 2^-24
+  return -fixed_logf(-fixed_logf(u));
+}
+
+// The 8 noise words of tokens [8c, 8c+8) of `row`.
+__device__ inline void noise_group(uint64_t seed, uint64_t step, uint64_t row, uint64_t c,
+                                   uint32_t out[kGroup]) {
+  uint64_t w[4] = {c, row, 0, 0};
+  philox4x64_10(w, seed, step);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = (uint32_t)w[i];
+    out[2 * i + 1] = (uint32_t)(w[i] >> 32);
+  }
+}
+
+struct Partial { float m, s, key; int idx; };  // max z/T, sum exp(z/T - m), best key, token
+
+__device__ inline bool better(float k1, int i1, float k2, int i2) {
+  return k1 > k2 || (k1 == k2 && i1 < i2);
+}
+
+__device__ inline void combine(Partial& a, const Partial& b) {
+  if (better(b.key, b.idx, a.key, a.idx)) { a.key = b.key; a.idx = b.idx; }
+  const float m = fmaxf(a.m, b.m);
+  if (m == -INFINITY) return;
+  a.s = a.s * __expf(a.m - m) + b.s * __expf(b.m - m);
+  a.m = m;
+}
+
+struct SampleArgs {
+  const float* logits; int rows, vocab, chunk, splits;
+  float T; uint64_t seed, step;
+  Partial* part;
+};
+
+__global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) {
+  const int sp = blockIdx.x, r = blockIdx.y;
+  const int v0 = sp * a.chunk, v1 = min(a.vocab, v0 + a.chunk);
+  const float* z = a.logits + (long)r * a.vocab;
+  Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
+  if (a.T == 0.f) {
+    for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
+      const float zv = z[v];
+      if (better(zv, v, p.key, p.idx)) { p.key = zv; p.idx = v; }
+    }
+  } else {
+    for (int v = v0 + threadIdx.x * kGroup; v < v1; v += kThreads * kGroup) {
+      uint32_t bits[kGroup];
+      noise_group(a.seed, a.step, (uint64_t)r, (uint64_t)(v / kGroup), bits);
+      float zt[kGroup];
+      float gm = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < kGroup; ++i) {
+        zt[i] = (v + i < v1) ? z[v + i] / a.T : -INFINITY;  // IEEE division
+        gm = fmaxf(gm, zt[i]);
+      }
+      if (gm > p.m) { p.s *= __expf(p.m - gm); p.m = gm; }
+#pragma unroll
+      for (int i = 0; i < kGroup; ++i) {
+        if (v + i < v1) {
+          p.s += __expf(zt[i] - p.m);
+          const float key = __fadd_rn(zt[i], gumbel_from_bits(bits[i]));
+          if (better(key, v + i, p.key, p.idx)) { p.key = key; p.idx = v + i; }
+        }
+      }
+    }
+  }
+  // block reduction of the partials
+  for (int off = 32; off >= 1; off >>= 1) {
+    Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
+              __shfl_xor(p.idx, off)};
+    combine(p, o);
+  }
+  __shared__ Partial red[kThreads / 64];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = p;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kThreads / 64; ++w) combine(p, red[w]);
+    a.part[(long)r * a.splits + sp] = p;
+  }
+}
+
+__global__ void __launch_bounds__(64) sample_merge_kernel(SampleArgs a, int32_t* tokens,
+                                                          float* lse, float* logq) {
+  const int r = blockIdx.x;
+  Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
+  for (int sp = threadIdx.x; sp < a.splits; sp += 64) combine(p, a.part[(long)r * a.splits + sp]);
+  for (int off = 32; off >= 1; off >>= 1) {
+    Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
+              __shfl_xor(p.idx, off)};
+    combine(p, o);
+  }
+  if (threadIdx.x == 0) {
+    tokens[r] = p.idx;
+    if (a.T == 0.f) {
+      lse[r] = p.key;
+      logq[r] = 0.f;
+    } else {
+      const float l = p.m + logf(p.s);
+      lse[r] = l;
+      logq[r] = a.logits[(long)r * a.vocab + p.idx] / a.T - l;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(kThreads) gumbel_fill_kernel(uint64_t seed, uint64_t step,
+                                                               int rows, int vocab, float* out) {
+  const int groups = (vocab + kGroup - 1) / kGroup;
+  const long total = (long)rows * groups;
+  for (long i = blockIdx.x * (long)kThreads + threadIdx.x; i < total;
+       i += (long)gridDim.x * kThreads) {
+    const int r = (int)(i / groups), c = (int)(i % groups);
+    uint32_t bits[kGroup];
+    noise_group(seed, step, (uint64_t)r, (uint64_t)c, bits);
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      const int v = c * kGroup + k;
+      if (v < vocab) out[(long)r * vocab + v] = gumbel_from_bits(bits[k]);
+    }
+  }
+}
+
+}  // namespace
+
+int sample_splits(int rows, int vocab) {
+  // about 1024 workgroups in flight, each chunk a multiple of one Philox sweep
+  int splits = rows >= 1024 ? 1 : 1024 / rows;
+  const int sweep = kThreads * kGroup;
+  const int max_splits = (vocab + sweep - 1) / sweep;
+  if (splits > max_splits) splits = max_splits;
+  return splits < 1 ? 1 : splits;
+}
+
+hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
+                         int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
+                         float* logq, void* ws, hipStream_t st) {
+  (void)top_k;
+  SampleArgs a;
+  a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
+  a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
+  a.splits = sample_splits(rows, vocab);
+  const int sweep = kThreads * kGroup;
+  a.chunk = ((vocab + a.splits - 1) / a.splits + sweep - 1) / sweep * sweep;
+  a.splits = (vocab + a.chunk - 1) / a.chunk;
+  hipLaunchKernelGGL(sample_partial_kernel, dim3(a.splits, rows), dim3(kThreads), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sample_merge_kernel, dim3(rows), dim3(64), 0, st, a, tokens, lse, logq);
+  return hipGetLastError();
+}
+
+hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
+                              hipStream_t st) {
+  const long groups = (long)rows * ((vocab + kGroup - 1) / kGroup);
+  long blocks = (groups + kThreads - 1) / kThreads;
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(gumbel_fill_kernel, dim3((int)(blocks > 0 ? blocks : 1)), dim3(kThreads),
+                     0, st, seed, step, rows, vocab, out);
+  return hipGetLastError();
+}
+
+}  // namespace ldr

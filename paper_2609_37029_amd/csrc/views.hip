@@ -1,0 +1,260 @@
+// Fixed-size context views on the GPU (Sec. 2.2; App. A.2, Eq. 10-11).
+//
+// One workgroup per (kv group g, layer j, sequence b) ingests the new rows of
+// that sequence for that head group:
+//  * ring write of the last min(n, W) rows into window slots (t + r) mod W;
+//  * for the rep * R summary queries of the group's query heads, the
+//    statistics of the new set N (Eq. 10) by a tiled online log-sum-exp over
+//    the rows, then the two-way merge with the stored (eta, m) (Eq. 11);
+//  * a slice of the boundary-state copy.
+// A one-thread-per-sequence commit kernel then advances t (or raises the
+// sticky range flag); it runs after the update kernel on the same stream, so
+// every workgroup read the old t.
+#include "ldr_internal.h"
+
+namespace ldr {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kTileRows = 32;   // rows of N staged in LDS per step
+
+__global__ void __launch_bounds__(kThreads)
+views_reset_kernel(uint8_t* arena, size_t stride, size_t eta_off, size_t eta_bytes,
+                   int batch, int64_t* pos) {
+  const size_t words = stride / 4;
+  const size_t total = words * (size_t)batch;
+  uint32_t* w = reinterpret_cast<uint32_t*>(arena);
+  for (size_t i = blockIdx.x * (size_t)kThreads + threadIdx.x; i < total;
+       i += (size_t)gridDim.x * kThreads) {
+    const size_t off = (i % words) * 4;
+    const bool is_eta = off >= eta_off && off < eta_off + eta_bytes;
+    w[i] = is_eta ? 0xff800000u : 0u;  // -inf log-normalizer, zero elsewhere
+  }
+  if (blockIdx.x == 0)
+    for (int b = threadIdx.x; b < batch; b += kThreads) pos[b] = 0;
+}
+
+struct UpdateArgs {
+  uint8_t* arena; size_t stride; size_t kw, vw, m, eta, h;
+  const int64_t* pos; const void* G; const int32_t* n_new; int max_new;
+  const void* K_new; const void* V_new; const void* h_new;
+  int D, hq, hkv, d, W, R, rep, hb_elems;  // hb_elems = L_b * hidden
+  float inv_sqrt_d;
+};
+
+// 16-byte copy of `n16` chunks.
+__device__ inline void copy16(void* dst, const void* src, int idx) {
+  reinterpret_cast<uint4*>(dst)[idx] = reinterpret_cast<const uint4*>(src)[idx];
+}
+
+// DPT: dims of the head each thread owns; TPQ = d / DPT threads share one
+// summary query, Q = rep * R queries per workgroup, Q * TPQ = kThreads.
+template <typename T, int DPT>
+__global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
+  const int g = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int n = a.n_new[b];
+  if (n <= 0 || n > a.max_new) return;  // empty set: identity; bad count: commit flags it
+  const int64_t t = a.pos[b];
+  const int d = a.d;
+  uint8_t* seq = a.arena + (size_t)b * a.stride;
+
+  // ---- window ring write (the last min(n, W) rows) -----------------------
+  {
+    T* Kw = reinterpret_cast<T*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * d;
+    T* Vw = reinterpret_cast<T*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * d;
+    const int r0 = n > a.W ? n - a.W : 0;
+    const int cpr = d * (int)sizeof(T) / 16;  // 16-byte chunks per row
+    const int total = (n - r0) * cpr;
+    for (int i = threadIdx.x; i < total; i += kThreads) {
+      const int r = r0 + i / cpr, c = i % cpr;
+      const size_t src = ((((size_t)b * a.max_new + r) * a.D + j) * a.hkv + g) * d;
+      const int slot = (int)((t + r) % a.W);
+      copy16(Kw + (size_t)slot * d, reinterpret_cast<const T*>(a.K_new) + src, c);
+      copy16(Vw + (size_t)slot * d, reinterpret_cast<const T*>(a.V_new) + src, c);
+    }
+  }
+  // ---- boundary states: this workgroup's slice ----------------------------
+  {
+    const int chunks = a.hb_elems * (int)sizeof(T) / 16;
+    const int wgs = a.D * a.hkv, wid = j * a.hkv + g;
+    const int per = (chunks + wgs - 1) / wgs;
+    const int c0 = wid * per, c1 = min(chunks, c0 + per);
+    T* hdst = reinterpret_cast<T*>(seq + a.h);
+    const T* hsrc = reinterpret_cast<const T*>(a.h_new) + (size_t)b * a.hb_elems;
+    for (int c = c0 + threadIdx.x; c < c1; c += kThreads) copy16(hdst, hsrc, c);
+  }
+
+  // ---- summary statistics of N and the merge -----------------------------
+  __shared__ float Ks[kTileRows][256 + 4];
+  __shared__ float Vs[kTileRows][256 + 4];
+  constexpr int NV = DPT / 4;         // float4 chunks per thread
+  const int tpq = d / DPT;
+  const int q = threadIdx.x / tpq;    // summary query of the group: hh * R + r
+  const int part = threadIdx.x % tpq;
+  const int hq0 = g * a.rep;          // first query head of the group
+  // query q of the group is (head hq0 + q / R, summary row q % R); the group's
+  // queries are contiguous in G, M and eta.
+  const size_t qrow = ((size_t)j * a.hq + hq0) * a.R + q;
+
+  float gq[DPT], acc[DPT];
+  {
+    const T* Gp = reinterpret_cast<const T*>(a.G) + qrow * d;
+#pragma unroll
+    for (int c = 0; c < NV; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int dim = (c * tpq + part) * 4 + e;
+        gq[c * 4 + e] = Elem<T>::load(Gp + dim) * a.inv_sqrt_d;
+        acc[c * 4 + e] = 0.f;
+      }
+  }
+  float mx = -INFINITY, l = 0.f;
+  for (int r0 = 0; r0 < n; r0 += kTileRows) {
+    const int nr = min(kTileRows, n - r0);
+    __syncthreads();
+    for (int i = threadIdx.x; i < nr * d; i += kThreads) {
+      const int r = i / d, e = i % d;
+      const size_t src = ((((size_t)b * a.max_new + r0 + r) * a.D + j) * a.hkv + g) * d + e;
+      Ks[r][e] = Elem<T>::load(reinterpret_cast<const T*>(a.K_new) + src);
+      Vs[r][e] = Elem<T>::load(reinterpret_cast<const T*>(a.V_new) + src);
+    }
+    __syncthreads();
+    float s[kTileRows];
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < kTileRows; ++r) {
+      float p = 0.f;
+      if (r < nr) {
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+          const float4 k4 = *reinterpret_cast<const float4*>(&Ks[r][(c * tpq + part) * 4]);
+          p += gq[c * 4 + 0] * k4.x + gq[c * 4 + 1] * k4.y + gq[c * 4 + 2] * k4.z +
+               gq[c * 4 + 3] * k4.w;
+        }
+      }
+      for (int off = 1; off < tpq; off <<= 1) p += __shfl_xor(p, off);
+      s[r] = r < nr ? p : -INFINITY;
+      tmax = fmaxf(tmax, s[r]);
+    }
+    const float nm = fmaxf(mx, tmax);
+    const float alpha = expf(mx - nm);  // mx = -inf on the first tile: 0
+    l *= alpha;
+#pragma unroll
+    for (int i = 0; i < DPT; ++i) acc[i] *= alpha;
+#pragma unroll
+    for (int r = 0; r < kTileRows; ++r) {
+      if (r < nr) {
+        const float p = expf(s[r] - nm);
+        l += p;
+#pragma unroll
+        for (int c = 0; c < NV; ++c) {
+          const float4 v4 = *reinterpret_cast<const float4*>(&Vs[r][(c * tpq + part) * 4]);
+          acc[c * 4 + 0] += p * v4.x;
+          acc[c * 4 + 1] += p * v4.y;
+          acc[c * 4 + 2] += p * v4.z;
+          acc[c * 4 + 3] += p * v4.w;
+        }
+      }
+    }
+    mx = nm;
+  }
+  // eta_N = log sum exp(s), m_N = sum exp(s - eta_N) v
+  const float eta_n = mx + logf(l);
+  const float inv_l = 1.f / l;
+  float* Mq = reinterpret_cast<float*>(seq + a.m) + qrow * d;
+  float* etaq = reinterpret_cast<float*>(seq + a.eta) + qrow;
+  const float eta_a = *etaq;
+  float wa, wn, eta;
+  if (eta_a == -INFINITY) {  // empty A: the merge returns N
+    wa = 0.f; wn = inv_l; eta = eta_n;
+  } else {
+    const float mu = fmaxf(eta_a, eta_n);
+    eta = mu + logf(expf(eta_a - mu) + expf(eta_n - mu));
+    wa = expf(eta_a - eta);
+    wn = expf(eta_n - eta) * inv_l;
+  }
+#pragma unroll
+  for (int c = 0; c < NV; ++c)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int dim = (c * tpq + part) * 4 + e;
+      const float ma = wa != 0.f ? Mq[dim] : 0.f;
+      Mq[dim] = wa * ma + wn * acc[c * 4 + e];
+    }
+  __syncthreads();  // every thread of the query read eta_a before it changes
+  if (part == 0) *etaq = eta;
+}
+
+__global__ void views_commit_kernel(int batch, int64_t* pos, const int32_t* n_new,
+                                    int max_new, int32_t* status) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= batch) return;
+  const int n = n_new[b];
+  if (n < 0 || n > max_new)
+    atomicOr(status, kFlagRange);
+  else
+    pos[b] += n;
+}
+
+template <typename T>
+hipError_t launch_update_t(const UpdateArgs& a, int dpt, dim3 grid, hipStream_t st) {
+  switch (dpt) {
+    case 4: hipLaunchKernelGGL((views_update_kernel<T, 4>), grid, dim3(kThreads), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((views_update_kernel<T, 8>), grid, dim3(kThreads), 0, st, a); break;
+    case 16: hipLaunchKernelGGL((views_update_kernel<T, 16>), grid, dim3(kThreads), 0, st, a); break;
+    case 32: hipLaunchKernelGGL((views_update_kernel<T, 32>), grid, dim3(kThreads), 0, st, a); break;
+    case 64: hipLaunchKernelGGL((views_update_kernel<T, 64>), grid, dim3(kThreads), 0, st, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// Threads per summary query: Q = rep * R queries share 256 threads.
+int views_dims_per_thread(const Shape& s) {
+  const int q = s.rep * s.R;
+  if (q <= 0 || q > kThreads || kThreads % q) return 0;
+  const int tpq = kThreads / q;
+  if (tpq > 64 || s.d % tpq || s.d > 256) return 0;
+  const int dpt = s.d / tpq;
+  return (dpt == 4 || dpt == 8 || dpt == 16 || dpt == 32 || dpt == 64) ? dpt : 0;
+}
+
+hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* arena,
+                              int64_t* pos, hipStream_t st) {
+  const size_t words = L.stride / 4 * (size_t)batch;
+  const int blocks = (int)((words + kThreads - 1) / kThreads < 4096
+                               ? (words + kThreads - 1) / kThreads : 4096);
+  const size_t eta_bytes = (size_t)s.D * s.hq * s.R * 4;
+  hipLaunchKernelGGL(views_reset_kernel, dim3(blocks > 0 ? blocks : 1), dim3(kThreads), 0, st,
+                     static_cast<uint8_t*>(arena), L.stride, L.eta, eta_bytes, batch, pos);
+  return hipGetLastError();
+}
+
+hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void* arena,
+                               const int64_t* pos, const void* G, const int32_t* n_new,
+                               int max_new, const void* K_new, const void* V_new,
+                               const void* h_new, hipStream_t st) {
+  UpdateArgs a;
+  a.arena = static_cast<uint8_t*>(arena); a.stride = L.stride;
+  a.kw = L.kw; a.vw = L.vw; a.m = L.m; a.eta = L.eta; a.h = L.h;
+  a.pos = pos; a.G = G; a.n_new = n_new; a.max_new = max_new;
+  a.K_new = K_new; a.V_new = V_new; a.h_new = h_new;
+  a.D = s.D; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.W = s.W; a.R = s.R; a.rep = s.rep;
+  a.hb_elems = s.Lb * s.hidden;
+  a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
+  const dim3 grid(s.hkv, s.D, batch);
+  const int dpt = views_dims_per_thread(s);
+  return s.dtype == LDR_BF16 ? launch_update_t<uint16_t>(a, dpt, grid, st)
+                             : launch_update_t<float>(a, dpt, grid, st);
+}
+
+hipError_t launch_views_commit(int batch, int64_t* pos, const int32_t* n_new, int max_new,
+                               int32_t* status, hipStream_t st) {
+  hipLaunchKernelGGL(views_commit_kernel, dim3((batch + 255) / 256), dim3(256), 0, st, batch,
+                     pos, n_new, max_new, status);
+  return hipGetLastError();
+}
+
+}  // namespace ldr

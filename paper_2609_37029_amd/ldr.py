@@ -1,0 +1,271 @@
+"""Python binding of libldr.so (include/ldr.h): argument marshalling only.
+
+Every computation of the drafting step runs in the library's HIP kernels;
+this module turns torch tensors (device memory, streams) into the C ABI's
+pointers and sizes. It raises if the library is missing: there is no other
+implementation behind these names.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libldr.so")
+
+LDR_OK, LDR_EINVAL, LDR_ERANGE, LDR_EHIP, LDR_ENOMEM = 0, -1, -2, -3, -4
+LDR_F32, LDR_BF16 = 0, 1
+
+
+class LdrError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {_lib().ldr_strerror(code).decode()} ({code})")
+        self.code = code
+
+
+class Config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "hidden", "n_q_heads", "n_kv_heads", "head_dim", "mlp", "vocab", "n_layers",
+        "n_feat_layers", "block", "window", "summary", "dtype")] + [
+        ("rope_theta", ctypes.c_float), ("ntk_alpha", ctypes.c_float),
+        ("rms_eps", ctypes.c_float)]
+
+
+LAYER_KEYS = ("in_norm", "wqkv", "q_norm", "k_norm", "wo", "post_norm", "w_gate_up", "w_down")
+TOP_KEYS = ("embed", "mask_emb", "pos_emb", "fc_w", "fc_norm", "final_norm", "lm_head")
+
+
+class LayerWeights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in LAYER_KEYS]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in TOP_KEYS] + [
+        ("layers", ctypes.POINTER(LayerWeights))]
+
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -m paper_2609_37029_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32, I64, SZ, U64 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t,
+                                ctypes.c_uint64)
+        CP = ctypes.POINTER(Config)
+        sig = {
+            "ldr_views_state_bytes": (SZ, [CP]),
+            "ldr_views_stride_bytes": (SZ, [CP]),
+            "ldr_views_layout": (ctypes.c_int, [CP, ctypes.POINTER(SZ)]),
+            "ldr_workspace_bytes": (SZ, [CP, I32]),
+            "ldr_config_check": (ctypes.c_int, [CP]),
+            "ldr_views_init": (ctypes.c_int, [ctypes.POINTER(P), CP, I32, P, P, P, P, I32, P, P,
+                                              P, P]),
+            "ldr_views_update": (ctypes.c_int, [P, P, I32, P, P, P, P]),
+            "ldr_views_status": (ctypes.c_int, [P, ctypes.c_int, P]),
+            "ldr_views_destroy": (None, [P]),
+            "ldr_draft_step": (ctypes.c_int, [P, ctypes.POINTER(Weights), P, P, P, SZ, P]),
+            "ldr_sample_workspace_bytes": (SZ, [I32, I32]),
+            "ldr_sample": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P, P, P,
+                                          SZ, P]),
+            "ldr_gumbel_fill": (ctypes.c_int, [U64, U64, I32, I32, P, P]),
+            "ldr_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _LIB = L
+    return _LIB
+
+
+def lib():
+    """The loaded ctypes library (raises if it was not built)."""
+    return _lib()
+
+
+def _check(rc: int, what: str):
+    if rc != LDR_OK:
+        raise LdrError(rc, what)
+
+
+def config(shape) -> Config:
+    """ldr_config of a synth.Shape-like object."""
+    return Config(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.mlp,
+                  shape.vocab, shape.n_layers, shape.n_feat_layers, shape.block, shape.window,
+                  shape.summary, LDR_BF16 if shape.dtype == "bf16" else LDR_F32,
+                  shape.rope_theta, shape.ntk_alpha, shape.rms_eps)
+
+
+def state_bytes(shape) -> int:
+    return _lib().ldr_views_state_bytes(ctypes.byref(config(shape)))
+
+
+def stride_bytes(shape) -> int:
+    return _lib().ldr_views_stride_bytes(ctypes.byref(config(shape)))
+
+
+def layout(shape):
+    off = (ctypes.c_size_t * 5)()
+    _check(_lib().ldr_views_layout(ctypes.byref(config(shape)), off), "ldr_views_layout")
+    return dict(zip(("kw", "vw", "m", "eta", "h"), list(off)))
+
+
+def workspace_bytes(shape, batch: int) -> int:
+    return _lib().ldr_workspace_bytes(ctypes.byref(config(shape)), batch)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class Views:
+    """The fixed-size views of `batch` sequences in one device arena."""
+
+    def __init__(self, shape, batch: int, G: torch.Tensor, device="cuda", stream=None):
+        self.shape, self.batch = shape, batch
+        self.cfg = config(shape)
+        self.stride = stride_bytes(shape)
+        self.layout = layout(shape)
+        self.arena = torch.empty(batch * self.stride, dtype=torch.uint8, device=device)
+        self.pos = torch.empty(batch, dtype=torch.int64, device=device)
+        self.G = G
+        self._h = ctypes.c_void_p()
+        self._stream = stream
+
+    def init(self, n_prefix=None, K=None, V=None, h=None):
+        """ldr_views_init: reset, then (if given) ingest a first prefix chunk."""
+        maxp = 0 if K is None else K.shape[1]
+        _check(_lib().ldr_views_init(ctypes.byref(self._h), ctypes.byref(self.cfg), self.batch,
+                                     _ptr(self.arena), _ptr(self.pos), _ptr(self.G),
+                                     _ptr(n_prefix), maxp, _ptr(K), _ptr(V), _ptr(h),
+                                     _stream(self._stream)), "ldr_views_init")
+        return self
+
+    def update(self, n_new: torch.Tensor, K: torch.Tensor, V: torch.Tensor, h: torch.Tensor):
+        """ldr_views_update with K/V [batch][max_new][D][Hkv][d], h [batch][L_b][hidden]."""
+        _check(_lib().ldr_views_update(self._h, _ptr(n_new), K.shape[1], _ptr(K), _ptr(V),
+                                       _ptr(h), _stream(self._stream)), "ldr_views_update")
+
+    def status(self, clear: bool = False) -> int:
+        return _lib().ldr_views_status(self._h, int(clear), _stream(self._stream))
+
+    @property
+    def handle(self):
+        return self._h
+
+    # Tensor views into the arena (for checks and snapshots).
+    def _region(self, off, shape, dtype):
+        el = torch.tensor([], dtype=dtype).element_size()
+        n = 1
+        for s in shape:
+            n *= s
+        per = self.arena.view(self.batch, self.stride)
+        return per[:, off:off + n * el].view(dtype).view(self.batch, *shape)
+
+    def window(self):
+        s = self.shape
+        shp = (s.n_layers, s.n_kv_heads, s.window, s.head_dim)
+        return (self._region(self.layout["kw"], shp, s.torch_dtype),
+                self._region(self.layout["vw"], shp, s.torch_dtype))
+
+    def summary(self):
+        s = self.shape
+        return (self._region(self.layout["m"], (s.n_layers, s.n_q_heads, s.summary, s.head_dim),
+                             torch.float32),
+                self._region(self.layout["eta"], (s.n_layers, s.n_q_heads, s.summary),
+                             torch.float32))
+
+    def boundary(self):
+        s = self.shape
+        return self._region(self.layout["h"], (s.n_feat_layers, s.hidden), s.torch_dtype)
+
+    def close(self):
+        if self._h:
+            _lib().ldr_views_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class DraftWeights:
+    """ldr_weights over a synth weight dict of device tensors (kept alive here)."""
+
+    def __init__(self, w: Dict):
+        self.w = w
+        n = len(w["layers"])
+        self._layers = (LayerWeights * n)()
+        for j, L in enumerate(w["layers"]):
+            for k in LAYER_KEYS:
+                setattr(self._layers[j], k, L[k].data_ptr())
+        self.c = Weights(*[w[k].data_ptr() for k in TOP_KEYS],
+                         ctypes.cast(self._layers, ctypes.POINTER(LayerWeights)))
+
+
+def draft_step(views: Views, weights: DraftWeights, anchor: torch.Tensor,
+               logits: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+               stream=None) -> torch.Tensor:
+    """ldr_draft_step: base logits fp32 [batch][B][V]."""
+    s = views.shape
+    if logits is None:
+        logits = torch.empty(views.batch, s.block, s.vocab, dtype=torch.float32,
+                             device=views.arena.device)
+    if workspace is None:
+        workspace = torch.empty(workspace_bytes(s, views.batch), dtype=torch.uint8,
+                                device=views.arena.device)
+    _check(_lib().ldr_draft_step(views.handle, ctypes.byref(weights.c), _ptr(anchor),
+                                 _ptr(logits), _ptr(workspace), workspace.numel(),
+                                 _stream(stream)), "ldr_draft_step")
+    return logits
+
+
+def sample_workspace_bytes(rows: int, vocab: int) -> int:
+    return _lib().ldr_sample_workspace_bytes(rows, vocab)
+
+
+def sample(logits: torch.Tensor, temperature: float, top_k: int, seed: int, step: int,
+           out=None, workspace: Optional[torch.Tensor] = None, stream=None):
+    """ldr_sample over a [rows][V] fp32 tensor: (tokens int32, lse fp32, logq fp32)."""
+    V = logits.shape[-1]
+    rows = logits.numel() // V
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(rows, dtype=torch.int32, device=dev),
+               torch.empty(rows, dtype=torch.float32, device=dev),
+               torch.empty(rows, dtype=torch.float32, device=dev))
+    if workspace is None:
+        workspace = torch.empty(sample_workspace_bytes(rows, V), dtype=torch.uint8, device=dev)
+    tok, lse, logq = out
+    _check(_lib().ldr_sample(_ptr(logits), rows, V, float(temperature), int(top_k), int(seed),
+                             int(step), _ptr(tok), _ptr(lse), _ptr(logq), _ptr(workspace),
+                             workspace.numel(), _stream(stream)), "ldr_sample")
+    return out
+
+
+def gumbel_fill(seed: int, step: int, rows: int, vocab: int, device="cuda", stream=None):
+    out = torch.empty(rows, vocab, dtype=torch.float32, device=device)
+    _check(_lib().ldr_gumbel_fill(int(seed), int(step), rows, vocab, _ptr(out), _stream(stream)),
+           "ldr_gumbel_fill")
+    return out
+
+
+def device_weights(w: Dict, device="cuda") -> Dict:
+    """A synth weight dict moved to `device`."""
+    out = {k: v.to(device) for k, v in w.items() if k != "layers"}
+    out["layers"] = [{k: v.to(device) for k, v in L.items()} for L in w["layers"]]
+    return out

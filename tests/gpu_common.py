@@ -1,0 +1,125 @@
+"""Helpers of the GPU parity tests: drive the HIP views and the oracle views
+with the same seeded inputs (drawn once, on the GPU, and copied to the host
+for the oracle), and compare logits per row against the tolerances of the
+drafting step."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import synth
+from oracle import views as OV
+
+
+class Pair:
+    """GPU views of `batch` sequences plus the oracle's views of the same rows."""
+
+    def __init__(self, ldr, shape, batch, G, oracle_seqs=None):
+        self.ldr, self.s, self.batch = ldr, shape, batch
+        self.G = G
+        self.G64 = synth.to_f64(G)
+        self.views = ldr.Views(shape, batch, G).init()
+        self.seqs = list(range(batch)) if oracle_seqs is None else list(oracle_seqs)
+        self.ost = {b: OV.empty(shape) for b in self.seqs}
+
+    def ingest(self, n, K, V, h):
+        """n: list of per-sequence row counts (<= K.shape[1])."""
+        nt = torch.tensor(n, dtype=torch.int32, device=K.device)
+        self.views.update(nt, K, V, h)
+        for b in self.seqs:
+            nb = int(n[b])
+            self.ost[b] = OV.update(self.s, self.ost[b], self.G64, synth.to_f64(K[b, :nb]),
+                                    synth.to_f64(V[b, :nb]),
+                                    synth.to_f64(h[b]) if nb > 0 else self.ost[b].h)
+
+    def prefill(self, prefix, chunk, ragged=0):
+        """Ingest a synthetic prefix in chunks; sequence b gets `ragged * b` fewer rows
+        in the last chunk."""
+        for i, (K, V, h) in enumerate(synth.prefix_chunks(self.s, self.batch, prefix, chunk,
+                                                          device="cuda")):
+            n = [K.shape[1]] * self.batch
+            if ragged and (i + 1) * chunk >= prefix:
+                n = [max(0, K.shape[1] - ragged * b) for b in range(self.batch)]
+            self.ingest(n, K, V, h)
+
+    def decode(self, steps, n_max, rng):
+        for st in range(steps):
+            K, V, h = synth.decode_rows(self.s, self.batch, n_max, st, device="cuda")
+            n = [int(x) for x in rng.integers(0, n_max + 1, self.batch)]
+            self.ingest(n, K, V, h)
+
+
+def check_views(pair, rtol_m=1e-4, atol_m=1e-6):
+    torch.cuda.synchronize()
+    v = pair.views
+    pos = v.pos.cpu().numpy()
+    Kw, Vw = (t.cpu() for t in v.window())
+    M, eta = (t.cpu().numpy() for t in v.summary())
+    hb = v.boundary().cpu()
+    for b in pair.seqs:
+        o = pair.ost[b]
+        assert pos[b] == o.t, (b, pos[b], o.t)
+        # window rows and boundary states are copies: bit-exact
+        assert np.array_equal(synth.to_f64(Kw[b]), o.Kw), f"window K of sequence {b}"
+        assert np.array_equal(synth.to_f64(Vw[b]), o.Vw), f"window V of sequence {b}"
+        assert np.array_equal(synth.to_f64(hb[b]), o.h), f"boundary of sequence {b}"
+        if o.t == 0:
+            assert np.all(np.isneginf(eta[b]))
+            assert np.all(M[b] == 0)
+            continue
+        np.testing.assert_allclose(eta[b], o.eta, rtol=1e-5, atol=1e-5)
+        scale = np.abs(o.M).max()
+        np.testing.assert_allclose(M[b], o.M, rtol=rtol_m, atol=atol_m * max(scale, 1.0))
+
+
+def row_errors(z_gpu, z_ref):
+    """Per row: max |dz| / max |z_ref| and the cosine similarity."""
+    z_gpu = np.asarray(z_gpu, dtype=np.float64)
+    z_ref = np.asarray(z_ref, dtype=np.float64)
+    err = np.abs(z_gpu - z_ref).max(axis=-1) / np.abs(z_ref).max(axis=-1)
+    cos = (z_gpu * z_ref).sum(-1) / (np.linalg.norm(z_gpu, axis=-1) *
+                                     np.linalg.norm(z_ref, axis=-1))
+    return err, cos
+
+
+def check_logits(z_gpu, z_ref, shape):
+    err, cos = row_errors(z_gpu, z_ref)
+    if shape.dtype == "f32":
+        assert err.max() <= 1e-4, err.max()
+    else:
+        assert err.max() <= 2e-2, err.max()
+        assert cos.min() >= 0.999, cos.min()
+    return err, cos
+
+
+class LazyRows:
+    """Rows of a device tensor converted to float64 on indexing."""
+
+    def __init__(self, t):
+        self.t = t
+
+    def __getitem__(self, idx):
+        if isinstance(idx, np.ndarray):
+            idx = torch.from_numpy(idx).to(self.t.device)
+        return synth.to_f64(self.t[idx])
+
+
+class LazyLayers:
+    def __init__(self, layers):
+        self.layers = layers
+
+    def __getitem__(self, j):
+        return {k: synth.to_f64(v) for k, v in self.layers[j].items()}
+
+    def __len__(self):
+        return len(self.layers)
+
+
+def lazy_weights_f64(w):
+    """A weight dict for the oracle whose big tensors are converted on access."""
+    out = {k: synth.to_f64(v) for k, v in w.items()
+           if k not in ("layers", "embed", "lm_head")}
+    out["embed"] = LazyRows(w["embed"])
+    out["lm_head"] = LazyRows(w["lm_head"])
+    out["layers"] = LazyLayers(w["layers"])
+    return out

@@ -1,0 +1,95 @@
+"""Host-side checks of libldr.so that need no GPU: every symbol that
+include/ldr.h declares is exported, the state-size and layout formulas, the
+configuration checks and the synchronous argument validation."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import synth
+from oracle import views as oviews
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2609_37029_amd import ldr
+    if not os.path.exists(ldr.LIB_PATH):
+        pytest.fail("libldr.so is not built (python -m paper_2609_37029_amd.build)")
+    return ldr
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "ldr.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ldr_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert len(names) >= 14
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+@pytest.mark.parametrize("shape,expected", [(synth.QWEN3_8B, 6_604_800),
+                                            (synth.QWEN3_32B, 7_936_000),
+                                            (synth.TINY, 150_784)])
+def test_state_bytes(L, shape, expected):
+    assert L.state_bytes(shape) == expected == oviews.state_bytes(shape)
+    assert L.stride_bytes(shape) % 256 == 0 and L.stride_bytes(shape) >= expected
+
+
+def test_layout_regions(L):
+    s = synth.QWEN3_8B
+    off = L.layout(s)
+    win = s.n_layers * s.n_kv_heads * s.window * s.head_dim * 2
+    assert off["kw"] == 0 and off["vw"] == win and off["m"] == 2 * win
+    assert off["eta"] - off["m"] == s.n_layers * s.n_q_heads * s.summary * s.head_dim * 4
+    assert off["h"] - off["eta"] == s.n_layers * s.n_q_heads * s.summary * 4
+    assert all(v % 256 == 0 for v in off.values())
+
+
+def test_config_check(L):
+    good = L.config(synth.QWEN3_8B)
+    assert L.lib().ldr_config_check(ctypes.byref(good)) == L.LDR_OK
+    bad = [dict(n_kv_heads=7), dict(head_dim=96), dict(block=17), dict(block=0), dict(dtype=5),
+           dict(hidden=4000), dict(window=0), dict(rms_eps=0.0), dict(mlp=100)]
+    for kw in bad:
+        c = L.config(synth.QWEN3_8B)
+        for k, v in kw.items():
+            setattr(c, k, v)
+        assert L.lib().ldr_config_check(ctypes.byref(c)) == L.LDR_EINVAL, kw
+        assert L.lib().ldr_views_state_bytes(ctypes.byref(c)) == 0
+
+
+def test_workspace_grows_with_batch(L):
+    s = synth.QWEN3_8B
+    sizes = [L.workspace_bytes(s, b) for b in (1, 16, 64)]
+    assert 0 < sizes[0] < sizes[1] < sizes[2]
+    assert L.workspace_bytes(s, 0) == 0
+
+
+def test_host_validation_needs_no_gpu(L):
+    lib = L.lib()
+    h = ctypes.c_void_p()
+    cfg = L.config(synth.TINY)
+    # null arena / pos / G: rejected before any device call
+    assert lib.ldr_views_init(ctypes.byref(h), ctypes.byref(cfg), 1, None, None, None, None, 0,
+                              None, None, None, None) == L.LDR_EINVAL
+    assert lib.ldr_views_init(None, ctypes.byref(cfg), 1, None, None, None, None, 0, None, None,
+                              None, None) == L.LDR_EINVAL
+    assert lib.ldr_views_update(None, None, 17, None, None, None, None) == L.LDR_EINVAL
+    assert lib.ldr_draft_step(None, None, None, None, None, 0, None) == L.LDR_EINVAL
+    assert lib.ldr_sample(None, 4, 10, 1.0, 0, 0, 0, None, None, None, None, 0, None) == \
+        L.LDR_EINVAL
+    assert lib.ldr_gumbel_fill(0, 0, 0, 10, None, None) == L.LDR_EINVAL
+    assert lib.ldr_views_status(None, 0, None) == L.LDR_EINVAL
+    lib.ldr_views_destroy(None)
+    assert lib.ldr_sample_workspace_bytes(0, 10) == 0
+    assert lib.ldr_sample_workspace_bytes(256, 151936) > 0
+    for code in (0, -1, -2, -3, -4):
+        assert lib.ldr_strerror(code)

@@ -1,0 +1,113 @@
+"""GPU parity of the draft step (Eq. 4, Eq. 6; Sec. 2.3; App. A.1): base
+logits of the HIP path against the fp64 oracle forward over the oracle's own
+views of the same inputs, plus the structural properties (depends only on
+the views, deterministic, t = 0 and partial windows)."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from gpu_common import Pair, check_logits, lazy_weights_f64, row_errors
+from oracle import draft as OD
+
+pytestmark = pytest.mark.gpu
+
+MINI_BF16 = synth.QWEN3_8B.replace(name="mini-bf16", hidden=512, n_q_heads=8, n_kv_heads=2,
+                                   mlp=1024, vocab=5003, n_layers=2, n_feat_layers=3,
+                                   window=64)
+
+
+def setup(gpu_lib, shape, batch, prefix, gain_std=0.1, decode=3):
+    G = synth.make_G(shape, device="cuda")
+    p = Pair(gpu_lib, shape, batch, G)
+    if prefix:
+        p.prefill(prefix, max(prefix // 2, 1), ragged=3)
+    if decode:
+        p.decode(decode, shape.block + 1, np.random.default_rng(7))
+    w = synth.make_weights(shape, gain_std=gain_std, device="cuda")
+    dw = gpu_lib.DraftWeights(w)
+    anchor = synth.make_anchors(shape, batch, device="cuda")
+    return p, w, dw, anchor
+
+
+def oracle_logits(p, w, anchor, seqs=None, vocab_idx=None, lazy=False):
+    Wt = lazy_weights_f64(w) if lazy else synth.weights_f64(w)
+    a = anchor.cpu().numpy()
+    seqs = p.seqs if seqs is None else seqs
+    return {b: OD.forward(p.s, Wt, p.ost[b], p.G64, int(a[b]), vocab_idx=vocab_idx) for b in seqs}
+
+
+@pytest.mark.parametrize("shape,batch,prefix", [
+    (synth.TINY, 1, 2048),     # the fp32 parity configuration
+    (synth.TINY, 3, 40),       # partial window (t < W)
+    (MINI_BF16, 3, 300),       # bf16, GQA, ragged vocab, 48 rows
+    (MINI_BF16, 17, 150),      # bf16, 272 rows: two M tiles, the last ragged
+])
+def test_logits_match_oracle(gpu_lib, shape, batch, prefix):
+    p, w, dw, anchor = setup(gpu_lib, shape, batch, prefix)
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    torch.cuda.synchronize()
+    ref = oracle_logits(p, w, anchor)
+    zc = z.cpu().numpy()
+    for b in p.seqs:
+        check_logits(zc[b], ref[b], shape)
+
+
+@pytest.mark.parametrize("shape", [synth.TINY, MINI_BF16])
+def test_empty_views(gpu_lib, shape):
+    # t = 0: no window rows, no summary; only the block attends to itself
+    p, w, dw, anchor = setup(gpu_lib, shape, 2, 0, decode=0)
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    torch.cuda.synchronize()
+    ref = oracle_logits(p, w, anchor)
+    for b in p.seqs:
+        check_logits(z.cpu().numpy()[b], ref[b], shape)
+
+
+def test_deterministic_and_depends_only_on_views(gpu_lib):
+    s = MINI_BF16
+    p, w, dw, anchor = setup(gpu_lib, s, 4, 200)
+    z1 = gpu_lib.draft_step(p.views, dw, anchor).clone()
+    z2 = gpu_lib.draft_step(p.views, dw, anchor).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(z1, z2)
+    # snapshot the arena and positions, move the views on, restore: identical logits
+    snap, pos = p.views.arena.clone(), p.views.pos.clone()
+    K, V, h = synth.decode_rows(s, 4, s.block + 1, 99, device="cuda")
+    p.views.update(torch.full((4,), s.block + 1, dtype=torch.int32, device="cuda"), K, V, h)
+    z3 = gpu_lib.draft_step(p.views, dw, anchor).clone()
+    torch.cuda.synchronize()
+    assert not torch.equal(z1, z3)
+    # poison the rows that were just ingested: the draft reads only the views
+    K.fill_(float("nan")); V.fill_(float("nan")); h.fill_(float("nan"))
+    p.views.arena.copy_(snap)
+    p.views.pos.copy_(pos)
+    z4 = gpu_lib.draft_step(p.views, dw, anchor)
+    torch.cuda.synchronize()
+    assert torch.equal(z1, z4)
+
+
+@pytest.mark.slow
+def test_full_size_qwen3_8b_sampled(gpu_lib):
+    """Qwen3-8B shape, batch 16, prefix 32768: the configuration the benchmark
+    times. Oracle on two sequences, all 16 slots, a 2048-token vocabulary
+    sample."""
+    s = synth.QWEN3_8B
+    G = synth.make_G(s, device="cuda")
+    p = Pair(gpu_lib, s, 16, G, oracle_seqs=[0, 11])
+    p.prefill(32768, 4096)
+    K, V, h = synth.decode_rows(s, 16, 17, 0, device="cuda")
+    p.ingest([17] * 16, K, V, h)
+    w = synth.make_weights(s, device="cuda")
+    dw = gpu_lib.DraftWeights(w)
+    anchor = synth.make_anchors(s, 16, device="cuda")
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    torch.cuda.synchronize()
+    idx = np.sort(np.random.default_rng(3).choice(s.vocab, 2048, replace=False))
+    idx = np.concatenate([[0], idx, [s.vocab - 1]])
+    ref = oracle_logits(p, w, anchor, vocab_idx=idx, lazy=True)
+    zc = z[:, :, torch.from_numpy(idx).cuda()].cpu().numpy()
+    for b in p.seqs:
+        err, cos = row_errors(zc[b], ref[b])
+        assert err.max() <= 2e-2, err.max()
+        assert cos.min() >= 0.999, cos.min()

@@ -1,0 +1,67 @@
+"""GPU parity of per-position sampling (Eq. 8): the Gumbel noise bit for bit,
+tokens exactly, lse and log q within fp32 tolerance, against the oracle fed
+the same fp32 logits buffer."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import sample as OS
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("rows,vocab", [(3, 151936), (37, 1001), (5, 7)])
+def test_gumbel_noise_is_bit_exact(gpu_lib, rows, vocab):
+    g = gpu_lib.gumbel_fill(1234, 9, rows, vocab).cpu().numpy()
+    ref = OS.gumbel(1234, 9, np.arange(rows)[:, None], np.arange(vocab)[None, :])
+    assert g.dtype == np.float32
+    assert np.array_equal(g.view(np.uint32), ref.view(np.uint32))
+
+
+def _logits(rows, vocab, seed, scale=1.3):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    return torch.randn(rows, vocab, generator=g, device="cuda") * scale
+
+
+@pytest.mark.parametrize("rows,vocab,T", [(32, 151936, 1.0), (16, 151936, 0.7),
+                                          (300, 5003, 1.0), (9, 2049, 1.7), (4, 3, 1.0)])
+def test_tokens_exact_given_the_same_logits(gpu_lib, rows, vocab, T):
+    z = _logits(rows, vocab, rows * 7 + vocab)
+    tok, lse, logq = gpu_lib.sample(z, T, 0, seed=77, step=5)
+    torch.cuda.synchronize()
+    y, l, lq = OS.sample(z.cpu().numpy(), T, 0, 77, 5)
+    assert np.array_equal(tok.cpu().numpy().astype(np.int64), y)
+    np.testing.assert_allclose(lse.cpu().numpy(), l, rtol=2e-6, atol=2e-5)
+    np.testing.assert_allclose(logq.cpu().numpy(), lq, rtol=1e-5, atol=2e-4)
+
+
+def test_greedy_and_ties(gpu_lib):
+    z = _logits(50, 151936, 3)
+    z[4, 1000] = 50.0
+    z[4, 70000] = 50.0          # tie: the lower index wins
+    z[7, :] = 0.0               # all equal: token 0
+    tok, lse, logq = gpu_lib.sample(z, 0.0, 0, seed=0, step=0)
+    torch.cuda.synchronize()
+    y, l, lq = OS.sample(z.cpu().numpy(), 0.0, 0, 0, 0)
+    assert np.array_equal(tok.cpu().numpy().astype(np.int64), y)
+    assert tok[4].item() == 1000 and tok[7].item() == 0
+    assert np.array_equal(lse.cpu().numpy(), l.astype(np.float32))
+    assert np.all(logq.cpu().numpy() == 0)
+
+
+def test_steps_and_seeds_change_the_draw(gpu_lib):
+    z = torch.zeros(256, 4096, device="cuda")
+    a = gpu_lib.sample(z, 1.0, 0, seed=1, step=0)[0].cpu()
+    b = gpu_lib.sample(z, 1.0, 0, seed=1, step=1)[0].cpu()
+    c = gpu_lib.sample(z, 1.0, 0, seed=2, step=0)[0].cpu()
+    assert (a != b).float().mean() > 0.9 and (a != c).float().mean() > 0.9
+    # uniform logits: every token is equally likely, lse = log V exactly in exact arithmetic
+    lse = gpu_lib.sample(z, 1.0, 0, seed=1, step=0)[1].cpu().numpy()
+    np.testing.assert_allclose(lse, np.log(4096.0), rtol=1e-6)
+
+
+def test_top_k_not_yet_accepted(gpu_lib):
+    z = _logits(2, 100, 1)
+    with pytest.raises(gpu_lib.LdrError):
+        gpu_lib.sample(z, 1.0, 5, seed=0, step=0)
