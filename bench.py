@@ -1,0 +1,358 @@
+#!/usr/bin/env python3
+"""Benchmark of the fixed-cost drafting step on one MI355X.
+
+One step is one pass of the whole hot path for `batch` sequences: the views
+ingest the 17 rows a verification pass commits (ldr_views_update), the
+drafter proposes B = 16 tokens per sequence from the views alone
+(ldr_draft_step), and every position is sampled (ldr_sample, temperature 1,
+seeded Gumbel noise). The metric is drafted tokens per second, batch * B per
+step, with every input resident in HBM before timing starts.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --sweep [--sweep-out PATH]   # latency vs prefix length and batch
+
+Prints one JSON line. Inputs are seeded synthetic tensors with the shapes of
+the workload (random-init weights, N(0, 1) target K/V rows and hidden states).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+DEFAULT_WORKLOAD = "qwen3-8b-b16-t32768"
+METRIC = "drafted tokens/sec and µs/draft step vs prefix length (Qwen3-8B shape, batch 16)"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seqs", type=int, default=2,
+                    help="sequences in the CPU-oracle sample")
+    ap.add_argument("--sweep", action="store_true")
+    ap.add_argument("--sweep-out", default=os.path.join(ROOT, "gpurun_out", "sweep.json"))
+    ap.add_argument("--sweep-prefix", default="1024,4096,16384,65536,131072,262144")
+    ap.add_argument("--sweep-batch", default="1,16,64")
+    return ap.parse_args()
+
+
+# ---- algorithmic bytes and flops of each launch kind --------------------------------------
+
+def launch_costs(s, batch):
+    """(bytes, flops) per launch of every draft-step kernel kind: weights read
+    once, activations in, outputs out (fp32 outputs where the path keeps fp32)."""
+    M = batch * s.block
+    el = 2 if s.dtype == "bf16" else 4
+    H, V = s.hidden, s.vocab
+
+    def gemm(m, n, k, out_el):
+        return n * k * el + m * k * el + m * n * out_el, 2 * m * n * k
+
+    c = {
+        "fc_gemm": gemm(batch, H, s.n_feat_layers * H, 4),
+        "qkv_gemm": gemm(M, s.qkv_out, H, 4),
+        "o_gemm": gemm(M, H, s.n_q_heads * s.head_dim, 4),
+        "gate_up_gemm": (2 * s.mlp * H * el + M * H * el + M * s.mlp * el, 2 * M * 2 * s.mlp * H),
+        "down_gemm": gemm(M, H, s.mlp, 4),
+        "lm_head": gemm(M, V, H, 4),
+    }
+    # attention: window K/V of the layer + G and M of its heads + block q/k/v in, o out
+    win = batch * 2 * s.n_kv_heads * s.window * s.head_dim * el
+    summ = s.n_q_heads * s.summary * s.head_dim * el + batch * s.n_q_heads * s.summary * \
+        s.head_dim * 4
+    qkv = M * s.qkv_out * 4 + M * s.n_q_heads * s.head_dim * el
+    nk = s.block + s.window + s.summary
+    c["attention"] = (win + summ + qkv, 4 * M * s.n_q_heads * nk * s.head_dim)
+    norm = M * H * 4 * 2 + M * H * el
+    c["post_norm"] = (norm, 0)
+    c["next_norm"] = (norm, 0)
+    c["slot_init"] = (batch * H * 4 + M * H * (4 + el) + s.block * H * el, 0)
+    return c
+
+
+def update_bytes(s, batch, n):
+    el = 2 if s.dtype == "bf16" else 4
+    rows = batch * n * s.n_layers * s.n_kv_heads * s.head_dim * el * 2     # K/V in
+    window = rows                                                        # ring write
+    summ = batch * s.n_layers * s.n_q_heads * s.summary * (s.head_dim + 1) * 4 * 2  # M, eta RMW
+    G = s.n_layers * s.n_q_heads * s.summary * s.head_dim * el
+    h = batch * s.n_feat_layers * s.hidden * el * 2
+    return rows + window + summ + G + h
+
+
+# ---- setup -----------------------------------------------------------------------------
+
+class Rig:
+    """Device-resident inputs and outputs of one workload."""
+
+    def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False):
+        self.torch, self.ldr, self.s, self.batch = torch, ldr, shape, batch
+        dev = "cuda"
+        self.w = synth.make_weights(shape, device=dev)
+        self.dw = ldr.DraftWeights(self.w)
+        self.G = synth.make_G(shape, device=dev)
+        self.views = ldr.Views(shape, batch, self.G).init()
+        if reuse_chunk:     # the same synthetic rows ingested repeatedly (timing sweeps)
+            K, V, h = synth.make_rows(shape, batch, min(chunk, prefix), synth.SEED_PREFIX,
+                                      device=dev) + (synth.make_h(shape, batch, synth.SEED_PREFIX,
+                                                                  device=dev),)
+            done = 0
+            while done < prefix:
+                n = min(K.shape[1], prefix - done)
+                self.views.update(torch.full((batch,), n, dtype=torch.int32, device=dev), K, V, h)
+                done += n
+            del K, V, h
+        else:
+            for K, V, h in synth.prefix_chunks(shape, batch, prefix, chunk, device=dev):
+                self.views.update(torch.full((batch,), K.shape[1], dtype=torch.int32,
+                                             device=dev), K, V, h)
+        self.n_new = shape.block + 1
+        self.rows = [synth.decode_rows(shape, batch, self.n_new, st, device=dev) for st in range(4)]
+        self.n = torch.full((batch,), self.n_new, dtype=torch.int32, device=dev)
+        self.anchor = synth.make_anchors(shape, batch, device=dev)
+        self.logits = torch.empty(batch, shape.block, shape.vocab, dtype=torch.float32,
+                                  device=dev)
+        self.ws = torch.empty(ldr.workspace_bytes(shape, batch), dtype=torch.uint8, device=dev)
+        rows = batch * shape.block
+        self.sws = torch.empty(ldr.sample_workspace_bytes(rows, shape.vocab), dtype=torch.uint8,
+                               device=dev)
+        self.out = (torch.empty(rows, dtype=torch.int32, device=dev),
+                    torch.empty(rows, dtype=torch.float32, device=dev),
+                    torch.empty(rows, dtype=torch.float32, device=dev))
+        self.kinds = ldr.draft_launches(shape)
+        torch.cuda.synchronize()
+        if self.views.status() != ldr.LDR_OK:
+            raise RuntimeError("views status error after prefill")
+
+    def step(self, i, events=None, temperature=1.0):
+        K, V, h = self.rows[i % len(self.rows)]
+        self.views.update(self.n, K, V, h)
+        if events is None:
+            self.ldr.draft_step(self.views, self.dw, self.anchor, self.logits, self.ws)
+        else:
+            self.ldr.draft_step_events(self.views, self.dw, self.anchor, self.logits, self.ws,
+                                       events)
+        self.ldr.sample(self.logits.view(-1, self.s.vocab), temperature, 0, 5, i, out=self.out,
+                        workspace=self.sws)
+
+
+def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
+    """Wall-clock of `steps` steps between two synchronisations; per-step
+    durations from events at step boundaries; optionally events around the
+    launches of kinds in `bracket` (summed per step)."""
+    for i in range(warmup):
+        rig.step(i)
+    torch.cuda.synchronize()
+    marks = [ev.create() for _ in range(steps + 1)] if ev else None
+    kern = None
+    if ev and bracket:
+        n = len(rig.kinds)
+        kern = []
+        for _ in range(steps):
+            evs = [None] * (n + 1)
+            for li, k in enumerate(rig.kinds):
+                if k in bracket:
+                    evs[li] = evs[li] or ev.create()
+                    evs[li + 1] = ev.create()
+            kern.append(evs)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        if marks:
+            ev.record(marks[i])
+        rig.step(warmup + i, events=kern[i] if kern else None)
+    if marks:
+        ev.record(marks[steps])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per_step = [ev.elapsed_ms(marks[i], marks[i + 1]) for i in range(steps)] if marks else []
+    kernel_ms = []
+    if kern:
+        for evs in kern:
+            tot, launches = 0.0, 0
+            for li, k in enumerate(rig.kinds):
+                if k in bracket:
+                    tot += ev.elapsed_ms(evs[li], evs[li + 1])
+                    launches += 1
+            kernel_ms.append((tot, launches))
+    return wall, per_step, kernel_ms
+
+
+def kind_breakdown(torch, ldr, rig, ev, reps=5):
+    """Milliseconds per step of each launch kind (events around every launch)."""
+    n = len(rig.kinds)
+    tot = {}
+    for r in range(reps):
+        evs = [ev.create() for _ in range(n + 1)]
+        K, V, h = rig.rows[r % 4]
+        rig.views.update(rig.n, K, V, h)
+        ldr.draft_step_events(rig.views, rig.dw, rig.anchor, rig.logits, rig.ws, evs)
+        torch.cuda.synchronize()
+        for li, k in enumerate(rig.kinds):
+            tot[k] = tot.get(k, 0.0) + ev.elapsed_ms(evs[li], evs[li + 1])
+    return {k: v / reps for k, v in tot.items()}
+
+
+def percentile(xs, q):
+    xs = sorted(xs)
+    if not xs:
+        return None
+    i = min(len(xs) - 1, max(0, int(round(q * (len(xs) - 1)))))
+    return xs[i]
+
+
+# ---- CPU oracle baseline ----------------------------------------------------------------
+
+def cpu_baseline(torch, synth, rig, n_seqs):
+    """The fp64 oracle on a bounded sample of the same step: views update of 17
+    rows + draft forward + sampling of the B positions, for n_seqs sequences
+    over views built from a 512-row prefix (the oracle's step cost does not
+    depend on the prefix length once the window is full)."""
+    import numpy as np
+    from oracle import draft as OD
+    from oracle import sample as OS
+    from oracle import views as OV
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    s = rig.s
+    Wt = synth.weights_f64(rig.w)
+    G64 = synth.to_f64(rig.G)
+    anchor = rig.anchor.cpu().numpy()
+    K, V, h = synth.make_rows(s, n_seqs, 512, 77) + (synth.make_h(s, n_seqs, 77),)
+    Kd, Vd, hd = synth.decode_rows(s, n_seqs, s.block + 1, 0)
+    states = []
+    for b in range(n_seqs):
+        states.append(OV.update(s, OV.empty(s), G64, synth.to_f64(K[b]), synth.to_f64(V[b]),
+                                synth.to_f64(h[b])))
+    t0 = time.perf_counter()
+    for b in range(n_seqs):
+        st = OV.update(s, states[b], G64, synth.to_f64(Kd[b]), synth.to_f64(Vd[b]),
+                       synth.to_f64(hd[b]))
+        z = OD.forward(s, Wt, st, G64, int(anchor[b]))
+        OS.sample(z.astype(np.float32), 1.0, 0, 5, 0, rows=np.arange(b * s.block,
+                                                                      (b + 1) * s.block))
+    el = time.perf_counter() - t0
+    del Wt
+    return {"value": n_seqs * s.block / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n_seqs} of the workload's sequences: views update (17 rows) + fp64 "
+                      f"draft forward + sampling of {s.block} positions over {s.vocab} tokens, "
+                      f"{el:.2f} s (BLAS threads {cores}; elementwise numpy single-threaded)"}
+
+
+# ---- main --------------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": f"--gpus {args.gpus}: this benchmark runs on one GPU only; "
+                                   "the drafting step shards by sequence with no exchange, so "
+                                   "N GPUs run N independent copies"}))
+        sys.exit(2)
+    import torch
+
+    import synth
+    from paper_2609_37029_amd import ldr
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    if args.sweep:
+        return sweep(args, torch, ldr, synth)
+
+    wl = synth.WORKLOADS[args.workload]
+    s, batch = wl.shape, wl.batch
+    rig = Rig(torch, ldr, synth, s, batch, wl.prefix)
+    ev = ldr.HipEvents()
+    costs = launch_costs(s, batch)
+    # which launch kind dominates the step (events around every launch, outside the timed run)
+    br = kind_breakdown(torch, ldr, rig, ev)
+    gemm_kinds = [k for k in br if k.endswith("gemm") or k == "lm_head"]
+    dom = max(br, key=lambda k: br[k])
+    wall, per_step, kern = time_steps(torch, rig, args.steps, args.warmup, ev=ev, bracket={dom})
+    torch.cuda.synchronize()
+    ms = wall / args.steps * 1e3
+    tokens = batch * s.block * args.steps
+    launches_of_dom = sum(1 for k in rig.kinds if k == dom)
+    dom_ms = statistics.mean(t for t, _ in kern) / launches_of_dom
+    dom_bytes = costs[dom][0]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    step_bytes = sum(costs[k][0] for k in rig.kinds) + update_bytes(s, batch, s.block + 1) + \
+        batch * s.block * s.vocab * 4
+    step_flops = sum(costs[k][1] for k in rig.kinds)
+    gemm_ms = sum(br[k] for k in gemm_kinds)
+    gemm_flops = sum(costs[k][1] * sum(1 for x in rig.kinds if x == k) for k in gemm_kinds)
+    out = {
+        "metric": METRIC, "value": tokens / wall, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": s.dtype,
+        "data": "synthetic (seeded random-init weights, N(0,1) target K/V rows and hidden "
+                "states; prefix rows ingested through ldr_views_update before timing)",
+        "config": {"workload": wl.name, "shape": s.name, "batch": batch, "block": s.block,
+                   "prefix": wl.prefix, "rows_per_update": s.block + 1, "temperature": 1.0,
+                   "window": s.window, "summary": s.summary, "draft_layers": s.n_layers},
+        "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,
+                        "p90": percentile(per_step, .9) * 1e3},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_launch": dom_bytes, "us_per_launch": dom_ms * 1e3,
+                     "launches_per_step": launches_of_dom},
+        "step_roofline": {"algorithmic_bytes": step_bytes, "flops": step_flops,
+                          "hbm_frac": step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
+                          "gemm_mfma_frac": gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
+        "breakdown_us": {k: v * 1e3 for k, v in sorted(br.items(), key=lambda kv: -kv[1])},
+        "state_bytes_per_seq": ldr.state_bytes(s),
+    }
+    ev.close()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(torch, synth, rig, args.cpu_seqs)
+    print(json.dumps(out), flush=True)
+
+
+def sweep(args, torch, ldr, synth):
+    s = synth.QWEN3_8B
+    ev = ldr.HipEvents()
+    res = []
+    for batch in [int(x) for x in args.sweep_batch.split(",")]:
+        for prefix in [int(x) for x in args.sweep_prefix.split(",")]:
+            rig = Rig(torch, ldr, synth, s, batch, prefix, reuse_chunk=True)
+            wall, per_step, _ = time_steps(torch, rig, args.steps, args.warmup, ev=ev)
+            r = {"batch": batch, "prefix": prefix, "us_p50": percentile(per_step, .5) * 1e3,
+                 "us_p10": percentile(per_step, .1) * 1e3,
+                 "us_p90": percentile(per_step, .9) * 1e3,
+                 "tokens_per_s": batch * s.block * args.steps / wall,
+                 "state_bytes_per_seq": ldr.state_bytes(s)}
+            res.append(r)
+            print(json.dumps(r), file=sys.stderr, flush=True)
+            del rig
+            torch.cuda.empty_cache()
+    flat = {}
+    for batch in sorted({r["batch"] for r in res}):
+        xs = [r["us_p50"] for r in res if r["batch"] == batch]
+        flat[str(batch)] = (max(xs) - min(xs)) / min(xs)
+    os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
+    with open(args.sweep_out, "w") as f:
+        json.dump({"shape": s.name, "points": res, "variation": flat}, f, indent=1)
+    print(json.dumps({"metric": "draft-step latency vs prefix length", "shape": s.name,
+                      "variation_max_over_min_minus_1": flat, "points": len(res),
+                      "out": args.sweep_out}), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -183,6 +183,33 @@ void ldr_views_destroy(ldr_views* v);
 int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
                    float* logits, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Kernel launches of one draft step, in order. */
+enum ldr_launch_kind {
+  LDR_LAUNCH_FC_GEMM = 0,      /* boundary fusion W_fc (split-K partials)          */
+  LDR_LAUNCH_SLOT_INIT = 1,    /* c_t norm, slot inputs, first pre-norm, RoPE table */
+  LDR_LAUNCH_QKV_GEMM = 2,     /* per layer: QKV projection                         */
+  LDR_LAUNCH_ATTENTION = 3,    /* per layer: block-view attention (Eq. 6)           */
+  LDR_LAUNCH_O_GEMM = 4,       /* per layer: output projection                      */
+  LDR_LAUNCH_POST_NORM = 5,    /* per layer: residual add + pre-MLP RMSNorm         */
+  LDR_LAUNCH_GATE_UP_GEMM = 6, /* per layer: gate/up projection + SwiGLU            */
+  LDR_LAUNCH_DOWN_GEMM = 7,    /* per layer: down projection                        */
+  LDR_LAUNCH_NEXT_NORM = 8,    /* per layer: residual add + next (or final) RMSNorm */
+  LDR_LAUNCH_LM_HEAD = 9       /* vocabulary head, fp32 logits                      */
+};
+
+/* Number of kernel launches of ldr_draft_step for this configuration
+ * (LDR_EINVAL if invalid); writes the kind of each, in order, to
+ * kinds[0 .. max_kinds). kinds may be NULL. */
+int32_t ldr_draft_step_launches(const ldr_config* cfg, int32_t* kinds, int32_t max_kinds);
+
+/* ldr_draft_step that also records caller-created hipEvent_t events on
+ * `stream`: events[i] right before launch i and events[n] after the last
+ * launch, n = ldr_draft_step_launches(cfg). n_events must be n + 1; NULL
+ * entries are skipped. For timing single kernels of the step. */
+int ldr_draft_step_events(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                          float* logits, void* workspace, size_t workspace_bytes,
+                          void* const* events, int32_t n_events, void* stream);
+
 /* Workspace bytes ldr_sample needs for `rows` rows of `vocab` logits. */
 size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
 

@@ -36,6 +36,11 @@ bool make_shape(const ldr_config* c, Shape* s) {
                  std::pow((double)c->ntk_alpha, (double)s->d / (double)(s->d - 2));
   s->el = c->dtype == LDR_BF16 ? 2 : 4;
   if (views_dims_per_thread(*s) == 0) return false;
+  if (s->dtype == LDR_BF16) {
+    if (!attention_mfma_supported(s->d, s->rep, s->B, s->R)) return false;
+    // GEMM K dimensions in whole pairs of 64-element steps of the bf16 main loop
+    if (s->hidden % 128 || s->mlp % 128 || (s->hq * s->d) % 128) return false;
+  }
   return true;
 }
 
@@ -240,15 +245,50 @@ static bool weights_ok(const Shape& s, const ldr_weights* w) {
   return true;
 }
 
-int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
-                   float* logits, void* workspace, size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+// The launch sequence of one draft step. `emit(kind, launch)` is called once
+// per kernel in order; `launch` performs it. Shared by the kernel-kind query
+// and the step itself so the two cannot disagree.
+template <typename Emit>
+static int draft_sequence(const Shape& s, int D, Emit&& emit) {
+  int rc = emit(LDR_LAUNCH_FC_GEMM, 0);
+  if (rc == LDR_OK) rc = emit(LDR_LAUNCH_SLOT_INIT, 0);
+  for (int j = 0; j < D && rc == LDR_OK; ++j) {
+    const int kinds[] = {LDR_LAUNCH_QKV_GEMM, LDR_LAUNCH_ATTENTION, LDR_LAUNCH_O_GEMM,
+                         LDR_LAUNCH_POST_NORM, LDR_LAUNCH_GATE_UP_GEMM, LDR_LAUNCH_DOWN_GEMM,
+                         LDR_LAUNCH_NEXT_NORM};
+    for (int k : kinds)
+      if (rc == LDR_OK) rc = emit(k, j);
+  }
+  if (rc == LDR_OK) rc = emit(LDR_LAUNCH_LM_HEAD, 0);
+  (void)s;
+  return rc;
+}
+
+extern "C" int32_t ldr_draft_step_launches(const ldr_config* cfg, int32_t* kinds,
+                                           int32_t max_kinds) {
+  Shape s;
+  if (!make_shape(cfg, &s)) return LDR_EINVAL;
+  int32_t n = 0;
+  draft_sequence(s, s.D, [&](int kind, int) {
+    if (kinds && n < max_kinds) kinds[n] = kind;
+    ++n;
+    return (int)LDR_OK;
+  });
+  return n;
+}
+
+static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                           float* logits, void* workspace, size_t workspace_bytes,
+                           void* const* events, int32_t n_events, hipStream_t st) {
   if (!v || !anchor || !logits || !workspace) return LDR_EINVAL;
   const Shape& s = v->s;
   if (!weights_ok(s, w) || !aligned(workspace, kAlign) || !aligned(logits, 16)) return LDR_EINVAL;
+  if (events && n_events != ldr_draft_step_launches(&v->cfg, nullptr, 0) + 1) return LDR_EINVAL;
   const int batch = v->batch, M = batch * s.B;
   const WsPlan ws = plan_ws(s, batch);
   if (workspace_bytes < ws.bytes) return LDR_EINVAL;
-  hipStream_t st = static_cast<hipStream_t>(stream);
   uint8_t* base = static_cast<uint8_t*>(workspace);
   DraftPtrs p;
   p.arena = v->arena; p.pos = v->pos; p.G = v->G; p.status = v->status;
@@ -257,43 +297,93 @@ int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anch
   p.nrm = base + ws.nrm; p.o = base + ws.o; p.act = base + ws.act;
   p.rope = reinterpret_cast<float*>(base + ws.rope);
 
-#define LDR_TRY(x) do { if ((x) != hipSuccess) return LDR_EHIP; } while (0)
-  // boundary fusion: W_fc over the stored boundary states (rows of the arena)
-  GemmArgs g;
-  g.A = v->arena + v->L.h; g.lda = (long)(v->L.stride / s.el);
-  g.W = w->fc_w; g.ldw = (long)s.Lb * s.hidden; g.out = p.part; g.ldo = s.hidden;
-  g.split_stride = (long)batch * s.hidden; g.M = batch; g.N = s.hidden; g.K = s.Lb * s.hidden;
-  g.splits = ws.fc.splits; g.mlp = 0;
-  LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.fc, g, st));
-  LDR_TRY(launch_slot_init(s, batch, p, ws.fc.splits, w, anchor, st));
-  for (int j = 0; j < s.D; ++j) {
-    const ldr_layer_weights& L = w->layers[j];
-    g.A = p.nrm; g.lda = s.hidden; g.W = L.wqkv; g.ldw = s.hidden; g.out = p.part;
-    g.ldo = s.qkv_out; g.split_stride = (long)M * s.qkv_out; g.M = M; g.N = s.qkv_out;
-    g.K = s.hidden; g.splits = ws.qkv.splits;
-    LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.qkv, g, st));
-    LDR_TRY(launch_attention(s, v->L, batch, p, ws.qkv.splits, j, &L, st));
-    g.A = p.o; g.lda = (long)s.hq * s.d; g.W = L.wo; g.ldw = (long)s.hq * s.d; g.out = p.part;
-    g.ldo = s.hidden; g.split_stride = (long)M * s.hidden; g.N = s.hidden; g.K = s.hq * s.d;
-    g.splits = ws.wo.splits;
-    LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.wo, g, st));
-    LDR_TRY(launch_resid_norm(s, M, p, ws.wo.splits, L.post_norm, st));
-    g.A = p.nrm; g.lda = s.hidden; g.W = L.w_gate_up; g.ldw = s.hidden; g.out = p.act;
-    g.ldo = s.mlp; g.split_stride = 0; g.N = 2 * s.mlp; g.K = s.hidden; g.splits = 1;
-    g.mlp = s.mlp;
-    LDR_TRY(launch_gemm(s.dtype, EPI_SWIGLU, ws.gu, g, st));
-    g.A = p.act; g.lda = s.mlp; g.W = L.w_down; g.ldw = s.mlp; g.out = p.part; g.ldo = s.hidden;
-    g.split_stride = (long)M * s.hidden; g.N = s.hidden; g.K = s.mlp; g.splits = ws.down.splits;
+  int li = 0;
+  auto mark = [&](int i) -> bool {
+    return !events || !events[i] ||
+           hipEventRecord(static_cast<hipEvent_t>(events[i]), st) == hipSuccess;
+  };
+  auto run = [&](int kind, int j) -> int {
+    if (!mark(li)) return LDR_EHIP;
+    GemmArgs g;
     g.mlp = 0;
-    LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.down, g, st));
-    const void* next = j + 1 < s.D ? w->layers[j + 1].in_norm : w->final_norm;
-    LDR_TRY(launch_resid_norm(s, M, p, ws.down.splits, next, st));
-  }
-  g.A = p.nrm; g.lda = s.hidden; g.W = w->lm_head; g.ldw = s.hidden; g.out = logits;
-  g.ldo = s.vocab; g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden; g.splits = 1;
-  LDR_TRY(launch_gemm(s.dtype, EPI_STORE, ws.lm, g, st));
-#undef LDR_TRY
-  return LDR_OK;
+    hipError_t e = hipSuccess;
+    const ldr_layer_weights& L = w->layers[j];
+    switch (kind) {
+      case LDR_LAUNCH_FC_GEMM:  // boundary fusion over the stored boundary states
+        g.A = v->arena + v->L.h; g.lda = (long)(v->L.stride / s.el);
+        g.W = w->fc_w; g.ldw = (long)s.Lb * s.hidden; g.out = p.part; g.ldo = s.hidden;
+        g.split_stride = (long)batch * s.hidden; g.M = batch; g.N = s.hidden;
+        g.K = s.Lb * s.hidden; g.splits = ws.fc.splits;
+        e = launch_gemm(s.dtype, EPI_STORE, ws.fc, g, st);
+        break;
+      case LDR_LAUNCH_SLOT_INIT:
+        e = launch_slot_init(s, batch, p, ws.fc.splits, w, anchor, st);
+        break;
+      case LDR_LAUNCH_QKV_GEMM:
+        g.A = p.nrm; g.lda = s.hidden; g.W = L.wqkv; g.ldw = s.hidden; g.out = p.part;
+        g.ldo = s.qkv_out; g.split_stride = (long)M * s.qkv_out; g.M = M; g.N = s.qkv_out;
+        g.K = s.hidden; g.splits = ws.qkv.splits;
+        e = launch_gemm(s.dtype, EPI_STORE, ws.qkv, g, st);
+        break;
+      case LDR_LAUNCH_ATTENTION:
+        e = launch_attention(s, v->L, batch, p, ws.qkv.splits, j, &L, st);
+        break;
+      case LDR_LAUNCH_O_GEMM:
+        g.A = p.o; g.lda = (long)s.hq * s.d; g.W = L.wo; g.ldw = (long)s.hq * s.d;
+        g.out = p.part; g.ldo = s.hidden; g.split_stride = (long)M * s.hidden; g.M = M;
+        g.N = s.hidden; g.K = s.hq * s.d; g.splits = ws.wo.splits;
+        e = launch_gemm(s.dtype, EPI_STORE, ws.wo, g, st);
+        break;
+      case LDR_LAUNCH_POST_NORM:
+        e = launch_resid_norm(s, M, p, ws.wo.splits, L.post_norm, st);
+        break;
+      case LDR_LAUNCH_GATE_UP_GEMM:
+        g.A = p.nrm; g.lda = s.hidden; g.W = L.w_gate_up; g.ldw = s.hidden; g.out = p.act;
+        g.ldo = s.mlp; g.split_stride = 0; g.M = M; g.N = 2 * s.mlp; g.K = s.hidden;
+        g.splits = 1; g.mlp = s.mlp;
+        e = launch_gemm(s.dtype, EPI_SWIGLU, ws.gu, g, st);
+        break;
+      case LDR_LAUNCH_DOWN_GEMM:
+        g.A = p.act; g.lda = s.mlp; g.W = L.w_down; g.ldw = s.mlp; g.out = p.part;
+        g.ldo = s.hidden; g.split_stride = (long)M * s.hidden; g.M = M; g.N = s.hidden;
+        g.K = s.mlp; g.splits = ws.down.splits;
+        e = launch_gemm(s.dtype, EPI_STORE, ws.down, g, st);
+        break;
+      case LDR_LAUNCH_NEXT_NORM:
+        e = launch_resid_norm(s, M, p, ws.down.splits,
+                              j + 1 < s.D ? w->layers[j + 1].in_norm : w->final_norm, st);
+        break;
+      case LDR_LAUNCH_LM_HEAD:
+        g.A = p.nrm; g.lda = s.hidden; g.W = w->lm_head; g.ldw = s.hidden; g.out = logits;
+        g.ldo = s.vocab; g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden;
+        g.splits = 1;
+        e = launch_gemm(s.dtype, EPI_LOGITS, ws.lm, g, st);
+        break;
+      default:
+        return LDR_EINVAL;
+    }
+    ++li;
+    return e == hipSuccess ? (int)LDR_OK : (int)LDR_EHIP;
+  };
+  int rc = draft_sequence(s, s.D, run);
+  if (rc == LDR_OK && !mark(li)) rc = LDR_EHIP;
+  return rc;
+}
+
+extern "C" {
+
+int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                   float* logits, void* workspace, size_t workspace_bytes, void* stream) {
+  return draft_step_impl(v, w, anchor, logits, workspace, workspace_bytes, nullptr, 0,
+                         static_cast<hipStream_t>(stream));
+}
+
+int ldr_draft_step_events(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                          float* logits, void* workspace, size_t workspace_bytes,
+                          void* const* events, int32_t n_events, void* stream) {
+  if (!events) return LDR_EINVAL;
+  return draft_step_impl(v, w, anchor, logits, workspace, workspace_bytes, events, n_events,
+                         static_cast<hipStream_t>(stream));
 }
 
 size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab) {

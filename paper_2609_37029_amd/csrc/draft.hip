@@ -43,54 +43,56 @@ struct SlotArgs {
   float eps; double base;
 };
 
+// One workgroup per (slot i, sequence b): every workgroup of a sequence
+// reduces the boundary-fusion partials itself (hidden floats per split, from
+// L2) so the slots proceed independently.
 template <typename T>
 __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
   extern __shared__ float smem[];
   float* c = smem;                 // [hidden]
   float* red = smem + a.hidden;    // [4]
-  const int b = blockIdx.x, H = a.hidden;
+  const int i = blockIdx.x, b = blockIdx.y, H = a.hidden;
+  const long m = (long)b * a.B + i;
   float ss = 0.f;
-  for (int k = threadIdx.x; k < H; k += kThreads) {
-    float v = 0.f;
-    for (int s = 0; s < a.splits; ++s) v += a.part[s * a.split_stride + (long)b * H + k];
-    c[k] = v;
-    ss += v * v;
+  for (int k = threadIdx.x * 4; k < H; k += kThreads * 4) {
+    float4 v = *reinterpret_cast<const float4*>(a.part + (long)b * H + k);
+    for (int s = 1; s < a.splits; ++s) {
+      const float4 u = *reinterpret_cast<const float4*>(a.part + s * a.split_stride + (long)b * H + k);
+      v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+    }
+    *reinterpret_cast<float4*>(c + k) = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float inv_c = rsqrtf(block_sum(ss, red) / H + a.eps);
-  for (int k = threadIdx.x; k < H; k += kThreads)
-    c[k] = c[k] * inv_c * Elem<T>::load(static_cast<const T*>(a.fc_norm) + k);
-  __syncthreads();
   int anchor = a.anchor[b];
   if (anchor < 0 || anchor >= a.vocab) {  // never read outside the embedding table
-    if (threadIdx.x == 0) atomicOr(a.status, kFlagAnchor);
+    if (threadIdx.x == 0 && i == 0) atomicOr(a.status, kFlagAnchor);
     anchor = 0;
   }
-  for (int i = 0; i < a.B; ++i) {
-    const long m = (long)b * a.B + i;
-    const T* e = i == 0 ? static_cast<const T*>(a.embed) + (long)anchor * H
-                        : static_cast<const T*>(a.mask_emb);
-    const T* p = static_cast<const T*>(a.pos_emb) + (long)i * H;
-    float sx = 0.f;
-    for (int k = threadIdx.x; k < H; k += kThreads) {
-      const float v = Elem<T>::load(e + k) + Elem<T>::load(p + k) + c[k];
-      a.x[m * H + k] = v;
-      sx += v * v;
-    }
-    const float inv = rsqrtf(block_sum(sx, red) / H + a.eps);
-    for (int k = threadIdx.x; k < H; k += kThreads)
-      Elem<T>::store(static_cast<T*>(a.nrm) + m * H + k,
-                     a.x[m * H + k] * inv * Elem<T>::load(static_cast<const T*>(a.in_norm0) + k));
+  const T* e = i == 0 ? static_cast<const T*>(a.embed) + (long)anchor * H
+                      : static_cast<const T*>(a.mask_emb);
+  const T* p = static_cast<const T*>(a.pos_emb) + (long)i * H;
+  const T* gfc = static_cast<const T*>(a.fc_norm);
+  float sx = 0.f;
+  for (int k = threadIdx.x; k < H; k += kThreads) {
+    const float v = Elem<T>::load(e + k) + Elem<T>::load(p + k) +
+                    c[k] * inv_c * Elem<T>::load(gfc + k);
+    c[k] = v;                      // each thread rewrites only the entries it read
+    a.x[m * H + k] = v;
+    sx += v * v;
   }
-  // rotary table for slots at absolute positions t + i
+  const float inv = rsqrtf(block_sum(sx, red) / H + a.eps);
+  const T* gin = static_cast<const T*>(a.in_norm0);
+  for (int k = threadIdx.x; k < H; k += kThreads)
+    Elem<T>::store(static_cast<T*>(a.nrm) + m * H + k, c[k] * inv * Elem<T>::load(gin + k));
+  // rotary table row of this slot, absolute position t + i
   const int half = a.d / 2;
   const long t = a.pos[b];
-  for (int idx = threadIdx.x; idx < a.B * half; idx += kThreads) {
-    const int i = idx / half, e = idx % half;
-    const double inv_freq = pow(a.base, -2.0 * e / a.d);
+  for (int e2 = threadIdx.x; e2 < half; e2 += kThreads) {
+    const double inv_freq = pow(a.base, -2.0 * e2 / a.d);
     const double ang = (double)(t + i) * inv_freq;
-    const long m = (long)b * a.B + i;
-    a.rope[m * half + e] = (float)cos(ang);
-    a.rope[(long)a.M * half + m * half + e] = (float)sin(ang);
+    a.rope[m * half + e2] = (float)cos(ang);
+    a.rope[(long)a.M * half + m * half + e2] = (float)sin(ang);
   }
 }
 
@@ -104,28 +106,29 @@ __global__ void __launch_bounds__(kThreads) resid_norm_kernel(ResidArgs a) {
   __shared__ float red[kThreads / 64];
   const long m = blockIdx.x;
   const int H = a.hidden;
+  float* x = a.x + m * H;
+  const float* part = a.part + m * H;
   float ss = 0.f;
-  for (int k = threadIdx.x; k < H; k += kThreads) {
-    float v = a.x[m * H + k];
-    for (int s = 0; s < a.splits; ++s) v += a.part[s * a.split_stride + m * H + k];
-    a.x[m * H + k] = v;
-    ss += v * v;
+  for (int k = threadIdx.x * 4; k < H; k += kThreads * 4) {
+    float4 v = *reinterpret_cast<const float4*>(x + k);
+    for (int s = 0; s < a.splits; ++s) {
+      const float4 u = *reinterpret_cast<const float4*>(part + s * a.split_stride + k);
+      v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+    }
+    *reinterpret_cast<float4*>(x + k) = v;
+    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float inv = rsqrtf(block_sum(ss, red) / H + a.eps);
-  for (int k = threadIdx.x; k < H; k += kThreads)
-    Elem<T>::store(static_cast<T*>(a.nrm) + m * H + k,
-                   a.x[m * H + k] * inv * Elem<T>::load(static_cast<const T*>(a.gain) + k));
+  const T* gain = static_cast<const T*>(a.gain);
+  T* out = static_cast<T*>(a.nrm) + m * H;
+  for (int k = threadIdx.x * 4; k < H; k += kThreads * 4) {
+    const float4 v = *reinterpret_cast<const float4*>(x + k);
+    Elem<T>::store(out + k + 0, v.x * inv * Elem<T>::load(gain + k + 0));
+    Elem<T>::store(out + k + 1, v.y * inv * Elem<T>::load(gain + k + 1));
+    Elem<T>::store(out + k + 2, v.z * inv * Elem<T>::load(gain + k + 2));
+    Elem<T>::store(out + k + 3, v.w * inv * Elem<T>::load(gain + k + 3));
+  }
 }
-
-struct AttnArgs {
-  const float* part; long split_stride; int splits;   // QKV split-K partials [M][qkv_out]
-  const uint8_t* arena; size_t stride; size_t kw, vw, m_off;
-  const int64_t* pos; const void* G; const float* rope;
-  const void* q_norm; const void* k_norm;
-  void* o;
-  int layer, hq, hkv, d, B, W, R, rep, qkv_out, M;
-  float eps, inv_sqrt_d;
-};
 
 // Generic attention over the concatenated context, one workgroup per (query
 // head h, sequence b): scores for all keys in LDS, one softmax, then P.V.
@@ -234,9 +237,9 @@ hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int f
   a.eps = s.eps; a.base = s.rope_base;
   const size_t shm = (s.hidden + 4) * sizeof(float);
   if (s.dtype == LDR_BF16)
-    hipLaunchKernelGGL(slot_init_kernel<uint16_t>, dim3(batch), dim3(kThreads), shm, st, a);
+    hipLaunchKernelGGL(slot_init_kernel<uint16_t>, dim3(s.B, batch), dim3(kThreads), shm, st, a);
   else
-    hipLaunchKernelGGL(slot_init_kernel<float>, dim3(batch), dim3(kThreads), shm, st, a);
+    hipLaunchKernelGGL(slot_init_kernel<float>, dim3(s.B, batch), dim3(kThreads), shm, st, a);
   return hipGetLastError();
 }
 
@@ -264,11 +267,9 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
   a.R = s.R; a.rep = s.rep; a.qkv_out = s.qkv_out; a.M = M;
   a.eps = s.eps; a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const size_t shm = (size_t)(3 * s.B * s.d + s.B * (s.B + s.W + s.R)) * sizeof(float);
+  if (s.dtype == LDR_BF16) return launch_attention_mfma(a, s.hkv, batch, st);
   const dim3 grid(s.hq, batch);
-  if (s.dtype == LDR_BF16)
-    hipLaunchKernelGGL(attention_valu_kernel<uint16_t>, grid, dim3(kThreads), shm, st, a);
-  else
-    hipLaunchKernelGGL(attention_valu_kernel<float>, grid, dim3(kThreads), shm, st, a);
+  hipLaunchKernelGGL(attention_valu_kernel<float>, grid, dim3(kThreads), shm, st, a);
   return hipGetLastError();
 }
 

@@ -48,6 +48,15 @@ __host__ __device__ inline uint16_t f32_to_bf16(float f) {
   return (uint16_t)(r >> 16);
 }
 
+// Workgroup barrier that orders LDS accesses only: each wave waits for its own
+// LDS operations, not for its global loads still in flight. __syncthreads()
+// also drains every outstanding global load, which would stall software
+// pipelines that keep prefetches in flight across the barrier. Register data
+// from those loads is still waited for where it is consumed.
+__device__ inline void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
   __device__ static float load(const float* p) { return *p; }
@@ -73,6 +82,7 @@ hipError_t launch_views_commit(int batch, int64_t* pos, const int32_t* n_new, in
 enum GemmEpi {
   EPI_STORE = 0,   // out fp32 [split][M][N] (split-K partials; split 0 only if S = 1)
   EPI_SWIGLU = 1,  // W rows are [gate; up] (N = 2 mlp): act[M][mlp] = silu(g) * u
+  EPI_LOGITS = 2,  // the vocabulary head: fp32 logits [M][V], never split
 };
 struct GemmArgs {
   const void* A; long lda;     // [M][K] activations (dtype), row stride in elements
@@ -83,7 +93,7 @@ struct GemmArgs {
   int M, N, K, splits;
   int mlp;                     // EPI_SWIGLU: N / 2
 };
-struct GemmPlan { int cfg, splits; int grid_x, grid_y; };
+struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile configuration
 // Tile configuration and split-K factor; splits = 1 unless allow_split.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
@@ -103,6 +113,20 @@ struct DraftPtrs {
 // Bits of the sticky device status word.
 constexpr int kFlagRange = 1;   // an update saw a row count outside [0, max_new]
 constexpr int kFlagAnchor = 2;  // a draft step saw an anchor outside [0, V)
+// Attention over [block; window; summary] of one layer (Eq. 6).
+struct AttnArgs {
+  const float* part; long split_stride; int splits;   // QKV split-K partials [M][qkv_out]
+  const uint8_t* arena; size_t stride; size_t kw, vw, m_off;
+  const int64_t* pos; const void* G; const float* rope;
+  const void* q_norm; const void* k_norm;
+  void* o;
+  int layer, hq, hkv, d, B, W, R, rep, qkv_out, M;
+  float eps, inv_sqrt_d;
+};
+// bf16 MFMA kernel (attn.hip): one workgroup per (kv group, sequence).
+hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st);
+bool attention_mfma_supported(int d, int rep, int B, int R);
+
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st);
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,

@@ -72,6 +72,9 @@ def _lib():
             "ldr_views_status": (ctypes.c_int, [P, ctypes.c_int, P]),
             "ldr_views_destroy": (None, [P]),
             "ldr_draft_step": (ctypes.c_int, [P, ctypes.POINTER(Weights), P, P, P, SZ, P]),
+            "ldr_draft_step_launches": (I32, [CP, P, I32]),
+            "ldr_draft_step_events": (ctypes.c_int, [P, ctypes.POINTER(Weights), P, P, P, SZ, P,
+                                                     I32, P]),
             "ldr_sample_workspace_bytes": (SZ, [I32, I32]),
             "ldr_sample": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P, P, P,
                                           SZ, P]),
@@ -232,6 +235,75 @@ def draft_step(views: Views, weights: DraftWeights, anchor: torch.Tensor,
                                  _ptr(logits), _ptr(workspace), workspace.numel(),
                                  _stream(stream)), "ldr_draft_step")
     return logits
+
+
+LAUNCH_KINDS = ("fc_gemm", "slot_init", "qkv_gemm", "attention", "o_gemm", "post_norm",
+                "gate_up_gemm", "down_gemm", "next_norm", "lm_head")
+
+
+def draft_launches(shape):
+    """Kinds (names) of the kernel launches of one draft step, in order."""
+    cfg = config(shape)
+    n = _lib().ldr_draft_step_launches(ctypes.byref(cfg), None, 0)
+    kinds = (ctypes.c_int32 * n)()
+    _lib().ldr_draft_step_launches(ctypes.byref(cfg), kinds, n)
+    return [LAUNCH_KINDS[k] for k in kinds]
+
+
+def draft_step_events(views: Views, weights: DraftWeights, anchor: torch.Tensor,
+                      logits: torch.Tensor, workspace: torch.Tensor, events, stream=None):
+    """ldr_draft_step recording raw hipEvent_t handles (ints or None) around its
+    launches: events[i] before launch i, events[n] after the last."""
+    arr = (ctypes.c_void_p * len(events))(*[e if e else None for e in events])
+    _check(_lib().ldr_draft_step_events(views.handle, ctypes.byref(weights.c), _ptr(anchor),
+                                        _ptr(logits), _ptr(workspace), workspace.numel(),
+                                        arr, len(events), _stream(stream)),
+           "ldr_draft_step_events")
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime this process already loaded
+    (the one torch uses), for timing single kernels on a stream."""
+
+    def __init__(self):
+        path = None
+        for line in open("/proc/self/maps"):
+            if "libamdhip64" in line:
+                path = line.split()[-1]
+                break
+        if path is None:
+            raise RuntimeError("the HIP runtime is not loaded (initialise torch.cuda first)")
+        self.rt = ctypes.CDLL(path)
+        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+        self.rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self._made = []
+
+    def create(self):
+        e = ctypes.c_void_p()
+        if self.rt.hipEventCreate(ctypes.byref(e)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        self._made.append(e.value)
+        return e.value
+
+    def record(self, e, stream=None):
+        if self.rt.hipEventRecord(e, _stream(stream)) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def elapsed_ms(self, a, b) -> float:
+        self.rt.hipEventSynchronize(b)
+        ms = ctypes.c_float()
+        if self.rt.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def close(self):
+        for e in self._made:
+            self.rt.hipEventDestroy(e)
+        self._made = []
 
 
 def sample_workspace_bytes(rows: int, vocab: int) -> int:
