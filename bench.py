@@ -69,11 +69,13 @@ def launch_costs(s, batch):
         "down_gemm": gemm(M, H, s.mlp, 4),
         "lm_head": gemm(M, V, H, 4),
     }
+    # QKV finishing: fp32 projection in, q/k/v rows out, rotary table and gains
+    c["qkv_finish"] = (M * s.qkv_out * (4 + el) + M * s.head_dim * 4 + 2 * s.head_dim * el, 0)
     # attention: window K/V of the layer + G and M of its heads + block q/k/v in, o out
     win = batch * 2 * s.n_kv_heads * s.window * s.head_dim * el
     summ = s.n_q_heads * s.summary * s.head_dim * el + batch * s.n_q_heads * s.summary * \
         s.head_dim * 4
-    qkv = M * s.qkv_out * 4 + M * s.n_q_heads * s.head_dim * el
+    qkv = M * s.qkv_out * el + M * s.n_q_heads * s.head_dim * el
     nk = s.block + s.window + s.summary
     c["attention"] = (win + summ + qkv, 4 * M * s.n_q_heads * nk * s.head_dim)
     norm = M * H * 4 * 2 + M * H * el

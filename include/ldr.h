@@ -194,7 +194,8 @@ enum ldr_launch_kind {
   LDR_LAUNCH_GATE_UP_GEMM = 6, /* per layer: gate/up projection + SwiGLU            */
   LDR_LAUNCH_DOWN_GEMM = 7,    /* per layer: down projection                        */
   LDR_LAUNCH_NEXT_NORM = 8,    /* per layer: residual add + next (or final) RMSNorm */
-  LDR_LAUNCH_LM_HEAD = 9       /* vocabulary head, fp32 logits                      */
+  LDR_LAUNCH_LM_HEAD = 9,      /* vocabulary head, fp32 logits                      */
+  LDR_LAUNCH_QKV_FINISH = 10   /* per layer: QKV split-K sum, q/k RMSNorm, RoPE     */
 };
 
 /* Number of kernel launches of ldr_draft_step for this configuration

@@ -35,7 +35,7 @@ bool make_shape(const ldr_config* c, Shape* s) {
   s->rope_base = (double)c->rope_theta *
                  std::pow((double)c->ntk_alpha, (double)s->d / (double)(s->d - 2));
   s->el = c->dtype == LDR_BF16 ? 2 : 4;
-  if (views_dims_per_thread(*s) == 0) return false;
+  if (views_dims_per_thread(*s) == 0 || !norm_hidden_supported(s->hidden)) return false;
   if (s->dtype == LDR_BF16) {
     if (!attention_mfma_supported(s->d, s->rep, s->B, s->R)) return false;
     // GEMM K dimensions in whole pairs of 64-element steps of the bf16 main loop
@@ -59,7 +59,7 @@ Layout make_layout(const Shape& s) {
 
 // Workspace regions of one draft step for `batch` sequences.
 struct WsPlan {
-  size_t part, x, nrm, o, act, rope, bytes;
+  size_t part, x, nrm, qkvb, o, act, rope, bytes;
   GemmPlan fc, qkv, wo, gu, down, lm;
 };
 
@@ -80,6 +80,7 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   w.part = off; off = align_up(off + part * 4);
   w.x = off; off = align_up(off + (size_t)M * s.hidden * 4);
   w.nrm = off; off = align_up(off + (size_t)M * s.hidden * s.el);
+  w.qkvb = off; off = align_up(off + (size_t)M * s.qkv_out * s.el);
   w.o = off; off = align_up(off + (size_t)M * s.hq * s.d * s.el);
   w.act = off; off = align_up(off + (size_t)M * s.mlp * s.el);
   w.rope = off; off = align_up(off + (size_t)2 * M * (s.d / 2) * 4);
@@ -255,7 +256,8 @@ static int draft_sequence(const Shape& s, int D, Emit&& emit) {
   int rc = emit(LDR_LAUNCH_FC_GEMM, 0);
   if (rc == LDR_OK) rc = emit(LDR_LAUNCH_SLOT_INIT, 0);
   for (int j = 0; j < D && rc == LDR_OK; ++j) {
-    const int kinds[] = {LDR_LAUNCH_QKV_GEMM, LDR_LAUNCH_ATTENTION, LDR_LAUNCH_O_GEMM,
+    const int kinds[] = {LDR_LAUNCH_QKV_GEMM, LDR_LAUNCH_QKV_FINISH, LDR_LAUNCH_ATTENTION,
+                         LDR_LAUNCH_O_GEMM,
                          LDR_LAUNCH_POST_NORM, LDR_LAUNCH_GATE_UP_GEMM, LDR_LAUNCH_DOWN_GEMM,
                          LDR_LAUNCH_NEXT_NORM};
     for (int k : kinds)
@@ -294,7 +296,7 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
   p.arena = v->arena; p.pos = v->pos; p.G = v->G; p.status = v->status;
   p.part = reinterpret_cast<float*>(base + ws.part);
   p.x = reinterpret_cast<float*>(base + ws.x);
-  p.nrm = base + ws.nrm; p.o = base + ws.o; p.act = base + ws.act;
+  p.nrm = base + ws.nrm; p.qkv = base + ws.qkvb; p.o = base + ws.o; p.act = base + ws.act;
   p.rope = reinterpret_cast<float*>(base + ws.rope);
 
   int li = 0;
@@ -325,8 +327,11 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         g.K = s.hidden; g.splits = ws.qkv.splits;
         e = launch_gemm(s.dtype, EPI_STORE, ws.qkv, g, st);
         break;
+      case LDR_LAUNCH_QKV_FINISH:
+        e = launch_qkv_finish(s, M, p, ws.qkv.splits, &L, st);
+        break;
       case LDR_LAUNCH_ATTENTION:
-        e = launch_attention(s, v->L, batch, p, ws.qkv.splits, j, &L, st);
+        e = launch_attention(s, v->L, batch, p, j, st);
         break;
       case LDR_LAUNCH_O_GEMM:
         g.A = p.o; g.lda = (long)s.hq * s.d; g.W = L.wo; g.ldw = (long)s.hq * s.d;

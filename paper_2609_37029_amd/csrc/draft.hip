@@ -43,27 +43,47 @@ struct SlotArgs {
   float eps; double base;
 };
 
-// One workgroup per (slot i, sequence b): every workgroup of a sequence
-// reduces the boundary-fusion partials itself (hidden floats per split, from
-// L2) so the slots proceed independently.
-template <typename T>
-__global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
-  extern __shared__ float smem[];
-  float* c = smem;                 // [hidden]
-  float* red = smem + a.hidden;    // [4]
-  const int i = blockIdx.x, b = blockIdx.y, H = a.hidden;
-  const long m = (long)b * a.B + i;
-  float ss = 0.f;
-  for (int k = threadIdx.x * 4; k < H; k += kThreads * 4) {
-    float4 v = *reinterpret_cast<const float4*>(a.part + (long)b * H + k);
-    for (int s = 1; s < a.splits; ++s) {
-      const float4 u = *reinterpret_cast<const float4*>(a.part + s * a.split_stride + (long)b * H + k);
-      v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
-    }
-    *reinterpret_cast<float4*>(c + k) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+// Loads and stores of 4 consecutive elements of the configuration dtype.
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  __device__ static float4 load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  __device__ static void store(float* p, float4 v) { *reinterpret_cast<float4*>(p) = v; }
+};
+template <> struct Vec4<uint16_t> {
+  __device__ static float4 load(const uint16_t* p) {
+    const uint2 u = *reinterpret_cast<const uint2*>(p);
+    return make_float4(bf16_to_f32(u.x & 0xffffu), bf16_to_f32(u.x >> 16),
+                       bf16_to_f32(u.y & 0xffffu), bf16_to_f32(u.y >> 16));
   }
-  const float inv_c = rsqrtf(block_sum(ss, red) / H + a.eps);
+  __device__ static void store(uint16_t* p, float4 v) {
+    uint2 u;
+    u.x = f32_to_bf16(v.x) | ((uint32_t)f32_to_bf16(v.y) << 16);
+    u.y = f32_to_bf16(v.z) | ((uint32_t)f32_to_bf16(v.w) << 16);
+    *reinterpret_cast<uint2*>(p) = u;
+  }
+};
+__device__ inline float4 f4add(float4 a, float4 b) {
+  return make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
+__device__ inline float f4dot(float4 a) { return a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w; }
+__device__ inline float4 f4scale(float4 a, float s, float4 g) {
+  return make_float4(a.x * s * g.x, a.y * s * g.y, a.z * s * g.z, a.w * s * g.w);
+}
+
+// Rows of `hidden` <= kMaxHidden elements: each thread owns float4 chunk
+// c of (threadIdx + c * kThreads) for c < kChunks. The loops over chunks and
+// splits have compile-time bounds, so every load is issued before the first
+// reduction instead of one memory round trip per loop iteration.
+constexpr int kChunks = 8, kMaxHidden = kThreads * 4 * kChunks;
+
+// One workgroup per (slot i, sequence b); every workgroup of a sequence
+// reduces the boundary-fusion partials itself (from L2).
+template <typename T, int SPLITS>
+__global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
+  __shared__ float red[kThreads / 64];
+  const int H = a.hidden;
+  const int i = blockIdx.x, b = blockIdx.y;
+  const long m = (long)b * a.B + i;
   int anchor = a.anchor[b];
   if (anchor < 0 || anchor >= a.vocab) {  // never read outside the embedding table
     if (threadIdx.x == 0 && i == 0) atomicOr(a.status, kFlagAnchor);
@@ -72,19 +92,40 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
   const T* e = i == 0 ? static_cast<const T*>(a.embed) + (long)anchor * H
                       : static_cast<const T*>(a.mask_emb);
   const T* p = static_cast<const T*>(a.pos_emb) + (long)i * H;
-  const T* gfc = static_cast<const T*>(a.fc_norm);
+  float4 c[kChunks], ep[kChunks], gfc[kChunks], gin[kChunks];
+  float ss = 0.f;
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kThreads) * 4;
+    if (k < H) {
+      float4 v = *reinterpret_cast<const float4*>(a.part + (long)b * H + k);
+#pragma unroll
+      for (int s = 1; s < SPLITS; ++s)
+        v = f4add(v, *reinterpret_cast<const float4*>(a.part + s * a.split_stride + (long)b * H + k));
+      c[ch] = v;
+      ep[ch] = f4add(Vec4<T>::load(e + k), Vec4<T>::load(p + k));
+      gfc[ch] = Vec4<T>::load(static_cast<const T*>(a.fc_norm) + k);
+      gin[ch] = Vec4<T>::load(static_cast<const T*>(a.in_norm0) + k);
+      ss += f4dot(v);
+    }
+  }
+  const float inv_c = rsqrtf(block_sum(ss, red) / H + a.eps);
   float sx = 0.f;
-  for (int k = threadIdx.x; k < H; k += kThreads) {
-    const float v = Elem<T>::load(e + k) + Elem<T>::load(p + k) +
-                    c[k] * inv_c * Elem<T>::load(gfc + k);
-    c[k] = v;                      // each thread rewrites only the entries it read
-    a.x[m * H + k] = v;
-    sx += v * v;
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kThreads) * 4;
+    if (k < H) {
+      c[ch] = f4add(ep[ch], f4scale(c[ch], inv_c, gfc[ch]));
+      *reinterpret_cast<float4*>(a.x + m * H + k) = c[ch];
+      sx += f4dot(c[ch]);
+    }
   }
   const float inv = rsqrtf(block_sum(sx, red) / H + a.eps);
-  const T* gin = static_cast<const T*>(a.in_norm0);
-  for (int k = threadIdx.x; k < H; k += kThreads)
-    Elem<T>::store(static_cast<T*>(a.nrm) + m * H + k, c[k] * inv * Elem<T>::load(gin + k));
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kThreads) * 4;
+    if (k < H) Vec4<T>::store(static_cast<T*>(a.nrm) + m * H + k, f4scale(c[ch], inv, gin[ch]));
+  }
   // rotary table row of this slot, absolute position t + i
   const int half = a.d / 2;
   const long t = a.pos[b];
@@ -101,32 +142,89 @@ struct ResidArgs {
   float* x; void* nrm; const void* gain; int hidden; float eps;
 };
 
-template <typename T>
+template <typename T, int SPLITS>
 __global__ void __launch_bounds__(kThreads) resid_norm_kernel(ResidArgs a) {
   __shared__ float red[kThreads / 64];
   const long m = blockIdx.x;
   const int H = a.hidden;
   float* x = a.x + m * H;
   const float* part = a.part + m * H;
+  float4 v[kChunks], g[kChunks];
   float ss = 0.f;
-  for (int k = threadIdx.x * 4; k < H; k += kThreads * 4) {
-    float4 v = *reinterpret_cast<const float4*>(x + k);
-    for (int s = 0; s < a.splits; ++s) {
-      const float4 u = *reinterpret_cast<const float4*>(part + s * a.split_stride + k);
-      v.x += u.x; v.y += u.y; v.z += u.z; v.w += u.w;
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kThreads) * 4;
+    if (k < H) {
+      float4 u = *reinterpret_cast<const float4*>(x + k);
+#pragma unroll
+      for (int s = 0; s < SPLITS; ++s)
+        u = f4add(u, *reinterpret_cast<const float4*>(part + s * a.split_stride + k));
+      v[ch] = u;
+      g[ch] = Vec4<T>::load(static_cast<const T*>(a.gain) + k);
+      ss += f4dot(u);
     }
-    *reinterpret_cast<float4*>(x + k) = v;
-    ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   const float inv = rsqrtf(block_sum(ss, red) / H + a.eps);
-  const T* gain = static_cast<const T*>(a.gain);
   T* out = static_cast<T*>(a.nrm) + m * H;
-  for (int k = threadIdx.x * 4; k < H; k += kThreads * 4) {
-    const float4 v = *reinterpret_cast<const float4*>(x + k);
-    Elem<T>::store(out + k + 0, v.x * inv * Elem<T>::load(gain + k + 0));
-    Elem<T>::store(out + k + 1, v.y * inv * Elem<T>::load(gain + k + 1));
-    Elem<T>::store(out + k + 2, v.z * inv * Elem<T>::load(gain + k + 2));
-    Elem<T>::store(out + k + 3, v.w * inv * Elem<T>::load(gain + k + 3));
+#pragma unroll
+  for (int ch = 0; ch < kChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kThreads) * 4;
+    if (k < H) {
+      *reinterpret_cast<float4*>(x + k) = v[ch];
+      Vec4<T>::store(out + k, f4scale(v[ch], inv, g[ch]));
+    }
+  }
+}
+
+struct QkvArgs {
+  const float* part; long split_stride;   // QKV split-K partials [splits][M][qkv_out]
+  void* out;                              // [M][qkv_out] of the configuration dtype
+  const void* q_norm; const void* k_norm; // per-head RMSNorm gains [d]
+  const float* rope;                      // cos / sin [M][d/2] each
+  int M, nh, hq, hkv, d, qkv_out;
+  float eps;
+};
+
+// Block q, k and v rows (Eq. 6 inputs): sum of the split-K partials, then for
+// q and k heads the per-head RMSNorm and the rotate-half RoPE at position
+// t + i (table of slot_init). One wave per (row m, head slot hs), where slots
+// [0, hq) are query heads, [hq, hq + hkv) key heads and the rest value heads;
+// lane e < d/2 owns the rotary pair (e, e + d/2).
+template <typename T, int SPLITS>
+__global__ void __launch_bounds__(kThreads) qkv_finish_kernel(QkvArgs a) {
+  const long wid = (long)blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (wid >= (long)a.M * a.nh) return;  // whole waves only
+  const int lane = threadIdx.x & 63, half = a.d / 2;
+  const long m = wid / a.nh;
+  const int hs = (int)(wid % a.nh);
+  const float* src = a.part + m * a.qkv_out + (long)hs * a.d;
+  float x1 = 0.f, x2 = 0.f;
+  if (lane < half) {
+    float p1[SPLITS], p2[SPLITS];
+#pragma unroll
+    for (int s = 0; s < SPLITS; ++s) {
+      p1[s] = src[s * a.split_stride + lane];
+      p2[s] = src[s * a.split_stride + lane + half];
+    }
+#pragma unroll
+    for (int s = 0; s < SPLITS; ++s) { x1 += p1[s]; x2 += p2[s]; }
+  }
+  if (hs < a.hq + a.hkv) {
+    const float inv = rsqrtf(wave_sum(x1 * x1 + x2 * x2) / a.d + a.eps);
+    if (lane < half) {
+      const T* gain = static_cast<const T*>(hs < a.hq ? a.q_norm : a.k_norm);
+      const float z1 = x1 * inv * Elem<T>::load(gain + lane);
+      const float z2 = x2 * inv * Elem<T>::load(gain + lane + half);
+      const float cs = a.rope[m * half + lane];
+      const float sn = a.rope[(long)a.M * half + m * half + lane];
+      x1 = z1 * cs - z2 * sn;
+      x2 = z1 * sn + z2 * cs;
+    }
+  }
+  if (lane < half) {
+    T* dst = static_cast<T*>(a.out) + m * a.qkv_out + (long)hs * a.d;
+    Elem<T>::store(dst + lane, x1);
+    Elem<T>::store(dst + lane + half, x2);
   }
 }
 
@@ -136,7 +234,7 @@ template <typename T>
 __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   extern __shared__ float smem[];
   const int h = blockIdx.x, b = blockIdx.y, g = h / a.rep;
-  const int d = a.d, B = a.B, half = d / 2;
+  const int d = a.d, B = a.B;
   const long t = a.pos[b];
   const int nv = (int)(t < a.W ? t : a.W);
   const int nsum = t > 0 ? a.R : 0;
@@ -147,36 +245,17 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   float* S = vs + B * d;            // [B][B + W + R]
   const int ldS = B + a.W + a.R;
 
-  // q (head h), k and v (group g) of the block, summed over the split-K partials
+  // q (head h), k and v (group g) of the block
+  const T* qkv = static_cast<const T*>(a.qkv);
   for (int idx = threadIdx.x; idx < 3 * B * d; idx += kThreads) {
     const int which = idx / (B * d), i = (idx / d) % B, e = idx % d;
     const int col = which == 0 ? h * d + e
                   : which == 1 ? (a.hq + g) * d + e : (a.hq + a.hkv + g) * d + e;
-    const long m = (long)b * B + i;
-    float v = 0.f;
-    for (int s = 0; s < a.splits; ++s) v += a.part[s * a.split_stride + m * a.qkv_out + col];
-    (which == 0 ? qs : which == 1 ? ks : vs)[i * d + e] = v;
+    (which == 0 ? qs : which == 1 ? ks : vs)[i * d + e] =
+        Elem<T>::load(qkv + ((long)b * B + i) * a.qkv_out + col);
   }
   __syncthreads();
-  // per-head RMSNorm and rotate-half RoPE on q and k: one wave per row
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int r = wave; r < 2 * B; r += kThreads / 64) {
-    float* row = r < B ? qs + r * d : ks + (r - B) * d;
-    const T* gain = static_cast<const T*>(r < B ? a.q_norm : a.k_norm);
-    const int i = r < B ? r : r - B;
-    float ss = 0.f;
-    for (int e = lane; e < d; e += 64) ss += row[e] * row[e];
-    const float inv = rsqrtf(wave_sum(ss) / d + a.eps);
-    const long m = (long)b * B + i;
-    for (int e = lane; e < half; e += 64) {
-      const float x1 = row[e] * inv * Elem<T>::load(gain + e);
-      const float x2 = row[e + half] * inv * Elem<T>::load(gain + e + half);
-      const float cs = a.rope[m * half + e], sn = a.rope[(long)a.M * half + m * half + e];
-      row[e] = x1 * cs - x2 * sn;
-      row[e + half] = x1 * sn + x2 * cs;
-    }
-  }
-  __syncthreads();
   const uint8_t* seq = a.arena + (size_t)b * a.stride;
   const T* Kw = reinterpret_cast<const T*>(seq + a.kw) + ((size_t)(a.layer * a.hkv + g) * a.W) * d;
   const T* Vw = reinterpret_cast<const T*>(seq + a.vw) + ((size_t)(a.layer * a.hkv + g) * a.W) * d;
@@ -224,7 +303,40 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   }
 }
 
+struct SlotLaunch {
+  template <typename T, int S>
+  static void go(dim3 grid, const SlotArgs& a, hipStream_t st) {
+    hipLaunchKernelGGL((slot_init_kernel<T, S>), grid, dim3(kThreads), 0, st, a);
+  }
+};
+struct QkvLaunch {
+  template <typename T, int S>
+  static void go(dim3 grid, const QkvArgs& a, hipStream_t st) {
+    hipLaunchKernelGGL((qkv_finish_kernel<T, S>), grid, dim3(kThreads), 0, st, a);
+  }
+};
+struct ResidLaunch {
+  template <typename T, int S>
+  static void go(dim3 grid, const ResidArgs& a, hipStream_t st) {
+    hipLaunchKernelGGL((resid_norm_kernel<T, S>), grid, dim3(kThreads), 0, st, a);
+  }
+};
+// Dispatch on the split-K factor (1, 2, 4 or 8).
+template <typename T, typename L, typename Args>
+hipError_t launch_split(int splits, dim3 grid, const Args& a, hipStream_t st) {
+  switch (splits) {
+    case 1: L::template go<T, 1>(grid, a, st); break;
+    case 2: L::template go<T, 2>(grid, a, st); break;
+    case 4: L::template go<T, 4>(grid, a, st); break;
+    case 8: L::template go<T, 8>(grid, a, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool norm_hidden_supported(int hidden) { return hidden % 4 == 0 && hidden <= kMaxHidden; }
 
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st) {
@@ -235,12 +347,8 @@ hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int f
   a.x = p.x; a.nrm = p.nrm; a.rope = p.rope; a.status = p.status;
   a.hidden = s.hidden; a.B = s.B; a.d = s.d; a.M = batch * s.B; a.vocab = s.vocab;
   a.eps = s.eps; a.base = s.rope_base;
-  const size_t shm = (s.hidden + 4) * sizeof(float);
-  if (s.dtype == LDR_BF16)
-    hipLaunchKernelGGL(slot_init_kernel<uint16_t>, dim3(s.B, batch), dim3(kThreads), shm, st, a);
-  else
-    hipLaunchKernelGGL(slot_init_kernel<float>, dim3(s.B, batch), dim3(kThreads), shm, st, a);
-  return hipGetLastError();
+  return s.dtype == LDR_BF16 ? launch_split<uint16_t, SlotLaunch>(fc_splits, dim3(s.B, batch), a, st)
+                            : launch_split<float, SlotLaunch>(fc_splits, dim3(s.B, batch), a, st);
 }
 
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
@@ -248,24 +356,32 @@ hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int spli
   ResidArgs a;
   a.part = p.part; a.split_stride = (long)M * s.hidden; a.splits = splits;
   a.x = p.x; a.nrm = p.nrm; a.gain = gain; a.hidden = s.hidden; a.eps = s.eps;
-  if (s.dtype == LDR_BF16)
-    hipLaunchKernelGGL(resid_norm_kernel<uint16_t>, dim3(M), dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL(resid_norm_kernel<float>, dim3(M), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+  return s.dtype == LDR_BF16 ? launch_split<uint16_t, ResidLaunch>(splits, dim3(M), a, st)
+                            : launch_split<float, ResidLaunch>(splits, dim3(M), a, st);
+}
+
+hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
+                             const ldr_layer_weights* lw, hipStream_t st) {
+  QkvArgs a;
+  a.part = p.part; a.split_stride = (long)M * s.qkv_out; a.out = p.qkv;
+  a.q_norm = lw->q_norm; a.k_norm = lw->k_norm; a.rope = p.rope;
+  a.M = M; a.nh = s.hq + 2 * s.hkv; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d;
+  a.qkv_out = s.qkv_out; a.eps = s.eps;
+  const int waves = kThreads / 64;
+  const dim3 grid((unsigned)(((long)M * a.nh + waves - 1) / waves));
+  return s.dtype == LDR_BF16 ? launch_split<uint16_t, QkvLaunch>(splits, grid, a, st)
+                            : launch_split<float, QkvLaunch>(splits, grid, a, st);
 }
 
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
-                            int qkv_splits, int layer, const ldr_layer_weights* lw,
-                            hipStream_t st) {
+                            int layer, hipStream_t st) {
   AttnArgs a;
-  const int M = batch * s.B;
-  a.part = p.part; a.split_stride = (long)M * s.qkv_out; a.splits = qkv_splits;
+  a.qkv = p.qkv;
   a.arena = p.arena; a.stride = L.stride; a.kw = L.kw; a.vw = L.vw; a.m_off = L.m;
-  a.pos = p.pos; a.G = p.G; a.rope = p.rope; a.q_norm = lw->q_norm; a.k_norm = lw->k_norm;
+  a.pos = p.pos; a.G = p.G;
   a.o = p.o; a.layer = layer; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.B = s.B; a.W = s.W;
-  a.R = s.R; a.rep = s.rep; a.qkv_out = s.qkv_out; a.M = M;
-  a.eps = s.eps; a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
+  a.R = s.R; a.rep = s.rep; a.qkv_out = s.qkv_out;
+  a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const size_t shm = (size_t)(3 * s.B * s.d + s.B * (s.B + s.W + s.R)) * sizeof(float);
   if (s.dtype == LDR_BF16) return launch_attention_mfma(a, s.hkv, batch, st);
   const dim3 grid(s.hq, batch);

@@ -250,8 +250,8 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
 }  // namespace
 
 // bf16: the smallest BM of {16, 32, 64, 256} that covers M (several M tiles
-// past 256). Split-K only where allowed, to about one workgroup per CU,
-// keeping an even number of at least 4 K steps per split.
+// past 256). Split-K (1, 2, 4 or 8) only where allowed, to about one workgroup
+// per CU, keeping an even number of at least 4 K steps per split.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split) {
   GemmPlan p;
   constexpr int kCUs = 256;
@@ -270,7 +270,8 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split) {
   int s = 1;
   if (allow_split) {
     const int tiles = p.grid_x * p.grid_y;
-    while (tiles * s * 2 <= kCUs && K % (2 * s * kstep) == 0 && K / (2 * s) >= 2 * kstep) s *= 2;
+    while (s < 8 && tiles * s * 2 <= kCUs && K % (2 * s * kstep) == 0 && K / (2 * s) >= 2 * kstep)
+      s *= 2;
   }
   p.splits = s;
   return p;

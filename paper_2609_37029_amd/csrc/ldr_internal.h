@@ -104,6 +104,7 @@ struct DraftPtrs {
   float* part;     // split-K partials
   float* x;        // residual stream fp32 [M][hidden]
   void* nrm;       // normalised activations (dtype) [M][hidden]
+  void* qkv;       // block q, k, v after RMSNorm and RoPE (dtype) [M][qkv_out]
   void* o;         // attention output (dtype) [M][hq d]
   void* act;       // SwiGLU output (dtype) [M][mlp]
   float* rope;     // cos/sin [batch][B][d/2] x 2
@@ -115,13 +116,12 @@ constexpr int kFlagRange = 1;   // an update saw a row count outside [0, max_new
 constexpr int kFlagAnchor = 2;  // a draft step saw an anchor outside [0, V)
 // Attention over [block; window; summary] of one layer (Eq. 6).
 struct AttnArgs {
-  const float* part; long split_stride; int splits;   // QKV split-K partials [M][qkv_out]
+  const void* qkv;   // block q, k, v rows (dtype) [M][qkv_out], normalised and rotated
   const uint8_t* arena; size_t stride; size_t kw, vw, m_off;
-  const int64_t* pos; const void* G; const float* rope;
-  const void* q_norm; const void* k_norm;
+  const int64_t* pos; const void* G;
   void* o;
-  int layer, hq, hkv, d, B, W, R, rep, qkv_out, M;
-  float eps, inv_sqrt_d;
+  int layer, hq, hkv, d, B, W, R, rep, qkv_out;
+  float inv_sqrt_d;
 };
 // bf16 MFMA kernel (attn.hip): one workgroup per (kv group, sequence).
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st);
@@ -129,11 +129,13 @@ bool attention_mfma_supported(int d, int rep, int B, int R);
 
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st);
+bool norm_hidden_supported(int hidden);
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const void* gain, hipStream_t st);
+hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
+                             const ldr_layer_weights* lw, hipStream_t st);
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
-                            int qkv_splits, int layer, const ldr_layer_weights* lw,
-                            hipStream_t st);
+                            int layer, hipStream_t st);
 
 // Sampler (sample.hip)
 int sample_splits(int rows, int vocab);

@@ -1,7 +1,7 @@
 // Fixed-size context views on the GPU (Sec. 2.2; App. A.2, Eq. 10-11).
 //
 // One workgroup per (kv group g, layer j, sequence b) ingests the new rows of
-// that sequence for that head group:
+// that sequence for that head group, reading each new row once:
 //  * ring write of the last min(n, W) rows into window slots (t + r) mod W;
 //  * for the rep * R summary queries of the group's query heads, the
 //    statistics of the new set N (Eq. 10) by a tiled online log-sum-exp over
@@ -58,21 +58,36 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
   const int d = a.d;
   uint8_t* seq = a.arena + (size_t)b * a.stride;
 
-  // ---- window ring write (the last min(n, W) rows) -----------------------
+  // Summary query q of the group is (head g*rep + q / R, summary row q % R);
+  // the group's queries are contiguous in G, M and eta. TPQ = d / DPT threads
+  // share a query; thread `part` owns dims (c * TPQ + part) * 4 + e.
+  constexpr int NV = DPT / 4;         // float4 chunks per thread
+  const int tpq = d / DPT;
+  const int q = threadIdx.x / tpq;
+  const int part = threadIdx.x % tpq;
+  const size_t qrow = ((size_t)j * a.hq + g * a.rep) * a.R + q;
+  float* Mq = reinterpret_cast<float*>(seq + a.m) + qrow * d;
+  float* etaq = reinterpret_cast<float*>(seq + a.eta) + qrow;
+
+  // The stored (eta, m) and the query are loaded first: the stores below go
+  // to the same arena, so these loads could not be moved ahead of them.
+  const float eta_a = *etaq;
+  float4 ma[NV];
+  float gq[DPT], acc[DPT];
   {
-    T* Kw = reinterpret_cast<T*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * d;
-    T* Vw = reinterpret_cast<T*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * d;
-    const int r0 = n > a.W ? n - a.W : 0;
-    const int cpr = d * (int)sizeof(T) / 16;  // 16-byte chunks per row
-    const int total = (n - r0) * cpr;
-    for (int i = threadIdx.x; i < total; i += kThreads) {
-      const int r = r0 + i / cpr, c = i % cpr;
-      const size_t src = ((((size_t)b * a.max_new + r) * a.D + j) * a.hkv + g) * d;
-      const int slot = (int)((t + r) % a.W);
-      copy16(Kw + (size_t)slot * d, reinterpret_cast<const T*>(a.K_new) + src, c);
-      copy16(Vw + (size_t)slot * d, reinterpret_cast<const T*>(a.V_new) + src, c);
+    const T* Gp = reinterpret_cast<const T*>(a.G) + qrow * d;
+#pragma unroll
+    for (int c = 0; c < NV; ++c) {
+      const int dim = (c * tpq + part) * 4;
+      ma[c] = *reinterpret_cast<const float4*>(Mq + dim);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        gq[c * 4 + e] = Elem<T>::load(Gp + dim + e) * a.inv_sqrt_d;
+        acc[c * 4 + e] = 0.f;
+      }
     }
   }
+
   // ---- boundary states: this workgroup's slice ----------------------------
   {
     const int chunks = a.hb_elems * (int)sizeof(T) / 16;
@@ -84,39 +99,35 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
     for (int c = c0 + threadIdx.x; c < c1; c += kThreads) copy16(hdst, hsrc, c);
   }
 
-  // ---- summary statistics of N and the merge -----------------------------
+  // ---- rows of the new set N, tile by tile: window ring write of the last
+  // min(n, W) rows (slot (t + r) mod W) and the tiled online log-sum-exp ----
   __shared__ float Ks[kTileRows][256 + 4];
   __shared__ float Vs[kTileRows][256 + 4];
-  constexpr int NV = DPT / 4;         // float4 chunks per thread
-  const int tpq = d / DPT;
-  const int q = threadIdx.x / tpq;    // summary query of the group: hh * R + r
-  const int part = threadIdx.x % tpq;
-  const int hq0 = g * a.rep;          // first query head of the group
-  // query q of the group is (head hq0 + q / R, summary row q % R); the group's
-  // queries are contiguous in G, M and eta.
-  const size_t qrow = ((size_t)j * a.hq + hq0) * a.R + q;
-
-  float gq[DPT], acc[DPT];
-  {
-    const T* Gp = reinterpret_cast<const T*>(a.G) + qrow * d;
-#pragma unroll
-    for (int c = 0; c < NV; ++c)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int dim = (c * tpq + part) * 4 + e;
-        gq[c * 4 + e] = Elem<T>::load(Gp + dim) * a.inv_sqrt_d;
-        acc[c * 4 + e] = 0.f;
-      }
-  }
+  constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
+  T* Kw = reinterpret_cast<T*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * d;
+  T* Vw = reinterpret_cast<T*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * d;
   float mx = -INFINITY, l = 0.f;
   for (int r0 = 0; r0 < n; r0 += kTileRows) {
     const int nr = min(kTileRows, n - r0);
     __syncthreads();
-    for (int i = threadIdx.x; i < nr * d; i += kThreads) {
-      const int r = i / d, e = i % d;
-      const size_t src = ((((size_t)b * a.max_new + r0 + r) * a.D + j) * a.hkv + g) * d + e;
-      Ks[r][e] = Elem<T>::load(reinterpret_cast<const T*>(a.K_new) + src);
-      Vs[r][e] = Elem<T>::load(reinterpret_cast<const T*>(a.V_new) + src);
+    const int cpr = d / EPC;
+    for (int i = threadIdx.x; i < nr * cpr; i += kThreads) {
+      const int r = i / cpr, e0 = (i % cpr) * EPC;
+      const size_t src = ((((size_t)b * a.max_new + r0 + r) * a.D + j) * a.hkv + g) * d + e0;
+      const uint4 kv = *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.K_new) + src);
+      const uint4 vv = *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.V_new) + src);
+      if (r0 + r >= n - a.W) {  // only the last W rows can survive in the ring
+        const size_t slot = (size_t)((t + r0 + r) % a.W);
+        *reinterpret_cast<uint4*>(Kw + slot * d + e0) = kv;
+        *reinterpret_cast<uint4*>(Vw + slot * d + e0) = vv;
+      }
+      const T* kp = reinterpret_cast<const T*>(&kv);
+      const T* vp = reinterpret_cast<const T*>(&vv);
+#pragma unroll
+      for (int e = 0; e < EPC; ++e) {
+        Ks[r][e0 + e] = Elem<T>::load(kp + e);
+        Vs[r][e0 + e] = Elem<T>::load(vp + e);
+      }
     }
     __syncthreads();
     float s[kTileRows];
@@ -158,12 +169,9 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
     }
     mx = nm;
   }
-  // eta_N = log sum exp(s), m_N = sum exp(s - eta_N) v
+  // eta_N = log sum exp(s), m_N = sum exp(s - eta_N) v, merged with (eta_A, m_A)
   const float eta_n = mx + logf(l);
   const float inv_l = 1.f / l;
-  float* Mq = reinterpret_cast<float*>(seq + a.m) + qrow * d;
-  float* etaq = reinterpret_cast<float*>(seq + a.eta) + qrow;
-  const float eta_a = *etaq;
   float wa, wn, eta;
   if (eta_a == -INFINITY) {  // empty A: the merge returns N
     wa = 0.f; wn = inv_l; eta = eta_n;
@@ -174,14 +182,16 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
     wn = expf(eta_n - eta) * inv_l;
   }
 #pragma unroll
-  for (int c = 0; c < NV; ++c)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int dim = (c * tpq + part) * 4 + e;
-      const float ma = wa != 0.f ? Mq[dim] : 0.f;
-      Mq[dim] = wa * ma + wn * acc[c * 4 + e];
-    }
-  __syncthreads();  // every thread of the query read eta_a before it changes
+  for (int c = 0; c < NV; ++c) {
+    const int dim = (c * tpq + part) * 4;
+    const float4 m_a = wa != 0.f ? ma[c] : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 r;
+    r.x = wa * m_a.x + wn * acc[c * 4 + 0];
+    r.y = wa * m_a.y + wn * acc[c * 4 + 1];
+    r.z = wa * m_a.z + wn * acc[c * 4 + 2];
+    r.w = wa * m_a.w + wn * acc[c * 4 + 3];
+    *reinterpret_cast<float4*>(Mq + dim) = r;
+  }
   if (part == 0) *etaq = eta;
 }
 

@@ -238,7 +238,7 @@ def draft_step(views: Views, weights: DraftWeights, anchor: torch.Tensor,
 
 
 LAUNCH_KINDS = ("fc_gemm", "slot_init", "qkv_gemm", "attention", "o_gemm", "post_norm",
-                "gate_up_gemm", "down_gemm", "next_norm", "lm_head")
+                "gate_up_gemm", "down_gemm", "next_norm", "lm_head", "qkv_finish")
 
 
 def draft_launches(shape):
