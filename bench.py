@@ -10,6 +10,8 @@ step, with every input resident in HBM before timing starts.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
     python bench.py --sweep [--sweep-out PATH]   # latency vs prefix length and batch
+    python bench.py --counters                   # short run for rocprofv3 --pmc passes
+    python bench.py --traffic FETCH.csv WRITE.csv  # counters -> profiles/traffic.json
 
 Prints one JSON line. Inputs are seeded synthetic tensors with the shapes of
 the workload (random-init weights, N(0, 1) target K/V rows and hidden states).
@@ -31,6 +33,8 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 DEFAULT_WORKLOAD = "qwen3-8b-b16-t32768"
 METRIC = "drafted tokens/sec and µs/draft step vs prefix length (Qwen3-8B shape, batch 16)"
+TRAFFIC_JSON = os.path.join(ROOT, "profiles", "traffic.json")
+COPY_BYTES = 1 << 30         # calibration kernel of the counter runs: reads and writes 1 GiB
 
 
 def parse():
@@ -40,12 +44,16 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-seqs", type=int, default=2,
+    ap.add_argument("--cpu-seqs", type=int, default=16,
                     help="sequences in the CPU-oracle sample")
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-out", default=os.path.join(ROOT, "gpurun_out", "sweep.json"))
     ap.add_argument("--sweep-prefix", default="1024,4096,16384,65536,131072,262144")
     ap.add_argument("--sweep-batch", default="1,16,64")
+    ap.add_argument("--counters", action="store_true",
+                    help="calibration copy + a few steps, to run under rocprofv3 --pmc")
+    ap.add_argument("--traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two counter_collection.csv files into profiles/traffic.json")
     return ap.parse_args()
 
 
@@ -257,10 +265,135 @@ def cpu_baseline(torch, synth, rig, n_seqs):
                       f"{el:.2f} s (BLAS threads {cores}; elementwise numpy single-threaded)"}
 
 
+# ---- HBM traffic from rocprofv3 counters -----------------------------------------------------
+
+def source_digest():
+    """sha256 over the library sources: counters taken on other sources are stale."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_37029_amd", "csrc")
+    files = sorted(os.path.join(csrc, f) for f in os.listdir(csrc)
+                   if f.endswith((".hip", ".cpp", ".h")))
+    for f in files + [os.path.join(ROOT, "include", "ldr.h")]:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def kernel_symbol(name):
+    """Kernel name as rocprofv3 prints it, without namespaces and arguments."""
+    name = name.replace("void ", "").replace("(anonymous namespace)::", "").replace("ldr::", "")
+    return name.split("(")[0]
+
+
+def counters_run(args, torch, ldr, synth):
+    """What the --pmc passes profile: a calibration kernel of known size
+    (elementwise negation of 1 GiB of fp32: reads 1 GiB, writes 1 GiB), then
+    warm-up and timed steps of the workload."""
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    del src, dst
+    wl = synth.WORKLOADS[args.workload]
+    rig = Rig(torch, ldr, synth, wl.shape, wl.batch, wl.prefix)
+    for i in range(4):
+        rig.step(i)
+    torch.cuda.synchronize()
+    print(json.dumps({"counters_run": wl.name, "steps": 4, "kinds": rig.kinds,
+                      "sources_sha256": source_digest()}), flush=True)
+
+
+def traffic_from_csv(fetch_csv, write_csv, workload):
+    """Per-launch FETCH_SIZE / WRITE_SIZE (KiB) of every launch kind of the draft
+    step, the views update and the sampler, each scaled by what the counter
+    reads for the calibration kernel (COPY_BYTES in, COPY_BYTES out)."""
+    import csv
+    sys.path.insert(0, ROOT)
+    import synth
+    from paper_2609_37029_amd import ldr
+    kinds = ldr.draft_launches(synth.WORKLOADS[workload].shape)
+
+    def load(path, counter):
+        disp = {}
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"] != counter:
+                continue
+            d = disp.setdefault(int(r["Dispatch_Id"]), [r["Kernel_Name"], 0.0])
+            d[1] += float(r["Counter_Value"])
+        return [(k, *disp[k]) for k in sorted(disp)]
+
+    out = {}
+    for counter, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        rows = load(path, counter)
+        first_ldr = next(i for i, r in enumerate(rows) if "ldr::" in r[1])
+        calib = [v for _, name, v in rows[:first_ldr] if "neg" in name]
+        if not calib:
+            raise RuntimeError(f"no calibration kernel in {path}")
+        kib = statistics.median(calib)
+        factor = COPY_BYTES / 1024 / kib
+        per = {}
+        for i, (_, name, _) in enumerate(rows):
+            if "views_commit_kernel" not in name or i + len(kinds) + 2 >= len(rows):
+                continue
+            seq = rows[i + 1:i + 1 + len(kinds)]
+            if "gemm" not in seq[0][1]:
+                continue          # an update of the prefill, not of a step
+            per.setdefault("views_update", []).append(rows[i - 1][2] + rows[i][2])
+            out.setdefault("symbols", {})["views_update"] = " + ".join(
+                kernel_symbol(r[1]) for r in rows[i - 1:i + 1])
+            for k, (_, kname, v) in zip(kinds, seq):
+                e = per.setdefault(k, [])
+                e.append(v)
+                out.setdefault("symbols", {})[k] = kernel_symbol(kname)
+            tail = rows[i + 1 + len(kinds):i + 3 + len(kinds)]
+            per.setdefault("sample", []).append(sum(v for _, _, v in tail))
+            out.setdefault("symbols", {})["sample"] = " + ".join(kernel_symbol(r[1]) for r in tail)
+        out.setdefault("calibration", {})[counter] = {"kib_read_by_counter": kib,
+                                                     "factor": factor}
+        for k, vs in per.items():
+            e = out.setdefault("kinds", {}).setdefault(k, {})
+            e[counter + "_kib_per_launch"] = statistics.mean(vs)
+            e["launches"] = len(vs)
+            e[counter.split("_")[0].lower() + "_bytes_per_launch"] = \
+                statistics.mean(vs) * 1024 * factor
+    for e in out["kinds"].values():
+        e["hbm_bytes_per_launch"] = e.get("fetch_bytes_per_launch", 0) + \
+            e.get("write_bytes_per_launch", 0)
+    out["workload"] = workload
+    out["sources_sha256"] = source_digest()
+    return out
+
+
+def traffic_for(kind):
+    """HBM bytes per launch of `kind` from profiles/traffic.json, or None when
+    absent or taken on other library sources."""
+    try:
+        with open(TRAFFIC_JSON) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_sha256") != source_digest():
+        return None
+    e = t.get("kinds", {}).get(kind)
+    return e.get("hbm_bytes_per_launch") if e else None
+
+
 # ---- main --------------------------------------------------------------------------------
 
 def main():
     args = parse()
+    if args.traffic:
+        t = traffic_from_csv(args.traffic[0], args.traffic[1], args.workload)
+        os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
+        with open(TRAFFIC_JSON, "w") as f:
+            json.dump(t, f, indent=1)
+        print(json.dumps({k: round(v["hbm_bytes_per_launch"] / 1e6, 2)
+                          for k, v in t["kinds"].items()}))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": f"--gpus {args.gpus}: this benchmark runs on one GPU only; "
                                    "the drafting step shards by sequence with no exchange, so "
@@ -276,6 +409,8 @@ def main():
     torch.cuda.set_device(0)
     if args.sweep:
         return sweep(args, torch, ldr, synth)
+    if args.counters:
+        return counters_run(args, torch, ldr, synth)
 
     wl = synth.WORKLOADS[args.workload]
     s, batch = wl.shape, wl.batch
@@ -311,7 +446,7 @@ def main():
         "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,
                         "p90": percentile(per_step, .9) * 1e3},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(dom),
                      "bytes_per_launch": dom_bytes, "us_per_launch": dom_ms * 1e3,
                      "launches_per_step": launches_of_dom},
         "step_roofline": {"algorithmic_bytes": step_bytes, "flops": step_flops,
