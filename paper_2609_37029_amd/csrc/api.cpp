@@ -69,7 +69,7 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   w.fc = plan_gemm(s.dtype, batch, s.hidden, s.Lb * s.hidden, true);
   w.qkv = plan_gemm(s.dtype, M, s.qkv_out, s.hidden, true);
   w.wo = plan_gemm(s.dtype, M, s.hidden, s.hq * s.d, true);
-  w.gu = plan_gemm(s.dtype, M, 2 * s.mlp, s.hidden, false);   // SwiGLU epilogue: no split
+  w.gu = plan_gemm(s.dtype, M, 2 * s.mlp, s.hidden, false, true);   // SwiGLU epilogue: no split
   w.down = plan_gemm(s.dtype, M, s.hidden, s.mlp, true);
   w.lm = plan_gemm(s.dtype, M, s.vocab, s.hidden, false);     // writes the logits directly
   size_t part = (size_t)w.fc.splits * batch * s.hidden;

@@ -235,13 +235,16 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 }
 
 // Tile configurations (cfg): 0: BM 16 (M <= 16), 1: BM 32, 2: BM 64, all
-// with 8 waves along N (BN 256); 3: BM 256 with 4 x 2 waves of 64 x 64 (BN 128).
+// with 8 waves along N (BN 256); 3: BM 256 with 4 x 2 waves of 64 x 64 (BN 128);
+// 4: BM 256 with 8 x 1 waves of 32 x 96 (BN 96), for the SwiGLU GEMM, whose
+// 2 x 12288 columns at the Qwen3-8B shape make exactly 256 tiles (one per CU).
 template <int EPI>
 hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
   switch (cfg) {
     case 0: hipLaunchKernelGGL((gemm_kernel<1, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 1: hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 2: hipLaunchKernelGGL((gemm_kernel<4, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((gemm_kernel<2, 6, 8, 1, EPI>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -250,18 +253,18 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
 }  // namespace
 
 // bf16: the smallest BM of {16, 32, 64, 256} that covers M (several M tiles
-// past 256). Split-K (1, 2, 4 or 8) only where allowed, to about one workgroup
+// past 256); the SwiGLU GEMM at BM 256 uses the 96-column tile. Split-K (1, 2, 4 or 8) only where allowed, to about one workgroup
 // per CU, keeping an even number of at least 4 K steps per split.
-GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split) {
+GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu) {
   GemmPlan p;
   constexpr int kCUs = 256;
   int bm, bn, kstep;
   if (dtype == LDR_F32) {
     p.cfg = -1; bm = 32; bn = 64; kstep = 16;
   } else {
-    p.cfg = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : 3;
-    bm = p.cfg == 3 ? 256 : 16 << p.cfg;
-    bn = p.cfg == 3 ? 128 : 256;
+    p.cfg = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : swiglu ? 4 : 3;
+    bm = p.cfg >= 3 ? 256 : 16 << p.cfg;
+    bn = p.cfg == 4 ? 96 : p.cfg == 3 ? 128 : 256;
     kstep = 2 * BK;
   }
   p.ntw = 0;

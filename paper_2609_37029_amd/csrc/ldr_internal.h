@@ -95,7 +95,7 @@ struct GemmArgs {
 };
 struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile configuration
 // Tile configuration and split-K factor; splits = 1 unless allow_split.
-GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split);
+GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
 
 // Draft step pieces (draft.hip)

@@ -3,7 +3,8 @@
 // Each row of fp32 logits is split into vocabulary chunks. One workgroup per
 // (chunk, row) streams its logits once and keeps, per thread, the best
 // Gumbel-max key with its token and the running max / sum of exp(z/T) for the
-// log-normaliser; a block reduction writes one partial per chunk. A merge
+// log-normaliser; a block reduction writes one partial per chunk. Exact keys
+// are computed only for tokens that a cheap upper bound cannot rule out. A merge
 // kernel combines the chunks of a row in vocabulary order (lower token wins
 // ties) and writes the token, lse and log q(y).
 //
@@ -101,6 +102,82 @@ struct SampleArgs {
   Partial* part;
 };
 
+// Upper bound of the Gumbel noise g = -log(-log u) of 23-bit uniform index k,
+// u = (2k + 1) 2^-24, from integer arithmetic: -log u >= 1 - u = n 2^-24 with
+// n = 2^24 - 1 - 2k, so g <= 24 ln2 - ln n, and ln n >= ln2 (e + m - 1) for
+// n = m 2^e, m in [1, 2) (log2 m >= m - 1 on [1, 2]).
+__device__ inline float gumbel_upper(uint32_t bits) {
+  const uint32_t n = 0xFFFFFFu - 2u * (bits >> 9);
+  const uint32_t nb = __float_as_uint((float)n);  // exact: n < 2^24
+  const float e = (float)((int)(nb >> 23) - 127);
+  const float m = __uint_as_float((nb & 0x7FFFFFu) | 0x3F800000u);
+  return __uint_as_float(0x3F317218u) * (25.0f - e - m);  // ln2 rounded up
+}
+
+// Temperature sampling. Every lane keeps the lse partial of its tokens and the
+// best (key, token) of the candidates it evaluated. A token is a candidate
+// unless zt + bound(g) + margin < the lane's best key, which proves that its
+// exact key loses; the margin (1e-3 plus 1e-6 relative) covers the rounding of
+// the test and of the fixed-sequence log, whose error is below 1e-5 here.
+// Candidates go through a per-wave queue in LDS so that the exact key (two
+// logs) is computed 64 at a time by full waves.
+template <bool UNIT_T>
+__device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0, int v1,
+                              Partial& p) {
+  struct Cand { float zt; uint32_t bits; int v; };
+  __shared__ Cand queue[kThreads / 64][128];
+  const int lane = threadIdx.x & 63;
+  Cand* q = queue[threadIdx.x >> 6];
+  int qn = 0;  // wave-uniform queue length
+  auto drain = [&](int count) {  // evaluate entries [0, count), count <= 64
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    if (lane < count) {
+      const Cand c = q[lane];
+      const float key = __fadd_rn(c.zt, gumbel_from_bits(c.bits));
+      if (better(key, c.v, p.key, p.idx)) { p.key = key; p.idx = c.v; }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+  };
+  for (int vb = v0; vb < v1; vb += kThreads * kGroup) {
+    const int v = vb + (threadIdx.x & ~63) * kGroup + lane * kGroup;
+    uint32_t bits[kGroup];
+    noise_group(a.seed, a.step, (uint64_t)r, (uint64_t)(v / kGroup), bits);
+    float zt[kGroup];
+    float gm = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const float zv = v + i < v1 ? z[v + i] : -INFINITY;
+      zt[i] = UNIT_T ? zv : zv / a.T;  // IEEE division
+      gm = fmaxf(gm, zt[i]);
+    }
+    if (gm > p.m) { p.s *= __expf(p.m - gm); p.m = gm; }
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) {
+      const bool valid = v + i < v1;
+      if (valid) p.s += __expf(zt[i] - p.m);
+      const float margin = 1e-3f + 1e-6f * (fabsf(zt[i]) + fabsf(p.key));
+      const bool need = valid && !(zt[i] + gumbel_upper(bits[i]) + margin < p.key);
+      const uint64_t mask = __ballot(need);
+      if (need) {
+        const int pos = qn + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+        q[pos] = Cand{zt[i], bits[i], v + i};
+      }
+      qn += __popcll(mask);
+      if (qn >= 64) {
+        drain(64);
+        if (lane < qn - 64) q[lane] = q[64 + lane];
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        qn -= 64;
+      }
+    }
+  }
+  if (qn > 0) drain(qn);
+}
+
 __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) {
   const int sp = blockIdx.x, r = blockIdx.y;
   const int v0 = sp * a.chunk, v1 = min(a.vocab, v0 + a.chunk);
@@ -111,27 +188,10 @@ __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) 
       const float zv = z[v];
       if (better(zv, v, p.key, p.idx)) { p.key = zv; p.idx = v; }
     }
+  } else if (a.T == 1.f) {
+    sample_tokens<true>(a, z, r, v0, v1, p);
   } else {
-    for (int v = v0 + threadIdx.x * kGroup; v < v1; v += kThreads * kGroup) {
-      uint32_t bits[kGroup];
-      noise_group(a.seed, a.step, (uint64_t)r, (uint64_t)(v / kGroup), bits);
-      float zt[kGroup];
-      float gm = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < kGroup; ++i) {
-        zt[i] = (v + i < v1) ? z[v + i] / a.T : -INFINITY;  // IEEE division
-        gm = fmaxf(gm, zt[i]);
-      }
-      if (gm > p.m) { p.s *= __expf(p.m - gm); p.m = gm; }
-#pragma unroll
-      for (int i = 0; i < kGroup; ++i) {
-        if (v + i < v1) {
-          p.s += __expf(zt[i] - p.m);
-          const float key = __fadd_rn(zt[i], gumbel_from_bits(bits[i]));
-          if (better(key, v + i, p.key, p.idx)) { p.key = key; p.idx = v + i; }
-        }
-      }
-    }
+    sample_tokens<false>(a, z, r, v0, v1, p);
   }
   // block reduction of the partials
   for (int off = 32; off >= 1; off >>= 1) {
