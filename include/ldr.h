@@ -94,7 +94,8 @@ typedef struct ldr_weights {
 typedef struct ldr_views ldr_views; /* opaque host handle */
 
 /* Per-sequence bytes of the fixed-size views (Sec. 2.4, Fixed-cost
- * complexity): window K and V [D][Hkv][W][d] (dtype), summary values
+ * complexity): window K [D][Hkv][W][d] and window V stored transposed,
+ * [D][Hkv][d][W] (dtype; slot p mod W of position p), summary values
  * [D][Hq][R][d] and log-normalizers [D][Hq][R] (fp32), boundary states
  * [L_b][hidden] (dtype), each region 256-byte aligned. No term depends on the
  * prefix length. Returns 0 for an invalid configuration. */

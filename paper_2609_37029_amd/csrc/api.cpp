@@ -37,7 +37,7 @@ bool make_shape(const ldr_config* c, Shape* s) {
   s->el = c->dtype == LDR_BF16 ? 2 : 4;
   if (views_dims_per_thread(*s) == 0 || !norm_hidden_supported(s->hidden)) return false;
   if (s->dtype == LDR_BF16) {
-    if (!attention_mfma_supported(s->d, s->rep, s->B, s->R)) return false;
+    if (!attention_mfma_supported(s->d, s->rep, s->B, s->R, s->W)) return false;
     // GEMM K dimensions in whole pairs of 64-element steps of the bf16 main loop
     if (s->hidden % 128 || s->mlp % 128 || (s->hq * s->d) % 128) return false;
   }

@@ -6,9 +6,9 @@
 //   chunk 0      the block's own k / v (B rows, normalised and rotated by the
 //                QKV finishing kernel);
 //   chunks 1..   the recent window of layer j, staged through LDS once for all
-//                heads of the group (K rows as stored, V transposed), the
-//                next chunk fetched into registers while the current one is
-//                consumed;
+//                heads of the group (K rows and the transposed V rows as
+//                stored in the views), the next chunks fetched into
+//                registers while the current one is consumed;
 //   last         the head's R summary entries: keys G[j,h] (bf16), values
 //                M[j,h] kept in fp32 and accumulated on the VALU; both are
 //                loaded at the start and parked in LDS after the prologue.
@@ -90,7 +90,8 @@ __global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
     const int idx_ = (threadIdx.x + i * NT) % CH;                                        \
     const int slot_ = min((c) * KC + idx_ / (D / 8), nv - 1), col_ = (idx_ % (D / 8)) * 8; \
     wk[p][i] = *reinterpret_cast<const u32x4*>(Kw + (size_t)slot_ * D + col_);         \
-    wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)slot_ * D + col_);         \
+    wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)(idx_ >> 2) * a.W +         \
+                                               (c) * KC + (idx_ & 3) * 8);               \
   }
   if (nwin > 0) {
 #pragma unroll
@@ -249,16 +250,13 @@ __global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
             pf, frag(&Vt[buf][(n * 16 + (lane & 15)) * LDV + (lane >> 4) * 8]), o[n], 0, 0, 0); \
     wave_lds_sync();                                                                     \
   }
-  // K rows as they are, V transposed, from ring slot 0
+  // K rows as they are; V^T rows (dim e, 32 keys) as stored, from ring slot 0
 #define LDR_STASH(buf)                                                                   \
   _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                       \
     const int idx_ = (threadIdx.x + i * NT) % CH;                                        \
     const int r_ = idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;                          \
     *reinterpret_cast<u32x4*>(&Ks[buf][r_ * LDQ + col_]) = wk[0][i];                     \
-    _Pragma("unroll") for (int j = 0; j < 4; ++j) {                                      \
-      Vt[buf][(col_ + 2 * j) * LDV + r_] = (uint16_t)(wv[0][i][j] & 0xffffu);            \
-      Vt[buf][(col_ + 2 * j + 1) * LDV + r_] = (uint16_t)(wv[0][i][j] >> 16);            \
-    }                                                                                    \
+    *reinterpret_cast<u32x4*>(&Vt[buf][(idx_ >> 2) * LDV + (idx_ & 3) * 8]) = wv[0][i];  \
   }
 
   if (nwin == 0) {
@@ -333,13 +331,13 @@ hipError_t launch_d(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
 
 }  // namespace
 
-bool attention_mfma_supported(int d, int rep, int B, int R) {
+bool attention_mfma_supported(int d, int rep, int B, int R, int W) {
   return (d == 64 || d == 128) && (rep == 1 || rep == 2 || rep % 4 == 0) && rep <= 64 &&
-         B <= QR && R <= 16;
+         B <= QR && R <= 16 && W % KC == 0;
 }
 
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
-  if (!attention_mfma_supported(a.d, a.rep, a.B, a.R)) return hipErrorInvalidValue;
+  if (!attention_mfma_supported(a.d, a.rep, a.B, a.R, a.W)) return hipErrorInvalidValue;
   return a.d == 128 ? launch_d<128>(a, hkv, batch, st) : launch_d<64>(a, hkv, batch, st);
 }
 

@@ -297,7 +297,7 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
     const float* p = S + i * ldS;
     float acc = 0.f;
     for (int k = 0; k < B; ++k) acc += p[k] * vs[k * d + e];
-    for (int k = 0; k < nv; ++k) acc += p[B + k] * Elem<T>::load(Vw + (size_t)k * d + e);
+    for (int k = 0; k < nv; ++k) acc += p[B + k] * Elem<T>::load(Vw + (size_t)e * a.W + k);
     for (int k = 0; k < nsum; ++k) acc += p[B + nv + k] * Mh[(size_t)k * d + e];
     Elem<T>::store(out + ((long)b * B + i) * (a.hq * d) + h * d + e, acc);
   }

@@ -125,7 +125,7 @@ struct AttnArgs {
 };
 // bf16 MFMA kernel (attn.hip): one workgroup per (kv group, sequence).
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st);
-bool attention_mfma_supported(int d, int rep, int B, int R);
+bool attention_mfma_supported(int d, int rep, int B, int R, int W);
 
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st);

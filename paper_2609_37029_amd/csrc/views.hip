@@ -3,6 +3,8 @@
 // One workgroup per (kv group g, layer j, sequence b) ingests the new rows of
 // that sequence for that head group, reading each new row once:
 //  * ring write of the last min(n, W) rows into window slots (t + r) mod W;
+//    K rows as they come ([W][d]), V transposed ([d][W]) so that attention
+//    reads V with the key index contiguous, as its P.V contraction needs;
 //  * for the rep * R summary queries of the group's query heads, the
 //    statistics of the new set N (Eq. 10) by a tiled online log-sum-exp over
 //    the rows, then the two-way merge with the stored (eta, m) (Eq. 11);
@@ -119,7 +121,6 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
       if (r0 + r >= n - a.W) {  // only the last W rows can survive in the ring
         const size_t slot = (size_t)((t + r0 + r) % a.W);
         *reinterpret_cast<uint4*>(Kw + slot * d + e0) = kv;
-        *reinterpret_cast<uint4*>(Vw + slot * d + e0) = vv;
       }
       const T* kp = reinterpret_cast<const T*>(&kv);
       const T* vp = reinterpret_cast<const T*>(&vv);
@@ -130,6 +131,15 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
       }
     }
     __syncthreads();
+    {  // window V, transposed: slots of consecutive rows are contiguous per dim
+      const int rs = max(0, n - a.W - r0);  // first row of the tile that survives
+      const int ns = nr - rs;
+      for (int i = threadIdx.x; i < ns * d; i += kThreads) {
+        const int e = i / ns, r = rs + i % ns;
+        const size_t slot = (size_t)((t + r0 + r) % a.W);
+        Elem<T>::store(Vw + (size_t)e * a.W + slot, Vs[r][e]);
+      }
+    }
     float s[kTileRows];
     float tmax = -INFINITY;
 #pragma unroll

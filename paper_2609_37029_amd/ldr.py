@@ -178,10 +178,13 @@ class Views:
         return per[:, off:off + n * el].view(dtype).view(self.batch, *shape)
 
     def window(self):
+        """Window K and V as [batch][D][Hkv][W][d] (V is stored transposed,
+        [D][Hkv][d][W]; this returns a transposed view of it)."""
         s = self.shape
         shp = (s.n_layers, s.n_kv_heads, s.window, s.head_dim)
+        vt = (s.n_layers, s.n_kv_heads, s.head_dim, s.window)
         return (self._region(self.layout["kw"], shp, s.torch_dtype),
-                self._region(self.layout["vw"], shp, s.torch_dtype))
+                self._region(self.layout["vw"], vt, s.torch_dtype).transpose(-1, -2))
 
     def summary(self):
         s = self.shape
