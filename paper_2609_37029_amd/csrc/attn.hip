@@ -1,17 +1,17 @@
 // Block-view attention on MFMA for bf16 views (Eq. 6; App. A.1; Sec. 2.4).
 //
 // One workgroup per (kv group g, sequence b) and up to 4 query heads of the
-// group, one wave per head. Keys and values are consumed in chunks of 32 under
-// one online softmax:
-//   chunk 0      the block's own k / v (B rows, normalised and rotated by the
-//                QKV finishing kernel);
-//   chunks 1..   the recent window of layer j, staged through LDS once for all
-//                heads of the group (K rows and the transposed V rows as
-//                stored in the views), the next chunks fetched into
-//                registers while the current one is consumed;
-//   last         the head's R summary entries: keys G[j,h] (bf16), values
-//                M[j,h] kept in fp32 and accumulated on the VALU; both are
-//                loaded at the start and parked in LDS after the prologue.
+// group, two waves per head, each taking half of the keys under its own
+// online softmax:
+//   half 0       the block's own k / v (B rows, normalised and rotated by the
+//                QKV finishing kernel), then the first half of the window;
+//   half 1       the second half of the window of layer j, then the head's R
+//                summary entries (keys G[j,h], values M[j,h] rounded to bf16);
+// window chunks of 32 keys are staged through LDS once for all heads of the
+// group (K rows and the transposed V rows as stored in the views), the next
+// chunks fetched into registers while the current one is consumed. The two
+// halves merge their (max, sum, O) in LDS, which is the split form of the one
+// softmax over all sources.
 // S = Q K^T and O += P V run on v_mfma_f32_16x16x32_bf16 (16 query rows per
 // wave = the B <= 16 slots); P goes through a per-wave LDS tile to change
 // from the C layout to the A layout.
@@ -27,12 +27,25 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int KC = 32;  // keys per chunk
 constexpr int QR = 16;  // query rows per wave (block slots, zero-padded)
 
-__device__ inline float sum16(float v) {  // over the 16 lanes of a row group
-  for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
+// Reductions over the 16 lanes of a row group with DPP lane swaps: quad
+// permutations (xor 1, xor 2), then half-row and row mirrors, which pair each
+// lane with one of the other half; every lane ends with the same value.
+template <int CTRL> __device__ inline float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL,
+                                                            0xF, 0xF, false));
+}
+__device__ inline float sum16(float v) {
+  v += dpp<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
   return v;
 }
 __device__ inline float max16(float v) {
-  for (int off = 1; off < 16; off <<= 1) v = fmaxf(v, __shfl_xor(v, off));
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
   return v;
 }
 __device__ inline float sum64(float v) {
@@ -48,58 +61,68 @@ __device__ inline void wave_lds_sync() {
 }
 
 // HPW query heads of one kv group per workgroup (a group with more heads
-// spreads over rep / HPW workgroups, each reading the group's window).
+// spreads over rep / HPW workgroups, each reading the group's window), two
+// waves per head: the waves of half 0 take the block's own k / v and the
+// first half of the window chunks, those of half 1 the second half and the
+// R summary entries; the halves merge their online-softmax states in LDS.
 template <int D, int HPW>
-__global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
-  constexpr int NT = 64 * HPW;
+__global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
+  constexpr int NT = 128 * HPW, HT = 64 * HPW;  // threads, threads per half
   constexpr int LDQ = D + 8;   // bf16 row of the Q / K tiles (conflict-free 16-row reads)
   constexpr int LDV = KC + 8;  // bf16 row of the V^T / P tiles
   constexpr int NDT = D / 16, KS = D / 32;
   constexpr int CH = KC * D / 8;              // 16-byte pieces of one chunk matrix
-  constexpr int PL = (CH + NT - 1) / NT;
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[HPW][QR * LDQ];
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][KC * LDQ];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][D * LDV];
-  __shared__ __attribute__((aligned(16))) uint16_t Pt[HPW][QR * LDV];
-  // summary entries of the workgroup's heads: keys G (bf16), values M (fp32)
+  constexpr int PL = (CH + HT - 1) / HT;      // pieces per thread of its half
   constexpr int RMAX = 16;
-  __shared__ __attribute__((aligned(16))) uint16_t Gs[HPW][RMAX * LDQ];
-  __shared__ __attribute__((aligned(16))) float Ms[HPW][RMAX * D];
+  // Chunk tiles [half][buffer]; after the loop the K area holds the summary
+  // keys G and then the merge data, the V area the summary values M^T.
+  constexpr int KTILE = KC * LDQ, VTILE = D * LDV;
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[HPW][QR * LDQ];
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][2][KTILE];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][2][VTILE];
+  __shared__ __attribute__((aligned(16))) uint16_t Pt[2 * HPW][QR * LDV];
+  static_assert(HPW * RMAX * LDQ <= 4 * KTILE && HPW * D * LDV <= 4 * VTILE, "summary tiles");
+  static_assert(HPW * (QR * D + 2 * QR) * 4 <= (int)sizeof(Ks), "merge area");
+  uint16_t* const Gs = &Ks[0][0][0];  // [HPW][RMAX * LDQ]
+  uint16_t* const Mt = &Vt[0][0][0];  // [HPW][D * LDV]
+  float* const Xo = reinterpret_cast<float*>(&Ks[0][0][0]);   // [HPW][QR][D]
+  float* const Xml = Xo + HPW * QR * D;                       // [HPW][QR][2]
 
   const int per_group = a.rep / HPW;
   const int g = blockIdx.x / per_group, b = blockIdx.y;
   const int h0 = g * a.rep + (blockIdx.x % per_group) * HPW;  // first head of the workgroup
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int h = h0 + w;
+  const int half = w / HPW, hh = w % HPW, h = h0 + hh;
+  const int ht = threadIdx.x - half * HT;  // thread index inside the half
   const int B = a.B;
-  const long t = a.pos[b];
-  const int nv = t < a.W ? (int)t : a.W;
-  const int nwin = (nv + KC - 1) / KC;
   const uint8_t* seq = a.arena + (size_t)b * a.stride;
   const size_t gw = (size_t)(a.layer * a.hkv + g) * a.W * D;
   const uint16_t* Kw = reinterpret_cast<const uint16_t*>(seq + a.kw) + gw;
   const uint16_t* Vw = reinterpret_cast<const uint16_t*>(seq + a.vw) + gw;
+  // window chunks of the half, assigned over the full window so that the first
+  // fetches do not wait for the position t (unfilled slots read as zeros and
+  // are masked)
+  const int nwf = a.W / KC, cbeg = half * (nwf / 2), cend = half ? nwf : nwf / 2;
 
-  // Window chunks in flight: wk[p] / wv[p] hold chunk c + p while chunk c is
-  // consumed (a ring of depth WD rotated by shifting). Fetches past the valid
-  // rows reload the last valid row: its scores are masked.
-  constexpr int WD = 3;
+  // Window chunks in flight: slot p of the ring holds the p-th next chunk of
+  // the half (depth WD, rotated by shifting). WD = 4 covers a half of a
+  // 256-slot window, so all of its loads are issued before the first wait.
+  constexpr int WD = 4;
   u32x4 wk[WD][PL], wv[WD][PL];
 #define LDR_FETCH(p, c)                                                                  \
   _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                       \
-    const int idx_ = (threadIdx.x + i * NT) % CH;                                        \
-    const int slot_ = min((c) * KC + idx_ / (D / 8), nv - 1), col_ = (idx_ % (D / 8)) * 8; \
+    const int idx_ = (ht + i * HT) % CH;                                                 \
+    const int slot_ = (c) * KC + idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;            \
     wk[p][i] = *reinterpret_cast<const u32x4*>(Kw + (size_t)slot_ * D + col_);         \
     wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)(idx_ >> 2) * a.W +         \
                                                (c) * KC + (idx_ & 3) * 8);               \
   }
-  if (nwin > 0) {
+  int nf = cbeg;  // next chunk to fetch (clamped to the half's last chunk)
 #pragma unroll
-    for (int p = 0; p < WD; ++p) { LDR_FETCH(p, min(p, nwin - 1)) }
-  }
+  for (int p = 0; p < WD; ++p) { LDR_FETCH(p, min(nf, cend - 1)) ++nf; }
 
-  // Summary keys and values of the group's heads, loaded now (the prologue
-  // hides their latency) and parked in LDS after it. Rows past R are zero.
+  // Summary keys and values of the group's heads: loaded now, kept in
+  // registers through the loop and parked in LDS after it. Rows past R are 0.
   constexpr int SG = HPW * RMAX * D / 8;      // 16-byte pieces of G (bf16)
   constexpr int SM = HPW * RMAX * D / 4;      // 16-byte pieces of M (fp32)
   constexpr int GL = (SG + NT - 1) / NT, ML = (SM + NT - 1) / NT;
@@ -111,23 +134,24 @@ __global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < GL; ++i) {
       const int idx = threadIdx.x + i * NT;
-      const int hh = idx / (RMAX * D / 8), r = (idx / (D / 8)) % RMAX, col = (idx % (D / 8)) * 8;
-      greg[i] = (idx < SG && r < a.R && t > 0)
-                    ? *reinterpret_cast<const uint4*>(Gg + ((size_t)hh * a.R + r) * D + col)
+      const int hq_ = idx / (RMAX * D / 8), r = (idx / (D / 8)) % RMAX, col = (idx % (D / 8)) * 8;
+      greg[i] = (idx < SG && r < a.R)
+                    ? *reinterpret_cast<const uint4*>(Gg + ((size_t)hq_ * a.R + r) * D + col)
                     : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < ML; ++i) {
       const int idx = threadIdx.x + i * NT;
-      const int hh = idx / (RMAX * D / 4), r = (idx / (D / 4)) % RMAX, col = (idx % (D / 4)) * 4;
-      mreg[i] = (idx < SM && r < a.R && t > 0)
-                    ? *reinterpret_cast<const uint4*>(Mg + ((size_t)hh * a.R + r) * D + col)
+      const int hq_ = idx / (RMAX * D / 4), r = idx % RMAX, col = ((idx / RMAX) % (D / 4)) * 4;
+      mreg[i] = (idx < SM && r < a.R)
+                    ? *reinterpret_cast<const uint4*>(Mg + ((size_t)hq_ * a.R + r) * D + col)
                     : make_uint4(0, 0, 0, 0);
     }
   }
 
   // ---- block rows: q of the workgroup's heads, k and v of the group (already
-  // normalised and rotated), zero past the B slots of the 16-row tile.
+  // normalised and rotated), zero past the B slots of the 16-row tile; k and v
+  // go to half 0's buffer 0.
   constexpr int QP = HPW * QR * D / 8, KP = QR * D / 8;  // 16-byte pieces
   constexpr int NP = QP + 2 * KP, PP = (NP + NT - 1) / NT;
   const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv) + (size_t)b * B * a.qkv_out;
@@ -143,6 +167,11 @@ __global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
                  ? *reinterpret_cast<const u32x4*>(qkv + (size_t)row * a.qkv_out + col)
                  : u32x4{0u, 0u, 0u, 0u};
   }
+  const long t = a.pos[b];
+  const int nv = t < a.W ? (int)t : a.W;
+  const int nwin = (nv + KC - 1) / KC;
+  const int nch = max(0, min(nwin, cend) - cbeg);      // window chunks of the half
+  const int items = (half == 0 ? 1 : 0) + nch;
 #pragma unroll
   for (int i = 0; i < PP; ++i) {
     const int idx = threadIdx.x + i * NT;
@@ -152,41 +181,44 @@ __global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
     if (idx < QP) {
       *reinterpret_cast<u32x4*>(&Qs[idx / (QR * D / 8)][row * LDQ + c8]) = pre[i];
     } else if (idx < QP + KP) {
-      *reinterpret_cast<u32x4*>(&Ks[0][row * LDQ + c8]) = pre[i];
+      *reinterpret_cast<u32x4*>(&Ks[0][0][row * LDQ + c8]) = pre[i];
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        Vt[0][(c8 + 2 * e) * LDV + row] = (uint16_t)(pre[i][e] & 0xffffu);
-        Vt[0][(c8 + 2 * e + 1) * LDV + row] = (uint16_t)(pre[i][e] >> 16);
+        Vt[0][0][(c8 + 2 * e) * LDV + row] = (uint16_t)(pre[i][e] & 0xffffu);
+        Vt[0][0][(c8 + 2 * e + 1) * LDV + row] = (uint16_t)(pre[i][e] >> 16);
       }
     }
   }
-  for (int idx = threadIdx.x; idx < (KC - QR) * D; idx += NT) {  // padding keys of chunk 0
+  for (int idx = threadIdx.x; idx < (KC - QR) * D; idx += NT) {  // padding keys of the block
     const int r = QR + idx / D, e = idx % D;
-    Ks[0][r * LDQ + e] = 0;
-    Vt[0][e * LDV + r] = 0;
+    Ks[0][0][r * LDQ + e] = 0;
+    Vt[0][0][e * LDV + r] = 0;
   }
-#pragma unroll
-  for (int i = 0; i < GL; ++i) {
-    const int idx = threadIdx.x + i * NT;
-    if (idx < SG) {
-      const int hh = idx / (RMAX * D / 8), r = (idx / (D / 8)) % RMAX, col = (idx % (D / 8)) * 8;
-      *reinterpret_cast<uint4*>(&Gs[hh][r * LDQ + col]) = greg[i];
-    }
+  // K rows and V^T rows of a window chunk, from ring slot 0, into a buffer
+#define LDR_STASH(kbuf, vbuf)                                                            \
+  _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                       \
+    const int idx_ = (ht + i * HT) % CH;                                                 \
+    const int r_ = idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;                          \
+    *reinterpret_cast<u32x4*>(&(kbuf)[r_ * LDQ + col_]) = wk[0][i];                      \
+    *reinterpret_cast<u32x4*>(&(vbuf)[(idx_ >> 2) * LDV + (idx_ & 3) * 8]) = wv[0][i];   \
   }
-#pragma unroll
-  for (int i = 0; i < ML; ++i) {
-    const int idx = threadIdx.x + i * NT;
-    if (idx < SM) {
-      const int hh = idx / (RMAX * D / 4), r = (idx / (D / 4)) % RMAX, col = (idx % (D / 4)) * 4;
-      *reinterpret_cast<uint4*>(&Ms[hh][r * D + col]) = mreg[i];
-    }
+#define LDR_ADVANCE                                                                      \
+  _Pragma("unroll") for (int p = 0; p + 1 < WD; ++p)                                     \
+      _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                   \
+    wk[p][i] = wk[p + 1][i];                                                             \
+    wv[p][i] = wv[p + 1][i];                                                             \
+  }                                                                                      \
+  LDR_FETCH(WD - 1, min(nf, cend - 1)) ++nf;
+  if (half == 1) {  // half 1 starts on a window chunk
+    LDR_STASH(Ks[1][0], Vt[1][0])
+    LDR_ADVANCE
   }
   __syncthreads();
 
   bf16x8 qf[KS];
 #pragma unroll
-  for (int kk = 0; kk < KS; ++kk) qf[kk] = frag(&Qs[w][(lane & 15) * LDQ + kk * 32 + (lane >> 4) * 8]);
+  for (int kk = 0; kk < KS; ++kk) qf[kk] = frag(&Qs[hh][(lane & 15) * LDQ + kk * 32 + (lane >> 4) * 8]);
 
   f32x4 o[NDT];
 #pragma unroll
@@ -210,109 +242,163 @@ __global__ void __launch_bounds__(64 * HPW) attention_mfma_kernel(AttnArgs a) {
         sc[kt][v] = s;
         cmax[v] = fmaxf(cmax[v], s);
       }
+    // The reference max of a row moves only when the tile's max exceeds it by
+    // more than 8 (or it is still -inf): below that, exp(s - m) stays under
+    // e^8, and O and l share the same stale reference, so the result is the
+    // same softmax. Rescaling O is rare and skipped by the whole wave.
+    bool grow = false;
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const float mnew = fmaxf(mrow[v], max16(cmax[v]));
-      const float alpha = __expf(mrow[v] - mnew);  // first tile: exp(-inf) = 0
-      mrow[v] = mnew;
-      lrow[v] *= alpha;
+      cmax[v] = max16(cmax[v]);
+      grow |= cmax[v] > mrow[v] + 8.f;
+    }
+    if (__ballot(grow) != 0) {
 #pragma unroll
-      for (int n = 0; n < NDT; ++n) o[n][v] *= alpha;
+      for (int v = 0; v < 4; ++v) {
+        const float mnew = cmax[v] > mrow[v] + 8.f ? cmax[v] : mrow[v];
+        const float alpha = __expf(mrow[v] - mnew);  // first tile: exp(-inf) = 0
+        mrow[v] = mnew;
+        lrow[v] *= alpha;
+#pragma unroll
+        for (int n = 0; n < NDT; ++n) o[n][v] *= alpha;
+      }
+    }
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
-        const float p = __expf(sc[kt][v] - mnew);
+        const float p = __expf(sc[kt][v] - mrow[v]);
         sc[kt][v] = p;
         lrow[v] += p;
       }
-    }
   };
 
-  // Scores of one 32-key chunk in LDS buffer `buf`, the online softmax, and
-  // O += P V on the same chunk.
-#define LDR_CHUNK(buf, nvalid)                                                           \
-  {                                                                                      \
-    f32x4 sc[2];                                                                         \
-    _Pragma("unroll") for (int kt = 0; kt < 2; ++kt) {                                   \
-      sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};                                                \
-      _Pragma("unroll") for (int kk = 0; kk < KS; ++kk) sc[kt] =                         \
-          __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                       \
-              qf[kk], frag(&Ks[buf][(kt * 16 + (lane & 15)) * LDQ + kk * 32 + (lane >> 4) * 8]), \
-              sc[kt], 0, 0, 0);                                                          \
-    }                                                                                    \
-    absorb(sc, nvalid);                                                                  \
-    _Pragma("unroll") for (int kt = 0; kt < 2; ++kt)                                     \
-        _Pragma("unroll") for (int v = 0; v < 4; ++v)                                    \
-            Pt[w][((lane >> 4) * 4 + v) * LDV + kt * 16 + (lane & 15)] = f32_to_bf16(sc[kt][v]); \
-    wave_lds_sync();                                                                     \
-    const bf16x8 pf = frag(&Pt[w][(lane & 15) * LDV + (lane >> 4) * 8]);                 \
-    _Pragma("unroll") for (int n = 0; n < NDT; ++n) o[n] =                               \
-        __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                         \
-            pf, frag(&Vt[buf][(n * 16 + (lane & 15)) * LDV + (lane >> 4) * 8]), o[n], 0, 0, 0); \
-    wave_lds_sync();                                                                     \
-  }
-  // K rows as they are; V^T rows (dim e, 32 keys) as stored, from ring slot 0
-#define LDR_STASH(buf)                                                                   \
-  _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                       \
-    const int idx_ = (threadIdx.x + i * NT) % CH;                                        \
-    const int r_ = idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;                          \
-    *reinterpret_cast<u32x4*>(&Ks[buf][r_ * LDQ + col_]) = wk[0][i];                     \
-    *reinterpret_cast<u32x4*>(&Vt[buf][(idx_ >> 2) * LDV + (idx_ & 3) * 8]) = wv[0][i];  \
-  }
-
-  if (nwin == 0) {
-    LDR_CHUNK(0, B)
-  } else {
-    // chunk 0 is the block; chunk c >= 1 is window chunk c - 1 (LDS buffer c & 1)
-    for (int c = 0; c <= nwin; ++c) {
-      const int buf = c & 1;
-      LDR_CHUNK(buf, c == 0 ? B : min(KC, nv - (c - 1) * KC))
-      LDR_STASH(buf ^ 1)  // window chunk c (past the end: never read)
+  // Scores of one 32-key tile (keys kbuf, values vbuf), the online softmax,
+  // and O += P V on the same tile.
+  auto item = [&](const uint16_t* kbuf, const uint16_t* vbuf, int nvalid) {
+    f32x4 sc[2];
 #pragma unroll
-      for (int p = 0; p + 1 < WD; ++p)
+    for (int kt = 0; kt < 2; ++kt) {
+      sc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int i = 0; i < PL; ++i) {
-          wk[p][i] = wk[p + 1][i];
-          wv[p][i] = wv[p + 1][i];
-        }
-      LDR_FETCH(WD - 1, min(c + WD, nwin - 1))
-      lds_barrier();
+      for (int kk = 0; kk < KS; ++kk)
+        sc[kt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            qf[kk], frag(&kbuf[(kt * 16 + (lane & 15)) * LDQ + kk * 32 + (lane >> 4) * 8]),
+            sc[kt], 0, 0, 0);
     }
+    absorb(sc, nvalid);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v)
+        Pt[w][((lane >> 4) * 4 + v) * LDV + kt * 16 + (lane & 15)] = f32_to_bf16(sc[kt][v]);
+    wave_lds_sync();
+    const bf16x8 pf = frag(&Pt[w][(lane & 15) * LDV + (lane >> 4) * 8]);
+#pragma unroll
+    for (int n = 0; n < NDT; ++n)
+      o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          pf, frag(&vbuf[(n * 16 + (lane & 15)) * LDV + (lane >> 4) * 8]), o[n], 0, 0, 0);
+    wave_lds_sync();
+  };
+
+  // ---- the halves walk their items in step (one barrier per step) ----
+  // half 0 always has the most items (the block, and its chunks come first):
+  // both halves take that many steps so that every wave meets every barrier
+  const int steps = 1 + max(0, min(nwin, nwf / 2));
+  for (int it = 0; it < steps; ++it) {
+    const int buf = it & 1;
+    if (it < items) {
+      const int chunk = cbeg + it - (half == 0 ? 1 : 0);  // -1: the block
+      item(Ks[half][buf], Vt[half][buf], chunk < cbeg ? B : min(KC, nv - chunk * KC));
+    }
+    LDR_STASH(Ks[half][buf ^ 1], Vt[half][buf ^ 1])  // the next chunk (past the end: unused)
+    LDR_ADVANCE
+    lds_barrier();
   }
+#undef LDR_ADVANCE
 #undef LDR_STASH
-#undef LDR_CHUNK
 #undef LDR_FETCH
 
-  // ---- summary entries of head h: keys G[j,h] (bf16), values M[j,h] (fp32) ----
-  if (t > 0) {
-    f32x4 sc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};  // keys >= 16 masked
+  // ---- summary of the heads (half 1): G rows as keys, M^T (bf16) as values,
+  // one more 32-key item with keys R .. 31 masked and their values zero ----
+#pragma unroll
+  for (int i = 0; i < GL; ++i) {
+    const int idx = threadIdx.x + i * NT;
+    if (idx < SG) {
+      const int hq_ = idx / (RMAX * D / 8), r = (idx / (D / 8)) % RMAX, col = (idx % (D / 8)) * 8;
+      *reinterpret_cast<uint4*>(&Gs[hq_ * RMAX * LDQ + r * LDQ + col]) = greg[i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < ML; ++i) {  // M^T in bf16: Mt[head][e][r]
+    const int idx = threadIdx.x + i * NT;
+    if (idx < SM) {
+      const int hq_ = idx / (RMAX * D / 4), r = idx % RMAX, col = ((idx / RMAX) % (D / 4)) * 4;
+      const uint32_t m4[4] = {mreg[i].x, mreg[i].y, mreg[i].z, mreg[i].w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        Mt[hq_ * VTILE + (col + k) * LDV + r] = f32_to_bf16(__uint_as_float(m4[k]));
+    }
+  }
+  for (int idx = threadIdx.x; idx < HPW * D * (KC - RMAX) / 8; idx += NT) {  // keys 16..31
+    const int hq_ = idx / (D * (KC - RMAX) / 8), rest = idx % (D * (KC - RMAX) / 8);
+    *reinterpret_cast<u32x4*>(&Mt[hq_ * VTILE + (rest / 2) * LDV + RMAX + (rest % 2) * 8]) =
+        u32x4{0u, 0u, 0u, 0u};
+  }
+  __syncthreads();
+  if (half == 1 && t > 0) {
+    f32x4 sc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)
       sc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-          qf[kk], frag(&Gs[w][(lane & 15) * LDQ + kk * 32 + (lane >> 4) * 8]), sc[0], 0, 0, 0);
+          qf[kk], frag(&Gs[hh * RMAX * LDQ + (lane & 15) * LDQ + kk * 32 + (lane >> 4) * 8]),
+          sc[0], 0, 0, 0);
     absorb(sc, a.R);
-    for (int r = 0; r < a.R; ++r) {  // O[q][e] += p[q][r] M[r][e] in fp32
-      const int src = (lane & 48) | (r & 15);
-      float pr[4];
 #pragma unroll
-      for (int v = 0; v < 4; ++v) pr[v] = __shfl(sc[0][v], src);
+    for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-      for (int n = 0; n < NDT; ++n) {
-        const float mv = Ms[w][r * D + n * 16 + (lane & 15)];
+      for (int v = 0; v < 4; ++v)
+        Pt[w][((lane >> 4) * 4 + v) * LDV + kt * 16 + (lane & 15)] = f32_to_bf16(sc[kt][v]);
+    wave_lds_sync();
+    const bf16x8 pf = frag(&Pt[w][(lane & 15) * LDV + (lane >> 4) * 8]);
 #pragma unroll
-        for (int v = 0; v < 4; ++v) o[n][v] += pr[v] * mv;
+    for (int n = 0; n < NDT; ++n)
+      o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+          pf, frag(&Mt[hh * VTILE + (n * 16 + (lane & 15)) * LDV + (lane >> 4) * 8]), o[n], 0, 0, 0);
+  }
+  __syncthreads();
+
+  // ---- merge: half 1 parks (O, m, l), half 0 combines and writes o ----
+  if (half == 1) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int q = (lane >> 4) * 4 + v;
+      const float l = sum16(lrow[v]);
+#pragma unroll
+      for (int n = 0; n < NDT; ++n) Xo[(hh * QR + q) * D + n * 16 + (lane & 15)] = o[n][v];
+      if ((lane & 15) == 0) {
+        Xml[(hh * QR + q) * 2] = mrow[v];
+        Xml[(hh * QR + q) * 2 + 1] = l;
       }
     }
   }
-
-  uint16_t* out = static_cast<uint16_t*>(a.o);
+  __syncthreads();
+  if (half == 0) {
+    uint16_t* out = static_cast<uint16_t*>(a.o);
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int q = (lane >> 4) * 4 + v;
-    const float inv = 1.f / sum16(lrow[v]);
-    if (q < B) {
-      uint16_t* row = out + ((long)b * B + q) * ((long)a.hq * D) + (long)h * D + (lane & 15);
+    for (int v = 0; v < 4; ++v) {
+      const int q = (lane >> 4) * 4 + v;
+      const float m1 = Xml[(hh * QR + q) * 2], l1 = Xml[(hh * QR + q) * 2 + 1];
+      const float m = fmaxf(mrow[v], m1);
+      const float w0 = __expf(mrow[v] - m), w1 = m1 == -INFINITY ? 0.f : __expf(m1 - m);
+      const float inv = 1.f / (w0 * sum16(lrow[v]) + w1 * l1);
+      if (q < B) {
+        uint16_t* row = out + ((long)b * B + q) * ((long)a.hq * D) + (long)h * D + (lane & 15);
 #pragma unroll
-      for (int n = 0; n < NDT; ++n) row[n * 16] = f32_to_bf16(o[n][v] * inv);
+        for (int n = 0; n < NDT; ++n)
+          row[n * 16] = f32_to_bf16(
+              (w0 * o[n][v] + w1 * Xo[(hh * QR + q) * D + n * 16 + (lane & 15)]) * inv);
+      }
     }
   }
 }
@@ -322,9 +408,9 @@ hipError_t launch_d(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
   const int hpw = a.rep < 4 ? a.rep : 4;
   const dim3 grid(hkv * (a.rep / hpw), batch);
   switch (hpw) {
-    case 1: hipLaunchKernelGGL((attention_mfma_kernel<D, 1>), grid, dim3(64), 0, st, a); break;
-    case 2: hipLaunchKernelGGL((attention_mfma_kernel<D, 2>), grid, dim3(128), 0, st, a); break;
-    default: hipLaunchKernelGGL((attention_mfma_kernel<D, 4>), grid, dim3(256), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((attention_mfma_kernel<D, 1>), grid, dim3(128), 0, st, a); break;
+    case 2: hipLaunchKernelGGL((attention_mfma_kernel<D, 2>), grid, dim3(256), 0, st, a); break;
+    default: hipLaunchKernelGGL((attention_mfma_kernel<D, 4>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
 }
@@ -333,7 +419,7 @@ hipError_t launch_d(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
 
 bool attention_mfma_supported(int d, int rep, int B, int R, int W) {
   return (d == 64 || d == 128) && (rep == 1 || rep == 2 || rep % 4 == 0) && rep <= 64 &&
-         B <= QR && R <= 16 && W % KC == 0;
+         B <= QR && R <= 16 && W % (2 * KC) == 0;
 }
 
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st) {

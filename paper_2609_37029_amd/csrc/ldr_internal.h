@@ -39,13 +39,18 @@ __host__ __device__ inline float bf16_to_f32(uint16_t h) {
   v.u = (uint32_t)h << 16;
   return v.f;
 }
+// Round to nearest even (the device uses the gfx950 conversion instruction).
 __host__ __device__ inline uint16_t f32_to_bf16(float f) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+#else
   union { uint32_t u; float f; } v;
   v.f = f;
   if ((v.u & 0x7f800000u) == 0x7f800000u && (v.u & 0x007fffffu))  // NaN stays NaN
     return (uint16_t)((v.u >> 16) | 0x40);
   uint32_t r = v.u + 0x7fffu + ((v.u >> 16) & 1u);
   return (uint16_t)(r >> 16);
+#endif
 }
 
 // Workgroup barrier that orders LDS accesses only: each wave waits for its own
