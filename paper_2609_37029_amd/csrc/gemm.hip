@@ -234,14 +234,15 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
   }
 }
 
-// Tile configurations (cfg): 0: BM 16 (M <= 16), 1: BM 32, 2: BM 64, all
-// with 8 waves along N (BN 256); 3: BM 256 with 4 x 2 waves of 64 x 64 (BN 128);
+// Tile configurations (cfg): 0: BM 16 (M <= 16) with 4 waves along N (BN 128);
+// 1: BM 32, 2: BM 64, with 8 waves along N (BN 256); 3: BM 256 with 4 x 2 waves
+// of 64 x 64 (BN 128);
 // 4: BM 256 with 8 x 1 waves of 32 x 96 (BN 96), for the SwiGLU GEMM, whose
 // 2 x 12288 columns at the Qwen3-8B shape make exactly 256 tiles (one per CU).
 template <int EPI>
 hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
   switch (cfg) {
-    case 0: hipLaunchKernelGGL((gemm_kernel<1, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
+    case 0: hipLaunchKernelGGL((gemm_kernel<1, 2, 1, 4, EPI>), grid, dim3(256), 0, st, a); break;
     case 1: hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 2: hipLaunchKernelGGL((gemm_kernel<4, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 4: hipLaunchKernelGGL((gemm_kernel<2, 6, 8, 1, EPI>), grid, dim3(512), 0, st, a); break;
@@ -264,7 +265,7 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
   } else {
     p.cfg = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : swiglu ? 4 : 3;
     bm = p.cfg >= 3 ? 256 : 16 << p.cfg;
-    bn = p.cfg == 4 ? 96 : p.cfg == 3 ? 128 : 256;
+    bn = p.cfg == 4 ? 96 : (p.cfg == 3 || p.cfg == 0) ? 128 : 256;
     kstep = 2 * BK;
   }
   p.ntw = 0;
