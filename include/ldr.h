@@ -225,6 +225,9 @@ size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
  * (v div 2) mod 4, u = (2 (bits >> 9) + 1) 2^-24) and a fixed-operation fp32
  * logarithm, so the tokens are reproducible bit for bit on any IEEE machine;
  * lse[r] = log sum_{v in S} exp(z_v / T); logq[r] = z_y / T - lse[r].
+ * top_k >= vocab is the full vocabulary; a negative top_k is LDR_EINVAL. With
+ * 0 < top_k < vocab an extra pass per row selects the exact top_k support
+ * (-0 and +0 compare equal).
  *   logits dev fp32 [rows][vocab]; tokens dev int32 [rows]; lse, logq dev fp32 [rows]
  *   workspace dev, ldr_sample_workspace_bytes(rows, vocab) bytes. */
 int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperature,

@@ -393,7 +393,7 @@ int ldr_draft_step_events(const ldr_views* v, const ldr_weights* w, const int32_
 
 size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab) {
   if (rows <= 0 || vocab <= 0) return 0;
-  return align_up((size_t)rows * sample_splits(rows, vocab) * 16);
+  return align_up(sample_part_bytes(rows, vocab)) + align_up((size_t)rows * 8);
 }
 
 int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperature,
@@ -402,11 +402,12 @@ int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperatu
   if (!logits || !tokens || !lse || !logq || !workspace) return LDR_EINVAL;
   if (rows <= 0 || vocab <= 0 || !(temperature >= 0.f) || std::isinf(temperature))
     return LDR_EINVAL;
-  if (top_k != 0) return LDR_EINVAL;
+  if (top_k < 0) return LDR_EINVAL;
   if (workspace_bytes < ldr_sample_workspace_bytes(rows, vocab) || !aligned(workspace, 16))
     return LDR_EINVAL;
   return launch_sample(logits, rows, vocab, temperature, top_k, seed, step, tokens, lse, logq,
-                       workspace, static_cast<hipStream_t>(stream)) == hipSuccess
+                       workspace, align_up(sample_part_bytes(rows, vocab)),
+                       static_cast<hipStream_t>(stream)) == hipSuccess
              ? LDR_OK : LDR_EHIP;
 }
 

@@ -144,9 +144,10 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
 
 // Sampler (sample.hip)
 int sample_splits(int rows, int vocab);
+size_t sample_part_bytes(int rows, int vocab);
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
-                         float* logq, void* ws, hipStream_t st);
+                         float* logq, void* ws, size_t sel_off, hipStream_t st);
 hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
                               hipStream_t st);
 

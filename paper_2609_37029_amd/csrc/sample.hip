@@ -96,11 +96,91 @@ __device__ inline void combine(Partial& a, const Partial& b) {
   a.m = m;
 }
 
+// Top-k support of a row: token v is inside iff key(z_v) > tau, or
+// key(z_v) == tau and v <= v_cut (ties at the boundary, lower index first).
+struct TopK { uint32_t tau; int v_cut; };
+
+// Order-preserving map of fp32 to uint32 (larger float, larger key); -0
+// counts as +0, as the two compare equal.
+__device__ inline uint32_t order_key(float z) {
+  uint32_t b = __float_as_uint(z);
+  if (b == 0x80000000u) b = 0u;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
 struct SampleArgs {
   const float* logits; int rows, vocab, chunk, splits;
   float T; uint64_t seed, step;
   Partial* part;
+  const TopK* sel;  // top-k support per row, or null for the full vocabulary
 };
+
+// Exact k-th largest logit of a row by radix selection on order_key (four
+// 8-bit digits, most significant first, LDS histograms), then the index cut
+// among the tokens equal to it. One workgroup per row.
+constexpr int kSelThreads = 1024;
+__global__ void __launch_bounds__(kSelThreads) topk_select_kernel(const float* logits, int vocab,
+                                                                  int k, TopK* sel) {
+  const float* z = logits + (long)blockIdx.x * vocab;
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t s_digit, s_above;
+  __shared__ int wcount[kSelThreads / 64];
+  __shared__ int s_base, s_cut;
+  uint32_t prefix = 0u, mask = 0u, count_eq = 0u;
+  int remaining = k;  // rank of the wanted value among the keys matching prefix
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    for (int i = threadIdx.x; i < 256; i += kSelThreads) hist[i] = 0u;
+    __syncthreads();
+    for (int v = threadIdx.x; v < vocab; v += kSelThreads) {
+      const uint32_t u = order_key(z[v]);
+      if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 0xFFu], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {  // the digit where the count from the top reaches `remaining`
+      uint32_t cum = 0u;
+      int d = 255;
+      for (; d > 0; --d) {
+        if (cum + hist[d] >= (uint32_t)remaining) break;
+        cum += hist[d];
+      }
+      s_digit = (uint32_t)d;
+      s_above = cum;
+    }
+    __syncthreads();
+    const uint32_t d = s_digit;
+    remaining -= (int)s_above;
+    prefix |= d << shift;
+    mask |= 0xFFu << shift;
+    count_eq = hist[d];
+    __syncthreads();
+  }
+  // `remaining` of the count_eq tokens equal to the k-th value are inside:
+  // the lowest indices first
+  int v_cut = vocab;
+  if (remaining < (int)count_eq) {
+    if (threadIdx.x == 0) { s_base = 0; s_cut = -1; }
+    __syncthreads();
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    for (int v0 = 0; v0 < vocab; v0 += kSelThreads) {
+      const int v = v0 + (int)threadIdx.x;
+      const bool eq = v < vocab && order_key(z[v]) == prefix;
+      const uint64_t ball = __ballot(eq);
+      if (lane == 0) wcount[w] = __popcll(ball);
+      __syncthreads();
+      int rank = s_base + __popcll(ball & ((1ull << lane) - 1ull)) + 1;
+      for (int i = 0; i < w; ++i) rank += wcount[i];
+      if (eq && rank == remaining) s_cut = v;
+      __syncthreads();
+      if (threadIdx.x == 0)
+        for (int i = 0; i < kSelThreads / 64; ++i) s_base += wcount[i];
+      __syncthreads();
+      if (s_cut >= 0) break;  // uniform: read after the barrier
+    }
+    v_cut = s_cut;
+  }
+  if (threadIdx.x == 0) sel[blockIdx.x] = TopK{prefix, v_cut};
+}
 
 // Upper bound of the Gumbel noise g = -log(-log u) of 23-bit uniform index k,
 // u = (2k + 1) 2^-24, from integer arithmetic: -log u >= 1 - u = n 2^-24 with
@@ -124,6 +204,7 @@ __device__ inline float gumbel_upper(uint32_t bits) {
 template <bool UNIT_T>
 __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0, int v1,
                               Partial& p) {
+  const TopK sel = a.sel ? a.sel[r] : TopK{0u, 0x7fffffff};
   struct Cand { float zt; uint32_t bits; int v; };
   __shared__ Cand queue[kThreads / 64][128];
   const int lane = threadIdx.x & 63;
@@ -146,16 +227,19 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
     noise_group(a.seed, a.step, (uint64_t)r, (uint64_t)(v / kGroup), bits);
     float zt[kGroup];
     float gm = -INFINITY;
+    bool in[kGroup];
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) {
       const float zv = v + i < v1 ? z[v + i] : -INFINITY;
-      zt[i] = UNIT_T ? zv : zv / a.T;  // IEEE division
+      const uint32_t u = order_key(zv);
+      in[i] = v + i < v1 && (u > sel.tau || (u == sel.tau && v + i <= sel.v_cut));
+      zt[i] = in[i] ? (UNIT_T ? zv : zv / a.T) : -INFINITY;  // IEEE division
       gm = fmaxf(gm, zt[i]);
     }
     if (gm > p.m) { p.s *= __expf(p.m - gm); p.m = gm; }
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) {
-      const bool valid = v + i < v1;
+      const bool valid = in[i];
       if (valid) p.s += __expf(zt[i] - p.m);
       const float margin = 1e-3f + 1e-6f * (fabsf(zt[i]) + fabsf(p.key));
       const bool need = valid && !(zt[i] + gumbel_upper(bits[i]) + margin < p.key);
@@ -259,13 +343,25 @@ int sample_splits(int rows, int vocab) {
   return splits < 1 ? 1 : splits;
 }
 
+size_t sample_part_bytes(int rows, int vocab) {
+  return (size_t)rows * sample_splits(rows, vocab) * sizeof(Partial);
+}
+
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
-                         float* logq, void* ws, hipStream_t st) {
-  (void)top_k;
+                         float* logq, void* ws, size_t sel_off, hipStream_t st) {
   SampleArgs a;
   a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
   a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
+  a.sel = nullptr;
+  if (temperature > 0.f && top_k > 0 && top_k < vocab) {  // T = 0 is the argmax either way
+    TopK* sel = reinterpret_cast<TopK*>(static_cast<uint8_t*>(ws) + sel_off);
+    hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, logits, vocab,
+                       top_k, sel);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    a.sel = sel;
+  }
   a.splits = sample_splits(rows, vocab);
   const int sweep = kThreads * kGroup;
   a.chunk = ((vocab + a.splits - 1) / a.splits + sweep - 1) / sweep * sweep;

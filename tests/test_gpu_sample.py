@@ -61,7 +61,48 @@ def test_steps_and_seeds_change_the_draw(gpu_lib):
     np.testing.assert_allclose(lse, np.log(4096.0), rtol=1e-6)
 
 
-def test_top_k_not_yet_accepted(gpu_lib):
+def _check_sample(gpu_lib, z, T, k, seed, step):
+    tok, lse, logq = gpu_lib.sample(z, T, k, seed=seed, step=step)
+    torch.cuda.synchronize()
+    y, l, lq = OS.sample(z.cpu().numpy(), T, k, seed, step)
+    assert np.array_equal(tok.cpu().numpy().astype(np.int64), y)
+    np.testing.assert_allclose(lse.cpu().numpy(), l, rtol=2e-6, atol=2e-5)
+    np.testing.assert_allclose(logq.cpu().numpy(), lq, rtol=1e-5, atol=2e-4)
+    return tok.cpu().numpy()
+
+
+@pytest.mark.parametrize("rows,vocab,T,k", [(16, 151936, 1.0, 50), (9, 2049, 0.7, 1),
+                                            (33, 5003, 1.0, 5002), (8, 1001, 1.3, 1000),
+                                            (4, 3, 1.0, 2), (64, 4096, 1.0, 7)])
+def test_top_k_tokens_exact(gpu_lib, rows, vocab, T, k):
+    z = _logits(rows, vocab, rows * 11 + vocab + k)
+    tok = _check_sample(gpu_lib, z, T, k, seed=91, step=3)
+    for r in range(rows):  # every token is inside the row's top-k support
+        assert tok[r] in set(OS.support(z[r].cpu().numpy(), k).tolist())
+
+
+def test_top_k_ties_at_the_boundary(gpu_lib):
+    # few distinct values: the k-th value is shared by many tokens, and the
+    # lowest indices among them are inside
+    z = torch.round(_logits(12, 20011, 5) * 2.0) / 2.0
+    z[3, :] = 0.25                                  # all equal: the first k tokens
+    z[5, ::2] = -0.0                                # -0 and +0 compare equal
+    z[5, 1::2] = 0.0
+    z[5, 17] = 1.0
+    for k in (1, 40, 333, 20010):
+        _check_sample(gpu_lib, z, 1.0, k, seed=k, step=1)
+
+
+def test_top_k_at_least_vocab_is_the_full_support(gpu_lib):
+    z = _logits(20, 3001, 8)
+    a = gpu_lib.sample(z, 1.0, 0, seed=4, step=2)
+    b = gpu_lib.sample(z, 1.0, 3001, seed=4, step=2)
+    c = gpu_lib.sample(z, 1.0, 10**6, seed=4, step=2)
+    for x, y in ((a, b), (a, c)):
+        assert torch.equal(x[0], y[0]) and torch.equal(x[1], y[1])
+
+
+def test_negative_top_k_is_rejected(gpu_lib):
     z = _logits(2, 100, 1)
     with pytest.raises(gpu_lib.LdrError):
-        gpu_lib.sample(z, 1.0, 5, seed=0, step=0)
+        gpu_lib.sample(z, 1.0, -1, seed=0, step=0)
