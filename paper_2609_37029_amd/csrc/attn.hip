@@ -30,10 +30,6 @@ constexpr int QR = 16;  // query rows per wave (block slots, zero-padded)
 // Reductions over the 16 lanes of a row group with DPP lane swaps: quad
 // permutations (xor 1, xor 2), then half-row and row mirrors, which pair each
 // lane with one of the other half; every lane ends with the same value.
-template <int CTRL> __device__ inline float dpp(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL,
-                                                            0xF, 0xF, false));
-}
 __device__ inline float sum16(float v) {
   v += dpp<0xB1>(v);   // quad_perm [1, 0, 3, 2]
   v += dpp<0x4E>(v);   // quad_perm [2, 3, 0, 1]

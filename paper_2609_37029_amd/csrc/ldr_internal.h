@@ -39,6 +39,17 @@ __host__ __device__ inline float bf16_to_f32(uint16_t h) {
   v.u = (uint32_t)h << 16;
   return v.f;
 }
+// Lane swap inside a row of 16 lanes (DPP control CTRL: 0xB1 / 0x4E quad
+// permutations xor 1 / xor 2, 0x141 half-row mirror, 0x140 row mirror).
+template <int CTRL> __device__ inline float dpp(float v) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL,
+                                                            0xF, 0xF, false));
+#else
+  return v;  // device code only
+#endif
+}
+
 // Round to nearest even (the device uses the gfx950 conversion instruction).
 __host__ __device__ inline uint16_t f32_to_bf16(float f) {
 #if defined(__HIP_DEVICE_COMPILE__)

@@ -201,10 +201,10 @@ __device__ inline float gumbel_upper(uint32_t bits) {
 // the test and of the fixed-sequence log, whose error is below 1e-5 here.
 // Candidates go through a per-wave queue in LDS so that the exact key (two
 // logs) is computed 64 at a time by full waves.
-template <bool UNIT_T>
+template <bool UNIT_T, bool TOPK>
 __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0, int v1,
                               Partial& p) {
-  const TopK sel = a.sel ? a.sel[r] : TopK{0u, 0x7fffffff};
+  const TopK sel = TOPK ? a.sel[r] : TopK{0u, 0};
   struct Cand { float zt; uint32_t bits; int v; };
   __shared__ Cand queue[kThreads / 64][128];
   const int lane = threadIdx.x & 63;
@@ -231,8 +231,11 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) {
       const float zv = v + i < v1 ? z[v + i] : -INFINITY;
-      const uint32_t u = order_key(zv);
-      in[i] = v + i < v1 && (u > sel.tau || (u == sel.tau && v + i <= sel.v_cut));
+      in[i] = v + i < v1;
+      if constexpr (TOPK) {
+        const uint32_t u = order_key(zv);
+        in[i] = in[i] && (u > sel.tau || (u == sel.tau && v + i <= sel.v_cut));
+      }
       zt[i] = in[i] ? (UNIT_T ? zv : zv / a.T) : -INFINITY;  // IEEE division
       gm = fmaxf(gm, zt[i]);
     }
@@ -272,10 +275,12 @@ __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) 
       const float zv = z[v];
       if (better(zv, v, p.key, p.idx)) { p.key = zv; p.idx = v; }
     }
-  } else if (a.T == 1.f) {
-    sample_tokens<true>(a, z, r, v0, v1, p);
+  } else if (a.sel) {
+    if (a.T == 1.f) sample_tokens<true, true>(a, z, r, v0, v1, p);
+    else sample_tokens<false, true>(a, z, r, v0, v1, p);
   } else {
-    sample_tokens<false>(a, z, r, v0, v1, p);
+    if (a.T == 1.f) sample_tokens<true, false>(a, z, r, v0, v1, p);
+    else sample_tokens<false, false>(a, z, r, v0, v1, p);
   }
   // block reduction of the partials
   for (int off = 32; off >= 1; off >>= 1) {

@@ -44,6 +44,18 @@ struct UpdateArgs {
   float inv_sqrt_d;
 };
 
+// Sum over aligned groups of tpq lanes (tpq a power of two): DPP lane swaps
+// inside rows of 16 (after each step every lane of a group holds the same
+// value), cross-row shuffles beyond.
+__device__ inline float group_sum(float v, int tpq) {
+  if (tpq >= 2) v += dpp<0xB1>(v);
+  if (tpq >= 4) v += dpp<0x4E>(v);
+  if (tpq >= 8) v += dpp<0x141>(v);
+  if (tpq >= 16) v += dpp<0x140>(v);
+  for (int off = 16; off < tpq; off <<= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
 // 16-byte copy of `n16` chunks.
 __device__ inline void copy16(void* dst, const void* src, int idx) {
   reinterpret_cast<uint4*>(dst)[idx] = reinterpret_cast<const uint4*>(src)[idx];
@@ -131,13 +143,14 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
       }
     }
     __syncthreads();
-    {  // window V, transposed: slots of consecutive rows are contiguous per dim
+    {  // window V, transposed: lanes take consecutive rows of one dim, whose
+       // slots are contiguous (apart from the wrap of the ring)
       const int rs = max(0, n - a.W - r0);  // first row of the tile that survives
-      const int ns = nr - rs;
-      for (int i = threadIdx.x; i < ns * d; i += kThreads) {
-        const int e = i / ns, r = rs + i % ns;
+      const int r = threadIdx.x % kTileRows;
+      if (r >= rs && r < nr) {
         const size_t slot = (size_t)((t + r0 + r) % a.W);
-        Elem<T>::store(Vw + (size_t)e * a.W + slot, Vs[r][e]);
+        for (int e = threadIdx.x / kTileRows; e < d; e += kThreads / kTileRows)
+          Elem<T>::store(Vw + (size_t)e * a.W + slot, Vs[r][e]);
       }
     }
     float s[kTileRows];
@@ -153,7 +166,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
                gq[c * 4 + 3] * k4.w;
         }
       }
-      for (int off = 1; off < tpq; off <<= 1) p += __shfl_xor(p, off);
+      p = group_sum(p, tpq);
       s[r] = r < nr ? p : -INFINITY;
       tmax = fmaxf(tmax, s[r]);
     }
