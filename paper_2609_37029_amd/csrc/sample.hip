@@ -25,12 +25,26 @@ constexpr int kGroup = 8;  // tokens per Philox block
 constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
 constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
 
+// 128-bit product M x, M a constant: four 32 x 32 + 64 multiply-adds
+// (v_mad_u64_u32), the middle column carried through p1 and p2.
+template <uint64_t M>
+__device__ inline void mulhilo(uint64_t x, uint64_t& hi, uint64_t& lo) {
+  constexpr uint32_t Ml = (uint32_t)M, Mh = (uint32_t)(M >> 32);
+  const uint32_t xl = (uint32_t)x, xh = (uint32_t)(x >> 32);
+  const uint64_t p0 = (uint64_t)Ml * xl;
+  const uint64_t p1 = (uint64_t)Mh * xl + (p0 >> 32);
+  const uint64_t p2 = (uint64_t)Ml * xh + (uint32_t)p1;
+  lo = (p2 << 32) | (uint32_t)p0;
+  hi = (uint64_t)Mh * xh + (p1 >> 32) + (p2 >> 32);
+}
+
 __device__ inline void philox4x64_10(uint64_t c[4], uint64_t k0, uint64_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r) { k0 += kW0; k1 += kW1; }
-    const uint64_t hi0 = __umul64hi(kM0, c[0]), lo0 = kM0 * c[0];
-    const uint64_t hi1 = __umul64hi(kM1, c[2]), lo1 = kM1 * c[2];
+    uint64_t hi0, lo0, hi1, lo1;
+    mulhilo<kM0>(c[0], hi0, lo0);
+    mulhilo<kM1>(c[2], hi1, lo1);
     const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
     c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
   }
