@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--row-major-head", action="store_true",
+                    help="run the vocabulary head on the row-major lm_head (no tiled copy)")
     ap.add_argument("--cpu-seqs", type=int, default=16,
                     help="sequences in the CPU-oracle sample")
     ap.add_argument("--sweep", action="store_true")
@@ -108,11 +110,14 @@ def update_bytes(s, batch, n):
 class Rig:
     """Device-resident inputs and outputs of one workload."""
 
-    def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False):
+    def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False,
+                 tiled_head=True):
         self.torch, self.ldr, self.s, self.batch = torch, ldr, shape, batch
         dev = "cuda"
         self.w = synth.make_weights(shape, device=dev)
-        self.dw = ldr.DraftWeights(self.w)
+        # the vocabulary head in the library's tiled layout (a one-time copy of a frozen weight)
+        self.tiled_head = tiled_head and shape.dtype == "bf16" and shape.hidden % 128 == 0
+        self.dw = ldr.DraftWeights(self.w, tiled_head=self.tiled_head)
         self.G = synth.make_G(shape, device=dev)
         self.views = ldr.Views(shape, batch, self.G).init()
         if reuse_chunk:     # the same synthetic rows ingested repeatedly (timing sweeps)
@@ -414,7 +419,7 @@ def main():
 
     wl = synth.WORKLOADS[args.workload]
     s, batch = wl.shape, wl.batch
-    rig = Rig(torch, ldr, synth, s, batch, wl.prefix)
+    rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head)
     ev = ldr.HipEvents()
     costs = launch_costs(s, batch)
     # which launch kind dominates the step (events around every launch, outside the timed run)
@@ -442,7 +447,8 @@ def main():
                 "states; prefix rows ingested through ldr_views_update before timing)",
         "config": {"workload": wl.name, "shape": s.name, "batch": batch, "block": s.block,
                    "prefix": wl.prefix, "rows_per_update": s.block + 1, "temperature": 1.0,
-                   "window": s.window, "summary": s.summary, "draft_layers": s.n_layers},
+                   "window": s.window, "summary": s.summary, "draft_layers": s.n_layers,
+                   "lm_head_layout": "tiled" if rig.tiled_head else "row-major"},
         "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,
                         "p90": percentile(per_step, .9) * 1e3},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
@@ -468,7 +474,8 @@ def sweep(args, torch, ldr, synth):
     res = []
     for batch in [int(x) for x in args.sweep_batch.split(",")]:
         for prefix in [int(x) for x in args.sweep_prefix.split(",")]:
-            rig = Rig(torch, ldr, synth, s, batch, prefix, reuse_chunk=True)
+            rig = Rig(torch, ldr, synth, s, batch, prefix, reuse_chunk=True,
+                      tiled_head=not args.row_major_head)
             wall, per_step, _ = time_steps(torch, rig, args.steps, args.warmup, ev=ev)
             r = {"batch": batch, "prefix": prefix, "us_p50": percentile(per_step, .5) * 1e3,
                  "us_p10": percentile(per_step, .1) * 1e3,

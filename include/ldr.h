@@ -89,6 +89,11 @@ typedef struct ldr_weights {
   const void* final_norm;  /* dev [hidden]                                       */
   const void* lm_head;     /* dev [V][hidden]                                    */
   const ldr_layer_weights* layers; /* host array of n_layers entries            */
+  const void* lm_head_tiled; /* dev, optional: lm_head in the tiled layout of
+                                ldr_tile_matrix (ldr_tiled_bytes(V, hidden)
+                                bytes), bf16 configurations with hidden % 128
+                                == 0 only; NULL: the head reads lm_head. Same
+                                logits up to fp32 summation order. */
 } ldr_weights;
 
 typedef struct ldr_views ldr_views; /* opaque host handle */
@@ -109,6 +114,22 @@ size_t ldr_views_stride_bytes(const ldr_config* cfg);
  * summary values, summary log-normalizers and boundary states (5 entries
  * written to `offsets`). Returns LDR_OK or LDR_EINVAL. */
 int ldr_views_layout(const ldr_config* cfg, size_t offsets[5]);
+
+/* Bytes of a bf16 [rows][cols] matrix in the tiled layout below. */
+size_t ldr_tiled_bytes(int32_t rows, int32_t cols);
+
+/* Enqueues a tiled copy of the row-major bf16 matrix src [rows][cols] (dev,
+ * row stride ld elements) into dst (dev, dst_bytes >= ldr_tiled_bytes):
+ * blocks of 256 rows x 32 columns, block (r / 256, c / 32) at element offset
+ * ((r / 256) * (cols / 32) + c / 32) * 8192 holding its 256 rows of 32
+ * elements one after another; rows from `rows` up to the next multiple of 256
+ * are zero. One K block of 256 weight rows is then one contiguous 16 KB
+ * stretch for the vocabulary head's GEMM (App. B.1 shares the target's head,
+ * V x hidden, so this is a one-time copy of a frozen weight). Needs
+ * cols % 32 == 0, ld >= cols and 16-byte aligned pointers and rows (ld % 8
+ * == 0), else LDR_EINVAL. The caller owns both buffers. */
+int ldr_tile_matrix(const void* src, int32_t rows, int32_t cols, int64_t ld, void* dst,
+                    size_t dst_bytes, void* stream);
 
 /* Workspace bytes ldr_draft_step needs for `batch` sequences. */
 size_t ldr_workspace_bytes(const ldr_config* cfg, int32_t batch);

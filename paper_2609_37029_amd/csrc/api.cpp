@@ -59,7 +59,7 @@ Layout make_layout(const Shape& s) {
 
 // Workspace regions of one draft step for `batch` sequences.
 struct WsPlan {
-  size_t part, x, nrm, qkvb, o, act, rope, bytes;
+  size_t part, x, nrm, qkvb, o, act, rope, nrmt, bytes;
   GemmPlan fc, qkv, wo, gu, down, lm;
 };
 
@@ -84,6 +84,8 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   w.o = off; off = align_up(off + (size_t)M * s.hq * s.d * s.el);
   w.act = off; off = align_up(off + (size_t)M * s.mlp * s.el);
   w.rope = off; off = align_up(off + (size_t)2 * M * (s.d / 2) * 4);
+  // final normalised rows in the tiled layout, for a tiled vocabulary head
+  w.nrmt = off; off = align_up(off + (s.dtype == LDR_BF16 ? tiled_elems(M, s.hidden) * 2 : 0));
   w.bytes = off;
   return w;
 }
@@ -130,6 +132,22 @@ int ldr_views_layout(const ldr_config* cfg, size_t offsets[5]) {
   const Layout L = make_layout(s);
   offsets[0] = L.kw; offsets[1] = L.vw; offsets[2] = L.m; offsets[3] = L.eta; offsets[4] = L.h;
   return LDR_OK;
+}
+
+size_t ldr_tiled_bytes(int32_t rows, int32_t cols) {
+  if (rows <= 0 || cols <= 0 || cols % 32) return 0;
+  return tiled_elems(rows, cols) * 2;
+}
+
+int ldr_tile_matrix(const void* src, int32_t rows, int32_t cols, int64_t ld, void* dst,
+                    size_t dst_bytes, void* stream) {
+  if (!src || !dst || rows <= 0 || cols <= 0 || cols % 32 || ld < cols || ld % 8 ||
+      !aligned(src, 16) || !aligned(dst, 16) || dst_bytes < ldr_tiled_bytes(rows, cols))
+    return LDR_EINVAL;
+  return launch_tile_matrix(src, ld, rows, cols, dst, static_cast<hipStream_t>(stream)) ==
+                 hipSuccess
+             ? LDR_OK
+             : LDR_EHIP;
 }
 
 size_t ldr_workspace_bytes(const ldr_config* cfg, int32_t batch) {
@@ -291,6 +309,10 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
   const int batch = v->batch, M = batch * s.B;
   const WsPlan ws = plan_ws(s, batch);
   if (workspace_bytes < ws.bytes) return LDR_EINVAL;
+  const bool tiled_head = w->lm_head_tiled != nullptr;
+  if (tiled_head && (s.dtype != LDR_BF16 || !aligned(w->lm_head_tiled, 16) ||
+                     !gemm_tiled_supported(M, s.vocab, s.hidden, 1)))
+    return LDR_EINVAL;
   uint8_t* base = static_cast<uint8_t*>(workspace);
   DraftPtrs p;
   p.arena = v->arena; p.pos = v->pos; p.G = v->G; p.status = v->status;
@@ -356,13 +378,19 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         break;
       case LDR_LAUNCH_NEXT_NORM:
         e = launch_resid_norm(s, M, p, ws.down.splits,
-                              j + 1 < s.D ? w->layers[j + 1].in_norm : w->final_norm, st);
+                              j + 1 < s.D ? w->layers[j + 1].in_norm : w->final_norm, st,
+                              j + 1 == s.D && tiled_head ? base + ws.nrmt : nullptr);
         break;
       case LDR_LAUNCH_LM_HEAD:
-        g.A = p.nrm; g.lda = s.hidden; g.W = w->lm_head; g.ldw = s.hidden; g.out = logits;
-        g.ldo = s.vocab; g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden;
-        g.splits = 1;
-        e = launch_gemm(s.dtype, EPI_LOGITS, ws.lm, g, st);
+        g.lda = s.hidden; g.ldw = s.hidden; g.out = logits; g.ldo = s.vocab;
+        g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden; g.splits = 1;
+        if (tiled_head) {
+          g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
+          e = launch_gemm_tiled(g, st);
+        } else {
+          g.A = p.nrm; g.W = w->lm_head;
+          e = launch_gemm(s.dtype, EPI_LOGITS, ws.lm, g, st);
+        }
         break;
       default:
         return LDR_EINVAL;

@@ -234,6 +234,181 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// GEMM on tiled operands (the vocabulary head).
+//
+// Both operands arrive tiled: a [rows][K] matrix is stored as blocks of
+// TR = 256 rows by TK = 32 columns, block (r / TR, k / TK) at
+// ((r / TR) * (K / TK) + k / TK) * TR * TK, its rows contiguous (TK elements
+// each), rows past the matrix padded. One K block of one tile is then 16 KB of
+// consecutive memory that HBM streams at full rate; the same 256 rows read in
+// row-major order are 64-byte pieces 8 KB apart, which it serves at about half.
+//
+// A workgroup of 8 waves owns a 256 x 256 output tile (wave tiles of 128 x 64).
+// Waves 0-3 and 4-7 form two groups that share the four SIMDs pairwise and take
+// turns, one barrier apart: while one group issues its 32 MFMAs for the current
+// K block, the other reads its fragments of that block from LDS and starts the
+// DMA (global_load_lds) of its half of the block D steps ahead: group 0 the A
+// rows, group 1 the W rows. Each SIMD's matrix unit is thus fed by one wave or
+// the other most of the time. Stages of 512 rows x 64 B live in NB = 4 LDS
+// buffers; the 16-byte chunk c of stage row r sits at chunk c ^ ((r >> 2) & 3),
+// so the 16 lanes of a fragment read hit 64 distinct banks.
+//
+// Ordering (t = K block, barriers numbered from the start of the loop):
+//  * group 0 reads block t between barriers 2t and 2t + 1, group 1 between
+//    2t + 1 and 2t + 2; each waits for its own LDS reads before the barrier that
+//    ends its memory phase, so a buffer's last reader is done two barriers
+//    before the DMA that refills it (D = NB - 1) is issued;
+//  * every wave waits for its own DMA of block t + 1 (vmcnt) before barrier
+//    2t + 2, after which block t + 1 is whole in LDS for both groups.
+constexpr int TR = 256, TK = 32;
+constexpr long TBLK = (long)TR * TK;
+
+__device__ inline int tile_swz(int r) { return (r >> 2) & 3; }
+
+template <int N> __device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ inline void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14)); }
+__device__ inline void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+__device__ inline void group_barrier() {
+  sched_fence();
+  __builtin_amdgcn_s_barrier();
+  sched_fence();
+}
+
+#define LDR_GP(p) ((__attribute__((address_space(1))) void*)(p))
+#define LDR_LP(p) ((__attribute__((address_space(3))) void*)(p))
+
+__global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a) {
+  constexpr int NB = 4, D = NB - 1;
+  constexpr int STAGE = 2 * TR * TK * 2;   // bytes: A rows 0..255, W rows 256..511
+  constexpr int MT = 8, NT = 4;            // 16 x 16 MFMA tiles per wave: 128 x 64
+  __shared__ __attribute__((aligned(1024))) uint8_t S0[STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t S1[STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t S2[STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t S3[STAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = wave >> 2, wq = wave & 3;
+  const int wm = grp, wn = wq;   // output rows wm * 128 .., columns wn * 64 ..
+  const int nkb = a.K / TK, kper = nkb / a.splits, kb0 = blockIdx.z * kper;
+  const uint16_t* tile =
+      grp == 0 ? static_cast<const uint16_t*>(a.A) + (long)blockIdx.y * nkb * TBLK
+               : static_cast<const uint16_t*>(a.W) + (long)blockIdx.x * nkb * TBLK;
+  // DMA: wave wq of a group moves rows wq * 64 + q * 16 + lane / 4 of its
+  // operand (4 lanes per 64-byte row, lane & 3 = destination chunk).
+  const uint16_t* src[4];
+  int dst[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = wq * 64 + q * 16 + (lane >> 2);
+    src[q] = tile + (long)kb0 * TBLK + r * TK + (((lane & 3) ^ tile_swz(r)) * 8);
+    dst[q] = (grp * TR + wq * 64 + q * 16) * 64;
+  }
+  // Blocks past the split's end reload its last one (never read).
+  auto issue = [&](uint8_t* buf, int t) {
+    const long off = (long)min(t, kper - 1) * TBLK;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      __builtin_amdgcn_global_load_lds(LDR_GP(src[q] + off), LDR_LP(buf + dst[q]), 16, 0, 0);
+  };
+  int aoff[MT], woff[NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    const int r = wm * 128 + i * 16 + (lane & 15);
+    aoff[i] = r * 64 + (((lane >> 4) ^ tile_swz(r)) * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int r = TR + wn * 64 + j * 16 + (lane & 15);
+    woff[j] = r * 64 + (((lane >> 4) ^ tile_swz(r)) * 16);
+  }
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 af[MT], bfr[NT];
+
+#define LDR_MEM(t, cur, nxt)                                                                   \
+  {                                                                                            \
+    sched_fence();                                                                             \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i) af[i] =                                     \
+        __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + aoff[i]));            \
+    _Pragma("unroll") for (int j = 0; j < NT; ++j) bfr[j] =                                    \
+        __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + woff[j]));            \
+    issue(nxt, (t) + D);                                                                       \
+    sched_fence();                                                                             \
+    wait_lgkmcnt0();                                                                           \
+  }
+#define LDR_MMA()                                                                              \
+  {                                                                                            \
+    sched_fence();                                                                             \
+    __builtin_amdgcn_s_setprio(1);                                                             \
+    _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
+      _Pragma("unroll") for (int j = 0; j < NT; ++j) acc[i][j] =                               \
+          __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);          \
+    __builtin_amdgcn_s_setprio(0);                                                             \
+    sched_fence();                                                                             \
+  }
+#define LDR_G0(t, cur, nxt) { LDR_MEM(t, cur, nxt) group_barrier(); LDR_MMA() wait_vmcnt<4 * (D - 1)>(); group_barrier(); }
+#define LDR_G1(t, cur, nxt) { LDR_MEM(t, cur, nxt) wait_vmcnt<4 * (D - 1)>(); group_barrier(); LDR_MMA() group_barrier(); }
+  issue(S0, 0);
+  issue(S1, 1);
+  issue(S2, 2);
+  wait_vmcnt<0>();
+  group_barrier();
+  if (grp == 0) {
+    for (int t = 0; t < kper; t += NB) {
+      LDR_G0(t, S0, S3) LDR_G0(t + 1, S1, S0) LDR_G0(t + 2, S2, S1) LDR_G0(t + 3, S3, S2)
+    }
+    group_barrier();   // pairs with group 1's offset barrier
+  } else {
+    group_barrier();   // offset: group 1 starts one barrier later
+    for (int t = 0; t < kper; t += NB) {
+      LDR_G1(t, S0, S3) LDR_G1(t + 1, S1, S0) LDR_G1(t + 2, S2, S1) LDR_G1(t + 3, S3, S2)
+    }
+  }
+#undef LDR_G1
+#undef LDR_G0
+#undef LDR_MMA
+#undef LDR_MEM
+  wait_vmcnt<0>();   // no DMA outlives the workgroup
+  const int crow = (lane >> 4) * 4, ccol = lane & 15;
+  float* out = static_cast<float*>(a.out) + (long)blockIdx.z * a.split_stride;
+  const int r0 = blockIdx.y * TR + wm * 128, c0 = blockIdx.x * TR + wn * 64;
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const int col = c0 + j * 16 + ccol;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = r0 + i * 16 + crow + v;
+        if (row < a.M && col < a.N) out[(long)row * a.ldo + col] = acc[i][j][v];
+      }
+    }
+}
+
+// Tiled copy of a row-major [rows][cols] 2-byte matrix: one thread per 16-byte
+// chunk of the destination; padding rows are zero.
+__global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, long ld, int rows,
+                                                          int cols, uint16_t* dst, long chunks) {
+  const int nkb = cols / TK;
+  for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < chunks;
+       e += (long)gridDim.x * blockDim.x) {
+    const long blk = e / (TBLK / 8);
+    const int in = (int)(e % (TBLK / 8));
+    const int r = in / (TK / 8), c = (in % (TK / 8)) * 8;
+    const long row = (blk / nkb) * TR + r;
+    const int col = (int)(blk % nkb) * TK + c;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (row < rows) v = *reinterpret_cast<const u32x4*>(src + row * ld + col);
+    *reinterpret_cast<u32x4*>(dst + e * 8) = v;
+  }
+}
+
 // Tile configurations (cfg): 0: BM 16 (M <= 16) with 4 waves along N (BN 128);
 // 1: BM 32, 2: BM 64, with 8 waves along N (BN 256); 3: BM 256 with 4 x 2 waves
 // of 64 x 64 (BN 128);
@@ -295,6 +470,29 @@ hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a,
   if (epi == EPI_SWIGLU) return launch_cfg<EPI_SWIGLU>(p.cfg, grid, a, st);
   if (epi == EPI_LOGITS) return launch_cfg<EPI_LOGITS>(p.cfg, grid, a, st);
   return launch_cfg<EPI_STORE>(p.cfg, grid, a, st);
+}
+
+bool gemm_tiled_supported(int M, int N, int K, int splits) {
+  return M > 0 && N > 0 && splits > 0 && K % (TK * 4 * splits) == 0;
+}
+
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st) {
+  if (!gemm_tiled_supported(a.M, a.N, a.K, a.splits)) return hipErrorInvalidValue;
+  const dim3 grid((a.N + TR - 1) / TR, (a.M + TR - 1) / TR, a.splits);
+  hipLaunchKernelGGL(gemm_tiled_kernel, grid, dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+size_t tiled_elems(long rows, long cols) { return (size_t)((rows + TR - 1) / TR) * TR * cols; }
+
+hipError_t launch_tile_matrix(const void* src, long ld, int rows, int cols, void* dst,
+                              hipStream_t st) {
+  const long chunks = (long)tiled_elems(rows, cols) / 8;
+  const long want = (chunks + 255) / 256, blocks = want < 8192 ? want : 8192;
+  hipLaunchKernelGGL(tile_matrix_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                     static_cast<const uint16_t*>(src), ld, rows, cols,
+                     static_cast<uint16_t*>(dst), chunks);
+  return hipGetLastError();
 }
 
 }  // namespace ldr

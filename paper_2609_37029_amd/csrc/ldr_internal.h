@@ -113,6 +113,15 @@ struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile con
 // Tile configuration and split-K factor; splits = 1 unless allow_split.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
+// bf16 GEMM on operands in the tiled layout of ldr_tile_matrix (A tiled over
+// its M rows, W over its N rows); fp32 out [splits][M][ldo]. Needs
+// K % (128 * splits) == 0.
+bool gemm_tiled_supported(int M, int N, int K, int splits);
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st);
+// Elements of a [rows][cols] matrix in the tiled layout (rows padded to 256).
+size_t tiled_elems(long rows, long cols);
+hipError_t launch_tile_matrix(const void* src, long ld, int rows, int cols, void* dst,
+                              hipStream_t st);
 
 // Draft step pieces (draft.hip)
 struct DraftPtrs {
@@ -146,8 +155,9 @@ bool attention_mfma_supported(int d, int rep, int B, int R, int W);
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st);
 bool norm_hidden_supported(int hidden);
+// tiled_out: write the normalised rows there in the tiled layout instead of to p.nrm.
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
-                             const void* gain, hipStream_t st);
+                             const void* gain, hipStream_t st, void* tiled_out = nullptr);
 hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const ldr_layer_weights* lw, hipStream_t st);
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,

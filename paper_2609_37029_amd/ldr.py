@@ -44,7 +44,7 @@ class LayerWeights(ctypes.Structure):
 
 class Weights(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in TOP_KEYS] + [
-        ("layers", ctypes.POINTER(LayerWeights))]
+        ("layers", ctypes.POINTER(LayerWeights)), ("lm_head_tiled", ctypes.c_void_p)]
 
 
 _LIB = None
@@ -65,6 +65,8 @@ def _lib():
             "ldr_views_stride_bytes": (SZ, [CP]),
             "ldr_views_layout": (ctypes.c_int, [CP, ctypes.POINTER(SZ)]),
             "ldr_workspace_bytes": (SZ, [CP, I32]),
+            "ldr_tiled_bytes": (SZ, [I32, I32]),
+            "ldr_tile_matrix": (ctypes.c_int, [P, I32, I32, I64, P, SZ, P]),
             "ldr_config_check": (ctypes.c_int, [CP]),
             "ldr_views_init": (ctypes.c_int, [ctypes.POINTER(P), CP, I32, P, P, P, P, I32, P, P,
                                               P, P]),
@@ -209,18 +211,35 @@ class Views:
             pass
 
 
-class DraftWeights:
-    """ldr_weights over a synth weight dict of device tensors (kept alive here)."""
+def tiled_bytes(rows: int, cols: int) -> int:
+    return _lib().ldr_tiled_bytes(rows, cols)
 
-    def __init__(self, w: Dict):
+
+def tile_matrix(m: torch.Tensor, stream=None) -> torch.Tensor:
+    """ldr_tile_matrix of a row-major bf16 [rows][cols] device tensor: a flat
+    bf16 tensor in the library's 256 x 32 tiled layout."""
+    rows, cols = m.shape
+    out = torch.empty(tiled_bytes(rows, cols) // 2, dtype=torch.bfloat16, device=m.device)
+    _check(_lib().ldr_tile_matrix(_ptr(m), rows, cols, m.stride(0), _ptr(out),
+                                  out.numel() * 2, _stream(stream)), "ldr_tile_matrix")
+    return out
+
+
+class DraftWeights:
+    """ldr_weights over a synth weight dict of device tensors (kept alive here).
+    tiled_head: also give the library a tiled copy of the vocabulary head."""
+
+    def __init__(self, w: Dict, tiled_head: bool = False):
         self.w = w
         n = len(w["layers"])
         self._layers = (LayerWeights * n)()
         for j, L in enumerate(w["layers"]):
             for k in LAYER_KEYS:
                 setattr(self._layers[j], k, L[k].data_ptr())
+        self.head_tiled = tile_matrix(w["lm_head"]) if tiled_head else None
         self.c = Weights(*[w[k].data_ptr() for k in TOP_KEYS],
-                         ctypes.cast(self._layers, ctypes.POINTER(LayerWeights)))
+                         ctypes.cast(self._layers, ctypes.POINTER(LayerWeights)),
+                         None if self.head_tiled is None else self.head_tiled.data_ptr())
 
 
 def draft_step(views: Views, weights: DraftWeights, anchor: torch.Tensor,

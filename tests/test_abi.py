@@ -104,3 +104,22 @@ def test_draft_step_launch_sequence():
         layer = ["qkv_gemm", "qkv_finish", "attention", "o_gemm", "post_norm", "gate_up_gemm",
                  "down_gemm", "next_norm"]
         assert kinds == ["fc_gemm", "slot_init"] + layer * shape.n_layers + ["lm_head"]
+
+
+def test_tiled_layout_sizes_and_validation(L):
+    """ldr_tiled_bytes: rows padded to 256, columns in blocks of 32; bad
+    arguments of ldr_tile_matrix are rejected on the host."""
+    lib = L.lib()
+    assert lib.ldr_tiled_bytes(1, 32) == 256 * 32 * 2
+    assert lib.ldr_tiled_bytes(300, 96) == 512 * 96 * 2
+    assert lib.ldr_tiled_bytes(151936, 4096) == 594 * 256 * 4096 * 2
+    assert lib.ldr_tiled_bytes(256, 48) == 0 and lib.ldr_tiled_bytes(0, 32) == 0
+    fake = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced: validation fails first
+    n = lib.ldr_tiled_bytes(256, 64)
+    assert lib.ldr_tile_matrix(None, 256, 64, 64, fake, n, None) == L.LDR_EINVAL
+    assert lib.ldr_tile_matrix(fake, 256, 48, 48, fake, n, None) == L.LDR_EINVAL     # cols % 32
+    assert lib.ldr_tile_matrix(fake, 256, 64, 60, fake, n, None) == L.LDR_EINVAL     # ld < cols
+    assert lib.ldr_tile_matrix(fake, 256, 64, 68, fake, n, None) == L.LDR_EINVAL     # ld % 8
+    assert lib.ldr_tile_matrix(fake, 256, 64, 64, fake, n - 2, None) == L.LDR_EINVAL  # too small
+    assert lib.ldr_tile_matrix(ctypes.c_void_p((1 << 20) + 8), 256, 64, 64, fake, n, None) == \
+        L.LDR_EINVAL                                                                  # alignment

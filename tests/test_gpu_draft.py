@@ -17,7 +17,7 @@ MINI_BF16 = synth.QWEN3_8B.replace(name="mini-bf16", hidden=512, n_q_heads=8, n_
                                    window=64)
 
 
-def setup(gpu_lib, shape, batch, prefix, gain_std=0.1, decode=3):
+def setup(gpu_lib, shape, batch, prefix, gain_std=0.1, decode=3, tiled_head=False):
     G = synth.make_G(shape, device="cuda")
     p = Pair(gpu_lib, shape, batch, G)
     if prefix:
@@ -25,7 +25,7 @@ def setup(gpu_lib, shape, batch, prefix, gain_std=0.1, decode=3):
     if decode:
         p.decode(decode, shape.block + 1, np.random.default_rng(7))
     w = synth.make_weights(shape, gain_std=gain_std, device="cuda")
-    dw = gpu_lib.DraftWeights(w)
+    dw = gpu_lib.DraftWeights(w, tiled_head=tiled_head)
     anchor = synth.make_anchors(shape, batch, device="cuda")
     return p, w, dw, anchor
 
@@ -51,6 +51,53 @@ def test_logits_match_oracle(gpu_lib, shape, batch, prefix):
     zc = z.cpu().numpy()
     for b in p.seqs:
         check_logits(zc[b], ref[b], shape)
+
+
+@pytest.mark.parametrize("batch,prefix", [(3, 300), (17, 150)])
+def test_tiled_head_matches_oracle_and_row_major(gpu_lib, batch, prefix):
+    """The vocabulary head on the tiled copy of lm_head (ldr_tile_matrix):
+    logits against the oracle, and against the row-major head, from which they
+    differ only in the fp32 summation order of the same bf16 products. 17
+    sequences: 272 rows, two M tiles, the last ragged; V = 5003: a ragged N
+    tile."""
+    s = MINI_BF16
+    p, w, dw, anchor = setup(gpu_lib, s, batch, prefix, tiled_head=True)
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    z_rm = gpu_lib.draft_step(p.views, gpu_lib.DraftWeights(w), anchor)
+    torch.cuda.synchronize()
+    ref = oracle_logits(p, w, anchor)
+    zc = z.cpu().numpy()
+    for b in p.seqs:
+        check_logits(zc[b], ref[b], s)
+    scale = z_rm.abs().amax(dim=-1, keepdim=True)
+    assert ((z - z_rm).abs() / scale).max().item() <= 1e-4
+
+
+def test_tile_matrix_layout(gpu_lib):
+    """ldr_tile_matrix: block (r / 256, c / 32) holds its 256 rows of 32
+    elements contiguously, padding rows zero; bit-exact (a pure copy)."""
+    rows, cols, ld = 300, 96, 104
+    g = torch.Generator(device="cuda").manual_seed(5)
+    base = torch.randn(rows, ld, device="cuda", generator=g).to(torch.bfloat16)
+    m = base[:, :cols]
+    t = gpu_lib.tile_matrix(m)
+    assert t.numel() * 2 == gpu_lib.tiled_bytes(rows, cols) == 512 * cols * 2
+    pad = torch.zeros(512, cols, dtype=torch.bfloat16, device="cuda")
+    pad[:rows] = m
+    ref = pad.view(2, 256, cols // 32, 32).permute(0, 2, 1, 3).reshape(-1)
+    torch.cuda.synchronize()
+    assert torch.equal(t.view(torch.int16), ref.view(torch.int16))
+
+
+def test_tiled_head_rejected_where_unsupported(gpu_lib):
+    # fp32 configurations have no tiled head
+    p, w, dw, anchor = setup(gpu_lib, synth.TINY, 1, 40, decode=0)
+    fake = torch.zeros(gpu_lib.tiled_bytes(synth.TINY.vocab, synth.TINY.hidden) // 2,
+                       dtype=torch.bfloat16, device="cuda")
+    dw.c.lm_head_tiled = fake.data_ptr()
+    with pytest.raises(gpu_lib.LdrError) as e:
+        gpu_lib.draft_step(p.views, dw, anchor)
+    assert e.value.code == gpu_lib.LDR_EINVAL
 
 
 @pytest.mark.parametrize("shape", [synth.TINY, MINI_BF16])
@@ -88,10 +135,11 @@ def test_deterministic_and_depends_only_on_views(gpu_lib):
 
 
 @pytest.mark.slow
-def test_full_size_qwen3_8b_sampled(gpu_lib):
+@pytest.mark.parametrize("tiled_head", [True, False])
+def test_full_size_qwen3_8b_sampled(gpu_lib, tiled_head):
     """Qwen3-8B shape, batch 16, prefix 32768: the configuration the benchmark
-    times. Oracle on two sequences, all 16 slots, a 2048-token vocabulary
-    sample."""
+    times (tiled head). Oracle on two sequences, all 16 slots, a 2048-token
+    vocabulary sample."""
     s = synth.QWEN3_8B
     G = synth.make_G(s, device="cuda")
     p = Pair(gpu_lib, s, 16, G, oracle_seqs=[0, 11])
@@ -99,7 +147,7 @@ def test_full_size_qwen3_8b_sampled(gpu_lib):
     K, V, h = synth.decode_rows(s, 16, 17, 0, device="cuda")
     p.ingest([17] * 16, K, V, h)
     w = synth.make_weights(s, device="cuda")
-    dw = gpu_lib.DraftWeights(w)
+    dw = gpu_lib.DraftWeights(w, tiled_head=tiled_head)
     anchor = synth.make_anchors(s, 16, device="cuda")
     z = gpu_lib.draft_step(p.views, dw, anchor)
     torch.cuda.synchronize()
