@@ -27,23 +27,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int KC = 32;  // keys per chunk
 constexpr int QR = 16;  // query rows per wave (block slots, zero-padded)
 
-// Reductions over the 16 lanes of a row group with DPP lane swaps: quad
-// permutations (xor 1, xor 2), then half-row and row mirrors, which pair each
-// lane with one of the other half; every lane ends with the same value.
-__device__ inline float sum16(float v) {
-  v += dpp<0xB1>(v);   // quad_perm [1, 0, 3, 2]
-  v += dpp<0x4E>(v);   // quad_perm [2, 3, 0, 1]
-  v += dpp<0x141>(v);  // row_half_mirror
-  v += dpp<0x140>(v);  // row_mirror
-  return v;
-}
-__device__ inline float max16(float v) {
-  v = fmaxf(v, dpp<0xB1>(v));
-  v = fmaxf(v, dpp<0x4E>(v));
-  v = fmaxf(v, dpp<0x141>(v));
-  v = fmaxf(v, dpp<0x140>(v));
-  return v;
-}
 __device__ inline float sum64(float v) {
   for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
   return v;

@@ -50,6 +50,24 @@ template <int CTRL> __device__ inline float dpp(float v) {
 #endif
 }
 
+// Reductions over the 16 lanes of a row group with DPP lane swaps: quad
+// permutations (xor 1, xor 2), then half-row and row mirrors, which pair each
+// lane with one of the other half; every lane ends with the same value.
+__device__ inline float sum16(float v) {
+  v += dpp<0xB1>(v);   // quad_perm [1, 0, 3, 2]
+  v += dpp<0x4E>(v);   // quad_perm [2, 3, 0, 1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  return v;
+}
+__device__ inline float max16(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  return v;
+}
+
 // Round to nearest even (the device uses the gfx950 conversion instruction).
 __host__ __device__ inline uint16_t f32_to_bf16(float f) {
 #if defined(__HIP_DEVICE_COMPILE__)

@@ -61,6 +61,20 @@ __device__ inline void copy16(void* dst, const void* src, int idx) {
   reinterpret_cast<uint4*>(dst)[idx] = reinterpret_cast<const uint4*>(src)[idx];
 }
 
+// This workgroup's slice of the boundary-state copy (the D * H_kv workgroups
+// of a sequence share it).
+template <typename T>
+__device__ inline void boundary_slice(const UpdateArgs& a, uint8_t* seq, int j, int g, int b,
+                                      int nthreads) {
+  const int chunks = a.hb_elems * (int)sizeof(T) / 16;
+  const int wgs = a.D * a.hkv, wid = j * a.hkv + g;
+  const int per = (chunks + wgs - 1) / wgs;
+  const int c0 = wid * per, c1 = min(chunks, c0 + per);
+  T* hdst = reinterpret_cast<T*>(seq + a.h);
+  const T* hsrc = reinterpret_cast<const T*>(a.h_new) + (size_t)b * a.hb_elems;
+  for (int c = c0 + (int)threadIdx.x; c < c1; c += nthreads) copy16(hdst, hsrc, c);
+}
+
 // DPT: dims of the head each thread owns; TPQ = d / DPT threads share one
 // summary query, Q = rep * R queries per workgroup, Q * TPQ = kThreads.
 template <typename T, int DPT>
@@ -102,16 +116,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
     }
   }
 
-  // ---- boundary states: this workgroup's slice ----------------------------
-  {
-    const int chunks = a.hb_elems * (int)sizeof(T) / 16;
-    const int wgs = a.D * a.hkv, wid = j * a.hkv + g;
-    const int per = (chunks + wgs - 1) / wgs;
-    const int c0 = wid * per, c1 = min(chunks, c0 + per);
-    T* hdst = reinterpret_cast<T*>(seq + a.h);
-    const T* hsrc = reinterpret_cast<const T*>(a.h_new) + (size_t)b * a.hb_elems;
-    for (int c = c0 + threadIdx.x; c < c1; c += kThreads) copy16(hdst, hsrc, c);
-  }
+  boundary_slice<T>(a, seq, j, g, b, kThreads);
 
   // ---- rows of the new set N, tile by tile: window ring write of the last
   // min(n, W) rows (slot (t + r) mod W) and the tiled online log-sum-exp ----
@@ -218,6 +223,170 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
   if (part == 0) *etaq = eta;
 }
 
+// bf16 path on the matrix cores (v_mfma_f32_16x16x32_bf16). One wave per 16
+// summary queries of the group (NW = rep * R / 16 waves); per tile of up to 32
+// new rows, K rows (row-major) and V^T go to LDS as bf16, then
+//  * S = G K^T on the matrix cores: bf16 products are exact in fp32 and the
+//    sums are fp32, as on the vector path;
+//  * the online log-sum-exp per query in fp32 (row max and sum over the 16
+//    lanes of a C-layout row group with DPP);
+//  * O += P V with P split into two bf16 terms, hi = bf16(P) and
+//    lo = bf16(P - hi), so P enters with a relative error near 2^-17 rather
+//    than bf16's 2^-9 (two MFMAs per tile instead of one);
+// then the merge of Eq. 11 with the stored (eta, m), as on the vector path.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ inline bf16x8 frag8(const uint16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+}
+__device__ inline void wave_lds_fence() {
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+template <int DH, int NW>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3)))
+views_update_mfma_kernel(UpdateArgs a) {
+  constexpr int KT = 32, KS = DH / 32, NT = DH / 16, NTH = NW * 64;
+  constexpr int KLD = DH + 8, VLD = KT + 8;   // padded LDS rows (elements)
+  __shared__ __attribute__((aligned(16))) uint16_t Kt[KT * KLD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[DH * VLD];
+  __shared__ __attribute__((aligned(16))) uint16_t Pt[NW][2][16 * VLD];
+  const int g = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int n = a.n_new[b];
+  if (n <= 0 || n > a.max_new) return;  // empty set: identity; bad count: commit flags it
+  const int64_t t = a.pos[b];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  uint8_t* seq = a.arena + (size_t)b * a.stride;
+
+  // the wave's queries: rows q0 .. q0 + 15 of G, M and eta (C layout: this
+  // lane holds rows q0 + lg * 4 + v, dims dt * 16 + lr)
+  const size_t q0 = ((size_t)j * a.hq + (size_t)g * a.rep) * a.R + (size_t)wave * 16;
+  float* Mq = reinterpret_cast<float*>(seq + a.m) + q0 * DH;
+  float* etaq = reinterpret_cast<float*>(seq + a.eta) + q0;
+  float ma[NT][4], eta_a[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    eta_a[v] = etaq[lg * 4 + v];
+#pragma unroll
+    for (int dt = 0; dt < NT; ++dt) ma[dt][v] = Mq[(size_t)(lg * 4 + v) * DH + dt * 16 + lr];
+  }
+  bf16x8 gf[KS];   // A layout: query row lr, dims ks * 32 + lg * 8 ..
+  {
+    const uint16_t* Gq = static_cast<const uint16_t*>(a.G) + (q0 + lr) * DH + lg * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) gf[ks] = frag8(Gq + ks * 32);
+  }
+
+  boundary_slice<uint16_t>(a, seq, j, g, b, NTH);
+
+  uint16_t* Kw = reinterpret_cast<uint16_t*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * DH;
+  uint16_t* Vw = reinterpret_cast<uint16_t*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * DH;
+  const uint16_t* Kn = static_cast<const uint16_t*>(a.K_new);
+  const uint16_t* Vn = static_cast<const uint16_t*>(a.V_new);
+  f32x4 o[NT];
+#pragma unroll
+  for (int dt = 0; dt < NT; ++dt) o[dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m[4], l[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) { m[v] = -INFINITY; l[v] = 0.f; }
+
+  for (int r0 = 0; r0 < n; r0 += KT) {
+    const int nr = min(KT, n - r0);
+    __syncthreads();   // the previous tile's LDS reads are done
+    // stage the tile (rows past nr as zeros) and ring-write the K rows that survive
+    for (int i = tid; i < KT * (DH / 8); i += NTH) {
+      const int r = i / (DH / 8), c8 = (i % (DH / 8)) * 8;
+      u32x4 kv = u32x4{0u, 0u, 0u, 0u}, vv = kv;
+      if (r < nr) {
+        const size_t src = ((((size_t)b * a.max_new + r0 + r) * a.D + j) * a.hkv + g) * DH + c8;
+        kv = *reinterpret_cast<const u32x4*>(Kn + src);
+        vv = *reinterpret_cast<const u32x4*>(Vn + src);
+        if (r0 + r >= n - a.W) {
+          const size_t slot = (size_t)((t + r0 + r) % a.W);
+          *reinterpret_cast<u32x4*>(Kw + slot * DH + c8) = kv;
+        }
+      }
+      *reinterpret_cast<u32x4*>(&Kt[r * KLD + c8]) = kv;
+      const uint16_t* vp = reinterpret_cast<const uint16_t*>(&vv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(c8 + e) * VLD + r] = vp[e];
+    }
+    __syncthreads();
+    {  // window V^T: lanes take consecutive rows of one dim (contiguous slots)
+      const int rs = max(0, n - a.W - r0);
+      const int r = tid % KT;
+      if (r >= rs && r < nr) {
+        const size_t slot = (size_t)((t + r0 + r) % a.W);
+        for (int e = tid / KT; e < DH; e += NTH / KT) Vw[(size_t)e * a.W + slot] = Vt[e * VLD + r];
+      }
+    }
+    // scores of keys nt * 16 + lr (C layout), scaled; keys past nr masked
+    f32x4 sc[2];
+#pragma unroll
+    for (int nt = 0; nt < 2; ++nt) {
+      sc[nt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        sc[nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            gf[ks], frag8(&Kt[(nt * 16 + lr) * KLD + ks * 32 + lg * 8]), sc[nt], 0, 0, 0);
+    }
+    uint16_t* Ph = Pt[wave][0];
+    uint16_t* Pl = Pt[wave][1];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const float x0 = lr < nr ? sc[0][v] * a.inv_sqrt_d : -INFINITY;
+      const float x1 = 16 + lr < nr ? sc[1][v] * a.inv_sqrt_d : -INFINITY;
+      const float mn = fmaxf(m[v], max16(fmaxf(x0, x1)));
+      const float alpha = expf(m[v] - mn);   // m = -inf on the first tile: 0
+      const float p0 = expf(x0 - mn), p1 = expf(x1 - mn);
+      l[v] = l[v] * alpha + sum16(p0 + p1);
+      m[v] = mn;
+#pragma unroll
+      for (int dt = 0; dt < NT; ++dt) o[dt][v] *= alpha;
+      const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
+      const int row = (lg * 4 + v) * VLD;
+      Ph[row + lr] = h0;
+      Ph[row + 16 + lr] = h1;
+      Pl[row + lr] = f32_to_bf16(p0 - bf16_to_f32(h0));
+      Pl[row + 16 + lr] = f32_to_bf16(p1 - bf16_to_f32(h1));
+    }
+    wave_lds_fence();
+    const bf16x8 phi = frag8(&Ph[lr * VLD + lg * 8]);
+    const bf16x8 plo = frag8(&Pl[lr * VLD + lg * 8]);
+#pragma unroll
+    for (int dt = 0; dt < NT; ++dt) {
+      const bf16x8 vf = frag8(&Vt[(dt * 16 + lr) * VLD + lg * 8]);
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(phi, vf, o[dt], 0, 0, 0);
+      o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vf, o[dt], 0, 0, 0);
+    }
+  }
+  // eta_N = m + log l, m_N = O / l, merged with (eta_A, m_A) (Eq. 11)
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const float eta_n = m[v] + logf(l[v]);
+    const float inv_l = 1.f / l[v];
+    float wa, wn, e;
+    if (eta_a[v] == -INFINITY) {  // empty A: the merge returns N
+      wa = 0.f; wn = inv_l; e = eta_n;
+    } else {
+      const float mu = fmaxf(eta_a[v], eta_n);
+      e = mu + logf(expf(eta_a[v] - mu) + expf(eta_n - mu));
+      wa = expf(eta_a[v] - e);
+      wn = expf(eta_n - e) * inv_l;
+    }
+#pragma unroll
+    for (int dt = 0; dt < NT; ++dt) {
+      const float mav = wa != 0.f ? ma[dt][v] : 0.f;
+      Mq[(size_t)(lg * 4 + v) * DH + dt * 16 + lr] = wa * mav + wn * o[dt][v];
+    }
+    if (lr == 0) etaq[lg * 4 + v] = e;
+  }
+}
+
 __global__ void views_commit_kernel(int batch, int64_t* pos, const int32_t* n_new,
                                     int max_new, int32_t* status) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -278,6 +447,17 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
   a.hb_elems = s.Lb * s.hidden;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const dim3 grid(s.hkv, s.D, batch);
+  const int q = s.rep * s.R;
+  if (s.dtype == LDR_BF16 && (s.d == 64 || s.d == 128) && q % 16 == 0) {
+    const int nw = q / 16;
+#define LDR_VU(DH, NW) \
+  if (s.d == DH && nw == NW) { \
+    hipLaunchKernelGGL((views_update_mfma_kernel<DH, NW>), grid, dim3(NW * 64), 0, st, a); \
+    return hipGetLastError(); \
+  }
+    LDR_VU(128, 4) LDR_VU(128, 2) LDR_VU(128, 8) LDR_VU(64, 4) LDR_VU(64, 2) LDR_VU(64, 8)
+#undef LDR_VU
+  }
   const int dpt = views_dims_per_thread(s);
   return s.dtype == LDR_BF16 ? launch_update_t<uint16_t>(a, dpt, grid, st)
                              : launch_update_t<float>(a, dpt, grid, st);
