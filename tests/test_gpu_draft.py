@@ -53,14 +53,19 @@ def test_logits_match_oracle(gpu_lib, shape, batch, prefix):
         check_logits(zc[b], ref[b], shape)
 
 
-@pytest.mark.parametrize("batch,prefix", [(3, 300), (17, 150)])
-def test_tiled_head_matches_oracle_and_row_major(gpu_lib, batch, prefix):
+# 66536 tokens: 260 column tiles of 256, more than one round over the 256 CUs
+MINI_BF16_WIDE_V = MINI_BF16.replace(name="mini-bf16-v66536", vocab=66536)
+
+
+@pytest.mark.parametrize("shape,batch,prefix", [(MINI_BF16, 3, 300), (MINI_BF16, 17, 150),
+                                                (MINI_BF16_WIDE_V, 3, 200)])
+def test_tiled_head_matches_oracle_and_row_major(gpu_lib, shape, batch, prefix):
     """The vocabulary head on the tiled copy of lm_head (ldr_tile_matrix):
     logits against the oracle, and against the row-major head, from which they
     differ only in the fp32 summation order of the same bf16 products. 17
     sequences: 272 rows, two M tiles, the last ragged; V = 5003: a ragged N
-    tile."""
-    s = MINI_BF16
+    tile; V = 66536: 260 tiles, more workgroups than CUs."""
+    s = shape
     p, w, dw, anchor = setup(gpu_lib, s, batch, prefix, tiled_head=True)
     z = gpu_lib.draft_step(p.views, dw, anchor)
     z_rm = gpu_lib.draft_step(p.views, gpu_lib.DraftWeights(w), anchor)
