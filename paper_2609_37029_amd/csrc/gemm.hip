@@ -44,20 +44,20 @@ __device__ inline int swiglu_row(int c, int mlp) {
 
 __device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
 
-template <int MTW, int NTW, int WM, int WN, int EPI>
-__global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
+// acc = A[m0 .., kbeg .. kbeg + nk BK) . W[n0 .., same]^T for one BM x BN tile
+// (SWI: W rows in the interleaved gate/up order), through the LDS buffers
+// As / Ws of the calling kernel. nk even (two steps per loop pass).
+template <int MTW, int NTW, int WM, int WN, bool SWI>
+__device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int kbeg, int nk,
+                                         uint16_t (&As)[2][WM * MTW * 16 * LDK],
+                                         uint16_t (&Ws)[2][WN * NTW * 16 * LDK],
+                                         f32x4 (&acc)[MTW][NTW]) {
   constexpr int NTHR = WM * WN * 64, TM = MTW * 16, TN = NTW * 16;
   constexpr int BM = WM * TM, BN = WN * TN;
   constexpr int ACH = BM * (BK / 8), WCH = BN * (BK / 8);   // 16-byte chunks per stage
   constexpr int AL = (ACH + NTHR - 1) / NTHR, WL = (WCH + NTHR - 1) / NTHR;
-  static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDK];
-
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, z = blockIdx.z;
-  const int kper = a.K / a.splits, kbeg = z * kper, nk = kper / BK;
   const uint16_t* A = static_cast<const uint16_t*>(a.A);
   const uint16_t* W = static_cast<const uint16_t*>(a.W);
 
@@ -76,7 +76,7 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
   for (int i = 0; i < WL; ++i) {
     const int c = (tid + i * NTHR) % WCH, row = c >> 3, col = (c & 7) * 8;
     const int gn = min(n0 + row, a.N - 1);
-    const int wrow = EPI == EPI_SWIGLU ? swiglu_row(gn, a.mlp) : gn;
+    const int wrow = SWI ? swiglu_row(gn, a.mlp) : gn;
     wsrc[i] = W + (long)wrow * a.ldw + kbeg + col;
     wdst[i] = row * LDK + col;
   }
@@ -85,12 +85,10 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
   // kt + 2 (roles swap every step). Constant indices only: registers.
   u32x4 wq[WPF][WL];
   u32x4 a0[AL], a1[AL];
-  f32x4 acc[MTW][NTW];
 #pragma unroll
   for (int i = 0; i < MTW; ++i)
 #pragma unroll
     for (int j = 0; j < NTW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
 #define LDR_LOAD(dst, src, kt) dst = *reinterpret_cast<const u32x4*>((src) + (kt) * BK)
 #define LDR_STORE(buf_arr, off, v) *reinterpret_cast<u32x4*>(&buf_arr[off]) = (v)
   // One K step: MFMAs on LDS buffer `buf` while stage kt + 2 of A and step
@@ -146,7 +144,16 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
 #undef LDR_STEP
 #undef LDR_STORE
 #undef LDR_LOAD
+}
 
+// Stores one tile's accumulators: EPI_STORE / EPI_LOGITS fp32 (split z at
+// z * split_stride), EPI_SWIGLU silu(gate) * up in the activation dtype.
+template <int MTW, int NTW, int WM, int WN, int EPI>
+__device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, int z,
+                                           const f32x4 (&acc)[MTW][NTW]) {
+  constexpr int TM = MTW * 16, TN = NTW * 16;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
   // C layout of a 16x16 tile: lane holds rows (lane/16)*4 + v, column lane%16.
   const int crow = (lane >> 4) * 4, ccol = lane & 15;
   if constexpr (EPI == EPI_STORE || EPI == EPI_LOGITS) {
@@ -177,6 +184,19 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
         }
     }
   }
+}
+
+template <int MTW, int NTW, int WM, int WN, int EPI>
+__global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
+  constexpr int BM = WM * MTW * 16, BN = WN * NTW * 16;
+  static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
+  __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDK];
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, z = blockIdx.z;
+  const int kper = a.K / a.splits, kbeg = z * kper, nk = kper / BK;
+  f32x4 acc[MTW][NTW];
+  tile_mma<MTW, NTW, WM, WN, EPI == EPI_SWIGLU>(a, n0, m0, kbeg, nk, As, Ws, acc);
+  store_tile<MTW, NTW, WM, WN, EPI>(a, n0, m0, z, acc);
 }
 
 // fp32 SIMT tile: 32 x 64 outputs per 256 threads, each 2 rows x 4 columns
@@ -413,7 +433,10 @@ __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, l
 // 1: BM 32, 2: BM 64, with 8 waves along N (BN 256); 3: BM 256 with 4 x 2 waves
 // of 64 x 64 (BN 128);
 // 4: BM 256 with 8 x 1 waves of 32 x 96 (BN 96), for the SwiGLU GEMM, whose
-// 2 x 12288 columns at the Qwen3-8B shape make exactly 256 tiles (one per CU).
+// 2 x 12288 columns at the Qwen3-8B shape make exactly 256 tiles (one per CU);
+// 5: BM 256 with 4 x 2 waves of 64 x 32 (BN 64), in place of cfg 3 when cfg 3
+// would split K eight ways into pieces of at most 512: as fast there (the O
+// projection) with half the split-K partials for the next kernel to read.
 template <int EPI>
 hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
   switch (cfg) {
@@ -421,6 +444,7 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
     case 1: hipLaunchKernelGGL((gemm_kernel<2, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 2: hipLaunchKernelGGL((gemm_kernel<4, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 4: hipLaunchKernelGGL((gemm_kernel<2, 6, 8, 1, EPI>), grid, dim3(512), 0, st, a); break;
+    case 5: hipLaunchKernelGGL((gemm_kernel<4, 2, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -439,8 +463,13 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
     p.cfg = -1; bm = 32; bn = 64; kstep = 16;
   } else {
     p.cfg = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : swiglu ? 4 : 3;
+    if (p.cfg == 3 && allow_split) {
+      const int t128 = ((N + 127) / 128) * ((M + 255) / 256);
+      if (t128 * 8 <= kCUs && t128 * 16 > kCUs && K / 8 <= 512 && K % (4 * 2 * 2 * BK) == 0)
+        p.cfg = 5;
+    }
     bm = p.cfg >= 3 ? 256 : 16 << p.cfg;
-    bn = p.cfg == 4 ? 96 : (p.cfg == 3 || p.cfg == 0) ? 128 : 256;
+    bn = p.cfg == 5 ? 64 : p.cfg == 4 ? 96 : (p.cfg == 3 || p.cfg == 0) ? 128 : 256;
     kstep = 2 * BK;
   }
   p.ntw = 0;
