@@ -92,8 +92,10 @@ typedef struct ldr_weights {
   const void* lm_head_tiled; /* dev, optional: lm_head in the tiled layout of
                                 ldr_tile_matrix (ldr_tiled_bytes(V, hidden)
                                 bytes), bf16 configurations with hidden % 128
-                                == 0 only; NULL: the head reads lm_head. Same
-                                logits up to fp32 summation order. */
+                                == 0 only; read when batch * B > 64 (smaller
+                                steps use lm_head); NULL: the head always reads
+                                lm_head. Same logits up to fp32 summation
+                                order. */
 } ldr_weights;
 
 typedef struct ldr_views ldr_views; /* opaque host handle */

@@ -309,10 +309,12 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
   const int batch = v->batch, M = batch * s.B;
   const WsPlan ws = plan_ws(s, batch);
   if (workspace_bytes < ws.bytes) return LDR_EINVAL;
-  const bool tiled_head = w->lm_head_tiled != nullptr;
-  if (tiled_head && (s.dtype != LDR_BF16 || !aligned(w->lm_head_tiled, 16) ||
-                     !gemm_tiled_supported(M, s.vocab, s.hidden, 1)))
+  if (w->lm_head_tiled && (s.dtype != LDR_BF16 || !aligned(w->lm_head_tiled, 16) ||
+                           !gemm_tiled_supported(M, s.vocab, s.hidden, 1)))
     return LDR_EINVAL;
+  // The tiled head computes 256-row tiles: below 65 rows the row-major head's
+  // 16- to 64-row tiles stream the same weights with less MFMA work.
+  const bool tiled_head = w->lm_head_tiled != nullptr && M > 64;
   uint8_t* base = static_cast<uint8_t*>(workspace);
   DraftPtrs p;
   p.arena = v->arena; p.pos = v->pos; p.G = v->G; p.status = v->status;

@@ -57,14 +57,15 @@ def test_logits_match_oracle(gpu_lib, shape, batch, prefix):
 MINI_BF16_WIDE_V = MINI_BF16.replace(name="mini-bf16-v66536", vocab=66536)
 
 
-@pytest.mark.parametrize("shape,batch,prefix", [(MINI_BF16, 3, 300), (MINI_BF16, 17, 150),
-                                                (MINI_BF16_WIDE_V, 3, 200)])
+@pytest.mark.parametrize("shape,batch,prefix", [(MINI_BF16, 5, 300), (MINI_BF16, 17, 150),
+                                                (MINI_BF16_WIDE_V, 5, 200)])
 def test_tiled_head_matches_oracle_and_row_major(gpu_lib, shape, batch, prefix):
-    """The vocabulary head on the tiled copy of lm_head (ldr_tile_matrix):
-    logits against the oracle, and against the row-major head, from which they
-    differ only in the fp32 summation order of the same bf16 products. 17
-    sequences: 272 rows, two M tiles, the last ragged; V = 5003: a ragged N
-    tile; V = 66536: 260 tiles, more workgroups than CUs."""
+    """The vocabulary head on the tiled copy of lm_head (ldr_tile_matrix),
+    used above 64 rows: logits against the oracle, and against the row-major
+    head, from which they differ only in the fp32 summation order of the same
+    bf16 products. 5 sequences: 80 rows in one ragged M tile; 17 sequences:
+    272 rows, two M tiles, the last ragged; V = 5003: a ragged N tile;
+    V = 66536: 260 tiles, more workgroups than CUs."""
     s = shape
     p, w, dw, anchor = setup(gpu_lib, s, batch, prefix, tiled_head=True)
     z = gpu_lib.draft_step(p.views, dw, anchor)
@@ -76,6 +77,16 @@ def test_tiled_head_matches_oracle_and_row_major(gpu_lib, shape, batch, prefix):
         check_logits(zc[b], ref[b], s)
     scale = z_rm.abs().amax(dim=-1, keepdim=True)
     assert ((z - z_rm).abs() / scale).max().item() <= 1e-4
+
+
+def test_small_steps_keep_the_row_major_head(gpu_lib):
+    """At 64 rows or fewer the head reads lm_head even when a tiled copy is
+    given: the logits are bit-identical to the row-major head's."""
+    p, w, dw, anchor = setup(gpu_lib, MINI_BF16, 3, 120, tiled_head=True)
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    z_rm = gpu_lib.draft_step(p.views, gpu_lib.DraftWeights(w), anchor)
+    torch.cuda.synchronize()
+    assert torch.equal(z, z_rm)
 
 
 def test_tile_matrix_layout(gpu_lib):
