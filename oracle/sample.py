@@ -24,6 +24,16 @@ IEEE fp32 operation. The noise is fully specified here:
   by its odd power series to the f^11 term.
 
 lse and log q are computed in float64 here.
+
+Markov-corrected sampling (Eq. 7-8): with y_0 the anchor, position i's logits
+are z_i = z_i^(0) + W_c E_c(y_{i-1}) and y_i is drawn from softmax(z_i / T)
+as above, so positions are taken in order. The correction c = W_c E_c(y) is,
+for each vocabulary entry v, the sum over the rank index k = 0, 1, ..., r-1
+in that order of the fp32 products W_c[v, k] E_c[y, k], every product and
+partial sum rounded to fp32 (none fused), and z_i = fl(z_i^(0) + c): the
+corrected logits, like the keys, are a fixed sequence of IEEE fp32 operations.
+Position i of sequence b uses the noise row b B + i - 1, the plain sampler's
+row of that logit row.
 """
 from __future__ import annotations
 
@@ -175,3 +185,35 @@ def sample_row(z, temperature, top_k, seed, step, row):
     y, lse, logq = sample(np.asarray(z, dtype=np.float32)[None], temperature, top_k, seed,
                           step, rows=[row])
     return int(y[0]), float(lse[0]), float(logq[0])
+
+
+def correction(E_c, W_c, y):
+    """c = W_c E_c(y) (Eq. 7) for the previous tokens y [n]: fp32 [n][V], each
+    entry summed over the rank index in order, products and sums in fp32."""
+    E = np.asarray(E_c, dtype=np.float32)          # [V][r]
+    W = np.asarray(W_c, dtype=np.float32)          # [V][r]
+    e = E[np.asarray(y, dtype=np.int64)]           # [n][r]
+    c = np.zeros((e.shape[0], W.shape[0]), dtype=np.float32)
+    for k in range(W.shape[1]):
+        c = (c + (W[None, :, k] * e[:, k, None]).astype(np.float32)).astype(np.float32)
+    return c
+
+
+def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
+    """Sequential sampling of the corrected proposal (Eq. 7-8) for base logits
+    z0 [batch][B][V] (fp32) and anchors [batch]. Returns tokens [batch][B]
+    (int64), lse and log q [batch][B] (float64) of the corrected rows, and the
+    corrected logits [batch][B][V] (fp32)."""
+    z0 = np.asarray(z0, dtype=np.float32)
+    nb, B, V = z0.shape
+    y_prev = np.asarray(anchor, dtype=np.int64)
+    toks = np.zeros((nb, B), dtype=np.int64)
+    lses = np.zeros((nb, B))
+    logqs = np.zeros((nb, B))
+    z = np.empty_like(z0)
+    for i in range(B):
+        zi = (z0[:, i, :] + correction(E_c, W_c, y_prev)).astype(np.float32)
+        y, lse, logq = sample(zi, temperature, top_k, seed, step, rows=np.arange(nb) * B + i)
+        toks[:, i], lses[:, i], logqs[:, i], z[:, i, :] = y, lse, logq, zi
+        y_prev = y
+    return toks, lses, logqs, z

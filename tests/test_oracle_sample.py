@@ -136,3 +136,88 @@ def test_sampled_token_is_in_the_top_k_support():
     y, _, _ = Sm.sample(z, 1.0, 5, 9, 1)
     for r in range(40):
         assert y[r] in set(Sm.support(z[r], 5).tolist())
+
+
+# ---- Markov-corrected sampling (Eq. 7-8) ----------------------------------------------------
+
+def _markov_inputs(nb, B, V, r, seed, scale=0.5):
+    g = np.random.default_rng(seed)
+    z0 = g.normal(size=(nb, B, V)).astype(np.float32)
+    E = (g.normal(size=(V, r)) * scale).astype(np.float32)
+    W = (g.normal(size=(V, r)) * scale).astype(np.float32)
+    a = g.integers(0, V, size=nb)
+    return z0, a, E, W
+
+
+@pytest.mark.parametrize("T,top_k", [(1.0, 0), (0.6, 3), (0.0, 0)])
+def test_markov_without_correction_is_the_plain_sampler(T, top_k):
+    """W_c = 0: the corrected logits are the base logits and every output is
+    the plain sampler's on the [batch * B][V] rows."""
+    z0, a, E, W = _markov_inputs(5, 4, 37, 8, 1)
+    y, lse, logq, z = Sm.sample_markov(z0, a, E, np.zeros_like(W), T, top_k, 11, 3)
+    assert np.array_equal(z, z0)
+    y1, lse1, logq1 = Sm.sample(z0.reshape(-1, 37), T, top_k, 11, 3)
+    assert np.array_equal(y.reshape(-1), y1)
+    assert np.array_equal(lse.reshape(-1), lse1) and np.array_equal(logq.reshape(-1), logq1)
+
+
+def test_markov_correction_closed_form():
+    """One-hot correction embeddings pick one column of W_c: c_v = W_c[v, y mod r]."""
+    V, r = 12, 4
+    E = np.zeros((V, r), dtype=np.float32)
+    E[np.arange(V), np.arange(V) % r] = 1.0
+    W = np.random.default_rng(2).normal(size=(V, r)).astype(np.float32)
+    c = Sm.correction(E, W, [0, 5, 11])
+    assert np.array_equal(c, W[:, [0, 1, 3]].T)
+    # and an explicit fp32 chain for a dense case, summed by hand in order
+    E2 = np.random.default_rng(3).normal(size=(V, r)).astype(np.float32)
+    c2 = Sm.correction(E2, W, [7])[0]
+    for v in range(V):
+        acc = np.float32(0)
+        for k in range(r):
+            acc = np.float32(acc + np.float32(W[v, k] * E2[7, k]))
+        assert c2[v] == acc
+
+
+def test_markov_greedy_follows_the_predecessor():
+    """A correction that favours token (y_prev + 1) mod V turns greedy
+    decoding of flat base logits into a cycle from the anchor."""
+    V, B = 5, 7
+    E = np.eye(V, dtype=np.float32)
+    W = np.roll(np.eye(V, dtype=np.float32), 1, axis=0) * 3.0   # W[v, u] = 3 if v = u + 1
+    z0 = np.zeros((2, B, V), dtype=np.float32)
+    y, _, logq, z = Sm.sample_markov(z0, [2, 4], E, W, 0.0, 0, 0, 0)
+    assert y.tolist() == [[(2 + i) % V for i in range(1, B + 1)],
+                          [(4 + i) % V for i in range(1, B + 1)]]
+    assert np.all(logq == 0.0)
+    # top-1 support at T = 1 is the same deterministic chain
+    y1, _, _, _ = Sm.sample_markov(z0, [2, 4], E, W, 1.0, 1, 9, 9)
+    assert np.array_equal(y1, y)
+
+
+def test_markov_joint_distribution_follows_the_factorisation():
+    """Pairs (y_1, y_2) drawn over many sequences follow
+    q_1(y_1) q_2(y_2 | y_1) with q_i = softmax(z_i^(0) + W_c E_c(y_{i-1})) (Eq. 8)."""
+    V, r, n = 3, 2, 40_000
+    g = np.random.default_rng(4)
+    base = g.normal(size=(2, V)).astype(np.float32)
+    E = g.normal(size=(V, r)).astype(np.float32)
+    W = g.normal(size=(V, r)).astype(np.float32)
+    a = 1
+    y, _, logq, _ = Sm.sample_markov(np.tile(base[None], (n, 1, 1)), np.full(n, a), E, W, 1.0, 0,
+                                     5, 6)
+    def soft(x):
+        x = x.astype(np.float64)
+        p = np.exp(x - x.max())
+        return p / p.sum()
+    q1 = soft(base[0] + E[a] @ W.T)
+    joint = np.array([[q1[u] * soft(base[1] + E[u] @ W.T)[w] for w in range(V)] for u in range(V)])
+    counts = np.zeros((V, V))
+    np.add.at(counts, (y[:, 0], y[:, 1]), 1)
+    chi2 = scipy.stats.chisquare(counts.reshape(-1), joint.reshape(-1) * n)
+    assert chi2.pvalue > 1e-3
+    # log q of the second position is the log of the conditional probability
+    for u in range(V):
+        sel = y[:, 0] == u
+        cond = soft(base[1] + E[u] @ W.T)
+        assert np.allclose(logq[sel, 1], np.log(cond[y[sel, 1]]), atol=1e-5)
