@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--row-major-head", action="store_true",
                     help="run the vocabulary head on the row-major lm_head (no tiled copy)")
+    ap.add_argument("--markov-rank", type=int, default=0,
+                    help="sample with the Markov correction (Eq. 7) of this rank instead of the "
+                         "per-position sampler (0: off)")
     ap.add_argument("--cpu-seqs", type=int, default=16,
                     help="sequences in the CPU-oracle sample")
     ap.add_argument("--sweep", action="store_true")
@@ -111,7 +114,7 @@ class Rig:
     """Device-resident inputs and outputs of one workload."""
 
     def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False,
-                 tiled_head=True):
+                 tiled_head=True, markov_rank=0):
         self.torch, self.ldr, self.s, self.batch = torch, ldr, shape, batch
         dev = "cuda"
         self.w = synth.make_weights(shape, device=dev)
@@ -148,6 +151,16 @@ class Rig:
                     torch.empty(rows, dtype=torch.float32, device=dev),
                     torch.empty(rows, dtype=torch.float32, device=dev))
         self.kinds = ldr.draft_launches(shape)
+        # Markov correction (Eq. 7): seeded random correction embedding and output
+        # mapping [V][rank] in the model dtype (no trained weights exist)
+        self.markov_rank = markov_rank
+        if markov_rank:
+            g = torch.Generator(device=dev)
+            g.manual_seed(synth.SEED_WEIGHTS + 17)
+            self.Ec = (torch.randn(shape.vocab, markov_rank, generator=g, device=dev) *
+                       0.02).to(shape.torch_dtype)
+            self.Wc = (torch.randn(shape.vocab, markov_rank, generator=g, device=dev) *
+                       0.02).to(shape.torch_dtype)
         torch.cuda.synchronize()
         if self.views.status() != ldr.LDR_OK:
             raise RuntimeError("views status error after prefill")
@@ -160,8 +173,14 @@ class Rig:
         else:
             self.ldr.draft_step_events(self.views, self.dw, self.anchor, self.logits, self.ws,
                                        events)
-        self.ldr.sample(self.logits.view(-1, self.s.vocab), temperature, 0, 5, i, out=self.out,
-                        workspace=self.sws)
+        if self.markov_rank:
+            b, B = self.batch, self.s.block
+            self.ldr.sample_markov(self.logits, self.anchor, self.Ec, self.Wc, temperature, 0, 5,
+                                   i, out=tuple(t.view(b, B) for t in self.out),
+                                   workspace=self.sws)
+        else:
+            self.ldr.sample(self.logits.view(-1, self.s.vocab), temperature, 0, 5, i,
+                            out=self.out, workspace=self.sws)
 
 
 def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
@@ -419,7 +438,8 @@ def main():
 
     wl = synth.WORKLOADS[args.workload]
     s, batch = wl.shape, wl.batch
-    rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head)
+    rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head,
+              markov_rank=args.markov_rank)
     ev = ldr.HipEvents()
     costs = launch_costs(s, batch)
     # which launch kind dominates the step (events around every launch, outside the timed run)
@@ -448,7 +468,8 @@ def main():
         "config": {"workload": wl.name, "shape": s.name, "batch": batch, "block": s.block,
                    "prefix": wl.prefix, "rows_per_update": s.block + 1, "temperature": 1.0,
                    "window": s.window, "summary": s.summary, "draft_layers": s.n_layers,
-                   "lm_head_layout": "tiled" if rig.tiled_head else "row-major"},
+                   "lm_head_layout": "tiled" if rig.tiled_head else "row-major",
+                   "sampler": f"markov rank {rig.markov_rank}" if rig.markov_rank else "per-position"},
         "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,
                         "p90": percentile(per_step, .9) * 1e3},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,

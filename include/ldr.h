@@ -257,6 +257,30 @@ int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperatu
                int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
                float* logq, void* workspace, size_t workspace_bytes, void* stream);
 
+/* Markov-corrected sampling (Eq. 7-8; the low-rank sequential correction the
+ * paper takes from DSpark). For every sequence b and position i = 1 .. B in
+ * order, with y_0 = anchor[b]:
+ *   z_i <- fl(z_i + c),  c[v] = sum_{k = 0 .. rank-1, in order} fl(W_c[v][k] E_c[y_{i-1}][k])
+ * with every product and partial sum an fp32 operation (none fused), then
+ * y_i, lse and log q of row b * block + i - 1 exactly as ldr_sample computes
+ * them for that row of the corrected logits (same noise counter, temperature
+ * and top_k rules). The positions are sampled one after the other (each
+ * correction needs the previous token); the sequences in parallel.
+ *   logits   dev fp32 [batch][block][vocab]: the base logits z^(0) on entry,
+ *            the corrected logits z when the stream reaches the end of the call
+ *   anchor   dev int32 [batch] (outside [0, vocab) reads embedding row 0)
+ *   E_c, W_c dev [vocab][rank] in `dtype` (enum ldr_dtype): correction
+ *            embedding and output mapping; rank > 0, a multiple of 8, at
+ *            most 256
+ *   tokens   dev int32 [batch][block]; lse, logq dev fp32 [batch][block]
+ *   workspace dev, ldr_sample_workspace_bytes(batch, vocab) bytes.
+ * LDR_EINVAL on a bad argument (as ldr_sample, plus the rank and dtype). */
+int ldr_sample_markov(float* logits, int32_t batch, int32_t block, int32_t vocab,
+                      const int32_t* anchor, const void* E_c, const void* W_c, int32_t rank,
+                      int32_t dtype, float temperature, int32_t top_k, uint64_t seed,
+                      uint64_t step, int32_t* tokens, float* lse, float* logq, void* workspace,
+                      size_t workspace_bytes, void* stream);
+
 /* Writes the Gumbel noise ldr_sample uses: out[r][v] = g_v of row r, for
  * rows [0, rows) and tokens [0, vocab). out dev fp32 [rows][vocab]. */
 int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t rows, int32_t vocab, float* out,

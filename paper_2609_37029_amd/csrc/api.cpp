@@ -441,6 +441,26 @@ int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperatu
              ? LDR_OK : LDR_EHIP;
 }
 
+int ldr_sample_markov(float* logits, int32_t batch, int32_t block, int32_t vocab,
+                      const int32_t* anchor, const void* E_c, const void* W_c, int32_t rank,
+                      int32_t dtype, float temperature, int32_t top_k, uint64_t seed,
+                      uint64_t step, int32_t* tokens, float* lse, float* logq, void* workspace,
+                      size_t workspace_bytes, void* stream) {
+  if (!logits || !anchor || !E_c || !W_c || !tokens || !lse || !logq || !workspace)
+    return LDR_EINVAL;
+  if (batch <= 0 || block <= 0 || vocab <= 0 || !(temperature >= 0.f) || std::isinf(temperature))
+    return LDR_EINVAL;
+  if (top_k < 0 || (dtype != LDR_BF16 && dtype != LDR_F32)) return LDR_EINVAL;
+  if (rank <= 0 || rank > 256 || rank % 8) return LDR_EINVAL;
+  if (!aligned(E_c, 16) || !aligned(W_c, 16) || !aligned(workspace, 16)) return LDR_EINVAL;
+  if (workspace_bytes < ldr_sample_workspace_bytes(batch, vocab)) return LDR_EINVAL;
+  return launch_sample_markov(logits, batch, block, vocab, anchor, E_c, W_c, rank, dtype,
+                              temperature, top_k, seed, step, tokens, lse, logq, workspace,
+                              align_up(sample_part_bytes(batch, vocab)),
+                              static_cast<hipStream_t>(stream)) == hipSuccess
+             ? LDR_OK : LDR_EHIP;
+}
+
 int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t rows, int32_t vocab, float* out,
                     void* stream) {
   if (!out || rows <= 0 || vocab <= 0) return LDR_EINVAL;

@@ -186,7 +186,15 @@ int sample_splits(int rows, int vocab);
 size_t sample_part_bytes(int rows, int vocab);
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
-                         float* logq, void* ws, size_t sel_off, hipStream_t st);
+                         float* logq, void* ws, size_t sel_off, hipStream_t st, int row_mul = 1,
+                         int row_add = 0);
+// Markov-corrected sampling of [batch][B][V] logits (corrected in place), one
+// position after the other; ws / sel_off as for launch_sample with batch rows.
+hipError_t launch_sample_markov(float* logits, int batch, int B, int vocab, const int32_t* anchor,
+                                const void* E, const void* W, int rank, int dtype,
+                                float temperature, int top_k, uint64_t seed, uint64_t step,
+                                int32_t* tokens, float* lse, float* logq, void* ws,
+                                size_t sel_off, hipStream_t st);
 hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
                               hipStream_t st);
 

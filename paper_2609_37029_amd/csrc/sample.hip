@@ -127,6 +127,7 @@ struct SampleArgs {
   float T; uint64_t seed, step;
   Partial* part;
   const TopK* sel;  // top-k support per row, or null for the full vocabulary
+  int row_mul, row_add;  // row r of the launch is logits row (and noise row) r * mul + add
 };
 
 // Exact k-th largest logit of a row by radix selection on order_key (four
@@ -134,8 +135,9 @@ struct SampleArgs {
 // among the tokens equal to it. One workgroup per row.
 constexpr int kSelThreads = 1024;
 __global__ void __launch_bounds__(kSelThreads) topk_select_kernel(const float* logits, int vocab,
-                                                                  int k, TopK* sel) {
-  const float* z = logits + (long)blockIdx.x * vocab;
+                                                                  int k, TopK* sel, int row_mul,
+                                                                  int row_add) {
+  const float* z = logits + ((long)blockIdx.x * row_mul + row_add) * vocab;
   __shared__ uint32_t hist[256];
   __shared__ uint32_t s_digit, s_above;
   __shared__ int wcount[kSelThreads / 64];
@@ -238,7 +240,7 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
   for (int vb = v0; vb < v1; vb += kThreads * kGroup) {
     const int v = vb + (threadIdx.x & ~63) * kGroup + lane * kGroup;
     uint32_t bits[kGroup];
-    noise_group(a.seed, a.step, (uint64_t)r, (uint64_t)(v / kGroup), bits);
+    noise_group(a.seed, a.step, (uint64_t)r * a.row_mul + a.row_add, (uint64_t)(v / kGroup), bits);
     float zt[kGroup];
     float gm = -INFINITY;
     bool in[kGroup];
@@ -279,10 +281,94 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
   if (qn > 0) drain(qn);
 }
 
+// Eq. 7 for position i of every sequence: z[b][i][v] += (W_c E_c(y))[v] with
+// y = y_{i-1}(b), y_0 the anchor (an anchor outside [0, V) reads row 0). A
+// workgroup takes kMkV vocabulary entries: their W_c rows reach LDS through
+// coalesced 16-byte loads (rows padded by 16 bytes, so the lanes' row reads
+// spread over the banks), and the rank vectors of 16 sequences at a time sit
+// in LDS as fp32. Its 4 wave-sized groups of threads take 4 of every 16
+// sequences each. Each entry's sum runs over the rank index in order with
+// separate fp32 multiplies and adds (no fused multiply-add), so the corrected
+// logits are a fixed sequence of IEEE operations that the sampler then reads
+// like any other logits.
+constexpr int kMkRows = 16, kMkThreads = 256, kMkV = 64, kMkPer = kMkRows / (kMkThreads / kMkV);
+template <typename T>
+__global__ void __launch_bounds__(kMkThreads) markov_correct_kernel(
+    float* logits, int batch, int B, int vocab, int i, const int32_t* anchor,
+    const int32_t* tokens, const T* E, const T* W, int rank) {
+#pragma clang fp contract(off)   // products and sums rounded separately, as the oracle states
+  extern __shared__ __attribute__((aligned(16))) float e_lds[];   // [kMkRows][rank], then W
+  constexpr int EPV = 16 / sizeof(T);   // elements per 16-byte piece (8 or 4)
+  const int wld = rank + EPV;           // padded W row in LDS (elements)
+  T* w_lds = reinterpret_cast<T*>(e_lds + kMkRows * rank);
+  const int v0 = blockIdx.x * kMkV;
+  const int lv = threadIdx.x & (kMkV - 1), v = v0 + lv;
+  const int grp = threadIdx.x / kMkV;   // rows grp * kMkPer .. + kMkPer of each 16
+  {  // W_c rows v0 .. v0 + kMkV - 1 (rows past V repeat the last one)
+    const int per_row = rank / EPV;
+    for (int c = threadIdx.x; c < kMkV * per_row; c += kMkThreads) {
+      const int r = c / per_row, k = (c - r * per_row) * EPV;
+      const long row = min(v0 + r, vocab - 1);
+      *reinterpret_cast<uint4*>(w_lds + r * wld + k) =
+          *reinterpret_cast<const uint4*>(W + row * rank + k);
+    }
+  }
+  const T* wr = w_lds + lv * wld;
+  const float* e0 = e_lds + grp * kMkPer * rank;
+  for (int b0 = 0; b0 < batch; b0 += kMkRows) {
+    const int nb = min(kMkRows, batch - b0);
+    __syncthreads();   // the W tile is in; the previous chunk's reads are done
+    for (int idx = threadIdx.x; idx < kMkRows * rank; idx += kMkThreads) {
+      const int bb = idx / rank, k = idx - bb * rank;
+      float e = 0.f;
+      if (bb < nb) {
+        const int b = b0 + bb;
+        int y = i == 0 ? anchor[b] : tokens[(long)b * B + i - 1];
+        if (y < 0 || y >= vocab) y = 0;
+        e = Elem<T>::load(E + (long)y * rank + k);
+      }
+      e_lds[idx] = e;
+    }
+    __syncthreads();
+    float c[kMkPer];
+#pragma unroll
+    for (int r = 0; r < kMkPer; ++r) c[r] = 0.f;
+    for (int k0 = 0; k0 < rank; k0 += 8) {
+      float w[8];
+#pragma unroll
+      for (int h = 0; h < 8 / EPV; ++h) {
+        const uint4 raw = *reinterpret_cast<const uint4*>(wr + k0 + h * EPV);
+        const T* wv = reinterpret_cast<const T*>(&raw);
+#pragma unroll
+        for (int e = 0; e < EPV; ++e) w[h * EPV + e] = Elem<T>::load(wv + e);
+      }
+#pragma unroll
+      for (int r = 0; r < kMkPer; ++r) {
+        const float4 ea = *reinterpret_cast<const float4*>(e0 + r * rank + k0);
+        const float4 eb = *reinterpret_cast<const float4*>(e0 + r * rank + k0 + 4);
+        float x = c[r];
+        x = x + w[0] * ea.x; x = x + w[1] * ea.y; x = x + w[2] * ea.z; x = x + w[3] * ea.w;
+        x = x + w[4] * eb.x; x = x + w[5] * eb.y; x = x + w[6] * eb.z; x = x + w[7] * eb.w;
+        c[r] = x;
+      }
+    }
+    if (v < vocab) {
+#pragma unroll
+      for (int r = 0; r < kMkPer; ++r) {
+        const int bb = grp * kMkPer + r;
+        if (bb < nb) {
+          float* zp = logits + ((long)(b0 + bb) * B + i) * vocab + v;
+          *zp = *zp + c[r];
+        }
+      }
+    }
+  }
+}
+
 __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) {
   const int sp = blockIdx.x, r = blockIdx.y;
   const int v0 = sp * a.chunk, v1 = min(a.vocab, v0 + a.chunk);
-  const float* z = a.logits + (long)r * a.vocab;
+  const float* z = a.logits + ((long)r * a.row_mul + a.row_add) * a.vocab;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
   if (a.T == 0.f) {
     for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
@@ -322,14 +408,15 @@ __global__ void __launch_bounds__(64) sample_merge_kernel(SampleArgs a, int32_t*
     combine(p, o);
   }
   if (threadIdx.x == 0) {
-    tokens[r] = p.idx;
+    const long g = (long)r * a.row_mul + a.row_add;
+    tokens[g] = p.idx;
     if (a.T == 0.f) {
-      lse[r] = p.key;
-      logq[r] = 0.f;
+      lse[g] = p.key;
+      logq[g] = 0.f;
     } else {
       const float l = p.m + logf(p.s);
-      lse[r] = l;
-      logq[r] = a.logits[(long)r * a.vocab + p.idx] / a.T - l;
+      lse[g] = l;
+      logq[g] = a.logits[g * a.vocab + p.idx] / a.T - l;
     }
   }
 }
@@ -368,15 +455,16 @@ size_t sample_part_bytes(int rows, int vocab) {
 
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
-                         float* logq, void* ws, size_t sel_off, hipStream_t st) {
+                         float* logq, void* ws, size_t sel_off, hipStream_t st, int row_mul,
+                         int row_add) {
   SampleArgs a;
   a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
   a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
-  a.sel = nullptr;
+  a.sel = nullptr; a.row_mul = row_mul; a.row_add = row_add;
   if (temperature > 0.f && top_k > 0 && top_k < vocab) {  // T = 0 is the argmax either way
     TopK* sel = reinterpret_cast<TopK*>(static_cast<uint8_t*>(ws) + sel_off);
     hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, logits, vocab,
-                       top_k, sel);
+                       top_k, sel, row_mul, row_add);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     a.sel = sel;
@@ -400,6 +488,33 @@ hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab,
   hipLaunchKernelGGL(gumbel_fill_kernel, dim3((int)(blocks > 0 ? blocks : 1)), dim3(kThreads),
                      0, st, seed, step, rows, vocab, out);
   return hipGetLastError();
+}
+
+hipError_t launch_sample_markov(float* logits, int batch, int B, int vocab, const int32_t* anchor,
+                                const void* E, const void* W, int rank, int dtype,
+                                float temperature, int top_k, uint64_t seed, uint64_t step,
+                                int32_t* tokens, float* lse, float* logq, void* ws,
+                                size_t sel_off, hipStream_t st) {
+  const int esz = dtype == LDR_BF16 ? 2 : 4;
+  const size_t lds = (size_t)kMkRows * rank * sizeof(float) +
+                     (size_t)kMkV * (rank + 16 / esz) * esz;
+  const dim3 grid((unsigned)((vocab + kMkV - 1) / kMkV));
+  for (int i = 0; i < B; ++i) {
+    if (dtype == LDR_BF16)
+      hipLaunchKernelGGL((markov_correct_kernel<uint16_t>), grid, dim3(kMkThreads), lds, st,
+                         logits, batch, B, vocab, i, anchor, tokens,
+                         static_cast<const uint16_t*>(E), static_cast<const uint16_t*>(W), rank);
+    else
+      hipLaunchKernelGGL((markov_correct_kernel<float>), grid, dim3(kMkThreads), lds, st, logits,
+                         batch, B, vocab, i, anchor, tokens, static_cast<const float*>(E),
+                         static_cast<const float*>(W), rank);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = launch_sample(logits, batch, vocab, temperature, top_k, seed, step, tokens, lse, logq, ws,
+                      sel_off, st, B, i);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace ldr

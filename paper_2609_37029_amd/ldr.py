@@ -81,6 +81,9 @@ def _lib():
             "ldr_sample": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P, P, P,
                                           SZ, P]),
             "ldr_gumbel_fill": (ctypes.c_int, [U64, U64, I32, I32, P, P]),
+            "ldr_sample_markov": (ctypes.c_int, [P, I32, I32, I32, P, P, P, I32, I32,
+                                                 ctypes.c_float, I32, U64, U64, P, P, P, P, SZ,
+                                                 P]),
             "ldr_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
@@ -363,3 +366,27 @@ def device_weights(w: Dict, device="cuda") -> Dict:
     out = {k: v.to(device) for k, v in w.items() if k != "layers"}
     out["layers"] = [{k: v.to(device) for k, v in L.items()} for L in w["layers"]]
     return out
+
+
+def sample_markov(logits: torch.Tensor, anchor: torch.Tensor, E_c: torch.Tensor,
+                  W_c: torch.Tensor, temperature: float, top_k: int, seed: int, step: int,
+                  out=None, workspace: Optional[torch.Tensor] = None, stream=None):
+    """ldr_sample_markov over [batch][B][V] fp32 logits (corrected in place):
+    (tokens int32, lse fp32, logq fp32), each [batch][B]."""
+    batch, B, V = logits.shape
+    rank = E_c.shape[1]
+    dtype = LDR_BF16 if E_c.dtype == torch.bfloat16 else LDR_F32
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(batch, B, dtype=torch.int32, device=dev),
+               torch.empty(batch, B, dtype=torch.float32, device=dev),
+               torch.empty(batch, B, dtype=torch.float32, device=dev))
+    if workspace is None:
+        workspace = torch.empty(sample_workspace_bytes(batch, V), dtype=torch.uint8, device=dev)
+    tok, lse, logq = out
+    _check(_lib().ldr_sample_markov(_ptr(logits), batch, B, V, _ptr(anchor), _ptr(E_c),
+                                    _ptr(W_c), rank, dtype, float(temperature), int(top_k),
+                                    int(seed), int(step), _ptr(tok), _ptr(lse), _ptr(logq),
+                                    _ptr(workspace), workspace.numel(), _stream(stream)),
+           "ldr_sample_markov")
+    return tok, lse, logq

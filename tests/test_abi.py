@@ -87,6 +87,16 @@ def test_host_validation_needs_no_gpu(L):
     assert lib.ldr_sample(None, 4, 10, 1.0, 0, 0, 0, None, None, None, None, 0, None) == \
         L.LDR_EINVAL
     assert lib.ldr_gumbel_fill(0, 0, 0, 10, None, None) == L.LDR_EINVAL
+    fake = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced: validation fails first
+    ws = lib.ldr_sample_workspace_bytes(2, 64)
+    for args in ((None, 2, 2, 64, fake, fake, fake, 8, L.LDR_BF16),   # no logits
+                 (fake, 2, 2, 64, fake, fake, fake, 6, L.LDR_BF16),   # bf16 rank % 8
+                 (fake, 2, 2, 64, fake, fake, fake, 6, L.LDR_F32),    # fp32 rank % 4
+                 (fake, 2, 2, 64, fake, fake, fake, 264, L.LDR_F32),  # rank > 256
+                 (fake, 2, 2, 64, fake, fake, fake, 8, 7),            # dtype
+                 (fake, 0, 2, 64, fake, fake, fake, 8, L.LDR_BF16)):  # batch
+        assert lib.ldr_sample_markov(*args, 1.0, 0, 0, 0, fake, fake, fake, fake, ws,
+                                     None) == L.LDR_EINVAL
     assert lib.ldr_views_status(None, 0, None) == L.LDR_EINVAL
     lib.ldr_views_destroy(None)
     assert lib.ldr_sample_workspace_bytes(0, 10) == 0

@@ -106,3 +106,61 @@ def test_negative_top_k_is_rejected(gpu_lib):
     z = _logits(2, 100, 1)
     with pytest.raises(gpu_lib.LdrError):
         gpu_lib.sample(z, 1.0, -1, seed=0, step=0)
+
+
+# ---- Markov-corrected sampling (Eq. 7-8) ----------------------------------------------------
+
+def _markov_case(batch, B, vocab, rank, dtype, seed, scale=0.4):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    z0 = torch.randn(batch, B, vocab, generator=g, device="cuda") * 1.3
+    E = (torch.randn(vocab, rank, generator=g, device="cuda") * scale).to(dtype)
+    W = (torch.randn(vocab, rank, generator=g, device="cuda") * scale).to(dtype)
+    a = torch.randint(0, vocab, (batch,), generator=g, device="cuda", dtype=torch.int32)
+    return z0, a, E, W
+
+
+@pytest.mark.parametrize("batch,B,vocab,rank,dtype,T,k", [
+    (4, 8, 151936, 64, torch.bfloat16, 1.0, 0),     # the Qwen3 vocabulary
+    (3, 5, 1001, 8, torch.float32, 0.7, 0),         # fp32 correction, ragged vocab
+    (18, 3, 5003, 16, torch.bfloat16, 1.0, 40),     # more sequences than one LDS batch, top-k
+    (2, 6, 4099, 32, torch.bfloat16, 0.0, 0),       # greedy
+])
+def test_markov_matches_oracle(gpu_lib, batch, B, vocab, rank, dtype, T, k):
+    """Corrected logits bit for bit, tokens exactly, lse and log q within fp32
+    tolerance, against the oracle's sequential sampling from the same base
+    logits, anchors and correction weights."""
+    z0, a, E, W = _markov_case(batch, B, vocab, rank, dtype, batch * 31 + vocab + rank)
+    z0_host = z0.cpu().numpy()
+    z = z0.clone()
+    tok, lse, logq = gpu_lib.sample_markov(z, a, E, W, T, k, seed=13, step=4)
+    torch.cuda.synchronize()
+    y, l, lq, zc = OS.sample_markov(z0_host, a.cpu().numpy(), E.float().cpu().numpy(),
+                                    W.float().cpu().numpy(), T, k, 13, 4)
+    assert np.array_equal(z.cpu().numpy().view(np.uint32), zc.view(np.uint32))
+    assert np.array_equal(tok.cpu().numpy().astype(np.int64), y)
+    np.testing.assert_allclose(lse.cpu().numpy(), l, rtol=2e-6, atol=2e-5)
+    np.testing.assert_allclose(logq.cpu().numpy(), lq, rtol=1e-5, atol=2e-4)
+
+
+def test_markov_without_correction_is_ldr_sample(gpu_lib):
+    """W_c = 0 leaves the logits unchanged and draws what ldr_sample draws on
+    the [batch * B][V] rows."""
+    z0, a, E, W = _markov_case(5, 4, 4096, 8, torch.bfloat16, 3)
+    z = z0.clone()
+    tok, lse, logq = gpu_lib.sample_markov(z, a, E, torch.zeros_like(W), 1.0, 0, seed=2, step=8)
+    tok1, lse1, logq1 = gpu_lib.sample(z0.view(-1, 4096), 1.0, 0, seed=2, step=8)
+    torch.cuda.synchronize()
+    assert torch.equal(z, z0)
+    assert torch.equal(tok.view(-1), tok1) and torch.equal(lse.view(-1), lse1)
+    assert torch.equal(logq.view(-1), logq1)
+
+
+def test_markov_rejects_bad_arguments(gpu_lib):
+    z0, a, E, W = _markov_case(2, 2, 512, 8, torch.bfloat16, 1)
+    for kw in ({"E": E[:, :6].contiguous(), "W": W[:, :6].contiguous()},   # rank % 8
+               {"k": -1}):
+        with pytest.raises(gpu_lib.LdrError) as e:
+            gpu_lib.sample_markov(z0.clone(), a, kw.get("E", E), kw.get("W", W), 1.0,
+                                  kw.get("k", 0), seed=0, step=0)
+        assert e.value.code == gpu_lib.LDR_EINVAL
