@@ -217,3 +217,107 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
         toks[:, i], lses[:, i], logqs[:, i], z[:, i, :] = y, lse, logq, zi
         y_prev = y
     return toks, lses, logqs, z
+
+
+# ---- verification (Eq. 1-2) -------------------------------------------------------------------
+#
+# The target scores [a, y_1 .. y_B] in one pass and gives B + 1 distributions:
+# row j of the target logits P is p_{j+1}. Candidate y_i is accepted when
+# u_i < p_i(y_i) / q_i(y_i) (Eq. 1), tested in order; at the first rejection
+# the round emits a token drawn from [p_i - q_i]_+ normalised (Eq. 2), and
+# after B acceptances a bonus token drawn from p_{B+1}. p and q take the same
+# temperature T over the whole vocabulary: p_i = softmax(P_i / T),
+# q_i = softmax(z_i / T) (a top-k proposal is not verified here). The ratio,
+# p, q and the residual are float64 here.
+#
+# Readings where the paper is silent:
+#  * a candidate outside [0, V) has q = 0 and is rejected;
+#  * a residual with no positive mass (p_i = q_i up to rounding) draws from
+#    p_i with the bonus rule instead;
+#  * the bonus token is drawn exactly as the drafting sampler draws, from the
+#    fp32 keys fl(fl(P_v / T) + g_v), first maximum; the correction token is
+#    the first maximum of log w_v + g_v over w_v = [p_i(v) - q_i(v)]_+ > 0;
+#  * T = 0 verifies greedily: y_i is accepted when it is the first argmax of
+#    P_i, and the round emits the first argmax of the row where it stops.
+#
+# Noise (Philox4x64-10, key (seed, step), counter streams of their own):
+#  * u_i of sequence b: counter (i - 1, b, 1, 0), the upper 32 bits of word 0,
+#    made uniform like the drafting noise;
+#  * the emitted token's Gumbel noise g_v: counter (v div 8, b, 2, 0), word and
+#    32-bit half chosen as for the drafting noise.
+
+
+def verify_uniform(seed, step, b, i):
+    """u_i of sequence b (i = 1 .. B) as an exact fp32 value in (0, 1)."""
+    w = philox4x64_10((np.uint64(i - 1), np.uint64(b), np.uint64(1), np.uint64(0)),
+                      (np.uint64(seed), np.uint64(step)))
+    return uniform(np.uint32(int(w[0]) >> 32))
+
+
+def verify_gumbel(seed, step, b, v):
+    """Gumbel noise of token(s) v for the emitted token of sequence b."""
+    v = np.asarray(v, dtype=np.uint64)
+    zero = np.zeros_like(v)
+    key = (np.uint64(seed), np.uint64(step))
+    w = np.stack(philox4x64_10((v >> np.uint64(3), zero + np.uint64(b), zero + np.uint64(2), zero),
+                               key), axis=0)
+    word = np.take_along_axis(w, ((v >> np.uint64(1)) & np.uint64(3)).astype(np.int64)[None],
+                              axis=0)[0]
+    bits = ((word >> ((v & np.uint64(1)) * np.uint64(32))) & _M32).astype(np.uint32)
+    return -logf(-logf(uniform(bits)))
+
+
+def _softmax64(x):
+    x = np.asarray(x, dtype=np.float64)
+    m = x.max()
+    e = np.exp(x - m)
+    return e / e.sum()
+
+
+def verify(P, Z, y, temperature, seed, step):
+    """Speculative verification of one round for every sequence.
+    P: target logits [batch][B + 1][V]; Z: draft logits [batch][B][V] (the
+    proposal q_i = softmax(z_i / T)); y: drafted tokens [batch][B].
+    Returns (r [batch] accepted counts, token [batch] emitted after them,
+    ratio [batch][B] p_i(y_i) / q_i(y_i) in float64, u [batch][B]); ratio and
+    u are 0 past the first rejection and at T = 0."""
+    P = np.asarray(P, dtype=np.float32)
+    Z = np.asarray(Z, dtype=np.float32)
+    y = np.asarray(y, dtype=np.int64)
+    nb, B1, V = P.shape
+    B = B1 - 1
+    r = np.zeros(nb, dtype=np.int64)
+    tok = np.zeros(nb, dtype=np.int64)
+    ratio = np.zeros((nb, B))
+    us = np.zeros((nb, B))
+    for b in range(nb):
+        if temperature == 0.0:
+            i = 0
+            while i < B and int(np.argmax(P[b, i])) == y[b, i]:
+                i += 1
+            r[b], tok[b] = i, int(np.argmax(P[b, i]))
+            continue
+        T = np.float32(temperature)
+        stop = B
+        for i in range(B):
+            p = _softmax64(P[b, i].astype(np.float64) / float(T))
+            q = _softmax64(Z[b, i].astype(np.float64) / float(T))
+            yi = int(y[b, i])
+            ratio[b, i] = p[yi] / q[yi] if 0 <= yi < V else 0.0
+            us[b, i] = float(verify_uniform(seed, step, b, i + 1))
+            if not us[b, i] < ratio[b, i]:
+                stop = i
+                break
+        r[b] = stop
+        g = verify_gumbel(seed, step, b, np.arange(V))
+        w = None
+        if stop < B:
+            p = _softmax64(P[b, stop].astype(np.float64) / float(T))
+            w = np.maximum(p - _softmax64(Z[b, stop].astype(np.float64) / float(T)), 0.0)
+        if w is not None and np.any(w > 0):
+            key = np.full(V, -np.inf)
+            key[w > 0] = np.log(w[w > 0]) + g[w > 0].astype(np.float64)
+        else:
+            key = P[b, stop] / T + g                               # fp32, as the sampler
+        tok[b] = int(np.argmax(key))
+    return r, tok, ratio, us

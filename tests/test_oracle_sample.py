@@ -9,6 +9,7 @@ import pytest
 import scipy.stats
 
 from oracle import sample as Sm
+from oracle.sample import gumbel, sample, verify, verify_gumbel, verify_uniform
 
 
 @pytest.mark.parametrize("ctr,key", [
@@ -221,3 +222,106 @@ def test_markov_joint_distribution_follows_the_factorisation():
         sel = y[:, 0] == u
         cond = soft(base[1] + E[u] @ W.T)
         assert np.allclose(logq[sel, 1], np.log(cond[y[sel, 1]]), atol=1e-5)
+
+
+# ---- verification (Eq. 1-2) -------------------------------------------------------------------
+
+def _soft(x):
+    x = np.asarray(x, dtype=np.float64)
+    e = np.exp(x - x.max())
+    return e / e.sum()
+
+
+def test_verification_preserves_the_target_distribution():
+    """One candidate per round (B = 1): the first emitted token (y_1 when
+    accepted, the correction token otherwise) follows p_1 exactly, whatever
+    q_1 is (the property speculative sampling is built on)."""
+    V, n = 5, 30_000
+    g = np.random.default_rng(8)
+    p_logits = g.normal(size=V).astype(np.float32)
+    q_logits = g.normal(size=V).astype(np.float32)
+    P = np.tile(np.stack([p_logits, g.normal(size=V).astype(np.float32)])[None], (n, 1, 1))
+    Z = np.tile(q_logits[None, None], (n, 1, 1))
+    y, _, _ = sample(Z.reshape(n, V), 1.0, 0, 21, 0)            # y_1 ~ q_1 per sequence
+    r, tok, ratio, _ = verify(P, Z, y[:, None], 1.0, 21, 0)
+    first = np.where(r == 1, y, tok)
+    counts = np.bincount(first, minlength=V)
+    chi2 = scipy.stats.chisquare(counts, _soft(p_logits) * n)
+    assert chi2.pvalue > 1e-3
+    # acceptance rate = sum_v min(p(v), q(v))
+    acc = np.minimum(_soft(p_logits), _soft(q_logits)).sum()
+    assert abs(r.mean() - acc) < 0.015
+
+
+def test_correction_token_follows_the_residual():
+    """Given a rejection, the emitted token follows [p - q]_+ normalised."""
+    V, n = 4, 40_000
+    p_logits = np.float32([2.0, 0.5, -1.0, 1.2])
+    q_logits = np.float32([-1.0, 1.5, 0.8, 0.3])
+    P = np.tile(np.stack([p_logits, p_logits])[None], (n, 1, 1))
+    Z = np.tile(q_logits[None, None], (n, 1, 1))
+    y = np.full((n, 1), 2)                                      # a token q likes more than p
+    r, tok, _, _ = verify(P, Z, y, 1.0, 5, 1)
+    rej = r == 0
+    res = np.maximum(_soft(p_logits) - _soft(q_logits), 0)
+    res = res / res.sum()
+    counts = np.bincount(tok[rej], minlength=V)
+    nz = res > 0
+    assert counts[~nz].sum() == 0 and nz.sum() == 2
+    chi2 = scipy.stats.chisquare(counts[nz], res[nz] * rej.sum())
+    assert chi2.pvalue > 1e-3
+    # rejection probability of y = 2 is 1 - p(2) / q(2)
+    assert abs(rej.mean() - (1 - _soft(p_logits)[2] / _soft(q_logits)[2])) < 0.01
+
+
+def test_equal_distributions_accept_everything():
+    V, B, n = 6, 3, 200
+    g = np.random.default_rng(9)
+    Z = g.normal(size=(n, B, V)).astype(np.float32)
+    P = np.concatenate([Z, g.normal(size=(n, 1, V)).astype(np.float32)], axis=1)
+    y, _, _ = sample(Z.reshape(-1, V), 0.8, 0, 1, 1)
+    r, tok, ratio, _ = verify(P, Z, y.reshape(n, B), 0.8, 1, 1)
+    assert np.all(r == B) and np.allclose(ratio, 1.0)
+    assert np.all((tok >= 0) & (tok < V))
+
+
+def test_greedy_verification():
+    V, B = 7, 4
+    P = np.zeros((2, B + 1, V), dtype=np.float32)
+    for j, v in enumerate([3, 1, 4, 1, 5]):
+        P[:, j, v] = 1.0
+    y = np.array([[3, 1, 4, 1], [3, 2, 4, 1]])
+    r, tok, _, _ = verify(P, np.zeros((2, B, V), dtype=np.float32), y, 0.0, 0, 0)
+    assert r.tolist() == [4, 1] and tok.tolist() == [5, 1]
+
+
+def test_verification_noise_streams_are_their_own():
+    us = {float(verify_uniform(3, 4, b, i)) for b in range(8) for i in range(1, 5)}
+    assert len(us) == 32 and all(0 < u < 1 for u in us)
+    g = verify_gumbel(3, 4, 0, np.arange(64))
+    assert not np.array_equal(g, gumbel(3, 4, 0, np.arange(64)))
+
+
+def test_bonus_token_is_the_drafting_sampler_on_the_last_row():
+    """All candidates accepted: the bonus token is the plain sampler's draw
+    from p_{B+1}, with the verification noise (its own counter stream)."""
+    V, B = 300, 3
+    g = np.random.default_rng(10)
+    Z = g.normal(size=(2, B, V)).astype(np.float32)
+    P = np.concatenate([Z, g.normal(size=(2, 1, V)).astype(np.float32)], axis=1)
+    y, _, _ = sample(Z.reshape(-1, V), 1.0, 0, 4, 2)
+    r, tok, _, _ = verify(P, Z, y.reshape(2, B), 1.0, 4, 2)
+    assert np.all(r == B)
+    for b in range(2):
+        key = (P[b, B] / np.float32(1.0) + verify_gumbel(4, 2, b, np.arange(V))).astype(np.float32)
+        assert tok[b] == int(np.argmax(key))
+
+
+def test_out_of_range_candidates_are_rejected():
+    V, B = 10, 2
+    g = np.random.default_rng(11)
+    Z = g.normal(size=(1, B, V)).astype(np.float32)
+    P = np.concatenate([Z, Z[:, :1]], axis=1)
+    for bad in (-1, V):
+        r, tok, ratio, _ = verify(P, Z, np.array([[bad, 0]]), 1.0, 0, 0)
+        assert r[0] == 0 and ratio[0, 0] == 0.0 and 0 <= tok[0] < V
