@@ -232,8 +232,12 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
 #
 # Readings where the paper is silent:
 #  * a candidate outside [0, V) has q = 0 and is rejected;
-#  * a residual with no positive mass (p_i = q_i up to rounding) draws from
-#    p_i with the bonus rule instead;
+#  * the residual counts token v only when p_i(v) - q_i(v) > 2^-14 p_i(v):
+#    closer values are taken as equal (fp32 log-normalisers over 10^5 terms
+#    are not resolved better than that), so a proposal equal to the target up
+#    to rounding leaves no residual; the mass dropped is below 2^-14;
+#  * a residual with no positive mass draws from p_i with the bonus rule
+#    instead;
 #  * the bonus token is drawn exactly as the drafting sampler draws, from the
 #    fp32 keys fl(fl(P_v / T) + g_v), first maximum; the correction token is
 #    the first maximum of log w_v + g_v over w_v = [p_i(v) - q_i(v)]_+ > 0;
@@ -245,6 +249,9 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
 #    made uniform like the drafting noise;
 #  * the emitted token's Gumbel noise g_v: counter (v div 8, b, 2, 0), word and
 #    32-bit half chosen as for the drafting noise.
+
+
+RESIDUAL_REL = 2.0 ** -14   # a residual entry needs p - q above this fraction of p
 
 
 def verify_uniform(seed, step, b, i):
@@ -274,13 +281,15 @@ def _softmax64(x):
     return e / e.sum()
 
 
-def verify(P, Z, y, temperature, seed, step):
+def verify(P, Z, y, temperature, seed, step, keys=False):
     """Speculative verification of one round for every sequence.
     P: target logits [batch][B + 1][V]; Z: draft logits [batch][B][V] (the
     proposal q_i = softmax(z_i / T)); y: drafted tokens [batch][B].
     Returns (r [batch] accepted counts, token [batch] emitted after them,
     ratio [batch][B] p_i(y_i) / q_i(y_i) in float64, u [batch][B]); ratio and
-    u are 0 past the first rejection and at T = 0."""
+    u are 0 past the first rejection and at T = 0. keys=True appends the list
+    of each sequence's keys over the row it emits from (float64 [V]; the
+    token is their first argmax)."""
     P = np.asarray(P, dtype=np.float32)
     Z = np.asarray(Z, dtype=np.float32)
     y = np.asarray(y, dtype=np.int64)
@@ -290,12 +299,14 @@ def verify(P, Z, y, temperature, seed, step):
     tok = np.zeros(nb, dtype=np.int64)
     ratio = np.zeros((nb, B))
     us = np.zeros((nb, B))
+    all_keys = []
     for b in range(nb):
         if temperature == 0.0:
             i = 0
             while i < B and int(np.argmax(P[b, i])) == y[b, i]:
                 i += 1
             r[b], tok[b] = i, int(np.argmax(P[b, i]))
+            all_keys.append(P[b, i].astype(np.float64))
             continue
         T = np.float32(temperature)
         stop = B
@@ -313,11 +324,15 @@ def verify(P, Z, y, temperature, seed, step):
         w = None
         if stop < B:
             p = _softmax64(P[b, stop].astype(np.float64) / float(T))
-            w = np.maximum(p - _softmax64(Z[b, stop].astype(np.float64) / float(T)), 0.0)
+            w = p - _softmax64(Z[b, stop].astype(np.float64) / float(T))
+            w = np.where(w > RESIDUAL_REL * p, w, 0.0)
         if w is not None and np.any(w > 0):
             key = np.full(V, -np.inf)
             key[w > 0] = np.log(w[w > 0]) + g[w > 0].astype(np.float64)
         else:
             key = P[b, stop] / T + g                               # fp32, as the sampler
         tok[b] = int(np.argmax(key))
+        all_keys.append(key.astype(np.float64))
+    if keys:
+        return r, tok, ratio, us, all_keys
     return r, tok, ratio, us

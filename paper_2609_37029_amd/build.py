@@ -18,7 +18,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libldr.so")
-SOURCES = ["api.cpp", "views.hip", "gemm.hip", "draft.hip", "attn.hip", "sample.hip"]
+SOURCES = ["api.cpp", "views.hip", "gemm.hip", "draft.hip", "attn.hip", "sample.hip", "verify.hip"]
 
 
 def hipcc() -> str:

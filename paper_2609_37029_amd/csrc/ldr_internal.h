@@ -195,6 +195,12 @@ hipError_t launch_sample_markov(float* logits, int batch, int B, int vocab, cons
                                 float temperature, int top_k, uint64_t seed, uint64_t step,
                                 int32_t* tokens, float* lse, float* logq, void* ws,
                                 size_t sel_off, hipStream_t st);
+// Verification (verify.hip): Eq. 1-2 over [batch][B + 1][V] target logits.
+size_t verify_workspace_bytes(int batch, int B, int V);
+hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const float* qlse,
+                         int batch, int B, int V, float T, uint64_t seed, uint64_t step,
+                         int32_t* accepted, int32_t* token, int32_t* n_new, void* ws,
+                         hipStream_t st);
 hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
                               hipStream_t st);
 

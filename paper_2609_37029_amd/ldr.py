@@ -84,6 +84,9 @@ def _lib():
             "ldr_sample_markov": (ctypes.c_int, [P, I32, I32, I32, P, P, P, I32, I32,
                                                  ctypes.c_float, I32, U64, U64, P, P, P, P, SZ,
                                                  P]),
+            "ldr_verify_workspace_bytes": (SZ, [I32, I32, I32]),
+            "ldr_verify": (ctypes.c_int, [P, P, P, P, I32, I32, I32, ctypes.c_float, U64, U64, P,
+                                          P, P, P, SZ, P]),
             "ldr_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
@@ -390,3 +393,29 @@ def sample_markov(logits: torch.Tensor, anchor: torch.Tensor, E_c: torch.Tensor,
                                     _ptr(workspace), workspace.numel(), _stream(stream)),
            "ldr_sample_markov")
     return tok, lse, logq
+
+
+def verify_workspace_bytes(batch: int, block: int, vocab: int) -> int:
+    return int(_lib().ldr_verify_workspace_bytes(batch, block, vocab))
+
+
+def verify(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor],
+           draft_lse: Optional[torch.Tensor], draft_tokens: torch.Tensor, temperature: float,
+           seed: int, step: int, out=None, workspace: Optional[torch.Tensor] = None,
+           stream=None):
+    """ldr_verify: target logits [batch][B + 1][V], draft logits [batch][B][V]
+    with the sampler's lse [batch][B] and tokens [batch][B] ->
+    (accepted, next_token, n_new), int32 [batch] each."""
+    batch, B1, V = target_logits.shape
+    B = B1 - 1
+    dev = target_logits.device
+    if out is None:
+        out = tuple(torch.empty(batch, dtype=torch.int32, device=dev) for _ in range(3))
+    if workspace is None:
+        workspace = torch.empty(verify_workspace_bytes(batch, B, V), dtype=torch.uint8, device=dev)
+    acc, tok, n_new = out
+    _check(_lib().ldr_verify(_ptr(target_logits), _ptr(draft_logits), _ptr(draft_lse),
+                             _ptr(draft_tokens), batch, B, V, float(temperature), int(seed),
+                             int(step), _ptr(acc), _ptr(tok), _ptr(n_new), _ptr(workspace),
+                             workspace.numel(), _stream(stream)), "ldr_verify")
+    return out

@@ -29,6 +29,7 @@ SEED_PREFIX = 2
 SEED_ANCHOR = 3
 SEED_DECODE = 4  # decode step s uses SEED_DECODE + s
 SEED_GUMBEL = 5
+SEED_VERIFY = 6
 
 
 @dataclasses.dataclass(frozen=True)
@@ -209,6 +210,34 @@ def decode_rows(s: Shape, batch: int, n: int, step: int, device="cpu"):
     """K, V and h for decode step `step` (n rows per sequence)."""
     K, V = make_rows(s, batch, n, SEED_DECODE + step, device)
     return K, V, make_h(s, batch, SEED_DECODE + step, device)
+
+
+def verify_round(batch: int, block: int, vocab: int, seed: int = SEED_VERIFY, device="cpu",
+                 scale: float = 2.0, boost: float = 6.0, agree: float = 0.85,
+                 jitter: float = 0.3):
+    """A synthetic verification round: candidates y [batch][block] int32,
+    draft logits z [batch][block][vocab] and target logits P
+    [batch][block + 1][vocab], fp32. z ~ N(0, scale^2) plus `boost` on the
+    candidate's entry; target row i is z_i plus N(0, jitter^2) noise, and with
+    probability 1 - agree its boost moves from the candidate to another
+    uniform token; the last target row is N(0, scale^2) with a boost on a
+    uniform token."""
+    g = _gen(seed, device)
+    y = torch.randint(0, vocab, (batch, block), generator=g, device=device, dtype=torch.int64)
+    z = torch.randn(batch, block, vocab, generator=g, device=device) * scale
+    z.scatter_add_(2, y[..., None], torch.full((batch, block, 1), boost, device=device))
+    P = torch.empty(batch, block + 1, vocab, device=device)
+    P[:, :block] = z + torch.randn(batch, block, vocab, generator=g, device=device) * jitter
+    moved = torch.rand(batch, block, generator=g, device=device) >= agree
+    other = torch.randint(0, vocab, (batch, block), generator=g, device=device, dtype=torch.int64)
+    shift = torch.zeros(batch, block + 1, vocab, device=device)
+    shift[:, :block].scatter_add_(2, y[..., None], (-boost * moved.float())[..., None])
+    shift[:, :block].scatter_add_(2, other[..., None], (boost * moved.float())[..., None])
+    P[:, block] = torch.randn(batch, vocab, generator=g, device=device) * scale
+    last = torch.randint(0, vocab, (batch, 1), generator=g, device=device, dtype=torch.int64)
+    shift[:, block].scatter_add_(1, last, torch.full((batch, 1), boost, device=device))
+    P += shift
+    return y.to(torch.int32), z, P
 
 
 def to_f64(t: torch.Tensor):

@@ -97,6 +97,20 @@ def test_host_validation_needs_no_gpu(L):
                  (fake, 0, 2, 64, fake, fake, fake, 8, L.LDR_BF16)):  # batch
         assert lib.ldr_sample_markov(*args, 1.0, 0, 0, 0, fake, fake, fake, fake, ws,
                                      None) == L.LDR_EINVAL
+    vws = lib.ldr_verify_workspace_bytes(2, 3, 64)
+    assert vws > 0 and lib.ldr_verify_workspace_bytes(0, 3, 64) == 0
+    assert lib.ldr_verify_workspace_bytes(2, 0, 64) == 0
+    for args, T, n in (((None, fake, fake, fake, 2, 3, 64), 1.0, vws),    # no target logits
+                       ((fake, None, fake, fake, 2, 3, 64), 1.0, vws),    # T > 0, no draft logits
+                       ((fake, fake, None, fake, 2, 3, 64), 1.0, vws),    # T > 0, no draft lse
+                       ((fake, fake, fake, None, 2, 3, 64), 1.0, vws),    # no candidates
+                       ((fake, fake, fake, fake, 0, 3, 64), 1.0, vws),    # batch
+                       ((fake, fake, fake, fake, 2, 0, 64), 1.0, vws),    # block
+                       ((fake, fake, fake, fake, 2, 3, 64), -1.0, vws),   # temperature
+                       ((fake, fake, fake, fake, 2, 3, 64), float("nan"), vws),
+                       ((fake, fake, fake, fake, 2, 3, 64), float("inf"), vws),
+                       ((fake, fake, fake, fake, 2, 3, 64), 1.0, vws - 1)):  # short workspace
+        assert lib.ldr_verify(*args, T, 0, 0, fake, fake, fake, fake, n, None) == L.LDR_EINVAL
     assert lib.ldr_views_status(None, 0, None) == L.LDR_EINVAL
     lib.ldr_views_destroy(None)
     assert lib.ldr_sample_workspace_bytes(0, 10) == 0

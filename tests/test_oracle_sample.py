@@ -325,3 +325,20 @@ def test_out_of_range_candidates_are_rejected():
     for bad in (-1, V):
         r, tok, ratio, _ = verify(P, Z, np.array([[bad, 0]]), 1.0, 0, 0)
         assert r[0] == 0 and ratio[0, 0] == 0.0 and 0 <= tok[0] < V
+
+
+def test_residual_ignores_differences_below_the_cutoff():
+    """p above q by less than 2^-14 of p counts as equal: with no other
+    positive entry the round draws from p with the bonus rule."""
+    V = 6
+    q_logits = np.float32([1.0, 0.5, -0.2, 0.3, 2.0, -1.0])
+    P = np.tile(q_logits, (1, 2, 1)).astype(np.float32)
+    P[0, 0, 1] += np.float32(2e-5)          # p(1)/q(1) - 1 ~ 2e-5 < 2^-14 = 6.1e-5
+    Z = q_logits[None, None].astype(np.float32)
+    r, tok, _, _, keys = verify(P, Z, np.array([[V]]), 1.0, 3, 3, keys=True)
+    assert r[0] == 0
+    bonus = (P[0, 0] / np.float32(1.0) + verify_gumbel(3, 3, 0, np.arange(V))).astype(np.float32)
+    assert tok[0] == int(np.argmax(bonus)) and np.isfinite(keys[0]).all()
+    P[0, 0, 1] += np.float32(1e-3)          # now well above the cutoff: the only residual token
+    r, tok, _, _ = verify(P, Z, np.array([[V]]), 1.0, 3, 3)
+    assert r[0] == 0 and tok[0] == 1
