@@ -49,6 +49,9 @@ def parse():
     ap.add_argument("--markov-rank", type=int, default=0,
                     help="sample with the Markov correction (Eq. 7) of this rank instead of the "
                          "per-position sampler (0: off)")
+    ap.add_argument("--verify", action="store_true",
+                    help="verify each drafted block against synthetic target logits and "
+                         "commit r + 1 rows per step (closes the round on the device)")
     ap.add_argument("--cpu-seqs", type=int, default=16,
                     help="sequences in the CPU-oracle sample")
     ap.add_argument("--sweep", action="store_true")
@@ -114,7 +117,7 @@ class Rig:
     """Device-resident inputs and outputs of one workload."""
 
     def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False,
-                 tiled_head=True, markov_rank=0):
+                 tiled_head=True, markov_rank=0, verify=False):
         self.torch, self.ldr, self.s, self.batch = torch, ldr, shape, batch
         dev = "cuda"
         self.w = synth.make_weights(shape, device=dev)
@@ -161,6 +164,21 @@ class Rig:
                        0.02).to(shape.torch_dtype)
             self.Wc = (torch.randn(shape.vocab, markov_rank, generator=g, device=dev) *
                        0.02).to(shape.torch_dtype)
+        # Verification (Eq. 1-2) against a synthetic target: seeded fp32 logits
+        # [batch][B + 1][V] (no target model runs here). Each step then commits
+        # the r + 1 rows and the emitted token that the previous step's
+        # verification produced, on the device.
+        self.verify = verify
+        if verify:
+            B = shape.block
+            self.P = synth.normal((batch, B + 1, shape.vocab), 2.0, synth.SEED_VERIFY, device=dev)
+            self.vws = torch.empty(ldr.verify_workspace_bytes(batch, B, shape.vocab),
+                                   dtype=torch.uint8, device=dev)
+            self.vout = tuple(torch.empty(batch, dtype=torch.int32, device=dev) for _ in range(3))
+            self.n = self.vout[2]
+            self.n.fill_(self.n_new)
+            self.anchor = self.vout[1]
+            self.anchor.copy_(synth.make_anchors(shape, batch, device=dev))
         torch.cuda.synchronize()
         if self.views.status() != ldr.LDR_OK:
             raise RuntimeError("views status error after prefill")
@@ -181,6 +199,36 @@ class Rig:
         else:
             self.ldr.sample(self.logits.view(-1, self.s.vocab), temperature, 0, 5, i,
                             out=self.out, workspace=self.sws)
+        if self.verify:
+            self.verify_round(i, temperature)
+
+    def verify_round(self, i, temperature=1.0):
+        """ldr_verify of the step's draft; writes n (the next update's row
+        counts) and the next anchors in place."""
+        b, B = self.batch, self.s.block
+        self.ldr.verify(self.P, self.logits, self.out[1].view(b, B), self.out[0].view(b, B),
+                        temperature, 9, i, out=self.vout, workspace=self.vws)
+
+
+def verify_timing(torch, rig, ev, calls=20):
+    """ldr_verify alone, `calls` times between HIP events on the current
+    stream: µs per call and its algorithmic bytes (the B candidate rows of the
+    target read once by the lse pass; one target row and one draft row per
+    sequence read by the emit pass)."""
+    b, B, V = rig.batch, rig.s.block, rig.s.vocab
+    stream = torch.cuda.current_stream()
+    e0, e1 = ev.create(), ev.create()
+    rig.verify_round(0)
+    torch.cuda.synchronize()
+    ev.record(e0, stream)
+    for i in range(calls):
+        rig.verify_round(i)
+    ev.record(e1, stream)
+    torch.cuda.synchronize()
+    us = ev.elapsed_ms(e0, e1) * 1e3 / calls
+    nbytes = b * (B + 2) * V * 4
+    return {"us_per_call": us, "bytes_per_call": nbytes, "GB/s": nbytes / (us * 1e-6) / 1e9,
+            "hbm_frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
 
 
 def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
@@ -439,7 +487,7 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     s, batch = wl.shape, wl.batch
     rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head,
-              markov_rank=args.markov_rank)
+              markov_rank=args.markov_rank, verify=args.verify)
     ev = ldr.HipEvents()
     costs = launch_costs(s, batch)
     # which launch kind dominates the step (events around every launch, outside the timed run)
@@ -483,6 +531,9 @@ def main():
         "breakdown_us": {k: v * 1e3 for k, v in sorted(br.items(), key=lambda kv: -kv[1])},
         "state_bytes_per_seq": ldr.state_bytes(s),
     }
+    if rig.verify:
+        out["config"]["rows_per_update"] = "r + 1 from ldr_verify"
+        out["verify"] = verify_timing(torch, rig, ev)
     ev.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(torch, synth, rig, args.cpu_seqs)

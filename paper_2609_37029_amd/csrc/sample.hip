@@ -124,18 +124,6 @@ __global__ void __launch_bounds__(kSelThreads) topk_select_kernel(const float* l
   if (threadIdx.x == 0) sel[blockIdx.x] = TopK{prefix, v_cut};
 }
 
-// Upper bound of the Gumbel noise g = -log(-log u) of 23-bit uniform index k,
-// u = (2k + 1) 2^-24, from integer arithmetic: -log u >= 1 - u = n 2^-24 with
-// n = 2^24 - 1 - 2k, so g <= 24 ln2 - ln n, and ln n >= ln2 (e + m - 1) for
-// n = m 2^e, m in [1, 2) (log2 m >= m - 1 on [1, 2]).
-__device__ inline float gumbel_upper(uint32_t bits) {
-  const uint32_t n = 0xFFFFFFu - 2u * (bits >> 9);
-  const uint32_t nb = __float_as_uint((float)n);  // exact: n < 2^24
-  const float e = (float)((int)(nb >> 23) - 127);
-  const float m = __uint_as_float((nb & 0x7FFFFFu) | 0x3F800000u);
-  return __uint_as_float(0x3F317218u) * (25.0f - e - m);  // ln2 rounded up
-}
-
 // Temperature sampling. Every lane keeps the lse partial of its tokens and the
 // best (key, token) of the candidates it evaluated. A token is a candidate
 // unless zt + bound(g) + margin < the lane's best key, which proves that its

@@ -10,19 +10,19 @@
 // bonus draw from p_{B+1}. r accepted candidates advance the prefix by r + 1,
 // which is the row count the next views update takes.
 //
-// Three launches at T > 0:
+// Four launches at T > 0:
 //  1. lse pass: one workgroup per (vocabulary chunk, candidate row) streams the
 //     B target rows of every sequence once (16-byte loads) and writes the
 //     chunk's running max and sum of exp(P / T);
-//  2. emit pass: one workgroup per (vocabulary chunk, sequence) merges the lse
-//     partials, repeats the in-order acceptance test (B exponentials), and
-//     streams the one target row (and draft row) where the round stops: Gumbel
-//     keys log w_v + g_v over the residual w = [p - q]_+ (entries where p
-//     exceeds q by more than 2^-14 of p), and the bonus-rule
-//     keys fl(fl(P_v / T) + g_v) (the draw at a bonus, and the fallback when
-//     the residual has no positive mass); the first workgroup of a sequence
-//     writes r and r + 1;
-//  3. merge: the best key over the chunks, lower token first on ties.
+//  2. decide: one wave per sequence merges the lse partials, takes the
+//     in-order acceptance test (B exponentials) and writes r, r + 1 and the
+//     normalisers of the row where the round stops;
+//  3. emit pass: one workgroup per (sequence, vocabulary chunk) streams that
+//     target row (and draft row, 16-byte loads): Gumbel keys log w_v + g_v
+//     over the residual w = [p - q]_+ (entries where p exceeds q by more than
+//     2^-14 of p), and the bonus-rule keys fl(fl(P_v / T) + g_v) (the draw at
+//     a bonus, and the fallback when the residual has no positive mass);
+//  4. merge: the best key over the chunks, lower token first on ties.
 // T = 0 verifies greedily: pass 1 takes the first argmax of all B + 1 rows and
 // the merge compares them with the candidates.
 //
@@ -43,6 +43,7 @@ constexpr float kResidualRel = 6.103515625e-05f;   // 2^-14
 
 struct LsePart { float m, s; int idx, pad; };     // max P / T, sum exp(P / T - m); argmax at T = 0
 struct EmitPart { float kr; int ir; float kb; int ib; };  // best residual key / bonus-rule key
+struct Decision { int stop; float plse, qlse; int pad; };  // where a sequence stops, its normalisers
 
 __device__ inline bool better(float k1, int i1, float k2, int i2) {
   return k1 > k2 || (k1 == k2 && i1 < i2);
@@ -72,6 +73,7 @@ struct VerifyArgs {
   int chunk2, splits2;   // emit pass
   LsePart* lpart;        // [batch * rows][splits1]
   EmitPart* epart;       // [batch][splits2]
+  Decision* dec;         // [batch]
   int32_t* accepted; int32_t* token; int32_t* n_new;
 };
 
@@ -171,50 +173,107 @@ __device__ int stop_position(const VerifyArgs& a, int b) {
   return a.B;
 }
 
-template <bool UNIT_T>
+// One wave per sequence: the acceptance test, r and r + 1, and the
+// normalisers of the row where the round stops.
+__global__ void __launch_bounds__(64) verify_decide_kernel(VerifyArgs a) {
+  const int b = blockIdx.x;
+  const int stop = stop_position(a, b);
+  if (threadIdx.x == 0) {
+    Decision d{stop, 0.f, 0.f, 0};
+    if (stop < a.B) { d.plse = row_lse(a, b, stop); d.qlse = a.qlse[(long)b * a.B + stop]; }
+    a.dec[b] = d;
+    a.accepted[b] = stop;
+    a.n_new[b] = stop + 1;
+  }
+}
+
+template <bool UNIT_T, bool VEC>
 __global__ void __launch_bounds__(kThreads) verify_emit_kernel(VerifyArgs a) {
   const int b = blockIdx.x, sp = blockIdx.y;
-  __shared__ int s_stop;
-  __shared__ float s_plse, s_qlse;
-  if (threadIdx.x < 64) {
-    const int stop = stop_position(a, b);
-    if (threadIdx.x == 0) {
-      s_stop = stop;
-      if (stop < a.B) { s_plse = row_lse(a, b, stop); s_qlse = a.qlse[(long)b * a.B + stop]; }
-      if (sp == 0) {
-        a.accepted[b] = stop;
-        a.n_new[b] = stop + 1;
-      }
-    }
-  }
-  __syncthreads();
-  const int stop = s_stop;
+  const Decision d = a.dec[b];
+  const int stop = d.stop;
   const bool residual = stop < a.B;
-  const float plse = residual ? s_plse : 0.f, qlse = residual ? s_qlse : 0.f;
+  const float plse = d.plse, qlse = d.qlse;
   const float* p = a.P + ((long)b * (a.B + 1) + stop) * a.V;
   const float* z = residual ? a.z + ((long)b * a.B + stop) * a.V : nullptr;
   const int v0 = sp * a.chunk2, v1 = min(a.V, v0 + a.chunk2);
   EmitPart e{-INFINITY, kInvalid, -INFINITY, kInvalid};
-  for (int vb = v0 + (int)threadIdx.x * kGroup; vb < v1; vb += kThreads * kGroup) {
+  // A token's exact keys (two logarithms for g, more for the residual) are
+  // computed only where an upper bound from the noise bits cannot rule them
+  // out: g <= gumbel_upper(bits), so kb <= pt + bound and, as w <= p,
+  // kr <= pt - plse + bound. The bounds are tested against the best keys of
+  // the whole wave so far, seeded in each sweep by the exact keys of every
+  // lane's largest logit. The margin covers the rounding of the bound and of
+  // the exact keys: a token skipped has a key strictly below the best.
+  auto exact = [&](int v, float pt, float zv, uint32_t word, bool want_b, bool want_r) {
+    const float g = gumbel_from_bits(word);
+    if (want_b) {
+      const float kb = __fadd_rn(pt, g);
+      if (better(kb, v, e.kb, e.ib)) { e.kb = kb; e.ib = v; }
+    }
+    if (want_r) {
+      const float zt = UNIT_T ? zv : zv / a.T;
+      const float pv = expf(pt - plse);
+      const float w = pv - expf(zt - qlse);
+      if (w > kResidualRel * pv) {
+        const float kr = logf(w) + g;
+        if (better(kr, v, e.kr, e.ir)) { e.kr = kr; e.ir = v; }
+      }
+    }
+  };
+  for (int vb0 = v0; vb0 < v1; vb0 += kThreads * kGroup) {
+    const int vb = vb0 + (int)threadIdx.x * kGroup;
     uint32_t bits[kGroup];
     noise_group(a.seed, a.step, (uint64_t)b, 2, (uint64_t)(vb / kGroup), bits);
+    float pr[kGroup], zr[kGroup];
+    if (VEC && vb + kGroup <= v1) {   // 16-byte aligned: V % 4 == 0 and vb % 8 == 0
+      const float4 p0 = *reinterpret_cast<const float4*>(p + vb);
+      const float4 p1 = *reinterpret_cast<const float4*>(p + vb + 4);
+      pr[0] = p0.x; pr[1] = p0.y; pr[2] = p0.z; pr[3] = p0.w;
+      pr[4] = p1.x; pr[5] = p1.y; pr[6] = p1.z; pr[7] = p1.w;
+      if (residual) {
+        const float4 z0 = *reinterpret_cast<const float4*>(z + vb);
+        const float4 z1 = *reinterpret_cast<const float4*>(z + vb + 4);
+        zr[0] = z0.x; zr[1] = z0.y; zr[2] = z0.z; zr[3] = z0.w;
+        zr[4] = z1.x; zr[5] = z1.y; zr[6] = z1.z; zr[7] = z1.w;
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < kGroup; ++k) {
+        pr[k] = vb + k < v1 ? p[vb + k] : -INFINITY;
+        zr[k] = residual && vb + k < v1 ? z[vb + k] : 0.f;
+      }
+    }
+    float pt[kGroup];
+    int km = 0;
+#pragma unroll
+    for (int k = 0; k < kGroup; ++k) {
+      pt[k] = UNIT_T ? pr[k] : pr[k] / a.T;   // IEEE division, as the drafting sampler
+      if (pt[k] > pt[km]) km = k;
+    }
+    // seed: the exact keys of the lane's largest logit, then the wave's best
+    if (vb + km < v1) {
+      float zkm = zr[0];
+      uint32_t wkm = bits[0];
+#pragma unroll
+      for (int k = 1; k < kGroup; ++k)
+        if (k == km) { zkm = zr[k]; wkm = bits[k]; }
+      exact(vb + km, pt[km], zkm, wkm, true, residual);
+    }
+    float tb = e.kb, tr = e.kr;
+    for (int off = 32; off >= 1; off >>= 1) {
+      tb = fmaxf(tb, __shfl_xor(tb, off));
+      tr = fmaxf(tr, __shfl_xor(tr, off));
+    }
 #pragma unroll
     for (int k = 0; k < kGroup; ++k) {
       const int v = vb + k;
-      if (v >= v1) break;
-      const float g = gumbel_from_bits(bits[k]);
-      const float pt = UNIT_T ? p[v] : p[v] / a.T;   // IEEE division, as the drafting sampler
-      const float kb = __fadd_rn(pt, g);
-      if (better(kb, v, e.kb, e.ib)) { e.kb = kb; e.ib = v; }
-      if (residual) {
-        const float zt = UNIT_T ? z[v] : z[v] / a.T;
-        const float pv = expf(pt - plse);
-        const float w = pv - expf(zt - qlse);
-        if (w > kResidualRel * pv) {
-          const float kr = logf(w) + g;
-          if (better(kr, v, e.kr, e.ir)) { e.kr = kr; e.ir = v; }
-        }
-      }
+      if (v >= v1 || k == km) continue;
+      const float gu = gumbel_upper(bits[k]);
+      const bool need_b = !(pt[k] + gu + (1e-3f + 1e-6f * (fabsf(pt[k]) + fabsf(tb))) < tb);
+      const float lp = pt[k] - plse;
+      const bool need_r = residual && !(lp + gu + (1e-3f + 1e-6f * (fabsf(lp) + fabsf(tr))) < tr);
+      if (need_b || need_r) exact(v, pt[k], zr[k], bits[k], need_b, need_r);
     }
   }
   for (int off = 32; off >= 1; off >>= 1) {
@@ -297,9 +356,9 @@ Plan make_plan(int batch, int B, int V, bool greedy) {
   s1 = s1 < 1 ? 1 : (s1 > max1 ? max1 : s1);
   p.chunk1 = ((V + s1 - 1) / s1 + sweep1 - 1) / sweep1 * sweep1;
   p.splits1 = (V + p.chunk1 - 1) / p.chunk1;
-  // emit pass: about 1024 workgroups, chunks of whole Philox sweeps
+  // emit pass: about 512 workgroups, chunks of whole Philox sweeps
   const int sweep2 = kGroup * kThreads;
-  int s2 = batch >= 1024 ? 1 : 1024 / batch;
+  int s2 = batch >= 512 ? 1 : 512 / batch;
   const int max2 = (V + sweep2 - 1) / sweep2;
   s2 = s2 < 1 ? 1 : (s2 > max2 ? max2 : s2);
   p.chunk2 = ((V + s2 - 1) / s2 + sweep2 - 1) / sweep2 * sweep2;
@@ -313,7 +372,7 @@ size_t verify_workspace_bytes(int batch, int B, int V) {
   const Plan g = make_plan(batch, B, V, true), t = make_plan(batch, B, V, false);
   const size_t l1 = (size_t)batch * (B + 1) * g.splits1, l2 = (size_t)batch * B * t.splits1;
   const size_t lse = align_up((l1 > l2 ? l1 : l2) * sizeof(LsePart));
-  return lse + (size_t)batch * t.splits2 * sizeof(EmitPart);
+  return lse + align_up((size_t)batch * t.splits2 * sizeof(EmitPart)) + batch * sizeof(Decision);
 }
 
 hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const float* qlse,
@@ -331,8 +390,12 @@ hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const
   a.lpart = static_cast<LsePart*>(ws);
   a.epart = reinterpret_cast<EmitPart*>(static_cast<uint8_t*>(ws) +
                                         align_up((l1 > l2 ? l1 : l2) * sizeof(LsePart)));
+  a.dec = reinterpret_cast<Decision*>(reinterpret_cast<uint8_t*>(a.epart) +
+                                      align_up((size_t)batch * pl.splits2 * sizeof(EmitPart)));
   a.accepted = accepted; a.token = token; a.n_new = n_new;
-  const bool vec = V % 4 == 0;
+  // 16-byte loads need rows that start on 16 bytes
+  const bool vec = V % 4 == 0 && reinterpret_cast<uintptr_t>(P) % 16 == 0 &&
+                   reinterpret_cast<uintptr_t>(z) % 16 == 0;
   const int rows = batch * (greedy ? B + 1 : B);
   const dim3 g1(rows, pl.splits1);
   if (greedy) {
@@ -349,10 +412,18 @@ hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const dim3 g2(batch, pl.splits2);
-  if (T == 1.f) hipLaunchKernelGGL((verify_emit_kernel<true>), g2, dim3(kThreads), 0, st, a);
-  else hipLaunchKernelGGL((verify_emit_kernel<false>), g2, dim3(kThreads), 0, st, a);
+  hipLaunchKernelGGL(verify_decide_kernel, dim3(batch), dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 g2(batch, pl.splits2);
+  if (T == 1.f) {
+    if (vec) hipLaunchKernelGGL((verify_emit_kernel<true, true>), g2, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((verify_emit_kernel<true, false>), g2, dim3(kThreads), 0, st, a);
+  } else {
+    if (vec) hipLaunchKernelGGL((verify_emit_kernel<false, true>), g2, dim3(kThreads), 0, st, a);
+    else hipLaunchKernelGGL((verify_emit_kernel<false, false>), g2, dim3(kThreads), 0, st, a);
+  }
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(verify_merge_kernel, dim3(batch), dim3(64), 0, st, a);
   return hipGetLastError();
