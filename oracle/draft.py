@@ -96,12 +96,13 @@ def layer(s, L, x, st: _views.ViewState, G, j):
     pos = st.t + np.arange(B)
     base = rope_base(s)
     q, k = rope(q, pos, base), rope(k, pos, base)
-    valid = _views.window_valid(s, st.t)
+    valid = _views.window_valid(s, st.t) & _views.keeps(s, _views.DROP_WINDOW)
+    has_summary = st.t > 0 and _views.keeps(s, _views.DROP_SUMMARY)
     o = np.empty((B, Hq, d))
     for h in range(Hq):
         g = h // rep
         o[:, h] = block_attention(q[:, h], k[:, g], v[:, g], st.Kw[j, g], st.Vw[j, g],
-                                  valid, G[j, h], st.M[j, h], st.t > 0)
+                                  valid, G[j, h], st.M[j, h], has_summary)
     x = x + o.reshape(B, Hq * d) @ L["wo"].T
     n2 = rmsnorm(x, L["post_norm"], s.rms_eps)
     gu = n2 @ L["w_gate_up"].T
@@ -113,8 +114,13 @@ def forward(s, Wt, st: _views.ViewState, G, anchor, vocab_idx=None, trace=None):
     """Base logits z^(0) [B][V] (or [B][len(vocab_idx)] for a vocabulary
     sample) of one sequence. Wt: float64 weight dict (synth layout),
     st: that sequence's views, G: [D][Hq][R][d], anchor: the committed token.
-    `trace`, if a dict, receives c, the slot inputs and every layer output."""
-    c = boundary_fusion(s, Wt, st.h)
+    `trace`, if a dict, receives c, the slot inputs and every layer output.
+    A drafter without the boundary view (ablation variant) has c = 0; one
+    without the window or the summary attends to the other sources only."""
+    if _views.keeps(s, _views.DROP_BOUNDARY):
+        c = boundary_fusion(s, Wt, st.h)
+    else:
+        c = np.zeros(s.hidden)
     x = slot_init(s, Wt, c, int(anchor))
     if trace is not None:
         trace["c"], trace["x0"] = c, x.copy()

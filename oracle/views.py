@@ -79,28 +79,42 @@ def merge(eta_a, m_a, eta_n, m_n):
     return out_eta, out_m
 
 
+# Ablation variants (Sec. 3.4, Fig. "ablation"; App. D.3): a drafter built
+# without one of the three views neither keeps nor reads it. Bits of
+# `drop_views` in the shape:
+DROP_WINDOW, DROP_SUMMARY, DROP_BOUNDARY = 1, 2, 4
+
+
+def keeps(s, bit) -> bool:
+    """Whether the shape's drafter keeps the view `bit`."""
+    return not (getattr(s, "drop_views", 0) & bit)
+
+
 def update(s, st: ViewState, G, K_new, V_new, h_new) -> ViewState:
     """Ingest n new target rows (Sec. 2.4, Inference; App. A.2).
 
     K_new, V_new: [n][D][Hkv][d] rows for positions t..t+n-1. h_new:
     [L_b][hidden] boundary states at the new boundary. n = 0 returns the
     state unchanged, h included (no row was committed, the boundary did not
-    move)."""
+    move). A dropped view (ablation variants) stays as `empty` made it."""
     n = K_new.shape[0]
     out = st.copy()
     if n == 0:
         return out
     W, d = s.window, s.head_dim
     rep = s.n_q_heads // s.n_kv_heads
-    for r in range(n):                              # ring write, in order
-        out.Kw[:, :, (st.t + r) % W, :] = K_new[r]
-        out.Vw[:, :, (st.t + r) % W, :] = V_new[r]
-    for j in range(s.n_layers):
-        for h in range(s.n_q_heads):
-            g = h // rep                            # the head's K/V group
-            eta_n, m_n = set_statistics(G[j, h], K_new[:, j, g, :], V_new[:, j, g, :], d)
-            out.eta[j, h], out.M[j, h] = merge(st.eta[j, h], st.M[j, h], eta_n, m_n)
-    out.h = np.array(h_new, dtype=np.float64, copy=True)
+    if keeps(s, DROP_WINDOW):
+        for r in range(n):                          # ring write, in order
+            out.Kw[:, :, (st.t + r) % W, :] = K_new[r]
+            out.Vw[:, :, (st.t + r) % W, :] = V_new[r]
+    if keeps(s, DROP_SUMMARY):
+        for j in range(s.n_layers):
+            for h in range(s.n_q_heads):
+                g = h // rep                        # the head's K/V group
+                eta_n, m_n = set_statistics(G[j, h], K_new[:, j, g, :], V_new[:, j, g, :], d)
+                out.eta[j, h], out.M[j, h] = merge(st.eta[j, h], st.M[j, h], eta_n, m_n)
+    if keeps(s, DROP_BOUNDARY):
+        out.h = np.array(h_new, dtype=np.float64, copy=True)
     out.t = st.t + n
     return out
 
@@ -155,4 +169,5 @@ def state_bytes(s) -> int:
     window = 2 * s.n_layers * s.window * s.n_kv_heads * s.head_dim * el
     summary = s.n_layers * s.n_q_heads * s.summary * (s.head_dim + 1) * 4
     boundary = s.n_feat_layers * s.hidden * el
-    return window + summary + boundary
+    return (window * keeps(s, DROP_WINDOW) + summary * keeps(s, DROP_SUMMARY) +
+            boundary * keeps(s, DROP_BOUNDARY))

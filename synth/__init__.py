@@ -53,6 +53,7 @@ class Shape:
     ntk_alpha: float = 1.0
     rms_eps: float = 1.0e-6
     dtype: str = "bf16"  # "bf16" or "f32": weights, window rows, G, boundary h
+    drop_views: int = 0  # ablation variants: 1 no window, 2 no summary, 4 no boundary (sums)
 
     @property
     def qkv_out(self) -> int:

@@ -124,16 +124,20 @@ def _loop_matvec(Wm, x):            # Wm [out][in] (nn.Linear), y_o = sum_i W[o]
     return [sum(Wm[o][i] * x[i] for i in range(len(x))) for o in range(len(Wm))]
 
 
-def brute_forward(s, Wt, st, G, a):
+def brute_forward(s, Wt, st, G, a, no_window=False, no_summary=False, no_boundary=False):
+    """The whole forward with scalar loops; the flags leave a view's source out
+    (ablation variants), whatever `st` holds for it."""
     B, H, Hk, d, hid = s.block, s.n_q_heads, s.n_kv_heads, s.head_dim, s.hidden
     base = s.rope_theta * s.ntk_alpha ** (d / (d - 2))
     hcat = [v for l in range(s.n_feat_layers) for v in st.h[l]]
     c = _loop_rms(_loop_matvec(Wt["fc_w"], hcat), Wt["fc_norm"], s.rms_eps)
+    if no_boundary:
+        c = [0.0] * hid
     x = []
     for i in range(B):
         e = Wt["embed"][a] if i == 0 else Wt["mask_emb"]
         x.append([e[k] + Wt["pos_emb"][i][k] + c[k] for k in range(hid)])
-    nvalid = min(st.t, s.window)
+    nvalid = 0 if no_window else min(st.t, s.window)
     for j in range(s.n_layers):
         L = Wt["layers"][j]
         q = [[None] * H for _ in range(B)]
@@ -161,7 +165,7 @@ def brute_forward(s, Wt, st, G, a):
                 g = h // (H // Hk)
                 keys = [k[b][g] for b in range(B)] + [list(st.Kw[j, g, p]) for p in range(nvalid)]
                 vals = [v[b][g] for b in range(B)] + [list(st.Vw[j, g, p]) for p in range(nvalid)]
-                if st.t > 0:
+                if st.t > 0 and not no_summary:
                     keys += [list(G[j, h, r]) for r in range(s.summary)]
                     vals += [list(st.M[j, h, r]) for r in range(s.summary)]
                 sc = [sum(q[i][h][e] * kk[e] for e in range(d)) / math.sqrt(d) for kk in keys]
@@ -188,6 +192,57 @@ def test_forward_matches_loop_brute_force(t):
     ref = brute_forward(s, Wt, st, G, 6)
     assert got.shape == (s.block, s.vocab)
     np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-11)
+
+
+@pytest.mark.parametrize("drop", [1, 2, 4, 3, 7])
+@pytest.mark.parametrize("t", [0, 3, 12])
+def test_view_drop_variants_match_loop_brute_force(drop, t):
+    """Ablation variants (Sec. 3.4, App. D.3): the variant's own update and
+    forward equal the brute force over the full views with the dropped
+    sources left out."""
+    full = MICRO
+    s = MICRO.replace(drop_views=drop)
+    Wt = rand_weights(s, 11)
+    st_full, G = rand_state(full, t, 12)
+    st, _ = rand_state(s, t, 12)
+    got = Dr.forward(s, Wt, st, G, 6)
+    ref = brute_forward(full, Wt, st_full, G, 6, no_window=bool(drop & 1),
+                        no_summary=bool(drop & 2), no_boundary=bool(drop & 4))
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-11)
+    if t:
+        assert not np.allclose(got, Dr.forward(full, Wt, st_full, G, 6))
+
+
+def test_no_boundary_is_a_zero_fusion_weight():
+    """c = RMSNorm(0) = 0: dropping the boundary view equals W_fc = 0."""
+    s = MICRO.replace(drop_views=4)
+    Wt = rand_weights(s, 21)
+    st, G = rand_state(MICRO, 9, 22)
+    W0 = dict(Wt)
+    W0["fc_w"] = np.zeros_like(Wt["fc_w"])
+    np.testing.assert_allclose(Dr.forward(s, Wt, st, G, 3), Dr.forward(MICRO, W0, st, G, 3),
+                               rtol=1e-12, atol=1e-13)
+
+
+def test_dropped_views_are_not_kept_and_do_not_count():
+    """The variant keeps the other views exactly as the full drafter does, and
+    its state bytes lose exactly the dropped view's term."""
+    st_full, G = rand_state(MICRO, 9, 5)
+    for drop in (1, 2, 4):
+        s = MICRO.replace(drop_views=drop)
+        st, _ = rand_state(s, 9, 5)
+        assert st.t == st_full.t
+        assert np.array_equal(st.Kw, st_full.Kw) != bool(drop & 1)
+        assert np.array_equal(st.M, st_full.M) != bool(drop & 2)
+        assert np.array_equal(st.h, st_full.h) != bool(drop & 4)
+    el = 4
+    win = 2 * MICRO.n_layers * MICRO.window * MICRO.n_kv_heads * MICRO.head_dim * el
+    summ = MICRO.n_layers * MICRO.n_q_heads * MICRO.summary * (MICRO.head_dim + 1) * 4
+    bnd = MICRO.n_feat_layers * MICRO.hidden * el
+    assert V.state_bytes(MICRO) == win + summ + bnd
+    assert V.state_bytes(MICRO.replace(drop_views=1)) == summ + bnd
+    assert V.state_bytes(MICRO.replace(drop_views=2)) == win + bnd
+    assert V.state_bytes(MICRO.replace(drop_views=4)) == win + summ
 
 
 def test_gqa_equals_duplicated_kv_heads():
