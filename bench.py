@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--markov-rank", type=int, default=0,
                     help="sample with the Markov correction (Eq. 7) of this rank instead of the "
                          "per-position sampler (0: off)")
+    ap.add_argument("--drop-views", type=int, default=0,
+                    help="ablation variant: 1 no window, 2 no summary, 4 no boundary")
     ap.add_argument("--verify", action="store_true",
                     help="verify each drafted block against synthetic target logits and "
                          "commit r + 1 rows per step (closes the round on the device)")
@@ -88,11 +90,13 @@ def launch_costs(s, batch):
     # QKV finishing: fp32 projection in, q/k/v rows out, rotary table and gains
     c["qkv_finish"] = (M * s.qkv_out * (4 + el) + M * s.head_dim * 4 + 2 * s.head_dim * el, 0)
     # attention: window K/V of the layer + G and M of its heads + block q/k/v in, o out
-    win = batch * 2 * s.n_kv_heads * s.window * s.head_dim * el
-    summ = s.n_q_heads * s.summary * s.head_dim * el + batch * s.n_q_heads * s.summary * \
-        s.head_dim * 4
+    drop = getattr(s, "drop_views", 0)        # ablation variants read fewer sources
+    nw = 0 if drop & 1 else s.window
+    nr = 0 if drop & 2 else s.summary
+    win = batch * 2 * s.n_kv_heads * nw * s.head_dim * el
+    summ = s.n_q_heads * nr * s.head_dim * el + batch * s.n_q_heads * nr * s.head_dim * 4
     qkv = M * s.qkv_out * el + M * s.n_q_heads * s.head_dim * el
-    nk = s.block + s.window + s.summary
+    nk = s.block + nw + nr
     c["attention"] = (win + summ + qkv, 4 * M * s.n_q_heads * nk * s.head_dim)
     norm = M * H * 4 * 2 + M * H * el
     c["post_norm"] = (norm, 0)
@@ -486,6 +490,8 @@ def main():
 
     wl = synth.WORKLOADS[args.workload]
     s, batch = wl.shape, wl.batch
+    if args.drop_views:
+        s = s.replace(drop_views=args.drop_views)
     rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head,
               markov_rank=args.markov_rank, verify=args.verify)
     ev = ldr.HipEvents()
@@ -517,7 +523,9 @@ def main():
                    "prefix": wl.prefix, "rows_per_update": s.block + 1, "temperature": 1.0,
                    "window": s.window, "summary": s.summary, "draft_layers": s.n_layers,
                    "lm_head_layout": "tiled" if rig.tiled_head else "row-major",
-                   "sampler": f"markov rank {rig.markov_rank}" if rig.markov_rank else "per-position"},
+                   "sampler": f"markov rank {rig.markov_rank}" if rig.markov_rank else "per-position",
+                   "views": {0: "window + summary + boundary", 1: "no window", 2: "no summary",
+                             4: "no boundary"}.get(s.drop_views, f"drop {s.drop_views}")},
         "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,
                         "p90": percentile(per_step, .9) * 1e3},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,

@@ -45,6 +45,17 @@ enum ldr_status {
 
 enum ldr_dtype { LDR_F32 = 0, LDR_BF16 = 1 };
 
+/* Views an ablation variant leaves out (Sec. 3.4, App. D.3): bits of
+ * ldr_config.drop_views. A dropped view is neither kept nor read: its arena
+ * region has zero bytes, the update skips it and the draft step attends to
+ * the other sources only (no window rows; no summary entries), or takes
+ * c_t = 0 without the boundary-fusion GEMM. */
+enum ldr_view_drop {
+  LDR_DROP_WINDOW = 1,    /* no recent K/V window                          */
+  LDR_DROP_SUMMARY = 2,   /* no global summary (G may then be NULL)        */
+  LDR_DROP_BOUNDARY = 4   /* no boundary state (h may then be NULL)        */
+};
+
 /* Drafter shape (App. B.1: D = 5 Qwen3-style layers, W = 256, R = 16). */
 typedef struct ldr_config {
   int32_t hidden;        /* model width                                        */
@@ -63,6 +74,8 @@ typedef struct ldr_config {
   float rope_theta;      /* rotary base                                        */
   float ntk_alpha;       /* fixed NTK scaling: base = theta * alpha^(d/(d-2))  */
   float rms_eps;         /* RMSNorm epsilon                                    */
+  int32_t drop_views;    /* 0 (the full drafter) or a sum of ldr_view_drop bits
+                            that keeps at least one view                     */
 } ldr_config;
 
 /* Device pointers of one draft layer (Qwen3-style block, App. B.1). */
@@ -104,8 +117,9 @@ typedef struct ldr_views ldr_views; /* opaque host handle */
  * complexity): window K [D][Hkv][W][d] and window V stored transposed,
  * [D][Hkv][d][W] (dtype; slot p mod W of position p), summary values
  * [D][Hq][R][d] and log-normalizers [D][Hq][R] (fp32), boundary states
- * [L_b][hidden] (dtype), each region 256-byte aligned. No term depends on the
- * prefix length. Returns 0 for an invalid configuration. */
+ * [L_b][hidden] (dtype), each region 256-byte aligned; a view the
+ * configuration drops has zero bytes. No term depends on the prefix length.
+ * Returns 0 for an invalid configuration. */
 size_t ldr_views_state_bytes(const ldr_config* cfg);
 
 /* Byte stride between sequences in the arena (state bytes rounded up to 256),

@@ -26,6 +26,8 @@ bool make_shape(const ldr_config* c, Shape* s) {
   if (c->window < 1 || c->summary < 1) return false;
   if (c->dtype != LDR_F32 && c->dtype != LDR_BF16) return false;
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f) || !(c->ntk_alpha > 0.f)) return false;
+  const int all = LDR_DROP_WINDOW | LDR_DROP_SUMMARY | LDR_DROP_BOUNDARY;
+  if ((c->drop_views & ~all) || c->drop_views == all) return false;   // at least one view
   s->hidden = c->hidden; s->hq = c->n_q_heads; s->hkv = c->n_kv_heads; s->d = c->head_dim;
   s->mlp = c->mlp; s->vocab = c->vocab; s->D = c->n_layers; s->Lb = c->n_feat_layers;
   s->B = c->block; s->W = c->window; s->R = c->summary; s->dtype = c->dtype;
@@ -35,6 +37,9 @@ bool make_shape(const ldr_config* c, Shape* s) {
   s->rope_base = (double)c->rope_theta *
                  std::pow((double)c->ntk_alpha, (double)s->d / (double)(s->d - 2));
   s->el = c->dtype == LDR_BF16 ? 2 : 4;
+  s->keep_win = !(c->drop_views & LDR_DROP_WINDOW);
+  s->keep_sum = !(c->drop_views & LDR_DROP_SUMMARY);
+  s->keep_bnd = !(c->drop_views & LDR_DROP_BOUNDARY);
   if (views_dims_per_thread(*s) == 0 || !norm_hidden_supported(s->hidden)) return false;
   if (s->dtype == LDR_BF16) {
     if (!attention_mfma_supported(s->d, s->rep, s->B, s->R, s->W)) return false;
@@ -46,13 +51,15 @@ bool make_shape(const ldr_config* c, Shape* s) {
 
 Layout make_layout(const Shape& s) {
   Layout L;
-  const size_t win = (size_t)s.D * s.hkv * s.W * s.d * s.el;
+  // a dropped view has zero bytes (its offset is that of the next region)
+  const size_t win = s.keep_win ? (size_t)s.D * s.hkv * s.W * s.d * s.el : 0;
+  const size_t sum = s.keep_sum ? (size_t)s.D * s.hq * s.R : 0;
   L.kw = 0;
   L.vw = align_up(L.kw + win);
   L.m = align_up(L.vw + win);
-  L.eta = align_up(L.m + (size_t)s.D * s.hq * s.R * s.d * 4);
-  L.h = align_up(L.eta + (size_t)s.D * s.hq * s.R * 4);
-  L.bytes = L.h + (size_t)s.Lb * s.hidden * s.el;
+  L.eta = align_up(L.m + sum * s.d * 4);
+  L.h = align_up(L.eta + sum * 4);
+  L.bytes = L.h + (s.keep_bnd ? (size_t)s.Lb * s.hidden * s.el : 0);
   L.stride = align_up(L.bytes);
   return L;
 }
@@ -173,7 +180,7 @@ static int views_update_impl(ldr_views* v, const int32_t* n_new, int32_t max_new
   if (!v || !n_new || max_new < 0) return LDR_EINVAL;
   if (max_new > 0 && (!K_new || !V_new || !aligned(K_new, 16) || !aligned(V_new, 16)))
     return LDR_EINVAL;
-  if (!h_new || !aligned(h_new, 16)) return LDR_EINVAL;
+  if (v->s.keep_bnd && (!h_new || !aligned(h_new, 16))) return LDR_EINVAL;
   if (max_new > 0) {
     if (launch_views_update(v->s, v->L, v->batch, v->arena, v->pos, v->G, n_new, max_new, K_new,
                             V_new, h_new, st) != hipSuccess)
@@ -191,8 +198,9 @@ int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* 
   if (!out) return LDR_EINVAL;
   *out = nullptr;
   Shape s;
-  if (!make_shape(cfg, &s) || batch <= 0 || !arena || !pos || !G) return LDR_EINVAL;
-  if (!aligned(arena, kAlign) || !aligned(G, 16) || !aligned(pos, 8)) return LDR_EINVAL;
+  if (!make_shape(cfg, &s) || batch <= 0 || !arena || !pos) return LDR_EINVAL;
+  if (s.keep_sum && (!G || !aligned(G, 16))) return LDR_EINVAL;   // G: the summary's queries
+  if (!aligned(arena, kAlign) || !aligned(pos, 8)) return LDR_EINVAL;
   if (max_prefix < 0 || (max_prefix > 0 && !n_prefix)) return LDR_EINVAL;
   ldr_views* v = new (std::nothrow) ldr_views;
   if (!v) return LDR_ENOMEM;
@@ -250,10 +258,12 @@ void ldr_views_destroy(ldr_views* v) {
 
 static bool weights_ok(const Shape& s, const ldr_weights* w) {
   if (!w || !w->layers) return false;
-  const void* top[] = {w->embed, w->mask_emb, w->pos_emb, w->fc_w, w->fc_norm, w->final_norm,
-                       w->lm_head};
+  const void* top[] = {w->embed, w->mask_emb, w->pos_emb, w->final_norm, w->lm_head};
   for (const void* p : top)
     if (!p || !aligned(p, 16)) return false;
+  if (s.keep_bnd)   // the boundary fusion exists only with the boundary view
+    for (const void* p : {w->fc_w, w->fc_norm})
+      if (!p || !aligned(p, 16)) return false;
   for (int j = 0; j < s.D; ++j) {
     const ldr_layer_weights& L = w->layers[j];
     const void* ps[] = {L.in_norm, L.wqkv, L.q_norm, L.k_norm, L.wo, L.post_norm, L.w_gate_up,
@@ -271,7 +281,7 @@ static bool weights_ok(const Shape& s, const ldr_weights* w) {
 // and the step itself so the two cannot disagree.
 template <typename Emit>
 static int draft_sequence(const Shape& s, int D, Emit&& emit) {
-  int rc = emit(LDR_LAUNCH_FC_GEMM, 0);
+  int rc = s.keep_bnd ? emit(LDR_LAUNCH_FC_GEMM, 0) : (int)LDR_OK;   // no boundary: c = 0
   if (rc == LDR_OK) rc = emit(LDR_LAUNCH_SLOT_INIT, 0);
   for (int j = 0; j < D && rc == LDR_OK; ++j) {
     const int kinds[] = {LDR_LAUNCH_QKV_GEMM, LDR_LAUNCH_QKV_FINISH, LDR_LAUNCH_ATTENTION,
@@ -282,7 +292,6 @@ static int draft_sequence(const Shape& s, int D, Emit&& emit) {
       if (rc == LDR_OK) rc = emit(k, j);
   }
   if (rc == LDR_OK) rc = emit(LDR_LAUNCH_LM_HEAD, 0);
-  (void)s;
   return rc;
 }
 

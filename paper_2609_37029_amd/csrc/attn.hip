@@ -88,13 +88,20 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
   // 256-slot window, so all of its loads are issued before the first wait.
   constexpr int WD = 4;
   u32x4 wk[WD][PL], wv[WD][PL];
+#pragma unroll
+  for (int p = 0; p < WD; ++p)
+#pragma unroll
+    for (int i = 0; i < PL; ++i) wk[p][i] = wv[p][i] = u32x4{0u, 0u, 0u, 0u};
+  const bool win = a.use_window;  // a variant without the window has no window region
 #define LDR_FETCH(p, c)                                                                  \
-  _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                       \
-    const int idx_ = (ht + i * HT) % CH;                                                 \
-    const int slot_ = (c) * KC + idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;            \
-    wk[p][i] = *reinterpret_cast<const u32x4*>(Kw + (size_t)slot_ * D + col_);         \
-    wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)(idx_ >> 2) * a.W +         \
-                                               (c) * KC + (idx_ & 3) * 8);               \
+  if (win) {                                                                             \
+    _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                     \
+      const int idx_ = (ht + i * HT) % CH;                                               \
+      const int slot_ = (c) * KC + idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;          \
+      wk[p][i] = *reinterpret_cast<const u32x4*>(Kw + (size_t)slot_ * D + col_);       \
+      wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)(idx_ >> 2) * a.W +       \
+                                                 (c) * KC + (idx_ & 3) * 8);             \
+    }                                                                                    \
   }
   int nf = cbeg;  // next chunk to fetch (clamped to the half's last chunk)
 #pragma unroll
@@ -114,7 +121,7 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
     for (int i = 0; i < GL; ++i) {
       const int idx = threadIdx.x + i * NT;
       const int hq_ = idx / (RMAX * D / 8), r = (idx / (D / 8)) % RMAX, col = (idx % (D / 8)) * 8;
-      greg[i] = (idx < SG && r < a.R)
+      greg[i] = (a.use_summary && idx < SG && r < a.R)
                     ? *reinterpret_cast<const uint4*>(Gg + ((size_t)hq_ * a.R + r) * D + col)
                     : make_uint4(0, 0, 0, 0);
     }
@@ -122,7 +129,7 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
     for (int i = 0; i < ML; ++i) {
       const int idx = threadIdx.x + i * NT;
       const int hq_ = idx / (RMAX * D / 4), r = idx % RMAX, col = ((idx / RMAX) % (D / 4)) * 4;
-      mreg[i] = (idx < SM && r < a.R)
+      mreg[i] = (a.use_summary && idx < SM && r < a.R)
                     ? *reinterpret_cast<const uint4*>(Mg + ((size_t)hq_ * a.R + r) * D + col)
                     : make_uint4(0, 0, 0, 0);
     }
@@ -147,7 +154,7 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
                  : u32x4{0u, 0u, 0u, 0u};
   }
   const long t = a.pos[b];
-  const int nv = t < a.W ? (int)t : a.W;
+  const int nv = !win ? 0 : t < a.W ? (int)t : a.W;
   const int nwin = (nv + KC - 1) / KC;
   const int nch = max(0, min(nwin, cend) - cbeg);      // window chunks of the half
   const int items = (half == 0 ? 1 : 0) + nch;
@@ -325,7 +332,7 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
         u32x4{0u, 0u, 0u, 0u};
   }
   __syncthreads();
-  if (half == 1 && t > 0) {
+  if (half == 1 && t > 0 && a.use_summary) {
     f32x4 sc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
     for (int kk = 0; kk < KS; ++kk)

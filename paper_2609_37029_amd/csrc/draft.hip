@@ -36,6 +36,7 @@ __device__ inline float block_sum(float v, float* red) {
 
 struct SlotArgs {
   const float* part; long split_stride; int splits;
+  int use_c;   // 0: no boundary view (ablation variant), c = 0
   const void* embed; const void* mask_emb; const void* pos_emb; const void* fc_norm;
   const void* in_norm0; const int32_t* anchor; const int64_t* pos;
   float* x; void* nrm; float* rope; int32_t* status;
@@ -98,13 +99,17 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
   for (int ch = 0; ch < kChunks; ++ch) {
     const int k = (threadIdx.x + ch * kThreads) * 4;
     if (k < H) {
-      float4 v = *reinterpret_cast<const float4*>(a.part + (long)b * H + k);
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      gfc[ch] = v;
+      if (a.use_c) {
+        v = *reinterpret_cast<const float4*>(a.part + (long)b * H + k);
 #pragma unroll
-      for (int s = 1; s < SPLITS; ++s)
-        v = f4add(v, *reinterpret_cast<const float4*>(a.part + s * a.split_stride + (long)b * H + k));
+        for (int s = 1; s < SPLITS; ++s)
+          v = f4add(v, *reinterpret_cast<const float4*>(a.part + s * a.split_stride + (long)b * H + k));
+        gfc[ch] = Vec4<T>::load(static_cast<const T*>(a.fc_norm) + k);
+      }
       c[ch] = v;
       ep[ch] = f4add(Vec4<T>::load(e + k), Vec4<T>::load(p + k));
-      gfc[ch] = Vec4<T>::load(static_cast<const T*>(a.fc_norm) + k);
       gin[ch] = Vec4<T>::load(static_cast<const T*>(a.in_norm0) + k);
       ss += f4dot(v);
     }
@@ -239,8 +244,8 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   const int h = blockIdx.x, b = blockIdx.y, g = h / a.rep;
   const int d = a.d, B = a.B;
   const long t = a.pos[b];
-  const int nv = (int)(t < a.W ? t : a.W);
-  const int nsum = t > 0 ? a.R : 0;
+  const int nv = a.use_window ? (int)(t < a.W ? t : a.W) : 0;
+  const int nsum = t > 0 && a.use_summary ? a.R : 0;
   const int NK = B + nv + nsum;
   float* qs = smem;                 // [B][d]
   float* ks = qs + B * d;           // [B][d]
@@ -262,7 +267,8 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   const uint8_t* seq = a.arena + (size_t)b * a.stride;
   const T* Kw = reinterpret_cast<const T*>(seq + a.kw) + ((size_t)(a.layer * a.hkv + g) * a.W) * d;
   const T* Vw = reinterpret_cast<const T*>(seq + a.vw) + ((size_t)(a.layer * a.hkv + g) * a.W) * d;
-  const T* Gh = static_cast<const T*>(a.G) + ((size_t)(a.layer * a.hq + h) * a.R) * d;
+  const T* Gh = nsum ? static_cast<const T*>(a.G) + ((size_t)(a.layer * a.hq + h) * a.R) * d
+                     : nullptr;
   const float* Mh = reinterpret_cast<const float*>(seq + a.m_off) + ((size_t)(a.layer * a.hq + h) * a.R) * d;
   for (int idx = threadIdx.x; idx < B * NK; idx += kThreads) {
     const int i = idx / NK, k = idx % NK;
@@ -345,6 +351,7 @@ hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int f
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st) {
   SlotArgs a;
   a.part = p.part; a.split_stride = (long)batch * s.hidden; a.splits = fc_splits;
+  a.use_c = s.keep_bnd;
   a.embed = w->embed; a.mask_emb = w->mask_emb; a.pos_emb = w->pos_emb; a.fc_norm = w->fc_norm;
   a.in_norm0 = w->layers[0].in_norm; a.anchor = anchor; a.pos = p.pos;
   a.x = p.x; a.nrm = p.nrm; a.rope = p.rope; a.status = p.status;
@@ -385,6 +392,7 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
   a.pos = p.pos; a.G = p.G;
   a.o = p.o; a.layer = layer; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.B = s.B; a.W = s.W;
   a.R = s.R; a.rep = s.rep; a.qkv_out = s.qkv_out;
+  a.use_window = s.keep_win; a.use_summary = s.keep_sum;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const size_t shm = (size_t)(3 * s.B * s.d + s.B * (s.B + s.W + s.R)) * sizeof(float);
   if (s.dtype == LDR_BF16) return launch_attention_mfma(a, s.hkv, batch, st);

@@ -28,6 +28,7 @@ struct Shape {
   float eps;
   double rope_base;
   size_t el;     // bytes per element of the configuration dtype
+  bool keep_win, keep_sum, keep_bnd;  // views kept (ablation variants drop some)
 };
 
 bool make_shape(const ldr_config* c, Shape* s);
@@ -164,6 +165,7 @@ struct AttnArgs {
   const int64_t* pos; const void* G;
   void* o;
   int layer, hq, hkv, d, B, W, R, rep, qkv_out;
+  int use_window, use_summary;   // sources kept (ablation variants drop one)
   float inv_sqrt_d;
 };
 // bf16 MFMA kernel (attn.hip): one workgroup per (kv group, sequence).

@@ -41,6 +41,7 @@ struct UpdateArgs {
   const int64_t* pos; const void* G; const int32_t* n_new; int max_new;
   const void* K_new; const void* V_new; const void* h_new;
   int D, hq, hkv, d, W, R, rep, hb_elems;  // hb_elems = L_b * hidden
+  int keep_win, keep_sum, keep_bnd;         // views kept (ablation variants drop some)
   float inv_sqrt_d;
 };
 
@@ -99,10 +100,15 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
 
   // The stored (eta, m) and the query are loaded first: the stores below go
   // to the same arena, so these loads could not be moved ahead of them.
-  const float eta_a = *etaq;
+  const bool sum = a.keep_sum, win = a.keep_win;
+  const float eta_a = sum ? *etaq : -INFINITY;
   float4 ma[NV];
   float gq[DPT], acc[DPT];
-  {
+#pragma unroll
+  for (int i = 0; i < DPT; ++i) gq[i] = acc[i] = 0.f;
+#pragma unroll
+  for (int c = 0; c < NV; ++c) ma[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (sum) {
     const T* Gp = reinterpret_cast<const T*>(a.G) + qrow * d;
 #pragma unroll
     for (int c = 0; c < NV; ++c) {
@@ -116,7 +122,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
     }
   }
 
-  boundary_slice<T>(a, seq, j, g, b, kThreads);
+  if (a.keep_bnd) boundary_slice<T>(a, seq, j, g, b, kThreads);
 
   // ---- rows of the new set N, tile by tile: window ring write of the last
   // min(n, W) rows (slot (t + r) mod W) and the tiled online log-sum-exp ----
@@ -126,7 +132,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
   T* Kw = reinterpret_cast<T*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * d;
   T* Vw = reinterpret_cast<T*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * d;
   float mx = -INFINITY, l = 0.f;
-  for (int r0 = 0; r0 < n; r0 += kTileRows) {
+  for (int r0 = 0; r0 < ((win || sum) ? n : 0); r0 += kTileRows) {
     const int nr = min(kTileRows, n - r0);
     __syncthreads();
     const int cpr = d / EPC;
@@ -135,7 +141,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
       const size_t src = ((((size_t)b * a.max_new + r0 + r) * a.D + j) * a.hkv + g) * d + e0;
       const uint4 kv = *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.K_new) + src);
       const uint4 vv = *reinterpret_cast<const uint4*>(reinterpret_cast<const T*>(a.V_new) + src);
-      if (r0 + r >= n - a.W) {  // only the last W rows can survive in the ring
+      if (win && r0 + r >= n - a.W) {  // only the last W rows can survive in the ring
         const size_t slot = (size_t)((t + r0 + r) % a.W);
         *reinterpret_cast<uint4*>(Kw + slot * d + e0) = kv;
       }
@@ -152,12 +158,13 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
        // slots are contiguous (apart from the wrap of the ring)
       const int rs = max(0, n - a.W - r0);  // first row of the tile that survives
       const int r = threadIdx.x % kTileRows;
-      if (r >= rs && r < nr) {
+      if (win && r >= rs && r < nr) {
         const size_t slot = (size_t)((t + r0 + r) % a.W);
         for (int e = threadIdx.x / kTileRows; e < d; e += kThreads / kTileRows)
           Elem<T>::store(Vw + (size_t)e * a.W + slot, Vs[r][e]);
       }
     }
+    if (!sum) continue;   // window only: no statistics
     float s[kTileRows];
     float tmax = -INFINITY;
 #pragma unroll
@@ -197,6 +204,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
     }
     mx = nm;
   }
+  if (!sum) return;
   // eta_N = log sum exp(s), m_N = sum exp(s - eta_N) v, merged with (eta_A, m_A)
   const float eta_n = mx + logf(l);
   const float inv_l = 1.f / l;
@@ -267,21 +275,25 @@ views_update_mfma_kernel(UpdateArgs a) {
   const size_t q0 = ((size_t)j * a.hq + (size_t)g * a.rep) * a.R + (size_t)wave * 16;
   float* Mq = reinterpret_cast<float*>(seq + a.m) + q0 * DH;
   float* etaq = reinterpret_cast<float*>(seq + a.eta) + q0;
+  const bool sum = a.keep_sum, win = a.keep_win;
   float ma[NT][4], eta_a[4];
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
-    eta_a[v] = etaq[lg * 4 + v];
+    eta_a[v] = sum ? etaq[lg * 4 + v] : -INFINITY;
 #pragma unroll
-    for (int dt = 0; dt < NT; ++dt) ma[dt][v] = Mq[(size_t)(lg * 4 + v) * DH + dt * 16 + lr];
+    for (int dt = 0; dt < NT; ++dt)
+      ma[dt][v] = sum ? Mq[(size_t)(lg * 4 + v) * DH + dt * 16 + lr] : 0.f;
   }
   bf16x8 gf[KS];   // A layout: query row lr, dims ks * 32 + lg * 8 ..
-  {
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) gf[ks] = bf16x8{};
+  if (sum) {
     const uint16_t* Gq = static_cast<const uint16_t*>(a.G) + (q0 + lr) * DH + lg * 8;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) gf[ks] = frag8(Gq + ks * 32);
   }
 
-  boundary_slice<uint16_t>(a, seq, j, g, b, NTH);
+  if (a.keep_bnd) boundary_slice<uint16_t>(a, seq, j, g, b, NTH);
 
   uint16_t* Kw = reinterpret_cast<uint16_t*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * DH;
   uint16_t* Vw = reinterpret_cast<uint16_t*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * DH;
@@ -294,7 +306,7 @@ views_update_mfma_kernel(UpdateArgs a) {
 #pragma unroll
   for (int v = 0; v < 4; ++v) { m[v] = -INFINITY; l[v] = 0.f; }
 
-  for (int r0 = 0; r0 < n; r0 += KT) {
+  for (int r0 = 0; r0 < ((win || sum) ? n : 0); r0 += KT) {
     const int nr = min(KT, n - r0);
     __syncthreads();   // the previous tile's LDS reads are done
     // stage the tile (rows past nr as zeros) and ring-write the K rows that survive
@@ -305,7 +317,7 @@ views_update_mfma_kernel(UpdateArgs a) {
         const size_t src = ((((size_t)b * a.max_new + r0 + r) * a.D + j) * a.hkv + g) * DH + c8;
         kv = *reinterpret_cast<const u32x4*>(Kn + src);
         vv = *reinterpret_cast<const u32x4*>(Vn + src);
-        if (r0 + r >= n - a.W) {
+        if (win && r0 + r >= n - a.W) {
           const size_t slot = (size_t)((t + r0 + r) % a.W);
           *reinterpret_cast<u32x4*>(Kw + slot * DH + c8) = kv;
         }
@@ -319,11 +331,12 @@ views_update_mfma_kernel(UpdateArgs a) {
     {  // window V^T: lanes take consecutive rows of one dim (contiguous slots)
       const int rs = max(0, n - a.W - r0);
       const int r = tid % KT;
-      if (r >= rs && r < nr) {
+      if (win && r >= rs && r < nr) {
         const size_t slot = (size_t)((t + r0 + r) % a.W);
         for (int e = tid / KT; e < DH; e += NTH / KT) Vw[(size_t)e * a.W + slot] = Vt[e * VLD + r];
       }
     }
+    if (!sum) continue;   // window only: no statistics
     // scores of keys nt * 16 + lr (C layout), scaled; keys past nr masked
     f32x4 sc[2];
 #pragma unroll
@@ -364,6 +377,7 @@ views_update_mfma_kernel(UpdateArgs a) {
       o[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(plo, vf, o[dt], 0, 0, 0);
     }
   }
+  if (!sum) return;
   // eta_N = m + log l, m_N = O / l, merged with (eta_A, m_A) (Eq. 11)
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
@@ -428,7 +442,7 @@ hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* 
   const size_t words = L.stride / 4 * (size_t)batch;
   const int blocks = (int)((words + kThreads - 1) / kThreads < 4096
                                ? (words + kThreads - 1) / kThreads : 4096);
-  const size_t eta_bytes = (size_t)s.D * s.hq * s.R * 4;
+  const size_t eta_bytes = s.keep_sum ? (size_t)s.D * s.hq * s.R * 4 : 0;
   hipLaunchKernelGGL(views_reset_kernel, dim3(blocks > 0 ? blocks : 1), dim3(kThreads), 0, st,
                      static_cast<uint8_t*>(arena), L.stride, L.eta, eta_bytes, batch, pos);
   return hipGetLastError();
@@ -445,6 +459,7 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
   a.K_new = K_new; a.V_new = V_new; a.h_new = h_new;
   a.D = s.D; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.W = s.W; a.R = s.R; a.rep = s.rep;
   a.hb_elems = s.Lb * s.hidden;
+  a.keep_win = s.keep_win; a.keep_sum = s.keep_sum; a.keep_bnd = s.keep_bnd;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const dim3 grid(s.hkv, s.D, batch);
   const int q = s.rep * s.R;

@@ -31,7 +31,10 @@ class Config(ctypes.Structure):
         "hidden", "n_q_heads", "n_kv_heads", "head_dim", "mlp", "vocab", "n_layers",
         "n_feat_layers", "block", "window", "summary", "dtype")] + [
         ("rope_theta", ctypes.c_float), ("ntk_alpha", ctypes.c_float),
-        ("rms_eps", ctypes.c_float)]
+        ("rms_eps", ctypes.c_float), ("drop_views", ctypes.c_int32)]
+
+# ldr_view_drop bits (ablation variants)
+LDR_DROP_WINDOW, LDR_DROP_SUMMARY, LDR_DROP_BOUNDARY = 1, 2, 4
 
 
 LAYER_KEYS = ("in_norm", "wqkv", "q_norm", "k_norm", "wo", "post_norm", "w_gate_up", "w_down")
@@ -111,7 +114,8 @@ def config(shape) -> Config:
     return Config(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.mlp,
                   shape.vocab, shape.n_layers, shape.n_feat_layers, shape.block, shape.window,
                   shape.summary, LDR_BF16 if shape.dtype == "bf16" else LDR_F32,
-                  shape.rope_theta, shape.ntk_alpha, shape.rms_eps)
+                  shape.rope_theta, shape.ntk_alpha, shape.rms_eps,
+                  getattr(shape, "drop_views", 0))
 
 
 def state_bytes(shape) -> int:
@@ -185,9 +189,15 @@ class Views:
         per = self.arena.view(self.batch, self.stride)
         return per[:, off:off + n * el].view(dtype).view(self.batch, *shape)
 
+    def _drops(self, bit) -> bool:
+        return bool(getattr(self.shape, "drop_views", 0) & bit)
+
     def window(self):
         """Window K and V as [batch][D][Hkv][W][d] (V is stored transposed,
-        [D][Hkv][d][W]; this returns a transposed view of it)."""
+        [D][Hkv][d][W]; this returns a transposed view of it); None without
+        the window view."""
+        if self._drops(LDR_DROP_WINDOW):
+            return None
         s = self.shape
         shp = (s.n_layers, s.n_kv_heads, s.window, s.head_dim)
         vt = (s.n_layers, s.n_kv_heads, s.head_dim, s.window)
@@ -195,6 +205,8 @@ class Views:
                 self._region(self.layout["vw"], vt, s.torch_dtype).transpose(-1, -2))
 
     def summary(self):
+        if self._drops(LDR_DROP_SUMMARY):
+            return None
         s = self.shape
         return (self._region(self.layout["m"], (s.n_layers, s.n_q_heads, s.summary, s.head_dim),
                              torch.float32),
@@ -202,6 +214,8 @@ class Views:
                              torch.float32))
 
     def boundary(self):
+        if self._drops(LDR_DROP_BOUNDARY):
+            return None
         s = self.shape
         return self._region(self.layout["h"], (s.n_feat_layers, s.hidden), s.torch_dtype)
 

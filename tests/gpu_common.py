@@ -50,19 +50,26 @@ class Pair:
 
 
 def check_views(pair, rtol_m=1e-4, atol_m=1e-6):
+    """Positions, window and boundary bit-exact, summary within tolerance; a
+    view the shape drops (ablation variants) has no region to compare."""
     torch.cuda.synchronize()
     v = pair.views
     pos = v.pos.cpu().numpy()
-    Kw, Vw = (t.cpu() for t in v.window())
-    M, eta = (t.cpu().numpy() for t in v.summary())
-    hb = v.boundary().cpu()
+    win, summ, bnd = v.window(), v.summary(), v.boundary()
+    Kw, Vw = (t.cpu() for t in win) if win is not None else (None, None)
+    M, eta = (t.cpu().numpy() for t in summ) if summ is not None else (None, None)
+    hb = bnd.cpu() if bnd is not None else None
     for b in pair.seqs:
         o = pair.ost[b]
         assert pos[b] == o.t, (b, pos[b], o.t)
         # window rows and boundary states are copies: bit-exact
-        assert np.array_equal(synth.to_f64(Kw[b]), o.Kw), f"window K of sequence {b}"
-        assert np.array_equal(synth.to_f64(Vw[b]), o.Vw), f"window V of sequence {b}"
-        assert np.array_equal(synth.to_f64(hb[b]), o.h), f"boundary of sequence {b}"
+        if Kw is not None:
+            assert np.array_equal(synth.to_f64(Kw[b]), o.Kw), f"window K of sequence {b}"
+            assert np.array_equal(synth.to_f64(Vw[b]), o.Vw), f"window V of sequence {b}"
+        if hb is not None:
+            assert np.array_equal(synth.to_f64(hb[b]), o.h), f"boundary of sequence {b}"
+        if M is None:
+            continue
         if o.t == 0:
             assert np.all(np.isneginf(eta[b]))
             assert np.all(M[b] == 0)

@@ -147,3 +147,22 @@ def test_tiled_layout_sizes_and_validation(L):
     assert lib.ldr_tile_matrix(fake, 256, 64, 64, fake, n - 2, None) == L.LDR_EINVAL  # too small
     assert lib.ldr_tile_matrix(ctypes.c_void_p((1 << 20) + 8), 256, 64, 64, fake, n, None) == \
         L.LDR_EINVAL                                                                  # alignment
+
+
+@pytest.mark.parametrize("drop", [0, 1, 2, 4, 3, 5, 6])
+def test_view_drop_variants_state_and_launches(L, drop):
+    """Ablation variants: the arena loses exactly the dropped view's bytes (the
+    oracle's accounting), and without the boundary the step launches no
+    boundary-fusion GEMM."""
+    from oracle import views as OV
+    from paper_2609_37029_amd import ldr
+    for shape in (synth.TINY, synth.QWEN3_8B):
+        s = shape.replace(drop_views=drop)
+        assert ldr.state_bytes(s) == OV.state_bytes(s)
+        kinds = ldr.draft_launches(s)
+        assert ("fc_gemm" in kinds) == (not drop & 4)
+        assert kinds[-1] == "lm_head"
+    for flags in (8, 7):          # an unknown bit; no view at all
+        bad = L.config(synth.TINY)
+        bad.drop_views = flags
+        assert L.lib().ldr_config_check(ctypes.byref(bad)) == L.LDR_EINVAL

@@ -194,7 +194,7 @@ def test_forward_matches_loop_brute_force(t):
     np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-11)
 
 
-@pytest.mark.parametrize("drop", [1, 2, 4, 3, 7])
+@pytest.mark.parametrize("drop", [1, 2, 4, 3, 6])
 @pytest.mark.parametrize("t", [0, 3, 12])
 def test_view_drop_variants_match_loop_brute_force(drop, t):
     """Ablation variants (Sec. 3.4, App. D.3): the variant's own update and
