@@ -54,15 +54,20 @@ def rope(x, pos, base):
     return np.concatenate([x1 * cos - x2 * sin, x1 * sin + x2 * cos], axis=-1)
 
 
-def block_attention(q, kb, vb, Kw, Vw, valid, G, M, has_summary):
+def block_attention(q, kb, vb, Kw, Vw, valid, G, M, has_summary, pooled=()):
     """Eq. 6 for one query head: q [B][d] against keys [kb; Kw[valid]; G]
-    and values [vb; Vw[valid]; M] with one softmax, scale 1/sqrt(d)."""
+    and values [vb; Vw[valid]; M] with one softmax, scale 1/sqrt(d).
+    `pooled`: (keys, values) of the mean-pooled summary's valid slots, which
+    join the concatenation in place of G and M."""
     d = q.shape[-1]
     keys = [kb, Kw[valid]]
     vals = [vb, Vw[valid]]
     if has_summary:
         keys.append(G)
         vals.append(M)
+    for pk, pv in pooled:
+        keys.append(pk)
+        vals.append(pv)
     K = np.concatenate(keys, axis=0)
     V = np.concatenate(vals, axis=0)
     p = scipy.special.softmax(q @ K.T / np.sqrt(d), axis=-1)
@@ -97,12 +102,16 @@ def layer(s, L, x, st: _views.ViewState, G, j):
     base = rope_base(s)
     q, k = rope(q, pos, base), rope(k, pos, base)
     valid = _views.window_valid(s, st.t) & _views.keeps(s, _views.DROP_WINDOW)
-    has_summary = st.t > 0 and _views.keeps(s, _views.DROP_SUMMARY)
+    has_summary = st.t > 0 and _views.learned_summary(s)
+    nval = ([_views.pooled_valid(s, st.t, bank) for bank in range(2)]
+            if _views.pooled_summary(s) else [])
     o = np.empty((B, Hq, d))
     for h in range(Hq):
         g = h // rep
+        pooled = [(st.PK[bank][j, g, :n], st.PV[bank][j, g, :n]) for bank, n in enumerate(nval)]
         o[:, h] = block_attention(q[:, h], k[:, g], v[:, g], st.Kw[j, g], st.Vw[j, g],
-                                  valid, G[j, h], st.M[j, h], has_summary)
+                                  valid, None if G is None else G[j, h], st.M[j, h],
+                                  has_summary, pooled)
     x = x + o.reshape(B, Hq * d) @ L["wo"].T
     n2 = rmsnorm(x, L["post_norm"], s.rms_eps)
     gu = n2 @ L["w_gate_up"].T

@@ -10,6 +10,14 @@ Per sequence the views are:
 * the boundary hidden states h of the selected layers at the last ingested
   position (Sec. 2.2, the input of the boundary fusion).
 
+The mean-pooled summary (the views as the configurations word them: strided
+means instead of learned queries) replaces the learned summary when the shape
+sets pool_slots: for each of two strides S, a ring of P slots in which slot
+c mod P holds the mean K row and mean V row of chunk c = rows [cS, (c+1)S) of
+every layer's K/V group, the open chunk with the mean of the rows it has so
+far. A mean is the learned-query statistics of Eq. 10 with G = 0 (all scores
+equal: uniform weights, eta = log of the count), merged chunk by chunk.
+
 All arithmetic is float64. Inputs are float64 arrays holding the values of
 the drawn tensors (bf16 values are exact in float64).
 """
@@ -29,10 +37,16 @@ class ViewState:
     M: np.ndarray     # [D][Hq][R][d]   summary values m
     eta: np.ndarray   # [D][Hq][R]      summary log-normalizers (-inf = empty)
     h: np.ndarray     # [L_b][hidden]   boundary hidden states
+    PK: np.ndarray = None   # [2][D][Hkv][P][d] pooled key means (mean-pooled summary)
+    PV: np.ndarray = None   # [2][D][Hkv][P][d] pooled value means
+    SK: np.ndarray = None   # [2][D][Hkv][d]    sums of the open chunk's keys
+    SV: np.ndarray = None   # [2][D][Hkv][d]    sums of the open chunk's values
 
     def copy(self) -> "ViewState":
+        cp = lambda a: None if a is None else a.copy()
         return ViewState(self.t, self.Kw.copy(), self.Vw.copy(), self.M.copy(),
-                         self.eta.copy(), self.h.copy())
+                         self.eta.copy(), self.h.copy(), cp(self.PK), cp(self.PV),
+                         cp(self.SK), cp(self.SV))
 
 
 def empty(s) -> ViewState:
@@ -42,11 +56,14 @@ def empty(s) -> ViewState:
     identity)."""
     D, Hq, Hkv, W, R, d = (s.n_layers, s.n_q_heads, s.n_kv_heads, s.window,
                            s.summary, s.head_dim)
+    P = pool_slots(s)
     return ViewState(
         t=0,
         Kw=np.zeros((D, Hkv, W, d)), Vw=np.zeros((D, Hkv, W, d)),
         M=np.zeros((D, Hq, R, d)), eta=np.full((D, Hq, R), -np.inf),
         h=np.zeros((s.n_feat_layers, s.hidden)),
+        PK=np.zeros((2, D, Hkv, P, d)), PV=np.zeros((2, D, Hkv, P, d)),
+        SK=np.zeros((2, D, Hkv, d)), SV=np.zeros((2, D, Hkv, d)),
     )
 
 
@@ -90,6 +107,26 @@ def keeps(s, bit) -> bool:
     return not (getattr(s, "drop_views", 0) & bit)
 
 
+def pool_slots(s) -> int:
+    """P of the mean-pooled summary, 0 for the learned summary."""
+    return int(getattr(s, "pool_slots", 0) or 0)
+
+
+def learned_summary(s) -> bool:
+    return keeps(s, DROP_SUMMARY) and pool_slots(s) == 0
+
+
+def pooled_summary(s) -> bool:
+    return keeps(s, DROP_SUMMARY) and pool_slots(s) > 0
+
+
+def pooled_valid(s, t: int, bank: int) -> int:
+    """Valid slots of a bank after t rows: the chunks begun so far, at most P
+    (they fill slots 0, 1, ... before the ring wraps)."""
+    S = s.pool_strides[bank]
+    return min(-(-t // S), pool_slots(s))
+
+
 def update(s, st: ViewState, G, K_new, V_new, h_new) -> ViewState:
     """Ingest n new target rows (Sec. 2.4, Inference; App. A.2).
 
@@ -107,7 +144,20 @@ def update(s, st: ViewState, G, K_new, V_new, h_new) -> ViewState:
         for r in range(n):                          # ring write, in order
             out.Kw[:, :, (st.t + r) % W, :] = K_new[r]
             out.Vw[:, :, (st.t + r) % W, :] = V_new[r]
-    if keeps(s, DROP_SUMMARY):
+    if pooled_summary(s):
+        P = pool_slots(s)
+        for bank, S in enumerate(s.pool_strides):
+            for r in range(n):                      # running mean of each chunk, in order
+                p = st.t + r
+                if p % S == 0:                      # a new chunk opens its slot
+                    out.SK[bank] = 0.0
+                    out.SV[bank] = 0.0
+                out.SK[bank] += K_new[r]
+                out.SV[bank] += V_new[r]
+                k = (p // S) % P
+                out.PK[bank][:, :, k] = out.SK[bank] / (p % S + 1)
+                out.PV[bank][:, :, k] = out.SV[bank] / (p % S + 1)
+    if learned_summary(s):
         for j in range(s.n_layers):
             for h in range(s.n_q_heads):
                 g = h // rep                        # the head's K/V group
@@ -139,6 +189,22 @@ def brute_summary(s, G, K_all, V_all):
     return M, eta
 
 
+def brute_pooled(s, K_all, V_all):
+    """Each bank's slots from the whole prefix at once: slot c mod P holds the
+    mean of the rows of chunk c, for the last P chunks begun."""
+    t = K_all.shape[0]
+    P = pool_slots(s)
+    PK = np.zeros((2, s.n_layers, s.n_kv_heads, P, s.head_dim))
+    PV = np.zeros_like(PK)
+    for bank, S in enumerate(s.pool_strides):
+        C = -(-t // S)                              # chunks begun
+        for c in range(max(0, C - P), C):
+            rows = slice(c * S, min((c + 1) * S, t))
+            PK[bank][:, :, c % P] = K_all[rows].mean(axis=0)
+            PV[bank][:, :, c % P] = V_all[rows].mean(axis=0)
+    return PK, PV
+
+
 def brute_window(s, K_all, V_all):
     """The last min(t, W) rows, each at slot position mod W, and the mask of
     valid slots."""
@@ -168,6 +234,9 @@ def state_bytes(s) -> int:
     el = 2 if s.dtype == "bf16" else 4
     window = 2 * s.n_layers * s.window * s.n_kv_heads * s.head_dim * el
     summary = s.n_layers * s.n_q_heads * s.summary * (s.head_dim + 1) * 4
+    if pool_slots(s):   # two banks of P key and value means, fp32 sums of the open chunks
+        summary = 2 * s.n_layers * s.n_kv_heads * s.head_dim * (
+            2 * pool_slots(s) * el + 2 * 4)
     boundary = s.n_feat_layers * s.hidden * el
     return (window * keeps(s, DROP_WINDOW) + summary * keeps(s, DROP_SUMMARY) +
             boundary * keeps(s, DROP_BOUNDARY))

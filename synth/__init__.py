@@ -54,6 +54,10 @@ class Shape:
     rms_eps: float = 1.0e-6
     dtype: str = "bf16"  # "bf16" or "f32": weights, window rows, G, boundary h
     drop_views: int = 0  # ablation variants: 1 no window, 2 no summary, 4 no boundary (sums)
+    # mean-pooled summary in place of the learned one: two banks of pool_slots
+    # slots, each slot the mean K and V row of pool_strides[i] consecutive rows
+    pool_strides: tuple = ()
+    pool_slots: int = 0
 
     @property
     def qkv_out(self) -> int:
@@ -73,6 +77,12 @@ TINY = Shape("tiny", hidden=256, n_q_heads=4, n_kv_heads=4, head_dim=64, mlp=102
 QWEN3_8B = Shape("qwen3-8b", hidden=4096, n_q_heads=32, n_kv_heads=8, head_dim=128,
                  mlp=12288, vocab=151936, n_layers=5, n_feat_layers=5, block=16,
                  window=256, summary=16, dtype="bf16")
+# The views as the configurations word them: the last 64 rows plus mean-pooled
+# summaries at strides 4 and 64 with 32 slots each (Tiny), and the same at 256
+# slots per scale for the Qwen3-8B shape.
+TINY_POOLED = TINY.replace(name="tiny-pooled", pool_strides=(4, 64), pool_slots=32)
+QWEN3_8B_POOLED = QWEN3_8B.replace(name="qwen3-8b-pooled", pool_strides=(4, 64),
+                                   pool_slots=256)
 QWEN3_32B = Shape("qwen3-32b", hidden=5120, n_q_heads=64, n_kv_heads=8, head_dim=128,
                   mlp=25600, vocab=151936, n_layers=5, n_feat_layers=5, block=16,
                   window=256, summary=16, dtype="bf16")

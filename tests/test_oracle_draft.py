@@ -124,9 +124,12 @@ def _loop_matvec(Wm, x):            # Wm [out][in] (nn.Linear), y_o = sum_i W[o]
     return [sum(Wm[o][i] * x[i] for i in range(len(x))) for o in range(len(Wm))]
 
 
-def brute_forward(s, Wt, st, G, a, no_window=False, no_summary=False, no_boundary=False):
+def brute_forward(s, Wt, st, G, a, no_window=False, no_summary=False, no_boundary=False,
+                  pooled=None):
     """The whole forward with scalar loops; the flags leave a view's source out
-    (ablation variants), whatever `st` holds for it."""
+    (ablation variants), whatever `st` holds for it. `pooled`: per bank, the
+    (keys, values) [D][Hkv][n][d] of the valid slots of a mean-pooled summary,
+    which then takes the learned summary's place."""
     B, H, Hk, d, hid = s.block, s.n_q_heads, s.n_kv_heads, s.head_dim, s.hidden
     base = s.rope_theta * s.ntk_alpha ** (d / (d - 2))
     hcat = [v for l in range(s.n_feat_layers) for v in st.h[l]]
@@ -165,7 +168,11 @@ def brute_forward(s, Wt, st, G, a, no_window=False, no_summary=False, no_boundar
                 g = h // (H // Hk)
                 keys = [k[b][g] for b in range(B)] + [list(st.Kw[j, g, p]) for p in range(nvalid)]
                 vals = [v[b][g] for b in range(B)] + [list(st.Vw[j, g, p]) for p in range(nvalid)]
-                if st.t > 0 and not no_summary:
+                if pooled is not None:
+                    for PKb, PVb in pooled:
+                        keys += [list(PKb[j, g, n_]) for n_ in range(PKb.shape[2])]
+                        vals += [list(PVb[j, g, n_]) for n_ in range(PVb.shape[2])]
+                elif st.t > 0 and not no_summary:
                     keys += [list(G[j, h, r]) for r in range(s.summary)]
                     vals += [list(st.M[j, h, r]) for r in range(s.summary)]
                 sc = [sum(q[i][h][e] * kk[e] for e in range(d)) / math.sqrt(d) for kk in keys]
@@ -211,6 +218,32 @@ def test_view_drop_variants_match_loop_brute_force(drop, t):
     np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-11)
     if t:
         assert not np.allclose(got, Dr.forward(full, Wt, st_full, G, 6))
+
+
+@pytest.mark.parametrize("t", [0, 1, 7, 12, 40])
+def test_pooled_summary_forward_matches_loop_brute_force(t):
+    """The mean-pooled summary's valid slots join the one softmax in place of
+    the learned summary: the forward over the incrementally kept slots equals
+    the loop brute force over slots recomputed from the whole prefix."""
+    s = MICRO.replace(pool_strides=(2, 5), pool_slots=3)
+    Wt = rand_weights(s, 31)
+    rng = np.random.default_rng(32)
+    K = rng.normal(size=(t, s.n_layers, s.n_kv_heads, s.head_dim))
+    Vv = rng.normal(size=K.shape)
+    st = V.empty(s)
+    off = 0
+    for n in (3, 1, 8, 2, 100):
+        n = min(n, t - off)
+        st = V.update(s, st, None, K[off:off + n], Vv[off:off + n],
+                      np.ones((s.n_feat_layers, s.hidden)))
+        off += n
+    assert st.t == t
+    PK, PV = V.brute_pooled(s, K, Vv)
+    pooled = [(PK[b][:, :, :V.pooled_valid(s, t, b)], PV[b][:, :, :V.pooled_valid(s, t, b)])
+              for b in range(2)]
+    got = Dr.forward(s, Wt, st, None, 4)
+    ref = brute_forward(s, Wt, st, None, 4, pooled=pooled)
+    np.testing.assert_allclose(got, ref, rtol=1e-10, atol=1e-11)
 
 
 def test_no_boundary_is_a_zero_fusion_weight():

@@ -148,3 +148,81 @@ def test_state_bytes_reproduce_the_papers_numbers():
     assert round(gold["dspark_mib_at_128k"] * MiB / b) == gold["reduction_at_128k"]
     assert V.state_bytes(synth.QWEN3_32B) == 7_936_000
     assert V.state_bytes(synth.TINY) == 150_784
+
+
+# ---- the mean-pooled summary (the views as the configurations word them) --------------------
+
+SP = S.replace(name="mini-pooled", pool_strides=(3, 8), pool_slots=4)
+
+
+def ingest_pooled(K, Vv, sizes, s=SP):
+    st = V.empty(s)
+    h = np.zeros((s.n_feat_layers, s.hidden))
+    off = 0
+    for n in sizes:
+        st = V.update(s, st, None, K[off:off + n], Vv[off:off + n], h + off)
+        off += n
+    return st
+
+
+@pytest.mark.parametrize("sizes", [[1] * 70, [40] + [17] * 5, [2, 5, 1, 31, 3, 9, 100],
+                                   [0, 3, 0, 1], [24], [23, 1, 8]])
+def test_pooled_incremental_equals_brute_force(sizes):
+    """Slot c mod P of each bank holds the mean of chunk c's rows, for the last
+    P chunks begun, however the rows arrive (chunks and the ring cross updates)."""
+    t = sum(sizes)
+    K, Vv = rows(t, 31)
+    st = ingest_pooled(K, Vv, sizes)
+    PK, PV = V.brute_pooled(SP, K, Vv)
+    assert st.t == t
+    np.testing.assert_allclose(st.PK, PK, rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(st.PV, PV, rtol=1e-12, atol=1e-12)
+    for bank, S_ in enumerate(SP.pool_strides):
+        assert V.pooled_valid(SP, t, bank) == min(-(-t // S_), SP.pool_slots)
+    # the learned summary is not kept
+    assert np.all(st.M == 0) and np.all(np.isneginf(st.eta))
+
+
+def test_pooled_slots_by_hand():
+    """Stride 3, 4 slots, 14 rows of scalar-like values: chunk means by hand."""
+    s = SP
+    K = np.zeros((14, s.n_layers, s.n_kv_heads, s.head_dim))
+    for p in range(14):
+        K[p] = p
+    st = ingest_pooled(K, -K, [5, 4, 5])
+    # chunks of 3: [0,1,2] [3,4,5] [6,7,8] [9,10,11] [12,13]; 5 chunks > 4 slots
+    want = {0: 12.5, 1: 4.0, 2: 7.0, 3: 10.0}       # slot 0 recycled by chunk 4
+    for k, m in want.items():
+        assert np.all(st.PK[0][:, :, k] == m) and np.all(st.PV[0][:, :, k] == -m)
+    # stride 8: [0..7] mean 3.5, [8..13] mean 10.5 (open chunk)
+    assert np.all(st.PK[1][:, :, 0] == 3.5) and np.all(st.PK[1][:, :, 1] == 10.5)
+    assert V.pooled_valid(s, 14, 0) == 4 and V.pooled_valid(s, 14, 1) == 2
+
+
+def test_pooled_constant_rows_pool_to_the_constant():
+    K, Vv = rows(50, 3)
+    K[:] = 0.625
+    Vv[:] = -1.75
+    st = ingest_pooled(K, Vv, [13, 20, 17])
+    assert np.all(st.PK[:, :, :, :, :] == 0.625) and np.all(st.PV == -1.75)
+
+
+def test_pooled_mean_is_the_zero_query_statistics():
+    """A slot is Eq. 10 with G = 0: uniform weights give the mean, and the
+    log-normaliser is the log of the chunk's row count."""
+    K, Vv = rows(8, 4)
+    st = ingest_pooled(K, Vv, [8])
+    j, g = 1, 1
+    eta, m = V.set_statistics(np.zeros((1, S.head_dim)), K[:, j, g], Vv[:, j, g], S.head_dim)
+    np.testing.assert_allclose(m[0], st.PV[1][j, g, 0], rtol=1e-13)
+    assert abs(eta[0] - np.log(8)) < 1e-13
+
+
+def test_pooled_state_bytes_are_fixed():
+    el = 4
+    s = SP
+    want = (2 * s.n_layers * s.window * s.n_kv_heads * s.head_dim * el
+            + 2 * s.n_layers * s.n_kv_heads * s.head_dim * (2 * s.pool_slots * el + 8)
+            + s.n_feat_layers * s.hidden * el)
+    assert V.state_bytes(s) == want
+    assert V.state_bytes(synth.TINY_POOLED) < V.state_bytes(synth.TINY_POOLED.replace(window=128))
