@@ -91,8 +91,9 @@ def launch_costs(s, batch):
     c["qkv_finish"] = (M * s.qkv_out * (4 + el) + M * s.head_dim * 4 + 2 * s.head_dim * el, 0)
     # attention: window K/V of the layer + G and M of its heads + block q/k/v in, o out
     drop = getattr(s, "drop_views", 0)        # ablation variants read fewer sources
-    nw = 0 if drop & 1 else s.window
-    nr = 0 if drop & 2 else s.summary
+    pool = 0 if drop & 2 else (getattr(s, "pool_slots", 0) or 0)
+    nw = (0 if drop & 1 else s.window) + 2 * pool  # window rows and pooled slot means
+    nr = 0 if (drop & 2 or pool) else s.summary
     win = batch * 2 * s.n_kv_heads * nw * s.head_dim * el
     summ = s.n_q_heads * nr * s.head_dim * el + batch * s.n_q_heads * nr * s.head_dim * 4
     qkv = M * s.qkv_out * el + M * s.n_q_heads * s.head_dim * el

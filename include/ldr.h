@@ -76,6 +76,13 @@ typedef struct ldr_config {
   float rms_eps;         /* RMSNorm epsilon                                    */
   int32_t drop_views;    /* 0 (the full drafter) or a sum of ldr_view_drop bits
                             that keeps at least one view                     */
+  int32_t pool_slots;    /* 0: the learned-query summary (Eq. 5). P > 0: the
+                            mean-pooled summary instead (the views as the
+                            configurations word them): two banks of P ring
+                            slots, slot c mod P holding the mean K and V row
+                            of chunk c (pool_stride rows); P % 32 == 0; the
+                            summary queries G and `summary` are then unused */
+  int32_t pool_stride[2];/* rows per chunk of the two banks, each >= 1      */
 } ldr_config;
 
 /* Device pointers of one draft layer (Qwen3-style block, App. B.1). */
@@ -115,7 +122,10 @@ typedef struct ldr_views ldr_views; /* opaque host handle */
 
 /* Per-sequence bytes of the fixed-size views (Sec. 2.4, Fixed-cost
  * complexity): window K [D][Hkv][W][d] and window V stored transposed,
- * [D][Hkv][d][W] (dtype; slot p mod W of position p), summary values
+ * [D][Hkv][d][W] (dtype; slot p mod W of position p; with the mean-pooled
+ * summary each (layer, group) holds W + 2P rows: the window, then bank 0's
+ * and bank 1's slot means, and fp32 sums of the open chunks [D][Hkv][2][2][d]
+ * follow the boundary region), summary values
  * [D][Hq][R][d] and log-normalizers [D][Hq][R] (fp32), boundary states
  * [L_b][hidden] (dtype), each region 256-byte aligned; a view the
  * configuration drops has zero bytes. No term depends on the prefix length.

@@ -23,7 +23,11 @@ bool make_shape(const ldr_config* c, Shape* s) {
   if (c->vocab <= 0) return false;
   if (c->n_layers <= 0 || c->n_feat_layers <= 0) return false;
   if (c->block < 1 || c->block > 16) return false;
-  if (c->window < 1 || c->summary < 1) return false;
+  if (c->window < 1) return false;
+  if (c->pool_slots < 0 || (c->pool_slots > 0 && (c->pool_slots % 32 || c->pool_stride[0] < 1 ||
+                                                   c->pool_stride[1] < 1)))
+    return false;
+  if (c->pool_slots == 0 && c->summary < 1) return false;
   if (c->dtype != LDR_F32 && c->dtype != LDR_BF16) return false;
   if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f) || !(c->ntk_alpha > 0.f)) return false;
   const int all = LDR_DROP_WINDOW | LDR_DROP_SUMMARY | LDR_DROP_BOUNDARY;
@@ -40,9 +44,15 @@ bool make_shape(const ldr_config* c, Shape* s) {
   s->keep_win = !(c->drop_views & LDR_DROP_WINDOW);
   s->keep_sum = !(c->drop_views & LDR_DROP_SUMMARY);
   s->keep_bnd = !(c->drop_views & LDR_DROP_BOUNDARY);
+  s->P = s->keep_sum ? c->pool_slots : 0;
+  s->S0 = c->pool_stride[0]; s->S1 = c->pool_stride[1];
+  s->learned = s->keep_sum && c->pool_slots == 0;
+  if (!s->learned) s->R = 0;   // no learned summary queries
+  s->Wr = s->keep_win ? s->W : 0;
+  s->Wx = s->Wr + 2 * s->P;
   if (views_dims_per_thread(*s) == 0 || !norm_hidden_supported(s->hidden)) return false;
   if (s->dtype == LDR_BF16) {
-    if (!attention_mfma_supported(s->d, s->rep, s->B, s->R, s->W)) return false;
+    if (!attention_mfma_supported(s->d, s->rep, s->B, s->R, s->Wx)) return false;
     // GEMM K dimensions in whole pairs of 64-element steps of the bf16 main loop
     if (s->hidden % 128 || s->mlp % 128 || (s->hq * s->d) % 128) return false;
   }
@@ -51,15 +61,17 @@ bool make_shape(const ldr_config* c, Shape* s) {
 
 Layout make_layout(const Shape& s) {
   Layout L;
-  // a dropped view has zero bytes (its offset is that of the next region)
-  const size_t win = s.keep_win ? (size_t)s.D * s.hkv * s.W * s.d * s.el : 0;
-  const size_t sum = s.keep_sum ? (size_t)s.D * s.hq * s.R : 0;
+  // a dropped view has zero bytes (its offset is that of the next region);
+  // the pooled banks' slot means follow the window rows of each (layer, group)
+  const size_t win = (size_t)s.D * s.hkv * s.Wx * s.d * s.el;
+  const size_t sum = s.learned ? (size_t)s.D * s.hq * s.R : 0;
   L.kw = 0;
   L.vw = align_up(L.kw + win);
   L.m = align_up(L.vw + win);
   L.eta = align_up(L.m + sum * s.d * 4);
   L.h = align_up(L.eta + sum * 4);
-  L.bytes = L.h + (s.keep_bnd ? (size_t)s.Lb * s.hidden * s.el : 0);
+  L.ps = align_up(L.h + (s.keep_bnd ? (size_t)s.Lb * s.hidden * s.el : 0));
+  L.bytes = L.ps + (s.P ? (size_t)s.D * s.hkv * 2 * 2 * s.d * 4 : 0);
   L.stride = align_up(L.bytes);
   return L;
 }
@@ -185,6 +197,9 @@ static int views_update_impl(ldr_views* v, const int32_t* n_new, int32_t max_new
     if (launch_views_update(v->s, v->L, v->batch, v->arena, v->pos, v->G, n_new, max_new, K_new,
                             V_new, h_new, st) != hipSuccess)
       return LDR_EHIP;
+    if (v->s.P && launch_views_pool(v->s, v->L, v->batch, v->arena, v->pos, n_new, max_new,
+                                    K_new, V_new, st) != hipSuccess)
+      return LDR_EHIP;
   }
   if (launch_views_commit(v->batch, v->pos, n_new, max_new, v->status, st) != hipSuccess)
     return LDR_EHIP;
@@ -199,7 +214,7 @@ int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* 
   *out = nullptr;
   Shape s;
   if (!make_shape(cfg, &s) || batch <= 0 || !arena || !pos) return LDR_EINVAL;
-  if (s.keep_sum && (!G || !aligned(G, 16))) return LDR_EINVAL;   // G: the summary's queries
+  if (s.learned && (!G || !aligned(G, 16))) return LDR_EINVAL;   // G: the summary's queries
   if (!aligned(arena, kAlign) || !aligned(pos, 8)) return LDR_EINVAL;
   if (max_prefix < 0 || (max_prefix > 0 && !n_prefix)) return LDR_EINVAL;
   ldr_views* v = new (std::nothrow) ldr_views;

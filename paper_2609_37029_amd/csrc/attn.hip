@@ -75,13 +75,13 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
   const int ht = threadIdx.x - half * HT;  // thread index inside the half
   const int B = a.B;
   const uint8_t* seq = a.arena + (size_t)b * a.stride;
-  const size_t gw = (size_t)(a.layer * a.hkv + g) * a.W * D;
+  const size_t gw = (size_t)(a.layer * a.hkv + g) * a.Wx * D;   // window rows, then pooled slots
   const uint16_t* Kw = reinterpret_cast<const uint16_t*>(seq + a.kw) + gw;
   const uint16_t* Vw = reinterpret_cast<const uint16_t*>(seq + a.vw) + gw;
   // window chunks of the half, assigned over the full window so that the first
   // fetches do not wait for the position t (unfilled slots read as zeros and
   // are masked)
-  const int nwf = a.W / KC, cbeg = half * (nwf / 2), cend = half ? nwf : nwf / 2;
+  const int nwf = a.Wx / KC, cbeg = half * (nwf / 2), cend = half ? nwf : nwf / 2;
 
   // Window chunks in flight: slot p of the ring holds the p-th next chunk of
   // the half (depth WD, rotated by shifting). WD = 4 covers a half of a
@@ -92,14 +92,14 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
   for (int p = 0; p < WD; ++p)
 #pragma unroll
     for (int i = 0; i < PL; ++i) wk[p][i] = wv[p][i] = u32x4{0u, 0u, 0u, 0u};
-  const bool win = a.use_window;  // a variant without the window has no window region
+  const bool win = a.Wx > 0;  // no window and no pooled summary: no rows to stage
 #define LDR_FETCH(p, c)                                                                  \
   if (win) {                                                                             \
     _Pragma("unroll") for (int i = 0; i < PL; ++i) {                                     \
       const int idx_ = (ht + i * HT) % CH;                                               \
       const int slot_ = (c) * KC + idx_ / (D / 8), col_ = (idx_ % (D / 8)) * 8;          \
       wk[p][i] = *reinterpret_cast<const u32x4*>(Kw + (size_t)slot_ * D + col_);       \
-      wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)(idx_ >> 2) * a.W +       \
+      wv[p][i] = *reinterpret_cast<const u32x4*>(Vw + (size_t)(idx_ >> 2) * a.Wx +      \
                                                  (c) * KC + (idx_ & 3) * 8);             \
     }                                                                                    \
   }
@@ -154,8 +154,21 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
                  : u32x4{0u, 0u, 0u, 0u};
   }
   const long t = a.pos[b];
-  const int nv = !win ? 0 : t < a.W ? (int)t : a.W;
-  const int nwin = (nv + KC - 1) / KC;
+  const int nv = t < a.W ? (int)t : a.W;   // valid window rows (W = 0 without the window)
+  // Mean-pooled summary: its banks' slots follow the window rows; slot k of a
+  // bank is valid once k chunks have begun. Every chunk of the region is then
+  // walked (the ones without a valid row are skipped), as at steady state.
+  int np0 = 0, np1 = 0;
+  if (a.P) {
+    np0 = (int)min((t + a.S0 - 1) / a.S0, (long)a.P);
+    np1 = (int)min((t + a.S1 - 1) / a.S1, (long)a.P);
+  }
+  auto chunk_valid = [&](int chunk) -> int {   // valid rows of a 32-row chunk
+    const int r0 = chunk * KC;
+    const int v = r0 < a.W ? nv - r0 : r0 < a.W + a.P ? np0 - (r0 - a.W) : np1 - (r0 - a.W - a.P);
+    return v < 0 ? 0 : v > KC ? KC : v;
+  };
+  const int nwin = a.P ? nwf : (nv + KC - 1) / KC;
   const int nch = max(0, min(nwin, cend) - cbeg);      // window chunks of the half
   const int items = (half == 0 ? 1 : 0) + nch;
 #pragma unroll
@@ -295,7 +308,8 @@ __global__ void __launch_bounds__(128 * HPW) attention_mfma_kernel(AttnArgs a) {
     const int buf = it & 1;
     if (it < items) {
       const int chunk = cbeg + it - (half == 0 ? 1 : 0);  // -1: the block
-      item(Ks[half][buf], Vt[half][buf], chunk < cbeg ? B : min(KC, nv - chunk * KC));
+      const int nvalid = chunk < cbeg ? B : chunk_valid(chunk);
+      if (nvalid > 0) item(Ks[half][buf], Vt[half][buf], nvalid);
     }
     LDR_STASH(Ks[half][buf ^ 1], Vt[half][buf ^ 1])  // the next chunk (past the end: unused)
     LDR_ADVANCE
@@ -403,7 +417,7 @@ hipError_t launch_d(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
 
 }  // namespace
 
-bool attention_mfma_supported(int d, int rep, int B, int R, int W) {
+bool attention_mfma_supported(int d, int rep, int B, int R, int W) {   // W: region rows
   return (d == 64 || d == 128) && (rep == 1 || rep == 2 || rep % 4 == 0) && rep <= 64 &&
          B <= QR && R <= 16 && W % (2 * KC) == 0;
 }

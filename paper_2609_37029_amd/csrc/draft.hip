@@ -244,14 +244,19 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   const int h = blockIdx.x, b = blockIdx.y, g = h / a.rep;
   const int d = a.d, B = a.B;
   const long t = a.pos[b];
-  const int nv = a.use_window ? (int)(t < a.W ? t : a.W) : 0;
+  // keys: block, valid window rows, the valid slots of the two pooled banks
+  // (mean-pooled summary; slot k valid once k chunks have begun), the learned
+  // summary entries
+  const int nv = (int)(t < a.W ? t : a.W);
+  const int np0 = a.P ? (int)min((t + a.S0 - 1) / a.S0, (long)a.P) : 0;
+  const int np1 = a.P ? (int)min((t + a.S1 - 1) / a.S1, (long)a.P) : 0;
   const int nsum = t > 0 && a.use_summary ? a.R : 0;
-  const int NK = B + nv + nsum;
+  const int NK = B + nv + np0 + np1 + nsum;
   float* qs = smem;                 // [B][d]
   float* ks = qs + B * d;           // [B][d]
   float* vs = ks + B * d;           // [B][d]
   float* S = vs + B * d;            // [B][B + W + R]
-  const int ldS = B + a.W + a.R;
+  const int ldS = B + a.Wx + a.R;
 
   // q (head h), k and v (group g) of the block
   const T* qkv = static_cast<const T*>(a.qkv);
@@ -265,8 +270,13 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
   __syncthreads();
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const uint8_t* seq = a.arena + (size_t)b * a.stride;
-  const T* Kw = reinterpret_cast<const T*>(seq + a.kw) + ((size_t)(a.layer * a.hkv + g) * a.W) * d;
-  const T* Vw = reinterpret_cast<const T*>(seq + a.vw) + ((size_t)(a.layer * a.hkv + g) * a.W) * d;
+  const T* Kw = reinterpret_cast<const T*>(seq + a.kw) + ((size_t)(a.layer * a.hkv + g) * a.Wx) * d;
+  const T* Vw = reinterpret_cast<const T*>(seq + a.vw) + ((size_t)(a.layer * a.hkv + g) * a.Wx) * d;
+  // region row of key k - B among the window and pooled keys
+  auto region_row = [&](int k) -> int {
+    return k < nv ? k : k < nv + np0 ? a.W + (k - nv) : a.W + a.P + (k - nv - np0);
+  };
+  const int nreg = nv + np0 + np1;
   const T* Gh = nsum ? static_cast<const T*>(a.G) + ((size_t)(a.layer * a.hq + h) * a.R) * d
                      : nullptr;
   const float* Mh = reinterpret_cast<const float*>(seq + a.m_off) + ((size_t)(a.layer * a.hq + h) * a.R) * d;
@@ -276,11 +286,11 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
     float dot = 0.f;
     if (k < B) {
       for (int e = 0; e < d; ++e) dot += q[e] * ks[k * d + e];
-    } else if (k < B + nv) {
-      const T* kr = Kw + (size_t)(k - B) * d;
+    } else if (k < B + nreg) {
+      const T* kr = Kw + (size_t)region_row(k - B) * d;
       for (int e = 0; e < d; ++e) dot += q[e] * Elem<T>::load(kr + e);
     } else {
-      const T* kr = Gh + (size_t)(k - B - nv) * d;
+      const T* kr = Gh + (size_t)(k - B - nreg) * d;
       for (int e = 0; e < d; ++e) dot += q[e] * Elem<T>::load(kr + e);
     }
     S[i * ldS + k] = dot * a.inv_sqrt_d;
@@ -306,8 +316,9 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
     const float* p = S + i * ldS;
     float acc = 0.f;
     for (int k = 0; k < B; ++k) acc += p[k] * vs[k * d + e];
-    for (int k = 0; k < nv; ++k) acc += p[B + k] * Elem<T>::load(Vw + (size_t)e * a.W + k);
-    for (int k = 0; k < nsum; ++k) acc += p[B + nv + k] * Mh[(size_t)k * d + e];
+    for (int k = 0; k < nreg; ++k)
+      acc += p[B + k] * Elem<T>::load(Vw + (size_t)e * a.Wx + region_row(k));
+    for (int k = 0; k < nsum; ++k) acc += p[B + nreg + k] * Mh[(size_t)k * d + e];
     Elem<T>::store(out + ((long)b * B + i) * (a.hq * d) + h * d + e, acc);
   }
 }
@@ -390,11 +401,12 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
   a.qkv = p.qkv;
   a.arena = p.arena; a.stride = L.stride; a.kw = L.kw; a.vw = L.vw; a.m_off = L.m;
   a.pos = p.pos; a.G = p.G;
-  a.o = p.o; a.layer = layer; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.B = s.B; a.W = s.W;
+  a.o = p.o; a.layer = layer; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.B = s.B; a.W = s.Wr;
+  a.Wx = s.Wx; a.P = s.P; a.S0 = s.S0; a.S1 = s.S1;
   a.R = s.R; a.rep = s.rep; a.qkv_out = s.qkv_out;
-  a.use_window = s.keep_win; a.use_summary = s.keep_sum;
+  a.use_summary = s.learned;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
-  const size_t shm = (size_t)(3 * s.B * s.d + s.B * (s.B + s.W + s.R)) * sizeof(float);
+  const size_t shm = (size_t)(3 * s.B * s.d + s.B * (s.B + s.Wx + s.R)) * sizeof(float);
   if (s.dtype == LDR_BF16) return launch_attention_mfma(a, s.hkv, batch, st);
   const dim3 grid(s.hq, batch);
   hipLaunchKernelGGL(attention_valu_kernel<float>, grid, dim3(kThreads), shm, st, a);

@@ -17,6 +17,7 @@ inline size_t align_up(size_t x, size_t a = kAlign) { return (x + a - 1) / a * a
 // Byte offsets of the views inside one sequence's arena slot.
 struct Layout {
   size_t kw, vw, m, eta, h;  // region offsets
+  size_t ps;                 // fp32 sums of the pooled banks' open chunks
   size_t bytes;              // sum of the (aligned) regions
   size_t stride;             // per-sequence stride, bytes rounded up to kAlign
 };
@@ -29,6 +30,9 @@ struct Shape {
   double rope_base;
   size_t el;     // bytes per element of the configuration dtype
   bool keep_win, keep_sum, keep_bnd;  // views kept (ablation variants drop some)
+  bool learned;  // the learned-query summary (Eq. 5) is kept
+  int P, S0, S1; // mean-pooled summary: slots per bank and the two strides (P = 0: none)
+  int Wr, Wx;    // window ring rows kept (W or 0) and rows per (layer, group): Wr + 2P
 };
 
 bool make_shape(const ldr_config* c, Shape* s);
@@ -110,6 +114,10 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
                                const int64_t* pos, const void* G, const int32_t* n_new,
                                int max_new, const void* K_new, const void* V_new,
                                const void* h_new, hipStream_t st);
+// Mean-pooled summary banks (views.hip); runs before the commit.
+hipError_t launch_views_pool(const Shape& s, const Layout& L, int batch, void* arena,
+                             const int64_t* pos, const int32_t* n_new, int max_new,
+                             const void* K_new, const void* V_new, hipStream_t st);
 hipError_t launch_views_commit(int batch, int64_t* pos, const int32_t* n_new, int max_new,
                                int32_t* status, hipStream_t st);
 
@@ -165,12 +173,15 @@ struct AttnArgs {
   const int64_t* pos; const void* G;
   void* o;
   int layer, hq, hkv, d, B, W, R, rep, qkv_out;
-  int use_window, use_summary;   // sources kept (ablation variants drop one)
+  int Wx;            // rows per (layer, group) region: the W window rows (0 if
+                     // dropped), then 2P pooled slot means
+  int P, S0, S1;     // mean-pooled summary (P = 0: none)
+  int use_summary;   // the learned summary is kept
   float inv_sqrt_d;
 };
 // bf16 MFMA kernel (attn.hip): one workgroup per (kv group, sequence).
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st);
-bool attention_mfma_supported(int d, int rep, int B, int R, int W);
+bool attention_mfma_supported(int d, int rep, int B, int R, int Wx);
 
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st);

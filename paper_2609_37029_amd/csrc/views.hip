@@ -42,6 +42,7 @@ struct UpdateArgs {
   const void* K_new; const void* V_new; const void* h_new;
   int D, hq, hkv, d, W, R, rep, hb_elems;  // hb_elems = L_b * hidden
   int keep_win, keep_sum, keep_bnd;         // views kept (ablation variants drop some)
+  int Wx;                                   // rows per (layer, group) region (window first)
   float inv_sqrt_d;
 };
 
@@ -129,8 +130,8 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
   __shared__ float Ks[kTileRows][256 + 4];
   __shared__ float Vs[kTileRows][256 + 4];
   constexpr int EPC = 16 / sizeof(T);  // elements per 16-byte chunk
-  T* Kw = reinterpret_cast<T*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * d;
-  T* Vw = reinterpret_cast<T*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * d;
+  T* Kw = reinterpret_cast<T*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.Wx) * d;
+  T* Vw = reinterpret_cast<T*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.Wx) * d;
   float mx = -INFINITY, l = 0.f;
   for (int r0 = 0; r0 < ((win || sum) ? n : 0); r0 += kTileRows) {
     const int nr = min(kTileRows, n - r0);
@@ -161,7 +162,7 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
       if (win && r >= rs && r < nr) {
         const size_t slot = (size_t)((t + r0 + r) % a.W);
         for (int e = threadIdx.x / kTileRows; e < d; e += kThreads / kTileRows)
-          Elem<T>::store(Vw + (size_t)e * a.W + slot, Vs[r][e]);
+          Elem<T>::store(Vw + (size_t)e * a.Wx + slot, Vs[r][e]);
       }
     }
     if (!sum) continue;   // window only: no statistics
@@ -295,8 +296,8 @@ views_update_mfma_kernel(UpdateArgs a) {
 
   if (a.keep_bnd) boundary_slice<uint16_t>(a, seq, j, g, b, NTH);
 
-  uint16_t* Kw = reinterpret_cast<uint16_t*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.W) * DH;
-  uint16_t* Vw = reinterpret_cast<uint16_t*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.W) * DH;
+  uint16_t* Kw = reinterpret_cast<uint16_t*>(seq + a.kw) + ((size_t)(j * a.hkv + g) * a.Wx) * DH;
+  uint16_t* Vw = reinterpret_cast<uint16_t*>(seq + a.vw) + ((size_t)(j * a.hkv + g) * a.Wx) * DH;
   const uint16_t* Kn = static_cast<const uint16_t*>(a.K_new);
   const uint16_t* Vn = static_cast<const uint16_t*>(a.V_new);
   f32x4 o[NT];
@@ -333,7 +334,7 @@ views_update_mfma_kernel(UpdateArgs a) {
       const int r = tid % KT;
       if (win && r >= rs && r < nr) {
         const size_t slot = (size_t)((t + r0 + r) % a.W);
-        for (int e = tid / KT; e < DH; e += NTH / KT) Vw[(size_t)e * a.W + slot] = Vt[e * VLD + r];
+        for (int e = tid / KT; e < DH; e += NTH / KT) Vw[(size_t)e * a.Wx + slot] = Vt[e * VLD + r];
       }
     }
     if (!sum) continue;   // window only: no statistics
@@ -401,6 +402,58 @@ views_update_mfma_kernel(UpdateArgs a) {
   }
 }
 
+// Mean-pooled summary (the views as the configurations word them): for each
+// of two strides S, slot c mod P of the bank holds the mean K and V row of
+// chunk c = rows [cS, (c+1)S). One workgroup per (kv group, layer, sequence);
+// thread (bank, e) owns dim e of one bank. The chunks the new rows touch are
+// summed in fp32 in row order, the open chunk continuing from its stored sums,
+// and each slot takes sum / rows so far; only the last P chunks are written
+// (older ones would be recycled by the same update). Slots are the bank rows
+// after the window rows of the (layer, group) region: K row-major, V
+// transposed, like the window.
+struct PoolArgs {
+  uint8_t* arena; size_t stride, kw, vw, ps;
+  const int64_t* pos; const int32_t* n_new; int max_new;
+  const void* K_new; const void* V_new;
+  int D, hkv, d, Wr, Wx, P, S0, S1;
+};
+
+template <typename T>
+__global__ void __launch_bounds__(256) views_pool_kernel(PoolArgs a) {
+  const int g = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
+  const int n = a.n_new[b];
+  if (n <= 0 || n > a.max_new) return;   // empty set: identity; bad count: commit flags it
+  const int d = a.d, bank = (int)threadIdx.x / d, e = (int)threadIdx.x % d;
+  const int64_t t = a.pos[b], S = bank ? a.S1 : a.S0;
+  uint8_t* seq = a.arena + (size_t)b * a.stride;
+  const size_t grp = (size_t)j * a.hkv + g;
+  T* Kw = reinterpret_cast<T*>(seq + a.kw) + grp * a.Wx * d;
+  T* Vw = reinterpret_cast<T*>(seq + a.vw) + grp * a.Wx * d;
+  float* ps = reinterpret_cast<float*>(seq + a.ps) + (grp * 2 + bank) * 2 * d;   // K sums, V sums
+  const T* Kn = static_cast<const T*>(a.K_new);
+  const T* Vn = static_cast<const T*>(a.V_new);
+  const int64_t c0 = t / S, c1 = (t + n - 1) / S;
+  const int64_t cfirst = c0 > c1 - a.P + 1 ? c0 : c1 - a.P + 1;
+  float sk = 0.f, sv = 0.f;
+  for (int64_t c = cfirst; c <= c1; ++c) {
+    const int64_t r0 = t > c * S ? t : c * S, r1 = t + n < (c + 1) * S ? t + n : (c + 1) * S;
+    const bool carry = c == c0 && t % S != 0;   // the chunk was opened by an earlier update
+    sk = carry ? ps[e] : 0.f;
+    sv = carry ? ps[d + e] : 0.f;
+    for (int64_t p = r0; p < r1; ++p) {
+      const size_t src = ((((size_t)b * a.max_new + (size_t)(p - t)) * a.D + j) * a.hkv + g) * d + e;
+      sk += Elem<T>::load(Kn + src);
+      sv += Elem<T>::load(Vn + src);
+    }
+    const float cnt = (float)(r1 - c * S);
+    const int slot = a.Wr + bank * a.P + (int)(c % a.P);
+    Elem<T>::store(Kw + (size_t)slot * d + e, sk / cnt);
+    Elem<T>::store(Vw + (size_t)e * a.Wx + slot, sv / cnt);
+  }
+  ps[e] = sk;   // the last chunk's sums (used next time only if it is still open)
+  ps[d + e] = sv;
+}
+
 __global__ void views_commit_kernel(int batch, int64_t* pos, const int32_t* n_new,
                                     int max_new, int32_t* status) {
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
@@ -429,6 +482,7 @@ hipError_t launch_update_t(const UpdateArgs& a, int dpt, dim3 grid, hipStream_t 
 
 // Threads per summary query: Q = rep * R queries share 256 threads.
 int views_dims_per_thread(const Shape& s) {
+  if (s.R == 0) return s.d % 16 == 0 ? 16 : 0;   // no learned queries: ring writes only
   const int q = s.rep * s.R;
   if (q <= 0 || q > kThreads || kThreads % q) return 0;
   const int tpq = kThreads / q;
@@ -442,7 +496,7 @@ hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* 
   const size_t words = L.stride / 4 * (size_t)batch;
   const int blocks = (int)((words + kThreads - 1) / kThreads < 4096
                                ? (words + kThreads - 1) / kThreads : 4096);
-  const size_t eta_bytes = s.keep_sum ? (size_t)s.D * s.hq * s.R * 4 : 0;
+  const size_t eta_bytes = s.learned ? (size_t)s.D * s.hq * s.R * 4 : 0;
   hipLaunchKernelGGL(views_reset_kernel, dim3(blocks > 0 ? blocks : 1), dim3(kThreads), 0, st,
                      static_cast<uint8_t*>(arena), L.stride, L.eta, eta_bytes, batch, pos);
   return hipGetLastError();
@@ -459,7 +513,8 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
   a.K_new = K_new; a.V_new = V_new; a.h_new = h_new;
   a.D = s.D; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.W = s.W; a.R = s.R; a.rep = s.rep;
   a.hb_elems = s.Lb * s.hidden;
-  a.keep_win = s.keep_win; a.keep_sum = s.keep_sum; a.keep_bnd = s.keep_bnd;
+  a.keep_win = s.keep_win; a.keep_sum = s.learned; a.keep_bnd = s.keep_bnd;
+  a.Wx = s.Wx;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const dim3 grid(s.hkv, s.D, batch);
   const int q = s.rep * s.R;
@@ -476,6 +531,22 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
   const int dpt = views_dims_per_thread(s);
   return s.dtype == LDR_BF16 ? launch_update_t<uint16_t>(a, dpt, grid, st)
                              : launch_update_t<float>(a, dpt, grid, st);
+}
+
+hipError_t launch_views_pool(const Shape& s, const Layout& L, int batch, void* arena,
+                             const int64_t* pos, const int32_t* n_new, int max_new,
+                             const void* K_new, const void* V_new, hipStream_t st) {
+  PoolArgs a;
+  a.arena = static_cast<uint8_t*>(arena); a.stride = L.stride; a.kw = L.kw; a.vw = L.vw;
+  a.ps = L.ps; a.pos = pos; a.n_new = n_new; a.max_new = max_new; a.K_new = K_new;
+  a.V_new = V_new; a.D = s.D; a.hkv = s.hkv; a.d = s.d; a.Wr = s.Wr; a.Wx = s.Wx; a.P = s.P;
+  a.S0 = s.S0; a.S1 = s.S1;
+  const dim3 grid(s.hkv, s.D, batch), block(2 * s.d);   // d <= 128
+  if (s.dtype == LDR_BF16)
+    hipLaunchKernelGGL(views_pool_kernel<uint16_t>, grid, block, 0, st, a);
+  else
+    hipLaunchKernelGGL(views_pool_kernel<float>, grid, block, 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_views_commit(int batch, int64_t* pos, const int32_t* n_new, int max_new,

@@ -31,7 +31,8 @@ class Config(ctypes.Structure):
         "hidden", "n_q_heads", "n_kv_heads", "head_dim", "mlp", "vocab", "n_layers",
         "n_feat_layers", "block", "window", "summary", "dtype")] + [
         ("rope_theta", ctypes.c_float), ("ntk_alpha", ctypes.c_float),
-        ("rms_eps", ctypes.c_float), ("drop_views", ctypes.c_int32)]
+        ("rms_eps", ctypes.c_float), ("drop_views", ctypes.c_int32),
+        ("pool_slots", ctypes.c_int32), ("pool_stride", ctypes.c_int32 * 2)]
 
 # ldr_view_drop bits (ablation variants)
 LDR_DROP_WINDOW, LDR_DROP_SUMMARY, LDR_DROP_BOUNDARY = 1, 2, 4
@@ -111,11 +112,13 @@ def _check(rc: int, what: str):
 
 def config(shape) -> Config:
     """ldr_config of a synth.Shape-like object."""
+    strides = tuple(getattr(shape, "pool_strides", ()) or (0, 0))
     return Config(shape.hidden, shape.n_q_heads, shape.n_kv_heads, shape.head_dim, shape.mlp,
                   shape.vocab, shape.n_layers, shape.n_feat_layers, shape.block, shape.window,
                   shape.summary, LDR_BF16 if shape.dtype == "bf16" else LDR_F32,
                   shape.rope_theta, shape.ntk_alpha, shape.rms_eps,
-                  getattr(shape, "drop_views", 0))
+                  getattr(shape, "drop_views", 0), getattr(shape, "pool_slots", 0) or 0,
+                  (ctypes.c_int32 * 2)(*strides))
 
 
 def state_bytes(shape) -> int:
@@ -192,20 +195,43 @@ class Views:
     def _drops(self, bit) -> bool:
         return bool(getattr(self.shape, "drop_views", 0) & bit)
 
+    def _pool(self) -> int:
+        return 0 if self._drops(LDR_DROP_SUMMARY) else int(getattr(self.shape, "pool_slots", 0)
+                                                           or 0)
+
+    def _rows(self):
+        """(window rows kept, rows per (layer, group) region) and the region as
+        K [batch][D][Hkv][rows][d] and V [batch][D][Hkv][rows][d] (a transposed
+        view of the stored V^T)."""
+        s = self.shape
+        wr = 0 if self._drops(LDR_DROP_WINDOW) else s.window
+        wx = wr + 2 * self._pool()
+        shp = (s.n_layers, s.n_kv_heads, wx, s.head_dim)
+        vt = (s.n_layers, s.n_kv_heads, s.head_dim, wx)
+        return wr, (self._region(self.layout["kw"], shp, s.torch_dtype),
+                    self._region(self.layout["vw"], vt, s.torch_dtype).transpose(-1, -2))
+
     def window(self):
         """Window K and V as [batch][D][Hkv][W][d] (V is stored transposed,
         [D][Hkv][d][W]; this returns a transposed view of it); None without
         the window view."""
         if self._drops(LDR_DROP_WINDOW):
             return None
-        s = self.shape
-        shp = (s.n_layers, s.n_kv_heads, s.window, s.head_dim)
-        vt = (s.n_layers, s.n_kv_heads, s.head_dim, s.window)
-        return (self._region(self.layout["kw"], shp, s.torch_dtype),
-                self._region(self.layout["vw"], vt, s.torch_dtype).transpose(-1, -2))
+        wr, (K, V) = self._rows()
+        return K[..., :wr, :], V[..., :wr, :]
+
+    def pooled(self):
+        """Slot means of the mean-pooled summary's two banks, K and V each
+        [batch][2][D][Hkv][P][d]; None with the learned summary."""
+        P = self._pool()
+        if not P:
+            return None
+        wr, (K, V) = self._rows()
+        return (torch.stack([K[..., wr + i * P:wr + (i + 1) * P, :] for i in range(2)], 1),
+                torch.stack([V[..., wr + i * P:wr + (i + 1) * P, :] for i in range(2)], 1))
 
     def summary(self):
-        if self._drops(LDR_DROP_SUMMARY):
+        if self._drops(LDR_DROP_SUMMARY) or self._pool():
             return None
         s = self.shape
         return (self._region(self.layout["m"], (s.n_layers, s.n_q_heads, s.summary, s.head_dim),

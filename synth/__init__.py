@@ -109,6 +109,8 @@ WORKLOADS = {
         Workload("qwen3-8b-b16-t32768", QWEN3_8B, 16, 32768, 1.0),
         Workload("qwen3-8b-b16-t131072-loop64", QWEN3_8B, 16, 131072, 1.0, 64, 17),
         Workload("qwen3-32b-b16-t65536", QWEN3_32B, 16, 65536, 1.0),
+        Workload("tiny-pooled-b1-t2048", TINY_POOLED, 1, 2048, 0.0),
+        Workload("qwen3-8b-pooled-b16-t32768", QWEN3_8B_POOLED, 16, 32768, 1.0),
     )
 }
 SWEEP_PREFIX = (1024, 4096, 16384, 65536, 131072, 262144)

@@ -17,7 +17,7 @@ class Pair:
     def __init__(self, ldr, shape, batch, G, oracle_seqs=None):
         self.ldr, self.s, self.batch = ldr, shape, batch
         self.G = G
-        self.G64 = synth.to_f64(G)
+        self.G64 = None if G is None else synth.to_f64(G)
         self.views = ldr.Views(shape, batch, G).init()
         self.seqs = list(range(batch)) if oracle_seqs is None else list(oracle_seqs)
         self.ost = {b: OV.empty(shape) for b in self.seqs}
@@ -55,7 +55,9 @@ def check_views(pair, rtol_m=1e-4, atol_m=1e-6):
     torch.cuda.synchronize()
     v = pair.views
     pos = v.pos.cpu().numpy()
-    win, summ, bnd = v.window(), v.summary(), v.boundary()
+    win, summ, bnd, pool = v.window(), v.summary(), v.boundary(), v.pooled()
+    PK, PV = (t.cpu() for t in pool) if pool is not None else (None, None)
+    bf16 = pair.s.dtype == "bf16"
     Kw, Vw = (t.cpu() for t in win) if win is not None else (None, None)
     M, eta = (t.cpu().numpy() for t in summ) if summ is not None else (None, None)
     hb = bnd.cpu() if bnd is not None else None
@@ -68,6 +70,11 @@ def check_views(pair, rtol_m=1e-4, atol_m=1e-6):
             assert np.array_equal(synth.to_f64(Vw[b]), o.Vw), f"window V of sequence {b}"
         if hb is not None:
             assert np.array_equal(synth.to_f64(hb[b]), o.h), f"boundary of sequence {b}"
+        if PK is not None:
+            # slot means: fp32 sums and one division, stored in the model dtype
+            rtol = 2.0 ** -8 if bf16 else 1e-6
+            np.testing.assert_allclose(synth.to_f64(PK[b]), o.PK, rtol=rtol, atol=2e-5)
+            np.testing.assert_allclose(synth.to_f64(PV[b]), o.PV, rtol=rtol, atol=2e-5)
         if M is None:
             continue
         if o.t == 0:

@@ -166,3 +166,16 @@ def test_view_drop_variants_state_and_launches(L, drop):
         bad = L.config(synth.TINY)
         bad.drop_views = flags
         assert L.lib().ldr_config_check(ctypes.byref(bad)) == L.LDR_EINVAL
+
+
+def test_pooled_summary_state_and_validation(L):
+    """The mean-pooled summary: arena bytes as the oracle accounts them, fixed
+    in the prefix; slots must be a multiple of 32 and strides positive."""
+    from oracle import views as OV
+    from paper_2609_37029_amd import ldr
+    for s in (synth.TINY_POOLED, synth.QWEN3_8B_POOLED,
+              synth.QWEN3_8B_POOLED.replace(drop_views=1)):
+        assert ldr.state_bytes(s) == OV.state_bytes(s) > 0
+    for kw in (dict(pool_slots=48), dict(pool_strides=(0, 4)), dict(pool_strides=(4, -1))):
+        c = L.config(synth.TINY_POOLED.replace(**kw))
+        assert L.lib().ldr_config_check(ctypes.byref(c)) == L.LDR_EINVAL, kw
