@@ -267,9 +267,10 @@ size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
  * on ties), lse[r] = that maximum, logq[r] = 0. temperature T > 0: support S =
  * all V tokens (top_k = 0) or the top_k largest logits (lower index first on
  * ties); tokens[r] = argmax over S of fl(fl(z_v / T) + g_v) (lowest index on
- * ties) with g_v = -log(-log(u_v)) Gumbel noise from Philox4x64-10 (key
- * (seed, step), counter (v div 8, r, 0, 0), 32-bit half v mod 2 of word
- * (v div 2) mod 4, u = (2 (bits >> 9) + 1) 2^-24) and a fixed-operation fp32
+ * ties) with g_v = -log(-log(u_v)) Gumbel noise from Philox4x32-10 (key
+ * (seed mod 2^32, seed div 2^32), counter (v div 4, r, step mod 2^32,
+ * (step div 2^32) mod 2^30), word v mod 4, u = (2 (bits >> 9) + 1) 2^-24; a
+ * step is unique below 2^62) and a fixed-operation fp32
  * logarithm, so the tokens are reproducible bit for bit on any IEEE machine;
  * lse[r] = log sum_{v in S} exp(z_v / T); logq[r] = z_y / T - lse[r].
  * top_k >= vocab is the full vocabulary; a negative top_k is LDR_EINVAL. With
@@ -320,10 +321,10 @@ size_t ldr_verify_workspace_bytes(int32_t batch, int32_t block, int32_t vocab);
  * as equal: the fp32 normalisers do not resolve them); after B acceptances, and
  * when the residual w has no positive mass, it emits the first argmax of
  * fl(fl(P_v / T) + g_v) over the row (the drafting sampler's rule). Noise:
- * Philox4x64-10 with key (seed, step); u_i from counter (i - 1, b, 1, 0), the
- * upper 32 bits of word 0; g_v from counter (v div 8, b, 2, 0), 32-bit half
- * v mod 2 of word (v div 2) mod 4; both through u = (2 (bits >> 9) + 1) 2^-24,
- * and g = -log(-log(u)) with ldr_sample's fixed-operation logarithm. T = 0
+ * ldr_sample's Philox4x32-10 layout with the top two bits of the last counter
+ * word set to a stream: u_i is word 0 of counter (i - 1, b, ...) in stream 1,
+ * g_v token v of row b in stream 2; both through u = (2 (bits >> 9) + 1)
+ * 2^-24, and g = -log(-log(u)) with ldr_sample's fixed-operation logarithm. T = 0
  * verifies greedily: y_i is accepted when it is the first argmax of P[b][i-1],
  * and the round emits the first argmax of the row where it stops (draft_logits
  * and draft_lse are not read and may be NULL). The ratio, the residual and the

@@ -13,10 +13,10 @@ The argmax is an integer decision taken from fp32 keys, so the keys are
 computed exactly as the GPU kernel does: fl(fl(z_v / T) + g_v), every step an
 IEEE fp32 operation. The noise is fully specified here:
 
-* bits: Philox4x64-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers:
-  as easy as 1, 2, 3", SC 2011) with key (seed, step) and counter
-  (v div 8, row, 0, 0); token v takes 32-bit half (v mod 2) of output word
-  ((v div 2) mod 4);
+* bits: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers:
+  as easy as 1, 2, 3", SC 2011) with key (seed mod 2^32, seed div 2^32) and
+  counter (v div 4, row, step mod 2^32, (step div 2^32) mod 2^30 + 2^30 s),
+  s the stream (0 for drafting); token v takes output word v mod 4;
 * uniform: k = bits >> 9, u = (2k + 1) * 2^-24, exact in fp32, in (0, 1);
 * Gumbel: g = -log(-log(u)) with the fp32 logarithm ``logf`` below, a fixed
   sequence of IEEE fp32 operations (no fused multiply-add): exponent split,
@@ -40,42 +40,40 @@ from __future__ import annotations
 import numpy as np
 import scipy.special
 
-# Philox4x64 multipliers and Weyl key increments (Salmon et al., SC 2011).
-PHILOX_M0 = np.uint64(0xD2E7470EE14C6C93)
-PHILOX_M1 = np.uint64(0xCA5A826395121157)
-PHILOX_W0 = np.uint64(0x9E3779B97F4A7C15)
-PHILOX_W1 = np.uint64(0xBB67AE8584CAA73B)
+# Philox4x32 multipliers and Weyl key increments (Salmon et al., SC 2011).
+PHILOX_M0 = np.uint64(0xD2511F53)
+PHILOX_M1 = np.uint64(0xCD9E8D57)
+PHILOX_W0 = np.uint64(0x9E3779B9)
+PHILOX_W1 = np.uint64(0xBB67AE85)
 _M32 = np.uint64(0xFFFFFFFF)
 _S32 = np.uint64(32)
 
 
-def _mulhilo64(a, b):
-    """(hi, lo) 64-bit halves of the 128-bit product a*b (a array, b scalar)."""
-    a = np.asarray(a, dtype=np.uint64)
-    al, ah = a & _M32, a >> _S32
-    bl, bh = b & _M32, b >> _S32
-    p0, p1, p2, p3 = al * bl, al * bh, ah * bl, ah * bh      # each < 2^64, exact
-    mid = (p0 >> _S32) + (p1 & _M32) + (p2 & _M32)
-    hi = p3 + (p1 >> _S32) + (p2 >> _S32) + (mid >> _S32)
-    with np.errstate(over="ignore"):
-        lo = a * b                                            # wraps mod 2^64
-    return hi, lo
-
-
-def philox4x64_10(ctr, key):
-    """Philox4x64 with 10 rounds. ctr: 4 uint64 arrays, key: 2 uint64 arrays
-    (broadcastable). Returns the 4 output words."""
-    c = [np.asarray(x, dtype=np.uint64) for x in ctr]
-    k0, k1 = (np.asarray(x, dtype=np.uint64) for x in key)
-    with np.errstate(over="ignore"):
-        for rnd in range(10):
-            if rnd:
-                k0 = k0 + PHILOX_W0
-                k1 = k1 + PHILOX_W1
-            hi0, lo0 = _mulhilo64(c[0], PHILOX_M0)
-            hi1, lo1 = _mulhilo64(c[2], PHILOX_M1)
-            c = [hi1 ^ c[1] ^ k0, lo1, hi0 ^ c[3] ^ k1, lo0]
+def philox4x32_10(ctr, key):
+    """Philox4x32 with 10 rounds. ctr: 4 arrays of 32-bit words, key: 2 (held
+    in uint64, broadcastable). Returns the 4 output words (uint64 < 2^32).
+    A round: (hi0, lo0) = M0 c0, (hi1, lo1) = M1 c2 (64-bit products, exact in
+    uint64), c <- (hi1 ^ c1 ^ k0, lo1, hi0 ^ c3 ^ k1, lo0); the key advances by
+    the Weyl constants before every round but the first."""
+    c = [np.asarray(x, dtype=np.uint64) & _M32 for x in ctr]
+    k0, k1 = (np.asarray(x, dtype=np.uint64) & _M32 for x in key)
+    for rnd in range(10):
+        if rnd:
+            k0 = (k0 + PHILOX_W0) & _M32
+            k1 = (k1 + PHILOX_W1) & _M32
+        p0 = c[0] * PHILOX_M0
+        p1 = c[2] * PHILOX_M1
+        c = [(p1 >> _S32) ^ c[1] ^ k0, p1 & _M32, (p0 >> _S32) ^ c[3] ^ k1, p0 & _M32]
     return c
+
+
+def _counter(seed, step, stream):
+    """Key and the two upper counter words of a (seed, step, stream)."""
+    seed, step = int(seed), int(step)
+    key = (np.uint64(seed & 0xFFFFFFFF), np.uint64((seed >> 32) & 0xFFFFFFFF))
+    c2 = np.uint64(step & 0xFFFFFFFF)
+    c3 = np.uint64(((step >> 32) & 0x3FFFFFFF) | (int(stream) << 30))
+    return key, c2, c3
 
 
 # fp32 constants of logf, as bit patterns (nearest fp32 to the exact value).
@@ -118,18 +116,14 @@ def logf(x):
     return (e * LN2_HI + (e * LN2_LO + r)).astype(np.float32)
 
 
-def philox_bits(seed, step, row, v):
-    """The 32 noise bits of token v in row `row` (uint32 arrays)."""
+def philox_bits(seed, step, row, v, stream=0):
+    """The 32 noise bits of token v in row `row` of a stream (uint32 arrays)."""
     v, row = np.broadcast_arrays(np.asarray(v, dtype=np.uint64),
                                  np.asarray(row, dtype=np.uint64))
-    zero = np.zeros_like(v)
-    key = (np.uint64(seed), np.uint64(step))
-    w = philox4x64_10((v >> np.uint64(3), row, zero, zero), key)
-    w = np.stack(w, axis=0)                                    # [4][...]
-    word = np.take_along_axis(w, ((v >> np.uint64(1)) & np.uint64(3)).astype(np.int64)[None],
-                              axis=0)[0]
-    half = (v & np.uint64(1)) * np.uint64(32)
-    return ((word >> half) & _M32).astype(np.uint32)
+    key, c2, c3 = _counter(seed, step, stream)
+    w = np.stack(philox4x32_10((v >> np.uint64(2), row, c2 + 0 * v, c3 + 0 * v), key), axis=0)
+    word = np.take_along_axis(w, (v & np.uint64(3)).astype(np.int64)[None], axis=0)[0]
+    return word.astype(np.uint32)
 
 
 def uniform(bits):
@@ -244,11 +238,10 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
 #  * T = 0 verifies greedily: y_i is accepted when it is the first argmax of
 #    P_i, and the round emits the first argmax of the row where it stops.
 #
-# Noise (Philox4x64-10, key (seed, step), counter streams of their own):
-#  * u_i of sequence b: counter (i - 1, b, 1, 0), the upper 32 bits of word 0,
-#    made uniform like the drafting noise;
-#  * the emitted token's Gumbel noise g_v: counter (v div 8, b, 2, 0), word and
-#    32-bit half chosen as for the drafting noise.
+# Noise (the drafting layout of Philox4x32-10 in streams of its own):
+#  * u_i of sequence b: word 0 of the block of counter i - 1 and row b in
+#    stream 1, made uniform like the drafting noise;
+#  * the emitted token's Gumbel noise g_v: token v of row b in stream 2.
 
 
 RESIDUAL_REL = 2.0 ** -14   # a residual entry needs p - q above this fraction of p
@@ -256,22 +249,14 @@ RESIDUAL_REL = 2.0 ** -14   # a residual entry needs p - q above this fraction o
 
 def verify_uniform(seed, step, b, i):
     """u_i of sequence b (i = 1 .. B) as an exact fp32 value in (0, 1)."""
-    w = philox4x64_10((np.uint64(i - 1), np.uint64(b), np.uint64(1), np.uint64(0)),
-                      (np.uint64(seed), np.uint64(step)))
-    return uniform(np.uint32(int(w[0]) >> 32))
+    key, c2, c3 = _counter(seed, step, 1)
+    w = philox4x32_10((np.uint64(i - 1), np.uint64(b), c2, c3), key)
+    return uniform(np.uint32(int(w[0])))
 
 
 def verify_gumbel(seed, step, b, v):
     """Gumbel noise of token(s) v for the emitted token of sequence b."""
-    v = np.asarray(v, dtype=np.uint64)
-    zero = np.zeros_like(v)
-    key = (np.uint64(seed), np.uint64(step))
-    w = np.stack(philox4x64_10((v >> np.uint64(3), zero + np.uint64(b), zero + np.uint64(2), zero),
-                               key), axis=0)
-    word = np.take_along_axis(w, ((v >> np.uint64(1)) & np.uint64(3)).astype(np.int64)[None],
-                              axis=0)[0]
-    bits = ((word >> ((v & np.uint64(1)) * np.uint64(32))) & _M32).astype(np.uint32)
-    return -logf(-logf(uniform(bits)))
+    return -logf(-logf(uniform(philox_bits(seed, step, b, v, stream=2))))
 
 
 def _softmax64(x):

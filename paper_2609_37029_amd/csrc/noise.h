@@ -1,8 +1,12 @@
-// Counter-based noise shared by the sampler and the verifier: Philox4x64-10
+// Counter-based noise shared by the sampler and the verifier: Philox4x32-10
 // (Salmon, Moraes, Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3",
-// SC 2011) keyed by (seed, step), a uniform made exactly from 23 of its bits,
-// and Gumbel noise from a logarithm written as a fixed sequence of IEEE fp32
-// operations, so that the noise is a pure function of (seed, step, counter).
+// SC 2011) keyed by the seed, a uniform made exactly from 23 of its bits, and
+// Gumbel noise from a logarithm written as a fixed sequence of IEEE fp32
+// operations, so that the noise is a pure function of (seed, step, stream,
+// row, token). Token v of row r in stream s is word v mod 4 of the block of
+// counter (v div 4, r, step mod 2^32, (step div 2^32) mod 2^30 + 2^30 s), key
+// (seed mod 2^32, seed div 2^32). The 32-bit variant gives each 32 x 32-bit
+// product (one v_mad_u64_u32) 32 output bits, twice the 64-bit variant's.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -10,34 +14,36 @@
 
 namespace ldr {
 
-constexpr int kGroup = 8;  // tokens per Philox block (4 words of 64 bits)
+constexpr int kGroup = 8;  // tokens per noise group: two Philox blocks of 4 words
 
-constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
-constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
+constexpr uint32_t kM0 = 0xD2511F53u, kM1 = 0xCD9E8D57u;   // multipliers
+constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;   // Weyl key increments
 
-// 128-bit product M x, M a constant: four 32 x 32 + 64 multiply-adds
-// (v_mad_u64_u32), the middle column carried through p1 and p2.
-template <uint64_t M>
-__device__ inline void mulhilo(uint64_t x, uint64_t& hi, uint64_t& lo) {
-  constexpr uint32_t Ml = (uint32_t)M, Mh = (uint32_t)(M >> 32);
-  const uint32_t xl = (uint32_t)x, xh = (uint32_t)(x >> 32);
-  const uint64_t p0 = (uint64_t)Ml * xl;
-  const uint64_t p1 = (uint64_t)Mh * xl + (p0 >> 32);
-  const uint64_t p2 = (uint64_t)Ml * xh + (uint32_t)p1;
-  lo = (p2 << 32) | (uint32_t)p0;
-  hi = (uint64_t)Mh * xh + (p1 >> 32) + (p2 >> 32);
-}
-
-__device__ inline void philox4x64_10(uint64_t c[4], uint64_t k0, uint64_t k1) {
+__device__ inline void philox4x32_10(uint32_t c[4], uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
     if (r) { k0 += kW0; k1 += kW1; }
-    uint64_t hi0, lo0, hi1, lo1;
-    mulhilo<kM0>(c[0], hi0, lo0);
-    mulhilo<kM1>(c[2], hi1, lo1);
-    const uint64_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
-    c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+    const uint64_t p0 = (uint64_t)kM0 * c[0], p1 = (uint64_t)kM1 * c[2];
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c[1] ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c[3] ^ k1;
+    c[0] = n0; c[1] = (uint32_t)p1; c[2] = n2; c[3] = (uint32_t)p0;
   }
+}
+
+// Key words and the two upper counter words of a (seed, step, stream).
+struct NoiseKey { uint32_t k0, k1, c2, c3; };
+__device__ inline NoiseKey noise_key(uint64_t seed, uint64_t step, uint32_t stream) {
+  return NoiseKey{(uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)step,
+                  ((uint32_t)(step >> 32) & 0x3FFFFFFFu) | (stream << 30)};
+}
+
+// The 4 words of block `blk` (tokens 4 blk .. 4 blk + 3) of `row`.
+__device__ inline void noise_block(const NoiseKey& k, uint32_t row, uint32_t blk,
+                                   uint32_t out[4]) {
+  uint32_t c[4] = {blk, row, k.c2, k.c3};
+  philox4x32_10(c, k.k0, k.k1);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) out[i] = c[i];
 }
 
 // Natural log of a positive normal float: x = 2^e m, m folded into
@@ -78,19 +84,13 @@ __device__ inline float gumbel_from_bits(uint32_t bits) {
   return -fixed_logf(-fixed_logf(uniform_from_bits(bits)));
 }
 
-// The 8 noise words of tokens [8c, 8c+8) of `row` in counter stream `stream`
-// (counter (c, row, stream, 0)).
-__device__ inline void noise_group(uint64_t seed, uint64_t step, uint64_t row, uint64_t stream,
-                                   uint64_t c, uint32_t out[kGroup]) {
-  uint64_t w[4] = {c, row, stream, 0};
-  philox4x64_10(w, seed, step);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    out[2 * i] = (uint32_t)w[i];
-    out[2 * i + 1] = (uint32_t)(w[i] >> 32);
-  }
+// The noise words of tokens [8 g, 8 g + 8) of `row` in stream `stream`.
+__device__ inline void noise_group(uint64_t seed, uint64_t step, uint64_t row, uint32_t stream,
+                                   uint64_t g, uint32_t out[kGroup]) {
+  const NoiseKey k = noise_key(seed, step, stream);
+  noise_block(k, (uint32_t)row, (uint32_t)(2 * g), out);
+  noise_block(k, (uint32_t)row, (uint32_t)(2 * g + 1), out + 4);
 }
-
 
 // Upper bound of the Gumbel noise g = -log(-log u) of 23-bit uniform index k,
 // u = (2k + 1) 2^-24, from integer arithmetic: -log u >= 1 - u = n 2^-24 with

@@ -8,12 +8,13 @@
 // kernel combines the chunks of a row in vocabulary order (lower token wins
 // ties) and writes the token, lse and log q(y).
 //
-// The noise is a pure function of (seed, step, row, token): Philox4x64-10
-// (Salmon et al., SC 2011; key (seed, step), counter (v/8, row, 0, 0)); one
-// Philox block serves 8 consecutive tokens, 32 bits each. The uniform
-// u = (2 (bits >> 9) + 1) 2^-24 is exact, and g = -log(-log u) uses a log
-// made of IEEE fp32 operations only (no contraction, correctly rounded
-// division), so the keys fl(fl(z/T) + g) are reproducible bit for bit.
+// The noise is a pure function of (seed, step, row, token): Philox4x32-10
+// (Salmon et al., SC 2011; key = the seed, counter (v/4, row, step, stream 0));
+// one Philox block serves 4 consecutive tokens, 32 bits each, and a lane takes
+// 8 tokens (two blocks) at a time. The uniform u = (2 (bits >> 9) + 1) 2^-24
+// is exact, and g = -log(-log u) uses a log made of IEEE fp32 operations only
+// (no contraction, correctly rounded division), so the keys fl(fl(z/T) + g)
+// are reproducible bit for bit.
 #include "ldr_internal.h"
 #include "noise.h"
 
@@ -54,6 +55,7 @@ struct SampleArgs {
   Partial* part;
   const TopK* sel;  // top-k support per row, or null for the full vocabulary
   int row_mul, row_add;  // row r of the launch is logits row (and noise row) r * mul + add
+  int vec;               // rows start on 16 bytes (V % 4 == 0, aligned logits): 16-byte loads
 };
 
 // Exact k-th largest logit of a row by radix selection on order_key (four
@@ -151,8 +153,28 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  for (int vb = v0; vb < v1; vb += kThreads * kGroup) {
-    const int v = vb + (threadIdx.x & ~63) * kGroup + lane * kGroup;
+  // the lane's 8 logits of a sweep: two 16-byte loads inside the chunk
+  auto load8 = [&](int v, float (&zz)[kGroup]) {
+    if (a.vec && v + kGroup <= v1) {
+      const float4 x = *reinterpret_cast<const float4*>(z + v);
+      const float4 y = *reinterpret_cast<const float4*>(z + v + 4);
+      zz[0] = x.x; zz[1] = x.y; zz[2] = x.z; zz[3] = x.w;
+      zz[4] = y.x; zz[5] = y.y; zz[6] = y.z; zz[7] = y.w;
+    } else {
+#pragma unroll
+      for (int i = 0; i < kGroup; ++i) zz[i] = v + i < v1 ? z[v + i] : -INFINITY;
+    }
+  };
+  constexpr int kSweep = kThreads * kGroup;
+  const int lane_off = (int)(threadIdx.x & ~63) * kGroup + lane * kGroup;
+  float znext[kGroup];
+  load8(v0 + lane_off, znext);
+  for (int vb = v0; vb < v1; vb += kSweep) {
+    const int v = vb + lane_off;
+    float zcur[kGroup];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) zcur[i] = znext[i];
+    if (vb + kSweep < v1) load8(v + kSweep, znext);   // the next sweep's logits in flight
     uint32_t bits[kGroup];
     noise_group(a.seed, a.step, (uint64_t)r * a.row_mul + a.row_add, 0, (uint64_t)(v / kGroup),
                 bits);
@@ -161,7 +183,7 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
     bool in[kGroup];
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) {
-      const float zv = v + i < v1 ? z[v + i] : -INFINITY;
+      const float zv = zcur[i];
       in[i] = v + i < v1;
       if constexpr (TOPK) {
         const uint32_t u = order_key(zv);
@@ -356,8 +378,9 @@ __global__ void __launch_bounds__(kThreads) gumbel_fill_kernel(uint64_t seed, ui
 }  // namespace
 
 int sample_splits(int rows, int vocab) {
-  // about 1024 workgroups in flight, each chunk a multiple of one Philox sweep
-  int splits = rows >= 1024 ? 1 : 1024 / rows;
+  // about 2048 workgroups (8 waves per SIMD; 4096 measured no faster), each
+  // chunk a multiple of one sweep
+  int splits = rows >= 2048 ? 1 : 2048 / rows;
   const int sweep = kThreads * kGroup;
   const int max_splits = (vocab + sweep - 1) / sweep;
   if (splits > max_splits) splits = max_splits;
@@ -376,6 +399,7 @@ hipError_t launch_sample(const float* logits, int rows, int vocab, float tempera
   a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
   a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
   a.sel = nullptr; a.row_mul = row_mul; a.row_add = row_add;
+  a.vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0;
   if (temperature > 0.f && top_k > 0 && top_k < vocab) {  // T = 0 is the argmax either way
     TopK* sel = reinterpret_cast<TopK*>(static_cast<uint8_t*>(ws) + sel_off);
     hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, logits, vocab,

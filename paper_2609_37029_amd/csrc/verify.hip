@@ -26,9 +26,9 @@
 // T = 0 verifies greedily: pass 1 takes the first argmax of all B + 1 rows and
 // the merge compares them with the candidates.
 //
-// Noise (Philox4x64-10, key (seed, step)): u_i from counter (i - 1, b, 1, 0),
-// the upper half of word 0; the emitted token's Gumbel noise from counter
-// (v div 8, b, 2, 0), word and half as the drafting sampler picks them.
+// Noise (the sampler's Philox4x32-10 layout): u_i is word 0 of block i - 1 of
+// row b in stream 1; the emitted token's Gumbel noise is token v of row b in
+// stream 2.
 #include "ldr_internal.h"
 #include "noise.h"
 
@@ -162,9 +162,9 @@ __device__ int stop_position(const VerifyArgs& a, int b) {
         const float lp = a.P[((long)b * (a.B + 1) + i) * a.V + y] / a.T - row_lse(a, b, i);
         const float lq = a.z[((long)b * a.B + i) * a.V + y] / a.T - a.qlse[(long)b * a.B + i];
         const float ratio = expf(lp - lq);
-        uint64_t w[4] = {(uint64_t)i, (uint64_t)b, 1, 0};
-        philox4x64_10(w, a.seed, a.step);
-        reject = !(uniform_from_bits((uint32_t)(w[0] >> 32)) < ratio);
+        uint32_t w[4];
+        noise_block(noise_key(a.seed, a.step, 1), (uint32_t)b, (uint32_t)i, w);
+        reject = !(uniform_from_bits(w[0]) < ratio);
       }
     }
     const uint64_t m = __ballot(reject);

@@ -1,8 +1,10 @@
-"""Pins of the sampler oracle (Eq. 8): Philox4x64-10 against numpy's own
-implementation, the fp32 logarithm against numpy's log, Gumbel moments
+"""Pins of the sampler oracle (Eq. 8): Philox4x32-10 against its published
+known-answer vectors, the fp32 logarithm against numpy's log, Gumbel moments
 (closed forms), Gumbel-max frequencies against softmax(z/T) (chi-square),
 greedy against numpy argmax, top-k support against a sort, lse closed forms."""
+import json
 import math
+import os
 
 import numpy as np
 import pytest
@@ -12,22 +14,27 @@ from oracle import sample as Sm
 from oracle.sample import gumbel, sample, verify, verify_gumbel, verify_uniform
 
 
-@pytest.mark.parametrize("ctr,key", [
-    ((0, 0, 0, 0), (0, 0)),
-    ((7, 3, 5, 9), (123, 456)),
-    ((2 ** 64 - 2, 2 ** 64 - 1, 1, 2 ** 63), (2 ** 64 - 1, 2 ** 63 + 5)),
-])
-def test_philox_matches_numpy(ctr, key):
-    # numpy's Philox bit generator increments the counter before each block
-    bg = np.random.Philox(counter=np.array(ctr, dtype=np.uint64),
-                          key=np.array(key, dtype=np.uint64))
-    ref = bg.random_raw(8)
-    as_int = sum(int(v) << (64 * i) for i, v in enumerate(ctr))
-    for blk in range(2):
-        c = (as_int + blk + 1) % 2 ** 256              # 256-bit counter increment
-        words = [np.uint64((c >> (64 * i)) & (2 ** 64 - 1)) for i in range(4)]
-        got = Sm.philox4x64_10(words, (np.uint64(key[0]), np.uint64(key[1])))
-        assert [int(g) for g in got] == [int(r) for r in ref[4 * blk:4 * blk + 4]]
+def test_philox_known_answers():
+    """Philox4x32-10 against the generator's published known-answer vectors."""
+    kat = json.load(open(os.path.join(os.path.dirname(__file__), "golden",
+                                      "philox4x32_10_kat.json")))
+    for vec in kat["vectors"]:
+        ctr = [np.uint64(int(x, 16)) for x in vec["ctr"]]
+        key = [np.uint64(int(x, 16)) for x in vec["key"]]
+        got = [int(w) for w in Sm.philox4x32_10(ctr, key)]
+        assert got == [int(x, 16) for x in vec["out"]]
+
+
+def test_noise_counter_layout():
+    """Token v of row r in stream s is word v mod 4 of the block of counter
+    (v div 4, r, step mod 2^32, (step div 2^32) mod 2^30 + 2^30 s), key the
+    seed's two halves."""
+    seed, step = 0x123456789ABCDEF0, 0x0000000500000007
+    for s_, r, v in ((0, 3, 10), (1, 0, 0), (2, 7, 4095)):
+        w = Sm.philox4x32_10((np.uint64(v // 4), np.uint64(r), np.uint64(7),
+                              np.uint64(5 | (s_ << 30))),
+                             (np.uint64(0x9ABCDEF0), np.uint64(0x12345678)))
+        assert int(Sm.philox_bits(seed, step, r, v, stream=s_)) == int(w[v % 4])
 
 
 def test_logf_within_three_ulp_of_numpy():
@@ -65,7 +72,8 @@ def test_noise_streams_differ_by_seed_step_and_row():
     a = Sm.philox_bits(1, 0, 0, v)
     assert len(set(a.tolist())) == 64
     for other in (Sm.philox_bits(2, 0, 0, v), Sm.philox_bits(1, 1, 0, v),
-                  Sm.philox_bits(1, 0, 1, v)):
+                  Sm.philox_bits(1, 0, 1, v), Sm.philox_bits(1, 0, 0, v, stream=2),
+                  Sm.philox_bits(1, 2 ** 32, 0, v)):
         assert np.mean(a == other) < 0.05
 
 
