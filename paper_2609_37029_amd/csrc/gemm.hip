@@ -463,7 +463,20 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
     p.cfg = -1; bm = 32; bn = 64; kstep = 16;
   } else {
     p.cfg = M <= 16 ? 0 : M <= 32 ? 1 : M <= 64 ? 2 : swiglu ? 4 : 3;
-    if (p.cfg == 3 && allow_split) {
+    if (p.cfg == 4) {
+      // SwiGLU tiles (no split-K): the column width whose rounds over the CUs
+      // times the bytes a tile streams (all its activation rows plus its
+      // weight columns) is least, among 96 (cfg 4), 128 (cfg 3) and 64 (cfg 5)
+      const int mt = (M + 255) / 256;
+      double best = 0.0;
+      const int cands[3][2] = {{4, 96}, {3, 128}, {5, 64}};
+      for (const auto& c : cands) {
+        const long tiles = (long)mt * ((N + c[1] - 1) / c[1]);
+        const double cost = (double)((tiles + kCUs - 1) / kCUs) * (256.0 + c[1]) * K;
+        if (best == 0.0 || cost < best) { best = cost; p.cfg = c[0]; }
+      }
+    }
+    if (p.cfg == 3 && allow_split && !swiglu) {
       const int t128 = ((N + 127) / 128) * ((M + 255) / 256);
       if (t128 * 8 <= kCUs && t128 * 16 > kCUs && K / 8 <= 512 && K % (4 * 2 * 2 * BK) == 0)
         p.cfg = 5;

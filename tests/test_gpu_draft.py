@@ -37,11 +37,17 @@ def oracle_logits(p, w, anchor, seqs=None, vocab_idx=None, lazy=False):
     return {b: OD.forward(p.s, Wt, p.ost[b], p.G64, int(a[b]), vocab_idx=vocab_idx) for b in seqs}
 
 
+# the Qwen3-32B MLP width: 51200 SwiGLU columns take 128-wide tiles (two rounds
+# over the CUs instead of three of 96)
+MINI_BF16_MLP32B = MINI_BF16.replace(name="mini-bf16-mlp25600", mlp=25600)
+
+
 @pytest.mark.parametrize("shape,batch,prefix", [
     (synth.TINY, 1, 2048),     # the fp32 parity configuration
     (synth.TINY, 3, 40),       # partial window (t < W)
     (MINI_BF16, 3, 300),       # bf16, GQA, ragged vocab, 48 rows
     (MINI_BF16, 17, 150),      # bf16, 272 rows: two M tiles, the last ragged
+    (MINI_BF16_MLP32B, 16, 100),
 ])
 def test_logits_match_oracle(gpu_lib, shape, batch, prefix):
     p, w, dw, anchor = setup(gpu_lib, shape, batch, prefix)
