@@ -320,7 +320,7 @@ def cpu_baseline(torch, synth, rig, n_seqs):
     s = rig.s
     Wt = synth.weights_f64(rig.w)
     G64 = synth.to_f64(rig.G)
-    anchor = rig.anchor.cpu().numpy()
+    anchor = synth.make_anchors(s, rig.batch).numpy()   # seeded input, never a GPU result
     K, V, h = synth.make_rows(s, n_seqs, 512, 77) + (synth.make_h(s, n_seqs, 77),)
     Kd, Vd, hd = synth.decode_rows(s, n_seqs, s.block + 1, 0)
     states = []
