@@ -62,6 +62,9 @@ def parse():
     ap.add_argument("--sweep-batch", default="1,16,64")
     ap.add_argument("--counters", action="store_true",
                     help="calibration copy + a few steps, to run under rocprofv3 --pmc")
+    ap.add_argument("--mfma", metavar="PMC_CSV",
+                    help="write profiles/mfma.json from a --pmc pass of SQ_VALU_MFMA_BUSY_CYCLES, "
+                         "SQ_INSTS_VALU_MFMA_MOPS_BF16 and GRBM_GUI_ACTIVE over --counters")
     ap.add_argument("--traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two counter_collection.csv files into profiles/traffic.json")
     return ap.parse_args()
@@ -445,6 +448,60 @@ def traffic_from_csv(fetch_csv, write_csv, workload):
     return out
 
 
+def mfma_from_csv(path, workload):
+    """Per-launch MFMA figures of the GEMM launch kinds from one rocprofv3 --pmc
+    pass over `bench.py --counters` with SQ_VALU_MFMA_BUSY_CYCLES,
+    SQ_INSTS_VALU_MFMA_MOPS_BF16 and GRBM_GUI_ACTIVE: the MFMA busy fraction
+    (busy cycles summed over the SIMDs / (GPU active cycles x SIMDs)), the bf16
+    flops the instructions did (MOPS x 512) and the dispatch duration. The CSV
+    holds one GRBM_GUI_ACTIVE value per dispatch summed over the 8 XCDs' GRBM
+    blocks, so the GPU's active cycles are that value / 8; `gui_vs_clock`
+    compares them with the dispatch duration at 2.4 GHz."""
+    import csv
+    sys.path.insert(0, ROOT)
+    import synth
+    from paper_2609_37029_amd import ldr
+    kinds = ldr.draft_launches(synth.WORKLOADS[workload].shape)
+    disp = {}
+    for r in csv.DictReader(open(path)):
+        d = disp.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "busy": 0.0,
+                                                    "mops": 0.0, "gui": 0.0,
+                                                    "ns": int(r["End_Timestamp"]) -
+                                                          int(r["Start_Timestamp"])})
+        v = float(r["Counter_Value"])
+        if r["Counter_Name"] == "SQ_VALU_MFMA_BUSY_CYCLES":
+            d["busy"] += v
+        elif r["Counter_Name"] == "SQ_INSTS_VALU_MFMA_MOPS_BF16":
+            d["mops"] += v
+        elif r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+            d["gui"] = max(d["gui"], v)
+    rows = [disp[k] for k in sorted(disp)]
+    simds, xcds, ghz = 256 * 4, 8, 2.4
+    per = {}
+    for i, r in enumerate(rows):
+        if "views_commit_kernel" not in r["name"] or i + len(kinds) >= len(rows):
+            continue
+        seq = rows[i + 1:i + 1 + len(kinds)]
+        if "gemm" not in seq[0]["name"]:
+            continue              # an update of the prefill, not of a step
+        for k, d in zip(kinds, seq):
+            if k.endswith("gemm") or k == "lm_head":
+                per.setdefault(k, []).append(d)
+    out = {"workload": workload, "sources_sha256": source_digest(), "simds": simds, "kinds": {}}
+    for k, ds in per.items():
+        busy = statistics.mean(d["busy"] / (d["gui"] / xcds * simds) for d in ds if d["gui"] > 0)
+        flops = statistics.mean(d["mops"] * 512 for d in ds)
+        ns = statistics.mean(d["ns"] for d in ds)
+        gui = statistics.mean(d["gui"] / xcds for d in ds)
+        out["kinds"][k] = {"symbol": kernel_symbol(ds[0]["name"]), "launches": len(ds),
+                           "mfma_busy_frac": busy, "bf16_flops_per_launch": flops,
+                           "us_per_launch_under_counters": ns / 1e3,
+                           "tflops_under_counters": flops / ns / 1e3,
+                           "frac_of_bf16_peak": flops / ns / 1e3 / BF16_PEAK_TFLOPS,
+                           "gui_vs_clock": gui / (ns * ghz)}
+    return out
+
+
 def traffic_for(kind):
     """HBM bytes per launch of `kind` from profiles/traffic.json, or None when
     absent or taken on other library sources."""
@@ -463,6 +520,12 @@ def traffic_for(kind):
 
 def main():
     args = parse()
+    if args.mfma:
+        m = mfma_from_csv(args.mfma, args.workload)
+        with open(os.path.join(ROOT, "profiles", "mfma.json"), "w") as f:
+            json.dump(m, f, indent=1)
+        print(json.dumps({k: round(v["mfma_busy_frac"], 3) for k, v in m["kinds"].items()}))
+        return
     if args.traffic:
         t = traffic_from_csv(args.traffic[0], args.traffic[1], args.workload)
         os.makedirs(os.path.dirname(TRAFFIC_JSON), exist_ok=True)
