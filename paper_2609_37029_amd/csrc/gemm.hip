@@ -33,7 +33,13 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BK = 64;        // K step: one LDS stage, two MFMA k-steps
-constexpr int LDK = BK + 8;   // padded LDS row (elements): 144 B
+constexpr int LDK = BK;       // LDS row (elements): 128 B, 16-byte chunks swizzled
+// Physical 16-byte chunk of logical chunk c (0..7) in LDS row r: rows r and
+// r + 1 sit in opposite halves of the 64 banks, and the 8 row pairs of any 16
+// consecutive rows get distinct chunk slots, so both a 16-lane pass of stores
+// (two rows of 8 chunks) and of fragment reads (16 rows, one chunk) hit 64
+// distinct banks.
+__device__ inline int lds_chunk(int r, int c) { return c ^ ((r >> 1) & 7); }
 constexpr int WPF = 4;        // weight steps in flight
 
 // Interleaved N index of the SwiGLU GEMM -> row of w_gate_up.
@@ -70,7 +76,7 @@ __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int 
   for (int i = 0; i < AL; ++i) {
     const int c = (tid + i * NTHR) % ACH, row = c >> 3, col = (c & 7) * 8;
     asrc[i] = A + (long)min(m0 + row, a.M - 1) * a.lda + kbeg + col;
-    adst[i] = row * LDK + col;
+    adst[i] = row * LDK + lds_chunk(row, c & 7) * 8;
   }
 #pragma unroll
   for (int i = 0; i < WL; ++i) {
@@ -78,8 +84,16 @@ __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int 
     const int gn = min(n0 + row, a.N - 1);
     const int wrow = SWI ? swiglu_row(gn, a.mlp) : gn;
     wsrc[i] = W + (long)wrow * a.ldw + kbeg + col;
-    wdst[i] = row * LDK + col;
+    wdst[i] = row * LDK + lds_chunk(row, c & 7) * 8;
   }
+
+  // LDS row offsets of this lane's fragment rows (rows are multiples of 16
+  // plus lane & 15, so the swizzle depends on lane & 15 alone)
+  int ard[MTW], wrd[NTW];
+#pragma unroll
+  for (int i = 0; i < MTW; ++i) ard[i] = (wm * TM + i * 16 + (lane & 15)) * LDK;
+#pragma unroll
+  for (int j = 0; j < NTW; ++j) wrd[j] = (wn * TN + j * 16 + (lane & 15)) * LDK;
 
   // wq[p]: weights of step kt + 1 + p; a0 / a1: activation stages kt + 1 and
   // kt + 2 (roles swap every step). Constant indices only: registers.
@@ -102,10 +116,10 @@ __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int 
       bf16x8 bfr[NTW];                                                                \
       _Pragma("unroll") for (int j = 0; j < NTW; ++j) bfr[j] =                        \
           __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(                 \
-              &Ws[buf][(wn * TN + j * 16 + (lane & 15)) * LDK + kk * 32 + (lane >> 4) * 8])); \
+              &Ws[buf][wrd[j] + lds_chunk(lane & 15, kk * 4 + (lane >> 4)) * 8]));       \
       _Pragma("unroll") for (int i = 0; i < MTW; ++i) {                               \
         const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>( \
-            &As[buf][(wm * TM + i * 16 + (lane & 15)) * LDK + kk * 32 + (lane >> 4) * 8])); \
+            &As[buf][ard[i] + lds_chunk(lane & 15, kk * 4 + (lane >> 4)) * 8]));         \
         _Pragma("unroll") for (int j = 0; j < NTW; ++j) acc[i][j] =                   \
             __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bfr[j], acc[i][j], 0, 0, 0);  \
       }                                                                               \
