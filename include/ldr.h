@@ -171,10 +171,13 @@ int ldr_config_check(const ldr_config* cfg);
  * prefix once, at prefill: Sec. 2.2, Fig. "global-summary").
  *   arena      dev [batch][stride] bytes, 256-byte aligned (kept in the handle)
  *   pos        dev int64 [batch]: rows ingested per sequence, t (kept)
- *   G          dev [D][Hq][R][d] dtype: the fixed summary queries (kept)
+ *   G          dev [D][Hq][R][d] dtype: the fixed summary queries (kept); may be
+ *              NULL when the configuration has no learned summary
+ *              (LDR_DROP_SUMMARY, or pool_slots > 0)
  *   n_prefix   dev int32 [batch] rows per sequence in the chunk, or NULL
  *   K_prefix, V_prefix  dev [batch][max_prefix][D][Hkv][d] dtype
- *   h_boundary dev [batch][L_b][hidden] dtype: boundary states after it
+ *   h_boundary dev [batch][L_b][hidden] dtype: boundary states after it (may be
+ *              NULL with LDR_DROP_BOUNDARY)
  * The handle also owns a 256-byte device status word, freed by
  * ldr_views_destroy. */
 int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* arena,
@@ -191,15 +194,20 @@ int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* 
  *    summary query r): s = G[j,h,r] . k / sqrt(d) over the head's K/V group,
  *    eta_N and m_N by log-sum-exp with max subtraction, merged into (eta, m)
  *    by Eq. 11;
+ *  - with the mean-pooled summary (pool_slots = P > 0) instead of the
+ *    previous point: for each bank of stride S, the slot c mod P of every
+ *    chunk c the rows reach takes the mean of chunk c's rows so far (fp32
+ *    sums, the open chunk continuing from its stored sums), K and V;
  *  - the boundary states become h_new[b];
  *  - t_b += n.
+ * A view the configuration drops (drop_views) is left out of this list.
  * n = 0 leaves that sequence's views and t bit-identical (App. A.2). A count
  * outside [0, max_new] leaves the sequence unchanged and sets the sticky
  * LDR_ERANGE flag.
  *   n_new       dev int32 [batch]
  *   K_new, V_new dev [batch][max_new][D][Hkv][d] dtype (row r of sequence b at
  *               [b][r]; rows r >= n_new[b] are ignored)
- *   h_new       dev [batch][L_b][hidden] dtype */
+ *   h_new       dev [batch][L_b][hidden] dtype (may be NULL with LDR_DROP_BOUNDARY) */
 int ldr_views_update(ldr_views* v, const int32_t* n_new, int32_t max_new, const void* K_new,
                      const void* V_new, const void* h_new, void* stream);
 
