@@ -67,3 +67,31 @@ def test_pooled_slots_track_single_row_updates(gpu_lib):
         K, V, h = synth.decode_rows(s, 2, 1, 100 + step, device="cuda")
         p.ingest([int(x) for x in rng.integers(0, 2, 2)], K, V, h)
     check_views(p)
+
+
+@pytest.mark.slow
+def test_pooled_full_size_qwen3_8b(gpu_lib):
+    """Qwen3-8B shape with the mean-pooled summary (W 256 + 2 x 256 slots), batch
+    16, 8192-row prefix plus a decode update: views of two sequences and their
+    logits on a 2048-token vocabulary sample against the oracle."""
+    from gpu_common import lazy_weights_f64, row_errors
+    s = synth.QWEN3_8B_POOLED
+    p = Pair(gpu_lib, s, 16, None, oracle_seqs=[0, 9])
+    p.prefill(8192, 4096)
+    K, V, h = synth.decode_rows(s, 16, 17, 0, device="cuda")
+    p.ingest([17] * 16, K, V, h)
+    check_views(p)
+    w = synth.make_weights(s, device="cuda")
+    dw = gpu_lib.DraftWeights(w, tiled_head=True)
+    anchor = synth.make_anchors(s, 16, device="cuda")
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    torch.cuda.synchronize()
+    idx = np.sort(np.random.default_rng(4).choice(s.vocab, 2048, replace=False))
+    Wt = lazy_weights_f64(w)
+    a = anchor.cpu().numpy()
+    zc = z[:, :, torch.from_numpy(idx).cuda()].cpu().numpy()
+    for b in p.seqs:
+        ref = OD.forward(s, Wt, p.ost[b], None, int(a[b]), vocab_idx=idx)
+        err, cos = row_errors(zc[b], ref)
+        assert err.max() <= 2e-2, err.max()
+        assert cos.min() >= 0.999, cos.min()
