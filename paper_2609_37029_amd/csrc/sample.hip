@@ -229,7 +229,9 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
 // logits are a fixed sequence of IEEE operations that the sampler then reads
 // like any other logits.
 constexpr int kMkRows = 16, kMkThreads = 256, kMkV = 64, kMkPer = kMkRows / (kMkThreads / kMkV);
-template <typename T>
+// 16 bytes as a native vector (arrays of HIP's struct uint4 end up in scratch)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+template <typename T, int RMAX>   // RMAX: the largest rank the registers hold (64 or 256)
 __global__ void __launch_bounds__(kMkThreads) markov_correct_kernel(
     float* logits, int batch, int B, int vocab, int i, const int32_t* anchor,
     const int32_t* tokens, const T* E, const T* W, int rank) {
@@ -241,30 +243,61 @@ __global__ void __launch_bounds__(kMkThreads) markov_correct_kernel(
   const int v0 = blockIdx.x * kMkV;
   const int lv = threadIdx.x & (kMkV - 1), v = v0 + lv;
   const int grp = threadIdx.x / kMkV;   // rows grp * kMkPer .. + kMkPer of each 16
-  {  // W_c rows v0 .. v0 + kMkV - 1 (rows past V repeat the last one)
-    const int per_row = rank / EPV;
-    for (int c = threadIdx.x; c < kMkV * per_row; c += kMkThreads) {
+  // Every global load is issued before the first barrier: the W_c rows of the
+  // tile, then per chunk of 16 sequences the logits this thread updates and
+  // the rank vectors E_c(y) (a token load, then its row); one barrier after
+  // they reach LDS. (W_c rows past V repeat the last one.)
+  constexpr int kWMax = kMkV * RMAX / EPV / kMkThreads;   // 16-byte pieces per thread
+  constexpr int kEMax = kMkRows * RMAX / kMkThreads;      // rank-vector entries per thread
+  const int per_row = rank / EPV, wpieces = kMkV * per_row;
+  u32x4 wreg[kWMax];
+#pragma unroll
+  for (int q = 0; q < kWMax; ++q) {
+    const int c = threadIdx.x + q * kMkThreads;
+    if (c < wpieces) {
       const int r = c / per_row, k = (c - r * per_row) * EPV;
-      const long row = min(v0 + r, vocab - 1);
-      *reinterpret_cast<uint4*>(w_lds + r * wld + k) =
-          *reinterpret_cast<const uint4*>(W + row * rank + k);
+      wreg[q] = *reinterpret_cast<const u32x4*>(W + (long)min(v0 + r, vocab - 1) * rank + k);
     }
   }
   const T* wr = w_lds + lv * wld;
   const float* e0 = e_lds + grp * kMkPer * rank;
   for (int b0 = 0; b0 < batch; b0 += kMkRows) {
     const int nb = min(kMkRows, batch - b0);
-    __syncthreads();   // the W tile is in; the previous chunk's reads are done
-    for (int idx = threadIdx.x; idx < kMkRows * rank; idx += kMkThreads) {
+    float zold[kMkPer];
+#pragma unroll
+    for (int r = 0; r < kMkPer; ++r) {
+      const int bb = grp * kMkPer + r;
+      zold[r] = v < vocab && bb < nb ? logits[((long)(b0 + bb) * B + i) * vocab + v] : 0.f;
+    }
+    float ereg[kEMax];
+#pragma unroll
+    for (int q = 0; q < kEMax; ++q) {
+      const int idx = threadIdx.x + q * kMkThreads;
       const int bb = idx / rank, k = idx - bb * rank;
       float e = 0.f;
-      if (bb < nb) {
+      if (idx < kMkRows * rank && bb < nb) {
         const int b = b0 + bb;
         int y = i == 0 ? anchor[b] : tokens[(long)b * B + i - 1];
         if (y < 0 || y >= vocab) y = 0;
         e = Elem<T>::load(E + (long)y * rank + k);
       }
-      e_lds[idx] = e;
+      ereg[q] = e;
+    }
+    if (b0 > 0) __syncthreads();   // the previous chunk's LDS reads are done
+    if (b0 == 0) {
+#pragma unroll
+      for (int q = 0; q < kWMax; ++q) {
+        const int c = threadIdx.x + q * kMkThreads;
+        if (c < wpieces) {
+          const int r = c / per_row, k = (c - r * per_row) * EPV;
+          *reinterpret_cast<u32x4*>(w_lds + r * wld + k) = wreg[q];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kEMax; ++q) {
+      const int idx = threadIdx.x + q * kMkThreads;
+      if (idx < kMkRows * rank) e_lds[idx] = ereg[q];
     }
     __syncthreads();
     float c[kMkPer];
@@ -293,10 +326,7 @@ __global__ void __launch_bounds__(kMkThreads) markov_correct_kernel(
 #pragma unroll
       for (int r = 0; r < kMkPer; ++r) {
         const int bb = grp * kMkPer + r;
-        if (bb < nb) {
-          float* zp = logits + ((long)(b0 + bb) * B + i) * vocab + v;
-          *zp = *zp + c[r];
-        }
+        if (bb < nb) logits[((long)(b0 + bb) * B + i) * vocab + v] = zold[r] + c[r];
       }
     }
   }
@@ -439,14 +469,16 @@ hipError_t launch_sample_markov(float* logits, int batch, int B, int vocab, cons
                      (size_t)kMkV * (rank + 16 / esz) * esz;
   const dim3 grid((unsigned)((vocab + kMkV - 1) / kMkV));
   for (int i = 0; i < B; ++i) {
-    if (dtype == LDR_BF16)
-      hipLaunchKernelGGL((markov_correct_kernel<uint16_t>), grid, dim3(kMkThreads), lds, st,
-                         logits, batch, B, vocab, i, anchor, tokens,
-                         static_cast<const uint16_t*>(E), static_cast<const uint16_t*>(W), rank);
-    else
-      hipLaunchKernelGGL((markov_correct_kernel<float>), grid, dim3(kMkThreads), lds, st, logits,
-                         batch, B, vocab, i, anchor, tokens, static_cast<const float*>(E),
-                         static_cast<const float*>(W), rank);
+#define LDR_MK(T, RM)                                                                        \
+  hipLaunchKernelGGL((markov_correct_kernel<T, RM>), grid, dim3(kMkThreads), lds, st, logits, \
+                     batch, B, vocab, i, anchor, tokens, static_cast<const T*>(E),            \
+                     static_cast<const T*>(W), rank)
+    if (dtype == LDR_BF16) {
+      if (rank <= 64) LDR_MK(uint16_t, 64); else LDR_MK(uint16_t, 256);
+    } else {
+      if (rank <= 64) LDR_MK(float, 64); else LDR_MK(float, 256);
+    }
+#undef LDR_MK
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = launch_sample(logits, batch, vocab, temperature, top_k, seed, step, tokens, lse, logq, ws,
