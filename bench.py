@@ -57,7 +57,7 @@ def parse():
     ap.add_argument("--cpu-seqs", type=int, default=16,
                     help="sequences in the CPU-oracle sample")
     ap.add_argument("--sweep", action="store_true")
-    ap.add_argument("--sweep-out", default=os.path.join(ROOT, "gpurun_out", "sweep.json"))
+    ap.add_argument("--sweep-out", default=os.path.join(ROOT, "sweep.json"))
     ap.add_argument("--sweep-prefix", default="1024,4096,16384,65536,131072,262144")
     ap.add_argument("--sweep-batch", default="1,16,64")
     ap.add_argument("--counters", action="store_true",
@@ -634,7 +634,7 @@ def sweep(args, torch, ldr, synth):
     for batch in sorted({r["batch"] for r in res}):
         xs = [r["us_p50"] for r in res if r["batch"] == batch]
         flat[str(batch)] = (max(xs) - min(xs)) / min(xs)
-    os.makedirs(os.path.dirname(args.sweep_out), exist_ok=True)
+    os.makedirs(os.path.dirname(os.path.abspath(args.sweep_out)), exist_ok=True)
     with open(args.sweep_out, "w") as f:
         json.dump({"shape": s.name, "points": res, "variation": flat}, f, indent=1)
     print(json.dumps({"metric": "draft-step latency vs prefix length", "shape": s.name,

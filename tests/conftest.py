@@ -16,7 +16,7 @@ def pytest_configure(config):
 @pytest.fixture(scope="session")
 def gpu_lib():
     """The HIP library's Python binding; the test fails (does not skip) when
-    the library is missing on a GPU machine."""
+    the library is missing on a machine with a GPU."""
     import torch
     if not torch.cuda.is_available():
         pytest.fail("gpu test collected on a machine without a GPU")
