@@ -49,6 +49,13 @@ def parse():
     ap.add_argument("--markov-rank", type=int, default=0,
                     help="sample with the Markov correction (Eq. 7) of this rank instead of the "
                          "per-position sampler (0: off)")
+    ap.add_argument("--temperature", type=float, default=1.0,
+                    help="sampling temperature of the drafted positions (0: greedy argmax)")
+    ap.add_argument("--fused-head", action="store_true",
+                    help="draft and sample through ldr_draft_step_sample (greedy steps take the "
+                         "argmax in the vocabulary head's epilogue)")
+    ap.add_argument("--no-logits", action="store_true",
+                    help="with --fused-head: do not write the fp32 logits")
     ap.add_argument("--drop-views", type=int, default=0,
                     help="ablation variant: 1 no window, 2 no summary, 4 no boundary")
     ap.add_argument("--verify", action="store_true",
@@ -125,8 +132,10 @@ class Rig:
     """Device-resident inputs and outputs of one workload."""
 
     def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False,
-                 tiled_head=True, markov_rank=0, verify=False):
+                 tiled_head=True, markov_rank=0, verify=False, fused_head=False,
+                 keep_logits=True, temperature=1.0):
         self.torch, self.ldr, self.s, self.batch = torch, ldr, shape, batch
+        self.temperature = temperature
         dev = "cuda"
         self.w = synth.make_weights(shape, device=dev)
         # the vocabulary head in the library's tiled layout (a one-time copy of a frozen weight)
@@ -162,6 +171,12 @@ class Rig:
                     torch.empty(rows, dtype=torch.float32, device=dev),
                     torch.empty(rows, dtype=torch.float32, device=dev))
         self.kinds = ldr.draft_launches(shape)
+        # per-position sampling fused into the vocabulary head (ldr_draft_step_sample)
+        self.fused_head = fused_head and self.tiled_head and batch * shape.block > 64
+        self.keep_logits = keep_logits
+        if self.fused_head:
+            self.fws = torch.empty(ldr.draft_step_sample_workspace_bytes(shape, batch),
+                                   dtype=torch.uint8, device=dev)
         # Markov correction (Eq. 7): seeded random correction embedding and output
         # mapping [V][rank] in the model dtype (no trained weights exist)
         self.markov_rank = markov_rank
@@ -191,9 +206,19 @@ class Rig:
         if self.views.status() != ldr.LDR_OK:
             raise RuntimeError("views status error after prefill")
 
-    def step(self, i, events=None, temperature=1.0):
+    def step(self, i, events=None):
+        temperature = self.temperature
         K, V, h = self.rows[i % len(self.rows)]
         self.views.update(self.n, K, V, h)
+        if self.fused_head and events is None and not self.markov_rank:
+            b, B = self.batch, self.s.block
+            self.ldr.draft_step_sample(self.views, self.dw, self.anchor, temperature, 5, i,
+                                       logits=self.logits if self.keep_logits else None,
+                                       out=tuple(t.view(b, B) for t in self.out),
+                                       workspace=self.fws)
+            if self.verify:
+                self.verify_round(i, temperature)
+            return
         if events is None:
             self.ldr.draft_step(self.views, self.dw, self.anchor, self.logits, self.ws)
         else:
@@ -210,12 +235,15 @@ class Rig:
         if self.verify:
             self.verify_round(i, temperature)
 
-    def verify_round(self, i, temperature=1.0):
+    def verify_round(self, i, temperature=None):
         """ldr_verify of the step's draft; writes n (the next update's row
         counts) and the next anchors in place."""
+        temperature = self.temperature if temperature is None else temperature
         b, B = self.batch, self.s.block
-        self.ldr.verify(self.P, self.logits, self.out[1].view(b, B), self.out[0].view(b, B),
-                        temperature, 9, i, out=self.vout, workspace=self.vws)
+        self.ldr.verify(self.P, self.logits if temperature > 0 else None,
+                        self.out[1].view(b, B) if temperature > 0 else None,
+                        self.out[0].view(b, B), temperature, 9, i, out=self.vout,
+                        workspace=self.vws)
 
 
 def verify_timing(torch, rig, ev, calls=20):
@@ -335,8 +363,8 @@ def cpu_baseline(torch, synth, rig, n_seqs):
         st = OV.update(s, states[b], G64, synth.to_f64(Kd[b]), synth.to_f64(Vd[b]),
                        synth.to_f64(hd[b]))
         z = OD.forward(s, Wt, st, G64, int(anchor[b]))
-        OS.sample(z.astype(np.float32), 1.0, 0, 5, 0, rows=np.arange(b * s.block,
-                                                                      (b + 1) * s.block))
+        OS.sample(z.astype(np.float32), rig.temperature, 0, 5, 0,
+                  rows=np.arange(b * s.block, (b + 1) * s.block))
     el = time.perf_counter() - t0
     del Wt
     return {"value": n_seqs * s.block / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
@@ -557,14 +585,26 @@ def main():
     if args.drop_views:
         s = s.replace(drop_views=args.drop_views)
     rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head,
-              markov_rank=args.markov_rank, verify=args.verify)
+              markov_rank=args.markov_rank, verify=args.verify, fused_head=args.fused_head,
+              keep_logits=not args.no_logits, temperature=args.temperature)
     ev = ldr.HipEvents()
     costs = launch_costs(s, batch)
     # which launch kind dominates the step (events around every launch, outside the timed run)
     br = kind_breakdown(torch, ldr, rig, ev)
     gemm_kinds = [k for k in br if k.endswith("gemm") or k == "lm_head"]
     dom = max(br, key=lambda k: br[k])
-    wall, per_step, kern = time_steps(torch, rig, args.steps, args.warmup, ev=ev, bracket={dom})
+    if rig.fused_head:
+        # ldr_draft_step_sample records no per-launch events: the timed run has
+        # events at step boundaries only, and the dominant kernel (a draft-layer
+        # launch, the same kernel on both paths) is timed over as many steps of
+        # the bracketed separate path right after it
+        wall, per_step, _ = time_steps(torch, rig, args.steps, args.warmup, ev=ev)
+        rig.fused_head = False
+        _, _, kern = time_steps(torch, rig, args.steps, 0, ev=ev, bracket={dom})
+        rig.fused_head = True
+    else:
+        wall, per_step, kern = time_steps(torch, rig, args.steps, args.warmup, ev=ev,
+                                          bracket={dom})
     torch.cuda.synchronize()
     ms = wall / args.steps * 1e3
     tokens = batch * s.block * args.steps
@@ -572,8 +612,9 @@ def main():
     dom_ms = statistics.mean(t for t, _ in kern) / launches_of_dom
     dom_bytes = costs[dom][0]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    # the separate sampler reads the fp32 logits once; the fused head reads none
     step_bytes = sum(costs[k][0] for k in rig.kinds) + update_bytes(s, batch, s.block + 1) + \
-        batch * s.block * s.vocab * 4
+        (0 if rig.fused_head else batch * s.block * s.vocab * 4)
     step_flops = sum(costs[k][1] for k in rig.kinds)
     gemm_ms = sum(br[k] for k in gemm_kinds)
     gemm_flops = sum(costs[k][1] * sum(1 for x in rig.kinds if x == k) for k in gemm_kinds)
@@ -584,10 +625,14 @@ def main():
         "data": "synthetic (seeded random-init weights, N(0,1) target K/V rows and hidden "
                 "states; prefix rows ingested through ldr_views_update before timing)",
         "config": {"workload": wl.name, "shape": s.name, "batch": batch, "block": s.block,
-                   "prefix": wl.prefix, "rows_per_update": s.block + 1, "temperature": 1.0,
+                   "prefix": wl.prefix, "rows_per_update": s.block + 1,
+                   "temperature": rig.temperature,
                    "window": s.window, "summary": s.summary, "draft_layers": s.n_layers,
                    "lm_head_layout": "tiled" if rig.tiled_head else "row-major",
-                   "sampler": f"markov rank {rig.markov_rank}" if rig.markov_rank else "per-position",
+                   "sampler": (f"markov rank {rig.markov_rank}" if rig.markov_rank else
+                               ("fused into the vocabulary head" +
+                                ("" if rig.keep_logits else ", logits not written"))
+                               if rig.fused_head else "per-position"),
                    "views": {0: "window + summary + boundary", 1: "no window", 2: "no summary",
                              4: "no boundary"}.get(s.drop_views, f"drop {s.drop_views}")},
         "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,

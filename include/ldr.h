@@ -267,6 +267,30 @@ int ldr_draft_step_events(const ldr_views* v, const ldr_weights* w, const int32_
                           float* logits, void* workspace, size_t workspace_bytes,
                           void* const* events, int32_t n_events, void* stream);
 
+/* Workspace bytes ldr_draft_step_sample needs for `batch` sequences. */
+size_t ldr_draft_step_sample_workspace_bytes(const ldr_config* cfg, int32_t batch);
+
+/* ldr_draft_step followed by per-position sampling of every row (Eq. 4 and
+ * Eq. 8): tokens, lse and logq are those of ldr_sample(logits, batch * B, V,
+ * temperature, top_k = 0, seed, step) on the step's logits. Greedy steps
+ * (temperature 0) whose head reads its tiled copy (w->lm_head_tiled set and
+ * batch * B > 64) take the argmax in the head's epilogue, from the fp32 logits
+ * it has just computed, so the logits need not be written (logits = NULL):
+ * tokens bit for bit the same. Other steps run the head and then ldr_sample's
+ * kernels, and need the logits. (A sampling epilogue for T > 0 was measured
+ * and dropped: with one workgroup per CU the head hides the per-token noise
+ * arithmetic far worse than the separate sampler does.)
+ *   logits  dev fp32 [batch][B][V], or NULL on the fused greedy path
+ *   tokens  dev int32 [batch][B]; lse, logq dev fp32 [batch][B]
+ *   workspace dev, ldr_draft_step_sample_workspace_bytes(cfg, batch) bytes,
+ *           256-byte aligned.
+ * LDR_EINVAL on a bad argument (as ldr_draft_step and ldr_sample), or NULL
+ * logits off the fused greedy path. */
+int ldr_draft_step_sample(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                          float* logits, float temperature, uint64_t seed, uint64_t step,
+                          int32_t* tokens, float* lse, float* logq, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
 /* Workspace bytes ldr_sample needs for `rows` rows of `vocab` logits. */
 size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
 

@@ -323,12 +323,21 @@ extern "C" int32_t ldr_draft_step_launches(const ldr_config* cfg, int32_t* kinds
   return n;
 }
 
+// Greedy sampling fused into the vocabulary head (tiled head only): outputs
+// and the partials' workspace; logits may then be NULL (not written).
+struct FusedSample {
+  int32_t* tokens; float* lse; float* logq;
+  void* parts;
+};
+
 static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
                            float* logits, void* workspace, size_t workspace_bytes,
-                           void* const* events, int32_t n_events, hipStream_t st) {
-  if (!v || !anchor || !logits || !workspace) return LDR_EINVAL;
+                           void* const* events, int32_t n_events, hipStream_t st,
+                           const FusedSample* fs = nullptr) {
+  if (!v || !anchor || !workspace || (!logits && !fs)) return LDR_EINVAL;
   const Shape& s = v->s;
-  if (!weights_ok(s, w) || !aligned(workspace, kAlign) || !aligned(logits, 16)) return LDR_EINVAL;
+  if (!weights_ok(s, w) || !aligned(workspace, kAlign) || (logits && !aligned(logits, 16)))
+    return LDR_EINVAL;
   if (events && n_events != ldr_draft_step_launches(&v->cfg, nullptr, 0) + 1) return LDR_EINVAL;
   const int batch = v->batch, M = batch * s.B;
   const WsPlan ws = plan_ws(s, batch);
@@ -410,7 +419,12 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
       case LDR_LAUNCH_LM_HEAD:
         g.lda = s.hidden; g.ldw = s.hidden; g.out = logits; g.ldo = s.vocab;
         g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden; g.splits = 1;
-        if (tiled_head) {
+        if (tiled_head && fs) {
+          g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
+          HeadSampleArgs hs{};
+          hs.parts = fs->parts; hs.store_logits = logits != nullptr;
+          e = launch_gemm_tiled_argmax(g, hs, fs->tokens, fs->lse, fs->logq, st);
+        } else if (tiled_head) {
           g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
           e = launch_gemm_tiled(g, st);
         } else {
@@ -435,6 +449,45 @@ int ldr_draft_step(const ldr_views* v, const ldr_weights* w, const int32_t* anch
                    float* logits, void* workspace, size_t workspace_bytes, void* stream) {
   return draft_step_impl(v, w, anchor, logits, workspace, workspace_bytes, nullptr, 0,
                          static_cast<hipStream_t>(stream));
+}
+
+size_t ldr_draft_step_sample_workspace_bytes(const ldr_config* cfg, int32_t batch) {
+  Shape s;
+  if (!make_shape(cfg, &s) || batch <= 0) return 0;
+  const int rows = batch * s.B;
+  const size_t draft = plan_ws(s, batch).bytes;
+  const size_t parts = head_sample_part_bytes(rows, s.vocab);
+  const size_t samp = ldr_sample_workspace_bytes(rows, s.vocab);
+  return align_up(draft) + align_up(parts > samp ? parts : samp);
+}
+
+int ldr_draft_step_sample(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
+                          float* logits, float temperature, uint64_t seed, uint64_t step,
+                          int32_t* tokens, float* lse, float* logq, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  if (!v || !w || !tokens || !lse || !logq || !workspace) return LDR_EINVAL;
+  if (!(temperature >= 0.f) || std::isinf(temperature)) return LDR_EINVAL;
+  const Shape& s = v->s;
+  const int rows = v->batch * s.B;
+  if (workspace_bytes < ldr_draft_step_sample_workspace_bytes(&v->cfg, v->batch) ||
+      !aligned(workspace, kAlign))
+    return LDR_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const size_t draft = align_up(plan_ws(s, v->batch).bytes);
+  uint8_t* extra = static_cast<uint8_t*>(workspace) + draft;
+  // greedy steps fuse the argmax into the head, which needs its tiled copy
+  // and runs above 64 rows
+  if (temperature == 0.f && w->lm_head_tiled && rows > 64) {
+    FusedSample fs{tokens, lse, logq, extra};
+    return draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st, &fs);
+  }
+  // otherwise the separate head and sampler (the same tokens): logits needed
+  if (!logits) return LDR_EINVAL;
+  const int rc = draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st);
+  if (rc != LDR_OK) return rc;
+  return launch_sample(logits, rows, s.vocab, temperature, 0, seed, step, tokens, lse, logq,
+                       extra, align_up(sample_part_bytes(rows, s.vocab)), st) == hipSuccess
+             ? LDR_OK : LDR_EHIP;
 }
 
 int ldr_draft_step_events(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,

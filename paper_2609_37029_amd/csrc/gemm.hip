@@ -315,7 +315,16 @@ __device__ inline void group_barrier() {
 #define LDR_GP(p) ((__attribute__((address_space(1))) void*)(p))
 #define LDR_LP(p) ((__attribute__((address_space(3))) void*)(p))
 
-__global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a) {
+// Greedy partial of the fused head: the largest logit of a column range and
+// its first token.
+struct HeadPart { float key; int idx; };
+
+__device__ inline void head_combine(HeadPart& a, const HeadPart& b) {
+  if (b.key > a.key || (b.key == a.key && b.idx < a.idx)) a = b;
+}
+
+template <bool SAMPLE>
+__global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSampleArgs hs) {
   constexpr int NB = 4, D = NB - 1;
   constexpr int STAGE = 2 * TR * TK * 2;   // bytes: A rows 0..255, W rows 256..511
   constexpr int MT = 8, NT = 4;            // 16 x 16 MFMA tiles per wave: 128 x 64
@@ -410,19 +419,75 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a) {
 #undef LDR_MEM
   wait_vmcnt<0>();   // no DMA outlives the workgroup
   const int crow = (lane >> 4) * 4, ccol = lane & 15;
-  float* out = static_cast<float*>(a.out) + (long)blockIdx.z * a.split_stride;
   const int r0 = blockIdx.y * TR + wm * 128, c0 = blockIdx.x * TR + wn * 64;
+  if (!SAMPLE || hs.store_logits) {
+    float* out = static_cast<float*>(a.out) + (long)blockIdx.z * a.split_stride;
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      const int col = c0 + j * 16 + ccol;
+      for (int j = 0; j < NT; ++j) {
+        const int col = c0 + j * 16 + ccol;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = r0 + i * 16 + crow + v;
+          if (row < a.M && col < a.N) out[(long)row * a.ldo + col] = acc[i][j][v];
+        }
+      }
+  }
+  if constexpr (SAMPLE) {
+    // Greedy epilogue (Eq. 8 at T = 0: the first argmax of each row). Per row
+    // of the tile: each lane's best of its 4 columns, the 16 lanes holding a
+    // row (its 64 columns of this wave) by DPP, the 4 waves of the row
+    // through LDS, one partial per (row, column tile).
+    __shared__ HeadPart tab[TR][4];
+    HeadPart* parts = static_cast<HeadPart*>(hs.parts);
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const int row = r0 + i * 16 + crow + v;
-        if (row < a.M && col < a.N) out[(long)row * a.ldo + col] = acc[i][j][v];
+        HeadPart p{-INFINITY, 0x7fffffff};
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          const int col = c0 + j * 16 + ccol;
+          if (col < a.N) head_combine(p, HeadPart{acc[i][j][v], col});
+        }
+        HeadPart o;
+        o.key = dpp<0xB1>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0xB1, 0xF, 0xF, false);
+        head_combine(p, o);
+        o.key = dpp<0x4E>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0x4E, 0xF, 0xF, false);
+        head_combine(p, o);
+        o.key = dpp<0x141>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0x141, 0xF, 0xF, false);
+        head_combine(p, o);
+        o.key = dpp<0x140>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0x140, 0xF, 0xF, false);
+        head_combine(p, o);
+        if (ccol == 0) tab[wm * 128 + i * 16 + crow + v][wn] = p;
       }
+    __syncthreads();
+    if (tid < TR) {
+      const int row = blockIdx.y * TR + tid;
+      HeadPart p = tab[tid][0];
+#pragma unroll
+      for (int q = 1; q < 4; ++q) head_combine(p, tab[tid][q]);
+      if (row < a.M) parts[(long)row * hs.nparts + blockIdx.x] = p;
     }
+  }
+}
+
+// One wave per row: the column tiles' partials, then the first argmax, its
+// logit as lse and log q = 0, as the separate sampler reports them at T = 0.
+__global__ void __launch_bounds__(64) head_argmax_merge_kernel(const HeadPart* parts, int nparts,
+                                                               int32_t* tokens, float* lse,
+                                                               float* logq) {
+  const int r = blockIdx.x;
+  HeadPart p{-INFINITY, 0x7fffffff};
+  for (int s = threadIdx.x; s < nparts; s += 64) head_combine(p, parts[(long)r * nparts + s]);
+  for (int off = 32; off >= 1; off >>= 1)
+    head_combine(p, HeadPart{__shfl_xor(p.key, off), __shfl_xor(p.idx, off)});
+  if (threadIdx.x == 0) {
+    tokens[r] = p.idx;
+    lse[r] = p.key;
+    logq[r] = 0.f;
+  }
 }
 
 // Tiled copy of a row-major [rows][cols] 2-byte matrix: one thread per 16-byte
@@ -535,7 +600,26 @@ bool gemm_tiled_supported(int M, int N, int K, int splits) {
 hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st) {
   if (!gemm_tiled_supported(a.M, a.N, a.K, a.splits)) return hipErrorInvalidValue;
   const dim3 grid((a.N + TR - 1) / TR, (a.M + TR - 1) / TR, a.splits);
-  hipLaunchKernelGGL(gemm_tiled_kernel, grid, dim3(512), 0, st, a);
+  HeadSampleArgs none{};
+  hipLaunchKernelGGL((gemm_tiled_kernel<false>), grid, dim3(512), 0, st, a, none);
+  return hipGetLastError();
+}
+
+size_t head_sample_part_bytes(int rows, int vocab) {
+  return (size_t)rows * ((vocab + TR - 1) / TR) * sizeof(HeadPart);
+}
+
+hipError_t launch_gemm_tiled_argmax(const GemmArgs& a, const HeadSampleArgs& hs0, int32_t* tokens,
+                                    float* lse, float* logq, hipStream_t st) {
+  if (!gemm_tiled_supported(a.M, a.N, a.K, 1) || a.splits != 1) return hipErrorInvalidValue;
+  HeadSampleArgs hs = hs0;
+  hs.nparts = (a.N + TR - 1) / TR;
+  const dim3 grid((a.N + TR - 1) / TR, (a.M + TR - 1) / TR, 1);
+  hipLaunchKernelGGL((gemm_tiled_kernel<true>), grid, dim3(512), 0, st, a, hs);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(head_argmax_merge_kernel, dim3(a.M), dim3(64), 0, st,
+                     static_cast<const HeadPart*>(hs.parts), hs.nparts, tokens, lse, logq);
   return hipGetLastError();
 }
 

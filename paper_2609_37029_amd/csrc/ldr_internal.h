@@ -145,6 +145,18 @@ hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a,
 // K % (128 * splits) == 0.
 bool gemm_tiled_supported(int M, int N, int K, int splits);
 hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st);
+// The vocabulary head with greedy sampling (T = 0) fused into its epilogue:
+// per row and column tile the first argmax goes to `parts`, then one merge per
+// row writes the token, lse (its logit) and log q = 0. The logits are written
+// only if store_logits.
+struct HeadSampleArgs {
+  void* parts;        // head_sample_part_bytes(M, V) bytes
+  int nparts;         // partials per row (set by the launcher)
+  int store_logits;
+};
+size_t head_sample_part_bytes(int rows, int vocab);
+hipError_t launch_gemm_tiled_argmax(const GemmArgs& a, const HeadSampleArgs& hs, int32_t* tokens,
+                                    float* lse, float* logq, hipStream_t st);
 // Elements of a [rows][cols] matrix in the tiled layout (rows padded to 256).
 size_t tiled_elems(long rows, long cols);
 hipError_t launch_tile_matrix(const void* src, long ld, int rows, int cols, void* dst,

@@ -88,6 +88,9 @@ def _lib():
             "ldr_sample_markov": (ctypes.c_int, [P, I32, I32, I32, P, P, P, I32, I32,
                                                  ctypes.c_float, I32, U64, U64, P, P, P, P, SZ,
                                                  P]),
+            "ldr_draft_step_sample_workspace_bytes": (SZ, [P, I32]),
+            "ldr_draft_step_sample": (ctypes.c_int, [P, P, P, P, ctypes.c_float, U64, U64, P, P,
+                                                     P, P, SZ, P]),
             "ldr_verify_workspace_bytes": (SZ, [I32, I32, I32]),
             "ldr_verify": (ctypes.c_int, [P, P, P, P, I32, I32, I32, ctypes.c_float, U64, U64, P,
                                           P, P, P, SZ, P]),
@@ -459,3 +462,32 @@ def verify(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor],
                              int(step), _ptr(acc), _ptr(tok), _ptr(n_new), _ptr(workspace),
                              workspace.numel(), _stream(stream)), "ldr_verify")
     return out
+
+
+def draft_step_sample_workspace_bytes(shape, batch: int) -> int:
+    return int(_lib().ldr_draft_step_sample_workspace_bytes(ctypes.byref(config(shape)), batch))
+
+
+def draft_step_sample(views: "Views", w: "DraftWeights", anchor: torch.Tensor, temperature: float,
+                      seed: int, step: int, logits=True, out=None,
+                      workspace: Optional[torch.Tensor] = None, stream=None):
+    """ldr_draft_step_sample: (logits or None, tokens, lse, logq); logits=True
+    allocates and fills [batch][B][V] fp32 logits, a tensor is filled, None
+    asks the fused head not to write them."""
+    s, batch = views.shape, views.batch
+    dev = anchor.device
+    if logits is True:
+        logits = torch.empty(batch, s.block, s.vocab, dtype=torch.float32, device=dev)
+    if out is None:
+        out = (torch.empty(batch, s.block, dtype=torch.int32, device=dev),
+               torch.empty(batch, s.block, dtype=torch.float32, device=dev),
+               torch.empty(batch, s.block, dtype=torch.float32, device=dev))
+    if workspace is None:
+        workspace = torch.empty(draft_step_sample_workspace_bytes(s, batch), dtype=torch.uint8,
+                                device=dev)
+    tok, lse, logq = out
+    _check(_lib().ldr_draft_step_sample(views.handle, ctypes.byref(w.c), _ptr(anchor), _ptr(logits),
+                                        float(temperature), int(seed), int(step), _ptr(tok),
+                                        _ptr(lse), _ptr(logq), _ptr(workspace), workspace.numel(),
+                                        _stream(stream)), "ldr_draft_step_sample")
+    return logits, tok, lse, logq
