@@ -40,7 +40,7 @@ COPY_BYTES = 1 << 30         # calibration kernel of the counter runs: reads and
 def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -322,6 +322,30 @@ def kind_breakdown(torch, ldr, rig, ev, reps=5):
         for li, k in enumerate(rig.kinds):
             tot[k] = tot.get(k, 0.0) + ev.elapsed_ms(evs[li], evs[li + 1])
     return {k: v / reps for k, v in tot.items()}
+
+
+def stream_bandwidth(torch, nbytes=1 << 30, reps=10):
+    """Achievable HBM stream rate on this GPU: torch's elementwise copy of
+    `nbytes` of fp32 (reads and writes nbytes each), median of `reps` after
+    a warm-up, in GB/s of bytes moved."""
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        ts.append((e0, e1))
+    torch.cuda.synchronize()
+    us = statistics.median(a.elapsed_time(b) * 1e3 for a, b in ts)
+    del src, dst
+    torch.cuda.empty_cache()
+    gbs = 2 * nbytes / (us * 1e-6) / 1e9
+    return {"copy_GBps": gbs, "of_peak": gbs / HBM_PEAK_GBS, "bytes_moved": 2 * nbytes,
+            "kernel": "torch copy_ (fp32, 1 GiB in, 1 GiB out)"}
 
 
 def percentile(xs, q):
@@ -648,6 +672,7 @@ def main():
         "breakdown_us": {k: v * 1e3 for k, v in sorted(br.items(), key=lambda kv: -kv[1])},
         "state_bytes_per_seq": ldr.state_bytes(s),
     }
+    out["stream_bw"] = stream_bandwidth(torch)
     if rig.verify:
         out["config"]["rows_per_update"] = "r + 1 from ldr_verify"
         out["verify"] = verify_timing(torch, rig, ev)
