@@ -267,10 +267,15 @@ def verify_timing(torch, rig, ev, calls=20):
             "hbm_frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
 
 
+BRACKET_EVERY = 4   # steps between two steps that time one launch of the bracketed kind
+
+
 def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
     """Wall-clock of `steps` steps between two synchronisations; per-step
-    durations from events at step boundaries; optionally events around the
-    launches of kinds in `bracket` (summed per step)."""
+    durations from events at step boundaries; optionally events around one
+    launch of the kind `bracket` in every BRACKET_EVERY-th step, taking its
+    launches in turn (each recorded event costs the step several µs, so the
+    timed run records few of them)."""
     for i in range(warmup):
         rig.step(i)
     torch.cuda.synchronize()
@@ -278,13 +283,14 @@ def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
     kern = None
     if ev and bracket:
         n = len(rig.kinds)
+        which = [li for li, k in enumerate(rig.kinds) if k == bracket]
         kern = []
-        for _ in range(steps):
-            evs = [None] * (n + 1)
-            for li, k in enumerate(rig.kinds):
-                if k in bracket:
-                    evs[li] = evs[li] or ev.create()
-                    evs[li + 1] = ev.create()
+        for i in range(steps):
+            evs = None
+            if i % BRACKET_EVERY == 0:
+                li = which[(i // BRACKET_EVERY) % len(which)]
+                evs = [None] * (n + 1)
+                evs[li], evs[li + 1] = ev.create(), ev.create()
             kern.append(evs)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -297,15 +303,13 @@ def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per_step = [ev.elapsed_ms(marks[i], marks[i + 1]) for i in range(steps)] if marks else []
-    kernel_ms = []
+    kernel_ms = []   # one bracketed launch per entry
     if kern:
         for evs in kern:
-            tot, launches = 0.0, 0
-            for li, k in enumerate(rig.kinds):
-                if k in bracket:
-                    tot += ev.elapsed_ms(evs[li], evs[li + 1])
-                    launches += 1
-            kernel_ms.append((tot, launches))
+            if evs is None:
+                continue
+            li = next(j for j in range(len(rig.kinds)) if evs[j] is not None)
+            kernel_ms.append(ev.elapsed_ms(evs[li], evs[li + 1]))
     return wall, per_step, kernel_ms
 
 
@@ -624,16 +628,16 @@ def main():
         # the bracketed separate path right after it
         wall, per_step, _ = time_steps(torch, rig, args.steps, args.warmup, ev=ev)
         rig.fused_head = False
-        _, _, kern = time_steps(torch, rig, args.steps, 0, ev=ev, bracket={dom})
+        _, _, kern = time_steps(torch, rig, args.steps, 0, ev=ev, bracket=dom)
         rig.fused_head = True
     else:
         wall, per_step, kern = time_steps(torch, rig, args.steps, args.warmup, ev=ev,
-                                          bracket={dom})
+                                          bracket=dom)
     torch.cuda.synchronize()
     ms = wall / args.steps * 1e3
     tokens = batch * s.block * args.steps
     launches_of_dom = sum(1 for k in rig.kinds if k == dom)
-    dom_ms = statistics.mean(t for t, _ in kern) / launches_of_dom
+    dom_ms = statistics.mean(kern)
     dom_bytes = costs[dom][0]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
     # the separate sampler reads the fp32 logits once; the fused head reads none
@@ -664,7 +668,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(dom),
                      "bytes_per_launch": dom_bytes, "us_per_launch": dom_ms * 1e3,
-                     "launches_per_step": launches_of_dom},
+                     "launches_per_step": launches_of_dom, "launches_timed": len(kern)},
         "step_roofline": {"algorithmic_bytes": step_bytes, "flops": step_flops,
                           "hbm_frac": step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
                           "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,

@@ -126,6 +126,40 @@ __global__ void __launch_bounds__(kSelThreads) topk_select_kernel(const float* l
   if (threadIdx.x == 0) sel[blockIdx.x] = TopK{prefix, v_cut};
 }
 
+// The lane's kGroup = 8 logits of a sweep at v: two 16-byte loads inside the
+// chunk [.., v1), else one load per token (-inf past v1).
+__device__ inline void load_group(const SampleArgs& a, const float* z, int v, int v1,
+                                  float (&zz)[kGroup]) {
+  if (a.vec && v + kGroup <= v1) {
+    const float4 x = *reinterpret_cast<const float4*>(z + v);
+    const float4 y = *reinterpret_cast<const float4*>(z + v + 4);
+    zz[0] = x.x; zz[1] = x.y; zz[2] = x.z; zz[3] = x.w;
+    zz[4] = y.x; zz[5] = y.y; zz[6] = y.z; zz[7] = y.w;
+  } else {
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) zz[i] = v + i < v1 ? z[v + i] : -INFINITY;
+  }
+}
+
+// Greedy steps (T = 0): the first argmax of the chunk, its logits streamed in
+// the sampling sweeps' pattern (the next sweep's loads in flight).
+__device__ void argmax_tokens(const SampleArgs& a, const float* z, int v0, int v1, Partial& p) {
+  constexpr int kSweep = kThreads * kGroup;
+  const int lane_off = (int)threadIdx.x * kGroup;
+  float znext[kGroup];
+  load_group(a, z, v0 + lane_off, v1, znext);
+  for (int vb = v0; vb < v1; vb += kSweep) {
+    const int v = vb + lane_off;
+    float zcur[kGroup];
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) zcur[i] = znext[i];
+    if (vb + kSweep < v1) load_group(a, z, v + kSweep, v1, znext);
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i)
+      if (v + i < v1 && better(zcur[i], v + i, p.key, p.idx)) { p.key = zcur[i]; p.idx = v + i; }
+  }
+}
+
 // Temperature sampling. Every lane keeps the lse partial of its tokens and the
 // best (key, token) of the candidates it evaluated. A token is a candidate
 // unless zt + bound(g) + margin < the lane's best key, which proves that its
@@ -153,18 +187,7 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  // the lane's 8 logits of a sweep: two 16-byte loads inside the chunk
-  auto load8 = [&](int v, float (&zz)[kGroup]) {
-    if (a.vec && v + kGroup <= v1) {
-      const float4 x = *reinterpret_cast<const float4*>(z + v);
-      const float4 y = *reinterpret_cast<const float4*>(z + v + 4);
-      zz[0] = x.x; zz[1] = x.y; zz[2] = x.z; zz[3] = x.w;
-      zz[4] = y.x; zz[5] = y.y; zz[6] = y.z; zz[7] = y.w;
-    } else {
-#pragma unroll
-      for (int i = 0; i < kGroup; ++i) zz[i] = v + i < v1 ? z[v + i] : -INFINITY;
-    }
-  };
+  auto load8 = [&](int v, float (&zz)[kGroup]) { load_group(a, z, v, v1, zz); };
   constexpr int kSweep = kThreads * kGroup;
   const int lane_off = (int)(threadIdx.x & ~63) * kGroup + lane * kGroup;
   float znext[kGroup];
@@ -338,10 +361,7 @@ __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) 
   const float* z = a.logits + ((long)r * a.row_mul + a.row_add) * a.vocab;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
   if (a.T == 0.f) {
-    for (int v = v0 + threadIdx.x; v < v1; v += kThreads) {
-      const float zv = z[v];
-      if (better(zv, v, p.key, p.idx)) { p.key = zv; p.idx = v; }
-    }
+    argmax_tokens(a, z, v0, v1, p);
   } else if (a.sel) {
     if (a.T == 1.f) sample_tokens<true, true>(a, z, r, v0, v1, p);
     else sample_tokens<false, true>(a, z, r, v0, v1, p);
