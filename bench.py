@@ -267,15 +267,14 @@ def verify_timing(torch, rig, ev, calls=20):
             "hbm_frac": nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS}
 
 
-BRACKET_EVERY = 4   # steps between two steps that time one launch of the bracketed kind
+BRACKET_EVERY = 1   # steps between two steps that time one launch of the bracketed kind
 
 
 def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
     """Wall-clock of `steps` steps between two synchronisations; per-step
     durations from events at step boundaries; optionally events around one
     launch of the kind `bracket` in every BRACKET_EVERY-th step, taking its
-    launches in turn (each recorded event costs the step several µs, so the
-    timed run records few of them)."""
+    launches in turn."""
     for i in range(warmup):
         rig.step(i)
     torch.cuda.synchronize()

@@ -334,7 +334,12 @@ def draft_step_events(views: Views, weights: DraftWeights, anchor: torch.Tensor,
 
 class HipEvents:
     """hipEvent_t handles from the HIP runtime this process already loaded
-    (the one torch uses), for timing single kernels on a stream."""
+    (the one torch uses), for timing single kernels on a stream. They are
+    created without the system-scope fence an event record performs by
+    default (an L2 write-back and invalidate that costs the following kernels
+    several µs): timing only, read after the device has synchronised."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000   # hipEventDisableSystemFence
 
     def __init__(self):
         path = None
@@ -345,7 +350,7 @@ class HipEvents:
         if path is None:
             raise RuntimeError("the HIP runtime is not loaded (initialise torch.cuda first)")
         self.rt = ctypes.CDLL(path)
-        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
                                                 ctypes.c_void_p]
         self.rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
@@ -355,8 +360,8 @@ class HipEvents:
 
     def create(self):
         e = ctypes.c_void_p()
-        if self.rt.hipEventCreate(ctypes.byref(e)) != 0:
-            raise RuntimeError("hipEventCreate failed")
+        if self.rt.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE) != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed")
         self._made.append(e.value)
         return e.value
 
