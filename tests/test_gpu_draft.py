@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import synth
-from gpu_common import Pair, check_logits, lazy_weights_f64, row_errors
+from gpu_common import Pair, check_logits, check_views, lazy_weights_f64, row_errors
 from oracle import draft as OD
 
 pytestmark = pytest.mark.gpu
@@ -181,3 +181,44 @@ def test_full_size_qwen3_8b_sampled(gpu_lib, tiled_head):
         err, cos = row_errors(zc[b], ref[b])
         assert err.max() <= 2e-2, err.max()
         assert cos.min() >= 0.999, cos.min()
+
+
+def _sampled_parity(gpu_lib, s, batch, prefix, seqs, tiled_head=True, chunk=4096):
+    """Views of `seqs` against the oracle's, then their logits on a 2048-token
+    vocabulary sample (plus the first and last token), all B slots."""
+    G = synth.make_G(s, device="cuda")
+    p = Pair(gpu_lib, s, batch, G, oracle_seqs=seqs)
+    p.prefill(prefix, chunk)
+    K, V, h = synth.decode_rows(s, batch, s.block + 1, 0, device="cuda")
+    p.ingest([s.block + 1] * batch, K, V, h)
+    check_views(p)
+    w = synth.make_weights(s, device="cuda")
+    dw = gpu_lib.DraftWeights(w, tiled_head=tiled_head)
+    anchor = synth.make_anchors(s, batch, device="cuda")
+    z = gpu_lib.draft_step(p.views, dw, anchor)
+    torch.cuda.synchronize()
+    assert p.views.status() == 0
+    idx = np.sort(np.random.default_rng(5).choice(s.vocab, 2048, replace=False))
+    idx = np.concatenate([[0], idx, [s.vocab - 1]])
+    ref = oracle_logits(p, w, anchor, vocab_idx=idx, lazy=True)
+    zc = z[:, :, torch.from_numpy(idx).cuda()].cpu().numpy()
+    for b in p.seqs:
+        err, cos = row_errors(zc[b], ref[b])
+        assert err.max() <= 2e-2, (b, err.max())
+        assert cos.min() >= 0.999, (b, cos.min())
+
+
+@pytest.mark.slow
+def test_full_size_qwen3_32b_sampled(gpu_lib):
+    """Qwen3-32B shape (hidden 5120, 64 query heads over 8 kv heads, MLP
+    25600), batch 16, prefix 65536: the 32B configuration. Oracle on two
+    sequences."""
+    _sampled_parity(gpu_lib, synth.QWEN3_32B, 16, 65536, [0, 13])
+
+
+@pytest.mark.slow
+def test_qwen3_8b_batch_64_sampled(gpu_lib):
+    """Qwen3-8B shape at 64 sequences, the sweep's largest batch: 1024 rows,
+    four row tiles in every GEMM and in the tiled head. Oracle on the first
+    and the last sequence."""
+    _sampled_parity(gpu_lib, synth.QWEN3_8B, 64, 1000, [0, 63], chunk=500)
