@@ -5,7 +5,10 @@
  * fixed-cost parallel drafter" (LongSpark): the fixed-size context views of
  * Sec. 2.2 and their incremental maintenance (App. A.2, Eq. 10-11), the
  * block-diffusion drafter forward (Sec. 2.3, Eq. 4 and Eq. 6, App. A.1,
- * App. B.1) and per-position sampling of the factorised proposal (Eq. 8).
+ * App. B.1) and per-position sampling of the factorised proposal (Eq. 8);
+ * around it, the ablation variants' views (Sec. 3.4), the low-rank Markov
+ * correction of the proposal (Eq. 7) and the speculative verification that
+ * closes a round (Eq. 1-2).
  *
  * Conventions shared by every entry point:
  *  - Pointers marked "dev" are device memory owned by the caller (for

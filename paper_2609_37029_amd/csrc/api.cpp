@@ -1,7 +1,8 @@
 // Host side of the C ABI: configuration checks, the per-sequence arena
 // layout, the workspace plan of one draft step, argument validation and the
 // launch sequence. Every step of the drafting computation runs in the HIP
-// kernels of views.hip, gemm.hip, draft.hip and sample.hip.
+// kernels of views.hip, gemm.hip, draft.hip, attn.hip, sample.hip and
+// verify.hip.
 #include <hip/hip_runtime.h>
 
 #include <cmath>

@@ -7,7 +7,8 @@
 //  * a workgroup owns a BM x BN output tile (BM = all M rows up to 256) and a
 //    1/splits share of K, with WM x WN waves of MTW x NTW 16x16 MFMA tiles;
 //  * both operands reach LDS through coalesced 16-byte loads (8 lanes per
-//    128-byte row segment), double-buffered, rows padded to 144 B so the
+//    128-byte row segment), double-buffered, in 128-byte rows whose 16-byte
+//    chunks are XOR-swizzled (lds_chunk) so that both the stores and the
 //    16-lane fragment reads of v_mfma_f32_16x16x32_bf16 are conflict-free;
 //  * weight loads run WPF steps ahead and activation loads 2 steps ahead in
 //    register rings, so HBM latency is covered by several steps of MFMAs;
