@@ -61,7 +61,7 @@ def parse():
     ap.add_argument("--verify", action="store_true",
                     help="verify each drafted block against synthetic target logits and "
                          "commit r + 1 rows per step (closes the round on the device)")
-    ap.add_argument("--cpu-seqs", type=int, default=16,
+    ap.add_argument("--cpu-seqs", type=int, default=48,
                     help="sequences in the CPU-oracle sample")
     ap.add_argument("--sweep", action="store_true")
     ap.add_argument("--sweep-out", default=os.path.join(ROOT, "sweep.json"))
@@ -378,7 +378,7 @@ def cpu_baseline(torch, synth, rig, n_seqs):
     s = rig.s
     Wt = synth.weights_f64(rig.w)
     G64 = synth.to_f64(rig.G)
-    anchor = synth.make_anchors(s, rig.batch).numpy()   # seeded input, never a GPU result
+    anchor = synth.make_anchors(s, n_seqs).numpy()   # seeded input, never a GPU result
     K, V, h = synth.make_rows(s, n_seqs, 512, 77) + (synth.make_h(s, n_seqs, 77),)
     Kd, Vd, hd = synth.decode_rows(s, n_seqs, s.block + 1, 0)
     states = []
@@ -395,7 +395,7 @@ def cpu_baseline(torch, synth, rig, n_seqs):
     el = time.perf_counter() - t0
     del Wt
     return {"value": n_seqs * s.block / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{n_seqs} of the workload's sequences: views update (17 rows) + fp64 "
+            "sample": f"{n_seqs} sequences of the workload's step: views update (17 rows) + fp64 "
                       f"draft forward + sampling of {s.block} positions over {s.vocab} tokens, "
                       f"{el:.2f} s (BLAS threads {cores}; elementwise numpy single-threaded)"}
 
