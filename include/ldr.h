@@ -347,38 +347,43 @@ size_t ldr_verify_workspace_bytes(int32_t batch, int32_t block, int32_t vocab);
 /* Speculative verification of one drafted block per sequence (Eq. 1-2), the
  * step that closes a round. The target has scored [a, y_1 .. y_B] in one pass:
  * target row j of sequence b is p_{j+1} = softmax(P[b][j] / T), j = 0 .. B; the
- * proposal is q_i = softmax(z[b][i-1] / T) over the whole vocabulary (the
- * logits ldr_sample or ldr_sample_markov drew y from, with the lse they
- * wrote). Candidates are tested in order: y_i is accepted when
- * u_i < p_i(y_i) / q_i(y_i); a candidate outside [0, vocab) is rejected. At
- * the first rejection, i, the round emits the first argmax of log w_v + g_v
- * over the residual w_v = p_i(v) - q_i(v) > 2^-14 p_i(v) (closer values count
- * as equal: the fp32 normalisers do not resolve them); after B acceptances, and
- * when the residual w has no positive mass, it emits the first argmax of
- * fl(fl(P_v / T) + g_v) over the row (the drafting sampler's rule). Noise:
- * ldr_sample's Philox4x32-10 layout with the top two bits of the last counter
- * word set to a stream: u_i is word 0 of counter (i - 1, b, ...) in stream 1,
- * g_v token v of row b in stream 2; both through u = (2 (bits >> 9) + 1)
- * 2^-24, and g = -log(-log(u)) with ldr_sample's fixed-operation logarithm. T = 0
- * verifies greedily: y_i is accepted when it is the first argmax of P[b][i-1],
- * and the round emits the first argmax of the row where it stops (draft_logits
- * and draft_lse are not read and may be NULL). The ratio, the residual and the
- * target's log-normalisers are fp32.
+ * proposal q_i is softmax(z[b][i-1] / T) over the drafting sampler's support
+ * (the whole vocabulary when top_k is 0 or >= vocab, else the top_k largest
+ * logits, lower index first on ties) and 0 outside it: the logits and top_k
+ * ldr_sample or ldr_sample_markov drew y from, with the lse it wrote.
+ * Candidates are tested in order: y_i is accepted when u_i < p_i(y_i) / q_i(y_i);
+ * a candidate outside [0, vocab) or outside the support is rejected. At the
+ * first rejection, i, the round emits the first argmax of log w_v + g_v over
+ * the residual w_v = [p_i(v) - q_i(v)]_+, every token with w_v > 0 as computed
+ * in fp32; after B acceptances, and when w has no positive entry, it emits the
+ * first argmax of fl(fl(P_v / T) + g_v) over the row (the drafting sampler's
+ * rule). Noise: ldr_sample's Philox4x32-10 layout with the top two bits of the
+ * last counter word set to a stream: u_i is word 0 of counter (i - 1, b, ...)
+ * in stream 1, g_v token v of row b in stream 2; both through
+ * u = (2 (bits >> 9) + 1) 2^-24, and g = -log(-log(u)) with ldr_sample's
+ * fixed-operation logarithm. T = 0 verifies greedily: y_i is accepted when it
+ * is the first argmax of P[b][i-1], and the round emits the first argmax of
+ * the row where it stops (draft_logits, draft_lse and top_k are not read and
+ * draft_logits / draft_lse may be NULL). The ratio, the residual and the
+ * target's log-normalisers are fp32, so decisions closer than their rounding
+ * (a ratio within ~1e-6 of u, residual entries within ~1e-6 of p) may differ
+ * from the exact ones.
  *   target_logits dev fp32 [batch][block + 1][vocab]
  *   draft_logits  dev fp32 [batch][block][vocab]; draft_lse dev fp32 [batch][block]
  *   draft_tokens  dev int32 [batch][block]
+ *   top_k         the sampler's support size (0: the whole vocabulary)
  *   accepted      dev int32 [batch]: r, the accepted candidates (0 .. block)
  *   next_token    dev int32 [batch]: the emitted token (the next anchor)
  *   n_new         dev int32 [batch]: r + 1, the rows the prefix advances by (the
  *                 per-sequence row count of the next ldr_views_update)
  *   workspace     dev, ldr_verify_workspace_bytes(batch, block, vocab) bytes.
- * LDR_EINVAL on a NULL pointer, a non-positive size, a negative, NaN or
- * infinite temperature, or a short or misaligned workspace. */
+ * LDR_EINVAL on a NULL pointer, a non-positive size, a negative top_k, a
+ * negative, NaN or infinite temperature, or a short or misaligned workspace. */
 int ldr_verify(const float* target_logits, const float* draft_logits, const float* draft_lse,
                const int32_t* draft_tokens, int32_t batch, int32_t block, int32_t vocab,
-               float temperature, uint64_t seed, uint64_t step, int32_t* accepted,
-               int32_t* next_token, int32_t* n_new, void* workspace, size_t workspace_bytes,
-               void* stream);
+               float temperature, int32_t top_k, uint64_t seed, uint64_t step,
+               int32_t* accepted, int32_t* next_token, int32_t* n_new, void* workspace,
+               size_t workspace_bytes, void* stream);
 
 /* Writes the Gumbel noise ldr_sample uses: out[r][v] = g_v of row r, for
  * rows [0, rows) and tokens [0, vocab). out dev fp32 [rows][vocab]. */

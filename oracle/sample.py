@@ -218,23 +218,22 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
 # The target scores [a, y_1 .. y_B] in one pass and gives B + 1 distributions:
 # row j of the target logits P is p_{j+1}. Candidate y_i is accepted when
 # u_i < p_i(y_i) / q_i(y_i) (Eq. 1), tested in order; at the first rejection
-# the round emits a token drawn from [p_i - q_i]_+ normalised (Eq. 2), and
-# after B acceptances a bonus token drawn from p_{B+1}. p and q take the same
-# temperature T over the whole vocabulary: p_i = softmax(P_i / T),
-# q_i = softmax(z_i / T) (a top-k proposal is not verified here). The ratio,
-# p, q and the residual are float64 here.
+# the round emits a token drawn from the residual w = [p_i - q_i]_+ normalised
+# (Eq. 2), and after B acceptances a bonus token drawn from p_{B+1}. p and q
+# take the same temperature T: p_i = softmax(P_i / T) over the whole
+# vocabulary, q_i = softmax(z_i / T) over the drafting sampler's support S_i
+# (all tokens, or the top_k largest z_i, lower index first on ties) and 0
+# outside it. The ratio, p, q and the residual are float64 here; the residual
+# is the plain positive part of p - q, with no threshold.
 #
 # Readings where the paper is silent:
-#  * a candidate outside [0, V) has q = 0 and is rejected;
-#  * the residual counts token v only when p_i(v) - q_i(v) > 2^-14 p_i(v):
-#    closer values are taken as equal (fp32 log-normalisers over 10^5 terms
-#    are not resolved better than that), so a proposal equal to the target up
-#    to rounding leaves no residual; the mass dropped is below 2^-14;
-#  * a residual with no positive mass draws from p_i with the bonus rule
-#    instead;
+#  * a candidate outside [0, V), or outside the support S_i, has q = 0 (the
+#    proposal cannot produce it) and is rejected;
+#  * a residual with no positive entry (p_i = q_i exactly, where a rejection
+#    has probability zero) draws from p_i with the bonus rule instead;
 #  * the bonus token is drawn exactly as the drafting sampler draws, from the
 #    fp32 keys fl(fl(P_v / T) + g_v), first maximum; the correction token is
-#    the first maximum of log w_v + g_v over w_v = [p_i(v) - q_i(v)]_+ > 0;
+#    the first maximum of log w_v + g_v over the tokens with w_v > 0;
 #  * T = 0 verifies greedily: y_i is accepted when it is the first argmax of
 #    P_i, and the round emits the first argmax of the row where it stops.
 #
@@ -242,9 +241,6 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
 #  * u_i of sequence b: word 0 of the block of counter i - 1 and row b in
 #    stream 1, made uniform like the drafting noise;
 #  * the emitted token's Gumbel noise g_v: token v of row b in stream 2.
-
-
-RESIDUAL_REL = 2.0 ** -14   # a residual entry needs p - q above this fraction of p
 
 
 def verify_uniform(seed, step, b, i):
@@ -266,15 +262,28 @@ def _softmax64(x):
     return e / e.sum()
 
 
-def verify(P, Z, y, temperature, seed, step, keys=False):
+def proposal(z, temperature, top_k=0):
+    """q = softmax(z / T) over the support of z (top_k as in ``support``),
+    0 outside it: float64 [V]."""
+    z = np.asarray(z, dtype=np.float32)
+    q = np.zeros(z.shape[0])
+    s = support(z, top_k)
+    q[s] = _softmax64(z[s].astype(np.float64) / float(np.float32(temperature)))
+    return q
+
+
+def verify(P, Z, y, temperature, seed, step, keys=False, top_k=0, detail=False):
     """Speculative verification of one round for every sequence.
     P: target logits [batch][B + 1][V]; Z: draft logits [batch][B][V] (the
-    proposal q_i = softmax(z_i / T)); y: drafted tokens [batch][B].
+    proposal q_i = softmax(z_i / T) over the top_k support, see ``proposal``);
+    y: drafted tokens [batch][B].
     Returns (r [batch] accepted counts, token [batch] emitted after them,
     ratio [batch][B] p_i(y_i) / q_i(y_i) in float64, u [batch][B]); ratio and
     u are 0 past the first rejection and at T = 0. keys=True appends the list
     of each sequence's keys over the row it emits from (float64 [V]; the
-    token is their first argmax)."""
+    token is their first argmax). detail=True appends, per sequence, a dict
+    with the stop row's p, q, residual w (None after B acceptances) and the
+    emission noise g."""
     P = np.asarray(P, dtype=np.float32)
     Z = np.asarray(Z, dtype=np.float32)
     y = np.asarray(y, dtype=np.int64)
@@ -284,7 +293,7 @@ def verify(P, Z, y, temperature, seed, step, keys=False):
     tok = np.zeros(nb, dtype=np.int64)
     ratio = np.zeros((nb, B))
     us = np.zeros((nb, B))
-    all_keys = []
+    all_keys, details = [], []
     for b in range(nb):
         if temperature == 0.0:
             i = 0
@@ -292,25 +301,26 @@ def verify(P, Z, y, temperature, seed, step, keys=False):
                 i += 1
             r[b], tok[b] = i, int(np.argmax(P[b, i]))
             all_keys.append(P[b, i].astype(np.float64))
+            details.append(None)
             continue
         T = np.float32(temperature)
         stop = B
         for i in range(B):
             p = _softmax64(P[b, i].astype(np.float64) / float(T))
-            q = _softmax64(Z[b, i].astype(np.float64) / float(T))
+            q = proposal(Z[b, i], T, top_k)
             yi = int(y[b, i])
-            ratio[b, i] = p[yi] / q[yi] if 0 <= yi < V else 0.0
+            ratio[b, i] = p[yi] / q[yi] if 0 <= yi < V and q[yi] > 0 else 0.0
             us[b, i] = float(verify_uniform(seed, step, b, i + 1))
             if not us[b, i] < ratio[b, i]:
                 stop = i
                 break
         r[b] = stop
         g = verify_gumbel(seed, step, b, np.arange(V))
-        w = None
+        w = p = q = None
         if stop < B:
             p = _softmax64(P[b, stop].astype(np.float64) / float(T))
-            w = p - _softmax64(Z[b, stop].astype(np.float64) / float(T))
-            w = np.where(w > RESIDUAL_REL * p, w, 0.0)
+            q = proposal(Z[b, stop], T, top_k)
+            w = np.maximum(p - q, 0.0)                           # Eq. 2: [p - q]_+
         if w is not None and np.any(w > 0):
             key = np.full(V, -np.inf)
             key[w > 0] = np.log(w[w > 0]) + g[w > 0].astype(np.float64)
@@ -318,6 +328,10 @@ def verify(P, Z, y, temperature, seed, step, keys=False):
             key = P[b, stop] / T + g                               # fp32, as the sampler
         tok[b] = int(np.argmax(key))
         all_keys.append(key.astype(np.float64))
+        details.append({"p": p, "q": q, "w": w, "g": g.astype(np.float64)})
+    out = (r, tok, ratio, us)
     if keys:
-        return r, tok, ratio, us, all_keys
-    return r, tok, ratio, us
+        out = out + (all_keys,)
+    if detail:
+        out = out + (details,)
+    return out

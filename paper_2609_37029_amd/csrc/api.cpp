@@ -546,18 +546,19 @@ size_t ldr_verify_workspace_bytes(int32_t batch, int32_t block, int32_t vocab) {
 
 int ldr_verify(const float* target_logits, const float* draft_logits, const float* draft_lse,
                const int32_t* draft_tokens, int32_t batch, int32_t block, int32_t vocab,
-               float temperature, uint64_t seed, uint64_t step, int32_t* accepted,
-               int32_t* next_token, int32_t* n_new, void* workspace, size_t workspace_bytes,
-               void* stream) {
+               float temperature, int32_t top_k, uint64_t seed, uint64_t step,
+               int32_t* accepted, int32_t* next_token, int32_t* n_new, void* workspace,
+               size_t workspace_bytes, void* stream) {
   if (!target_logits || !draft_tokens || !accepted || !next_token || !n_new || !workspace)
     return LDR_EINVAL;
   if (batch <= 0 || block <= 0 || vocab <= 0 || !(temperature >= 0.f) || std::isinf(temperature))
     return LDR_EINVAL;
   if (temperature > 0.f && (!draft_logits || !draft_lse)) return LDR_EINVAL;
+  if (top_k < 0) return LDR_EINVAL;
   if (workspace_bytes < ldr_verify_workspace_bytes(batch, block, vocab) || !aligned(workspace, 16))
     return LDR_EINVAL;
   return launch_verify(target_logits, draft_logits, draft_tokens, draft_lse, batch, block, vocab,
-                       temperature, seed, step, accepted, next_token, n_new, workspace,
+                       temperature, top_k, seed, step, accepted, next_token, n_new, workspace,
                        static_cast<hipStream_t>(stream)) == hipSuccess
              ? LDR_OK : LDR_EHIP;
 }

@@ -106,6 +106,23 @@ template <> struct Elem<uint16_t> {
   __device__ static void store(uint16_t* p, float v) { *p = f32_to_bf16(v); }
 };
 
+// Top-k support of a row of logits: token v is inside iff order_key(z_v) > tau,
+// or order_key(z_v) == tau and v <= v_cut (ties at the boundary, lower index
+// first).
+struct TopK { uint32_t tau; int v_cut; };
+
+// Order-preserving map of fp32 to uint32 (larger float, larger key); -0
+// counts as +0, as the two compare equal.
+__device__ inline uint32_t order_key(float z) {
+  uint32_t b = __float_as_uint(z);
+  if (b == 0x80000000u) b = 0u;
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ inline bool in_support(const TopK& t, float z, int v) {
+  const uint32_t u = order_key(z);
+  return u > t.tau || (u == t.tau && v <= t.v_cut);
+}
+
 // ---- kernel launchers -------------------------------------------------------
 // Views (views.hip)
 hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* arena,
@@ -223,9 +240,13 @@ hipError_t launch_sample_markov(float* logits, int batch, int B, int vocab, cons
 // Verification (verify.hip): Eq. 1-2 over [batch][B + 1][V] target logits.
 size_t verify_workspace_bytes(int batch, int B, int V);
 hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const float* qlse,
-                         int batch, int B, int V, float T, uint64_t seed, uint64_t step,
+                         int batch, int B, int V, float T, int top_k, uint64_t seed, uint64_t step,
                          int32_t* accepted, int32_t* token, int32_t* n_new, void* ws,
                          hipStream_t st);
+// Top-k support (tau, v_cut) of each of `rows` rows of [rows][vocab] logits,
+// 0 < k < vocab (sample.hip).
+hipError_t launch_topk_select(const float* logits, int rows, int vocab, int k, TopK* sel,
+                              hipStream_t st);
 hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
                               hipStream_t st);
 

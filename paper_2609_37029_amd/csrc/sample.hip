@@ -37,18 +37,6 @@ __device__ inline void combine(Partial& a, const Partial& b) {
   a.m = m;
 }
 
-// Top-k support of a row: token v is inside iff key(z_v) > tau, or
-// key(z_v) == tau and v <= v_cut (ties at the boundary, lower index first).
-struct TopK { uint32_t tau; int v_cut; };
-
-// Order-preserving map of fp32 to uint32 (larger float, larger key); -0
-// counts as +0, as the two compare equal.
-__device__ inline uint32_t order_key(float z) {
-  uint32_t b = __float_as_uint(z);
-  if (b == 0x80000000u) b = 0u;
-  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-
 struct SampleArgs {
   const float* logits; int rows, vocab, chunk, splits;
   float T; uint64_t seed, step;
@@ -439,6 +427,13 @@ int sample_splits(int rows, int vocab) {
 
 size_t sample_part_bytes(int rows, int vocab) {
   return (size_t)rows * sample_splits(rows, vocab) * sizeof(Partial);
+}
+
+hipError_t launch_topk_select(const float* logits, int rows, int vocab, int k, TopK* sel,
+                              hipStream_t st) {
+  hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, logits, vocab, k,
+                     sel, 1, 0);
+  return hipGetLastError();
 }
 
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,

@@ -19,12 +19,15 @@
 //     normalisers of the row where the round stops;
 //  3. emit pass: one workgroup per (sequence, vocabulary chunk) streams that
 //     target row (and draft row, 16-byte loads): Gumbel keys log w_v + g_v
-//     over the residual w = [p - q]_+ (entries where p exceeds q by more than
-//     2^-14 of p), and the bonus-rule keys fl(fl(P_v / T) + g_v) (the draw at
-//     a bonus, and the fallback when the residual has no positive mass);
+//     over the residual w = [p - q]_+ (every entry with w_v > 0 in fp32), and
+//     the bonus-rule keys fl(fl(P_v / T) + g_v) (the draw at a bonus, and the
+//     fallback when the residual has no positive mass);
 //  4. merge: the best key over the chunks, lower token first on ties.
 // T = 0 verifies greedily: pass 1 takes the first argmax of all B + 1 rows and
 // the merge compares them with the candidates.
+// A top-k proposal (the sampler's support, top_k > 0) has q = 0 outside the
+// support: a selection pass finds each draft row's support first; a candidate
+// outside it is rejected, and the residual there is p itself.
 //
 // Noise (the sampler's Philox4x32-10 layout): u_i is word 0 of block i - 1 of
 // row b in stream 1; the emitted token's Gumbel noise is token v of row b in
@@ -37,9 +40,6 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kInvalid = 0x7fffffff;
-// A residual entry counts only when p - q exceeds this fraction of p: closer
-// values are equal within the fp32 log-normalisers (sums over ~10^5 terms).
-constexpr float kResidualRel = 6.103515625e-05f;   // 2^-14
 
 struct LsePart { float m, s; int idx, pad; };     // max P / T, sum exp(P / T - m); argmax at T = 0
 struct EmitPart { float kr; int ir; float kb; int ib; };  // best residual key / bonus-rule key
@@ -66,6 +66,7 @@ struct VerifyArgs {
   const float* z;        // [batch][B][V]
   const int32_t* y;      // [batch][B]
   const float* qlse;     // [batch][B]
+  const TopK* sel;       // [batch][B] top-k support of the draft rows, or null (all tokens)
   int batch, B, V;
   float T;
   uint64_t seed, step;
@@ -156,11 +157,12 @@ __device__ int stop_position(const VerifyArgs& a, int b) {
     bool reject = false;
     if (i < a.B) {
       const int y = a.y[(long)b * a.B + i];
-      if (y < 0 || y >= a.V) {
-        reject = true;
+      const float* zi = a.z + ((long)b * a.B + i) * a.V;
+      if (y < 0 || y >= a.V || (a.sel && !in_support(a.sel[(long)b * a.B + i], zi[y], y))) {
+        reject = true;   // q(y) = 0: the proposal cannot produce y
       } else {
         const float lp = a.P[((long)b * (a.B + 1) + i) * a.V + y] / a.T - row_lse(a, b, i);
-        const float lq = a.z[((long)b * a.B + i) * a.V + y] / a.T - a.qlse[(long)b * a.B + i];
+        const float lq = zi[y] / a.T - a.qlse[(long)b * a.B + i];
         const float ratio = expf(lp - lq);
         uint32_t w[4];
         noise_block(noise_key(a.seed, a.step, 1), (uint32_t)b, (uint32_t)i, w);
@@ -196,6 +198,7 @@ __global__ void __launch_bounds__(kThreads) verify_emit_kernel(VerifyArgs a) {
   const float plse = d.plse, qlse = d.qlse;
   const float* p = a.P + ((long)b * (a.B + 1) + stop) * a.V;
   const float* z = residual ? a.z + ((long)b * a.B + stop) * a.V : nullptr;
+  const TopK sel = residual && a.sel ? a.sel[(long)b * a.B + stop] : TopK{0u, -1};
   const int v0 = sp * a.chunk2, v1 = min(a.V, v0 + a.chunk2);
   EmitPart e{-INFINITY, kInvalid, -INFINITY, kInvalid};
   // A token's exact keys (two logarithms for g, more for the residual) are
@@ -214,8 +217,10 @@ __global__ void __launch_bounds__(kThreads) verify_emit_kernel(VerifyArgs a) {
     if (want_r) {
       const float zt = UNIT_T ? zv : zv / a.T;
       const float pv = expf(pt - plse);
-      const float w = pv - expf(zt - qlse);
-      if (w > kResidualRel * pv) {
+      // q = 0 outside a top-k support (the whole vocabulary has tau = 0)
+      const float qv = in_support(sel, zv, v) ? expf(zt - qlse) : 0.f;
+      const float w = pv - qv;
+      if (w > 0.f) {   // Eq. 2: [p - q]_+
         const float kr = logf(w) + g;
         if (better(kr, v, e.kr, e.ir)) { e.kr = kr; e.ir = v; }
       }
@@ -372,13 +377,14 @@ size_t verify_workspace_bytes(int batch, int B, int V) {
   const Plan g = make_plan(batch, B, V, true), t = make_plan(batch, B, V, false);
   const size_t l1 = (size_t)batch * (B + 1) * g.splits1, l2 = (size_t)batch * B * t.splits1;
   const size_t lse = align_up((l1 > l2 ? l1 : l2) * sizeof(LsePart));
-  return lse + align_up((size_t)batch * t.splits2 * sizeof(EmitPart)) + batch * sizeof(Decision);
+  return lse + align_up((size_t)batch * t.splits2 * sizeof(EmitPart)) +
+         align_up(batch * sizeof(Decision)) + (size_t)batch * B * sizeof(TopK);
 }
 
 hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const float* qlse,
-                         int batch, int B, int V, float T, uint64_t seed, uint64_t step,
-                         int32_t* accepted, int32_t* token, int32_t* n_new, void* ws,
-                         hipStream_t st) {
+                         int batch, int B, int V, float T, int top_k, uint64_t seed,
+                         uint64_t step, int32_t* accepted, int32_t* token, int32_t* n_new,
+                         void* ws, hipStream_t st) {
   const bool greedy = T == 0.f;
   const Plan pl = make_plan(batch, B, V, greedy);
   VerifyArgs a;
@@ -393,6 +399,14 @@ hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const
   a.dec = reinterpret_cast<Decision*>(reinterpret_cast<uint8_t*>(a.epart) +
                                       align_up((size_t)batch * pl.splits2 * sizeof(EmitPart)));
   a.accepted = accepted; a.token = token; a.n_new = n_new;
+  a.sel = nullptr;
+  if (!greedy && top_k > 0 && top_k < V && B > 0) {   // the draft rows' top-k supports
+    TopK* sel = reinterpret_cast<TopK*>(reinterpret_cast<uint8_t*>(a.dec) +
+                                        align_up(batch * sizeof(Decision)));
+    const hipError_t e = launch_topk_select(z, batch * B, V, top_k, sel, st);
+    if (e != hipSuccess) return e;
+    a.sel = sel;
+  }
   // 16-byte loads need rows that start on 16 bytes
   const bool vec = V % 4 == 0 && reinterpret_cast<uintptr_t>(P) % 16 == 0 &&
                    reinterpret_cast<uintptr_t>(z) % 16 == 0;

@@ -92,8 +92,8 @@ def _lib():
             "ldr_draft_step_sample": (ctypes.c_int, [P, P, P, P, ctypes.c_float, U64, U64, P, P,
                                                      P, P, SZ, P]),
             "ldr_verify_workspace_bytes": (SZ, [I32, I32, I32]),
-            "ldr_verify": (ctypes.c_int, [P, P, P, P, I32, I32, I32, ctypes.c_float, U64, U64, P,
-                                          P, P, P, SZ, P]),
+            "ldr_verify": (ctypes.c_int, [P, P, P, P, I32, I32, I32, ctypes.c_float, I32, U64,
+                                          U64, P, P, P, P, SZ, P]),
             "ldr_strerror": (ctypes.c_char_p, [ctypes.c_int]),
         }
         for name, (res, args) in sig.items():
@@ -450,10 +450,10 @@ def verify_workspace_bytes(batch: int, block: int, vocab: int) -> int:
 def verify(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor],
            draft_lse: Optional[torch.Tensor], draft_tokens: torch.Tensor, temperature: float,
            seed: int, step: int, out=None, workspace: Optional[torch.Tensor] = None,
-           stream=None):
+           stream=None, top_k: int = 0):
     """ldr_verify: target logits [batch][B + 1][V], draft logits [batch][B][V]
-    with the sampler's lse [batch][B] and tokens [batch][B] ->
-    (accepted, next_token, n_new), int32 [batch] each."""
+    with the sampler's lse [batch][B] and tokens [batch][B] (drawn with
+    top_k) -> (accepted, next_token, n_new), int32 [batch] each."""
     batch, B1, V = target_logits.shape
     B = B1 - 1
     dev = target_logits.device
@@ -463,8 +463,9 @@ def verify(target_logits: torch.Tensor, draft_logits: Optional[torch.Tensor],
         workspace = torch.empty(verify_workspace_bytes(batch, B, V), dtype=torch.uint8, device=dev)
     acc, tok, n_new = out
     _check(_lib().ldr_verify(_ptr(target_logits), _ptr(draft_logits), _ptr(draft_lse),
-                             _ptr(draft_tokens), batch, B, V, float(temperature), int(seed),
-                             int(step), _ptr(acc), _ptr(tok), _ptr(n_new), _ptr(workspace),
+                             _ptr(draft_tokens), batch, B, V, float(temperature), int(top_k),
+                             int(seed), int(step), _ptr(acc), _ptr(tok), _ptr(n_new),
+                             _ptr(workspace),
                              workspace.numel(), _stream(stream)), "ldr_verify")
     return out
 

@@ -110,7 +110,9 @@ def test_host_validation_needs_no_gpu(L):
                        ((fake, fake, fake, fake, 2, 3, 64), float("nan"), vws),
                        ((fake, fake, fake, fake, 2, 3, 64), float("inf"), vws),
                        ((fake, fake, fake, fake, 2, 3, 64), 1.0, vws - 1)):  # short workspace
-        assert lib.ldr_verify(*args, T, 0, 0, fake, fake, fake, fake, n, None) == L.LDR_EINVAL
+        assert lib.ldr_verify(*args, T, 0, 0, 0, fake, fake, fake, fake, n, None) == L.LDR_EINVAL
+    assert lib.ldr_verify(fake, fake, fake, fake, 2, 3, 64, 1.0, -1, 0, 0, fake, fake, fake, fake,
+                          vws, None) == L.LDR_EINVAL                     # negative top_k
     assert lib.ldr_views_status(None, 0, None) == L.LDR_EINVAL
     lib.ldr_views_destroy(None)
     assert lib.ldr_sample_workspace_bytes(0, 10) == 0

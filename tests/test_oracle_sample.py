@@ -11,7 +11,7 @@ import pytest
 import scipy.stats
 
 from oracle import sample as Sm
-from oracle.sample import gumbel, sample, verify, verify_gumbel, verify_uniform
+from oracle.sample import gumbel, proposal, sample, verify, verify_gumbel, verify_uniform
 
 
 def test_philox_known_answers():
@@ -335,18 +335,81 @@ def test_out_of_range_candidates_are_rejected():
         assert r[0] == 0 and ratio[0, 0] == 0.0 and 0 <= tok[0] < V
 
 
-def test_residual_ignores_differences_below_the_cutoff():
-    """p above q by less than 2^-14 of p counts as equal: with no other
-    positive entry the round draws from p with the bonus rule."""
+def test_residual_keeps_every_positive_difference():
+    """Eq. 2 is the plain positive part of p - q: a token whose target
+    probability exceeds the proposal's by 2e-5 relative is the only one with
+    positive residual mass, so a rejection emits it with certainty."""
     V = 6
     q_logits = np.float32([1.0, 0.5, -0.2, 0.3, 2.0, -1.0])
     P = np.tile(q_logits, (1, 2, 1)).astype(np.float32)
-    P[0, 0, 1] += np.float32(2e-5)          # p(1)/q(1) - 1 ~ 2e-5 < 2^-14 = 6.1e-5
+    P[0, 0, 1] += np.float32(2e-5)          # p(1) > q(1) by ~2e-5 relative; p < q elsewhere
     Z = q_logits[None, None].astype(np.float32)
-    r, tok, _, _, keys = verify(P, Z, np.array([[V]]), 1.0, 3, 3, keys=True)
-    assert r[0] == 0
-    bonus = (P[0, 0] / np.float32(1.0) + verify_gumbel(3, 3, 0, np.arange(V))).astype(np.float32)
-    assert tok[0] == int(np.argmax(bonus)) and np.isfinite(keys[0]).all()
-    P[0, 0, 1] += np.float32(1e-3)          # now well above the cutoff: the only residual token
+    for seed in range(5):
+        r, tok, _, _, det = verify(P, Z, np.array([[V]]), 1.0, seed, 3, detail=True)
+        w = det[0]["w"]
+        assert r[0] == 0 and tok[0] == 1
+        assert np.count_nonzero(w) == 1 and w[1] > 0
+    # with p = q exactly the residual has no mass: the bonus-rule draw from p
+    P[0, 0] = q_logits
     r, tok, _, _ = verify(P, Z, np.array([[V]]), 1.0, 3, 3)
-    assert r[0] == 0 and tok[0] == 1
+    bonus = (P[0, 0] / np.float32(1.0) + verify_gumbel(3, 3, 0, np.arange(V))).astype(np.float32)
+    assert r[0] == 0 and tok[0] == int(np.argmax(bonus))
+
+
+def test_residual_on_a_hand_computed_row():
+    """p = (1/2, 1/4, 1/4), q = (1/4, 1/4, 1/2) from log-probabilities: the
+    residual is (1/4, 0, 0), so a rejected round emits token 0; the ratio of a
+    candidate 2 is p(2) / q(2) = 1/2."""
+    lp = np.log(np.array([0.5, 0.25, 0.25])).astype(np.float32)
+    lq = np.log(np.array([0.25, 0.25, 0.5])).astype(np.float32)
+    P = np.stack([lp, lp])[None].astype(np.float32)
+    Z = lq[None, None].astype(np.float32)
+    seen = set()
+    for seed in range(40):
+        r, tok, ratio, u, det = verify(P, Z, np.array([[2]]), 1.0, seed, 0, detail=True)
+        assert abs(ratio[0, 0] - 0.5) < 1e-6
+        assert r[0] == (1 if u[0, 0] < ratio[0, 0] else 0)
+        if r[0] == 0:
+            assert tok[0] == 0
+            assert np.allclose(det[0]["w"], [0.25, 0.0, 0.0], atol=1e-7)
+        seen.add(int(r[0]))
+    assert seen == {0, 1}
+
+
+def test_top_k_proposal_is_zero_outside_the_support():
+    """q over the top-k support: 0 outside it, softmax inside; a candidate
+    outside the support is rejected, and the residual there equals p."""
+    z = np.float32([0.3, 2.0, -1.0, 2.0, 0.9])
+    q = proposal(z, 1.0, top_k=2)
+    assert np.array_equal(q > 0, [False, True, False, True, False])
+    assert np.allclose(q[[1, 3]], [0.5, 0.5])
+    P = np.tile(np.float32([0.1, 0.2, 0.3, 0.4, 0.5]), (1, 2, 1)).astype(np.float32)
+    Z = z[None, None]
+    r, _, ratio, _, det = verify(P, Z, np.array([[0]]), 1.0, 1, 1, top_k=2, detail=True)
+    assert r[0] == 0 and ratio[0, 0] == 0.0
+    p = det[0]["p"]
+    w = det[0]["w"]
+    assert np.allclose(w[[0, 2, 4]], p[[0, 2, 4]]) and np.all(w[[1, 3]] == 0)
+
+
+def test_top_k_verification_preserves_the_target_distribution():
+    """The speculative sampling property holds for a top-k proposal too: the
+    first emitted token follows p_1 exactly (chi-square), and the acceptance
+    rate is sum_v min(p(v), q(v)) with q the top-k proposal."""
+    V, n, k = 6, 30_000, 3
+    g = np.random.default_rng(12)
+    p_logits = g.normal(size=V).astype(np.float32)
+    q_logits = g.normal(size=V).astype(np.float32)
+    P = np.tile(np.stack([p_logits, g.normal(size=V).astype(np.float32)])[None], (n, 1, 1))
+    Z = np.tile(q_logits[None, None], (n, 1, 1))
+    y, _, _ = sample(Z.reshape(n, V), 1.0, k, 23, 0)            # y_1 ~ q_1 over the support
+    r, tok, _, _ = verify(P, Z, y[:, None], 1.0, 23, 0, top_k=k)
+    first = np.where(r == 1, y, tok)
+    counts = np.bincount(first, minlength=V)
+    chi2 = scipy.stats.chisquare(counts, _soft(p_logits) * n)
+    assert chi2.pvalue > 1e-3
+    q = np.zeros(V)
+    top = np.argsort(-q_logits.astype(np.float64), kind="stable")[:k]
+    q[top] = _soft(q_logits[top])
+    acc = np.minimum(_soft(p_logits), q).sum()
+    assert abs(r.mean() - acc) < 0.015
