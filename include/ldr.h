@@ -43,7 +43,8 @@ enum ldr_status {
   LDR_EINVAL = -1,  /* bad argument, shape or alignment (host check)        */
   LDR_ERANGE = -2,  /* a per-sequence row count outside [0, max_new]        */
   LDR_EHIP = -3,    /* a HIP runtime call or kernel launch failed           */
-  LDR_ENOMEM = -4   /* the small host/device bookkeeping allocation failed  */
+  LDR_ENOMEM = -4,  /* the small host/device bookkeeping allocation failed  */
+  LDR_ESCRATCH = -5 /* the call needs more than the static scratch holds    */
 };
 
 enum ldr_dtype { LDR_F32 = 0, LDR_BF16 = 1 };
@@ -316,6 +317,29 @@ size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
 int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperature,
                int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
                float* logq, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of the library's static device scratch behind ldr_sample_noalloc. */
+#define LDR_NOALLOC_SCRATCH_BYTES ((size_t)1 << 20)
+
+/* ldr_sample for callers that cannot allocate device memory (code under HIP
+ * graph capture, serving loops that forbid allocation): the same kernels,
+ * tokens, lse and logq as ldr_sample with the same arguments, bit for bit, with
+ * the per-chunk partials and the top-k supports in a file-scope device array of
+ * LDR_NOALLOC_SCRATCH_BYTES bytes instead of a caller workspace. Each GPU the
+ * library runs on holds its own copy of that array until the process ends; its
+ * address is looked up once per device, on the first call with that device
+ * current. The call allocates nothing (no hipMalloc, no library routine that
+ * allocates). Every call on one GPU shares that GPU's array and leaves its
+ * contents behind; nothing in it needs to start at zero (each launch writes
+ * every entry it later reads), but calls whose stream work overlaps on the same
+ * GPU race on it: serialise them (one stream, or events). Requests with
+ * ldr_sample_workspace_bytes(rows, vocab) > LDR_NOALLOC_SCRATCH_BYTES (about
+ * 40000 rows) return LDR_ESCRATCH before anything is enqueued; bad arguments
+ * return LDR_EINVAL as in ldr_sample.
+ *   logits dev fp32 [rows][vocab]; tokens dev int32 [rows]; lse, logq dev fp32 [rows] */
+int ldr_sample_noalloc(const float* logits, int32_t rows, int32_t vocab, float temperature,
+                       int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
+                       float* logq, void* stream);
 
 /* Markov-corrected sampling (Eq. 7-8; the low-rank sequential correction the
  * paper takes from DSpark). For every sequence b and position i = 1 .. B in

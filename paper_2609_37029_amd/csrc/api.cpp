@@ -183,6 +183,7 @@ const char* ldr_strerror(int status) {
     case LDR_ERANGE: return "row count out of range";
     case LDR_EHIP: return "HIP runtime error";
     case LDR_ENOMEM: return "out of memory";
+    case LDR_ESCRATCH: return "request exceeds the static scratch of the allocation-free call";
     default: return "unknown status";
   }
 }
@@ -515,6 +516,22 @@ int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperatu
     return LDR_EINVAL;
   return launch_sample(logits, rows, vocab, temperature, top_k, seed, step, tokens, lse, logq,
                        workspace, align_up(sample_part_bytes(rows, vocab)),
+                       static_cast<hipStream_t>(stream)) == hipSuccess
+             ? LDR_OK : LDR_EHIP;
+}
+
+int ldr_sample_noalloc(const float* logits, int32_t rows, int32_t vocab, float temperature,
+                       int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
+                       float* logq, void* stream) {
+  if (!logits || !tokens || !lse || !logq) return LDR_EINVAL;
+  if (rows <= 0 || vocab <= 0 || !(temperature >= 0.f) || std::isinf(temperature))
+    return LDR_EINVAL;
+  if (top_k < 0) return LDR_EINVAL;
+  if (ldr_sample_workspace_bytes(rows, vocab) > LDR_NOALLOC_SCRATCH_BYTES) return LDR_ESCRATCH;
+  void* ws = nullptr;
+  if (noalloc_scratch(&ws) != hipSuccess) return LDR_EHIP;
+  return launch_sample(logits, rows, vocab, temperature, top_k, seed, step, tokens, lse, logq, ws,
+                       align_up(sample_part_bytes(rows, vocab)),
                        static_cast<hipStream_t>(stream)) == hipSuccess
              ? LDR_OK : LDR_EHIP;
 }

@@ -247,6 +247,9 @@ hipError_t launch_verify(const float* P, const float* z, const int32_t* y, const
 // 0 < k < vocab (sample.hip).
 hipError_t launch_topk_select(const float* logits, int rows, int vocab, int k, TopK* sel,
                               hipStream_t st);
+// Device address of the static scratch of ldr_sample_noalloc on the current
+// GPU (sample.hip); looked up once per device.
+hipError_t noalloc_scratch(void** out);
 hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
                               hipStream_t st);
 

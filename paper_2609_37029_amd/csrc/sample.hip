@@ -15,6 +15,8 @@
 // is exact, and g = -log(-log u) uses a log made of IEEE fp32 operations only
 // (no contraction, correctly rounded division), so the keys fl(fl(z/T) + g)
 // are reproducible bit for bit.
+#include <mutex>
+
 #include "ldr_internal.h"
 #include "noise.h"
 
@@ -427,6 +429,35 @@ int sample_splits(int rows, int vocab) {
 
 size_t sample_part_bytes(int rows, int vocab) {
   return (size_t)rows * sample_splits(rows, vocab) * sizeof(Partial);
+}
+
+// Static scratch of ldr_sample_noalloc: the sampler's partials and top-k
+// supports for callers that cannot allocate. Host code never passes the
+// array's name to a kernel (on the host it is only a stand-in for the symbol);
+// it uses the device address hipGetSymbolAddress returns for the current GPU.
+static __device__ __align__(256) uint8_t scratch[LDR_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+}  // namespace
+
+hipError_t noalloc_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  // once per device, with that device current (the calling thread's)
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* p = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    g_scratch_ptr[dev] = g_scratch_err[dev] == hipSuccess ? p : nullptr;
+  });
+  if (g_scratch_err[dev] != hipSuccess) return g_scratch_err[dev];
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_topk_select(const float* logits, int rows, int vocab, int k, TopK* sel,

@@ -16,7 +16,8 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libldr.so")
 
-LDR_OK, LDR_EINVAL, LDR_ERANGE, LDR_EHIP, LDR_ENOMEM = 0, -1, -2, -3, -4
+LDR_OK, LDR_EINVAL, LDR_ERANGE, LDR_EHIP, LDR_ENOMEM, LDR_ESCRATCH = 0, -1, -2, -3, -4, -5
+NOALLOC_SCRATCH_BYTES = 1 << 20   # LDR_NOALLOC_SCRATCH_BYTES
 LDR_F32, LDR_BF16 = 0, 1
 
 
@@ -85,6 +86,8 @@ def _lib():
             "ldr_sample": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P, P, P,
                                           SZ, P]),
             "ldr_gumbel_fill": (ctypes.c_int, [U64, U64, I32, I32, P, P]),
+            "ldr_sample_noalloc": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P,
+                                                  P, P]),
             "ldr_sample_markov": (ctypes.c_int, [P, I32, I32, I32, P, P, P, I32, I32,
                                                  ctypes.c_float, I32, U64, U64, P, P, P, P, SZ,
                                                  P]),
@@ -402,6 +405,24 @@ def sample(logits: torch.Tensor, temperature: float, top_k: int, seed: int, step
     _check(_lib().ldr_sample(_ptr(logits), rows, V, float(temperature), int(top_k), int(seed),
                              int(step), _ptr(tok), _ptr(lse), _ptr(logq), _ptr(workspace),
                              workspace.numel(), _stream(stream)), "ldr_sample")
+    return out
+
+
+def sample_noalloc(logits: torch.Tensor, temperature: float, top_k: int, seed: int, step: int,
+                   out=None, stream=None):
+    """ldr_sample_noalloc: ldr_sample with the library's static device scratch
+    in place of a workspace (no device allocation by the library)."""
+    V = logits.shape[-1]
+    rows = logits.numel() // V
+    dev = logits.device
+    if out is None:
+        out = (torch.empty(rows, dtype=torch.int32, device=dev),
+               torch.empty(rows, dtype=torch.float32, device=dev),
+               torch.empty(rows, dtype=torch.float32, device=dev))
+    tok, lse, logq = out
+    _check(_lib().ldr_sample_noalloc(_ptr(logits), rows, V, float(temperature), int(top_k),
+                                     int(seed), int(step), _ptr(tok), _ptr(lse), _ptr(logq),
+                                     _stream(stream)), "ldr_sample_noalloc")
     return out
 
 

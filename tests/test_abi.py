@@ -117,7 +117,7 @@ def test_host_validation_needs_no_gpu(L):
     lib.ldr_views_destroy(None)
     assert lib.ldr_sample_workspace_bytes(0, 10) == 0
     assert lib.ldr_sample_workspace_bytes(256, 151936) > 0
-    for code in (0, -1, -2, -3, -4):
+    for code in (0, -1, -2, -3, -4, -5):
         assert lib.ldr_strerror(code)
 
 
