@@ -64,10 +64,85 @@ def test_rope_is_a_complex_rotation_of_half_pairs():
     np.testing.assert_array_equal(Dr.rope(x, np.zeros(6), base), x)   # position 0: identity
 
 
-def test_rope_base_ntk():
+def _freqs(base, d):
+    """Rotation frequency of every half pair, read off the oracle's rope: the
+    angle of pair e at position 1 (a unit vector rotated once)."""
+    x = np.zeros((1, 1, d))
+    x[..., :d // 2] = 1.0
+    y = Dr.rope(x, np.array([1]), base)
+    return np.arctan2(y[0, 0, d // 2:], y[0, 0, :d // 2])
+
+
+@pytest.mark.parametrize("d,alpha", [(4, 2.0), (64, 4.0), (128, 4.0), (128, 8.0)])
+def test_rope_base_ntk_scales_the_lowest_frequency_by_alpha(d, alpha):
+    """Fixed NTK scaling by alpha stretches the wavelength of the lowest
+    rotary frequency by exactly alpha and leaves the highest (pair 0, one
+    radian per position) unchanged, with the frequencies between still
+    geometric; plain theta at alpha = 1."""
+    s = MICRO.replace(head_dim=d, rope_theta=1e6, ntk_alpha=alpha)
+    f1 = _freqs(Dr.rope_base(s.replace(ntk_alpha=1.0)), d)
+    fa = _freqs(Dr.rope_base(s), d)
+    assert Dr.rope_base(s.replace(ntk_alpha=1.0)) == 1e6
+    assert fa[0] == pytest.approx(1.0, rel=1e-15) and f1[0] == pytest.approx(1.0, rel=1e-15)
+    assert f1[-1] / fa[-1] == pytest.approx(alpha, rel=1e-9)
+    np.testing.assert_allclose(fa[1:] / fa[:-1], fa[1] / fa[0], rtol=1e-9)
+
+
+def test_boundary_fusion_closed_forms():
+    """c = RMSNorm(W_fc [h_0; ...; h_{L_b-1}]): zero boundary states give
+    c = 0; a unit entry k of feature layer l picks column l * hidden + k of
+    W_fc (layer-major concatenation, [out][in] weights); a hand-computed
+    2-wide case."""
     s = MICRO
-    assert Dr.rope_base(s) == pytest.approx(1e4 * 2.0 ** (4 / 2))
-    assert Dr.rope_base(s.replace(ntk_alpha=1.0)) == 1e4
+    Wt = rand_weights(s, 31)
+    h = np.zeros((s.n_feat_layers, s.hidden))
+    assert np.array_equal(Dr.boundary_fusion(s, Wt, h), np.zeros(s.hidden))
+    for l, k in ((0, 0), (1, 5), (2, 11)):
+        h = np.zeros((s.n_feat_layers, s.hidden))
+        h[l, k] = 1.0
+        col = Wt["fc_w"][:, l * s.hidden + k]
+        ref = col / np.sqrt(np.mean(col ** 2) + s.rms_eps) * Wt["fc_norm"]
+        np.testing.assert_allclose(Dr.boundary_fusion(s, Wt, h), ref, rtol=1e-14)
+    s2 = MICRO.replace(hidden=2, n_feat_layers=1, rms_eps=0.0)
+    W2 = {"fc_w": np.array([[3.0, 0.0], [0.0, 4.0]]), "fc_norm": np.array([1.0, 2.0])}
+    c = Dr.boundary_fusion(s2, W2, np.array([[1.0, 1.0]]))   # y = (3, 4), rms = sqrt(12.5)
+    np.testing.assert_allclose(c, [3 / math.sqrt(12.5), 8 / math.sqrt(12.5)], rtol=1e-15)
+
+
+def test_slot_init_closed_forms():
+    """x_i = E[u_i] + P_i + c: slot 0 holds the anchor's embedding, slots
+    1 .. B-1 the mask embedding; with E = 0 and c = 0 the slots are the
+    positional encodings alone."""
+    s = MICRO
+    Wt = rand_weights(s, 32)
+    zero_c = np.zeros(s.hidden)
+    W0 = dict(Wt)
+    W0["pos_emb"] = np.zeros_like(Wt["pos_emb"])
+    x = Dr.slot_init(s, W0, zero_c, 9)
+    assert np.array_equal(x[0], Wt["embed"][9])
+    assert all(np.array_equal(x[i], Wt["mask_emb"]) for i in range(1, s.block))
+    W1 = dict(Wt)
+    W1["embed"] = np.zeros_like(Wt["embed"])
+    W1["mask_emb"] = np.zeros_like(Wt["mask_emb"])
+    assert np.array_equal(Dr.slot_init(s, W1, zero_c, 3), Wt["pos_emb"])
+    c = np.arange(s.hidden, dtype=np.float64)
+    assert np.array_equal(Dr.slot_init(s, W1, c, 3), Wt["pos_emb"] + c)
+
+
+def test_positional_slots_reach_the_head_through_pass_through_layers():
+    """Zero boundary states (c = 0), zero embeddings and layers whose output
+    maps are zero: the logits are RMSNorm(P_i) W_lm^T, one row per slot."""
+    s = MICRO
+    Wt = rand_weights(s, 33)
+    Wt["embed"] = np.zeros_like(Wt["embed"])
+    Wt["mask_emb"] = np.zeros_like(Wt["mask_emb"])
+    for L in Wt["layers"]:
+        L["wo"][:] = 0
+        L["w_down"][:] = 0
+    st, G = rand_state(s, 6, 34)
+    st.h[:] = 0.0
+    ref = Dr.rmsnorm(Wt["pos_emb"], Wt["final_norm"], s.rms_eps) @ Wt["lm_head"].T
+    np.testing.assert_allclose(Dr.forward(s, Wt, st, G, 4), ref, rtol=1e-13)
 
 
 def test_block_attention_is_sdpa_over_the_concatenation():

@@ -178,14 +178,25 @@ def test_markov_correction_closed_form():
     W = np.random.default_rng(2).normal(size=(V, r)).astype(np.float32)
     c = Sm.correction(E, W, [0, 5, 11])
     assert np.array_equal(c, W[:, [0, 1, 3]].T)
-    # and an explicit fp32 chain for a dense case, summed by hand in order
-    E2 = np.random.default_rng(3).normal(size=(V, r)).astype(np.float32)
-    c2 = Sm.correction(E2, W, [7])[0]
-    for v in range(V):
-        acc = np.float32(0)
-        for k in range(r):
-            acc = np.float32(acc + np.float32(W[v, k] * E2[7, k]))
-        assert c2[v] == acc
+
+
+
+def test_markov_correction_is_exact_on_integer_values():
+    """Small integers make every fp32 product and partial sum exact, so the
+    ordered fp32 chain must equal the float64 product W_c E_c(y) exactly
+    (a dropped term, a transposed operand or a wrong row would not)."""
+    V, r = 37, 24
+    g = np.random.default_rng(4)
+    E = g.integers(-8, 9, size=(V, r)).astype(np.float32)
+    W = g.integers(-8, 9, size=(V, r)).astype(np.float32)
+    y = np.array([0, 5, 36, 17])
+    c = Sm.correction(E, W, y)
+    ref = E.astype(np.float64)[y] @ W.astype(np.float64).T      # [n][V]
+    assert c.dtype == np.float32 and np.array_equal(c.astype(np.float64), ref)
+    # the rank index runs over all r terms: a correction from E row y only
+    E1 = np.zeros_like(E)
+    E1[5] = E[5]
+    assert np.array_equal(Sm.correction(E1, W, [5])[0], c[1])
 
 
 def test_markov_greedy_follows_the_predecessor():

@@ -226,3 +226,53 @@ def test_pooled_state_bytes_are_fixed():
             + s.n_feat_layers * s.hidden * el)
     assert V.state_bytes(s) == want
     assert V.state_bytes(synth.TINY_POOLED) < V.state_bytes(synth.TINY_POOLED.replace(window=128))
+
+
+def test_nan_in_a_key_row_stays_in_its_group_and_layer():
+    """A NaN entry in the key of row p, layer j, group g: the window slot
+    p mod W of (j, g) holds it until row p + W replaces it; the summary of
+    the query heads reading group g in layer j becomes NaN and stays NaN (Eq. 5
+    covers every row ever ingested); every other layer, group and head stays
+    finite, and the boundary is untouched."""
+    G = Gq()
+    K, Vv = rows(30, 41)
+    p, j, g = 5, 1, 0
+    K[p, j, g, 3] = np.nan
+    st = ingest(G, K[:9], Vv[:9], [4, 5])
+    rep = S.n_q_heads // S.n_kv_heads
+    heads = list(range(g * rep, (g + 1) * rep))
+    assert np.isnan(st.Kw[j, g, p % S.window]).any()
+    bad = np.zeros(st.Kw.shape, dtype=bool)
+    bad[j, g, p % S.window] = True
+    assert np.all(np.isfinite(st.Kw[~bad])) and np.all(np.isfinite(st.Vw))
+    for jj in range(S.n_layers):
+        for h in range(S.n_q_heads):
+            nan = jj == j and h in heads
+            assert np.isnan(st.eta[jj, h]).all() == nan
+            assert np.isnan(st.M[jj, h]).all() == nan
+            if not nan:
+                assert np.all(np.isfinite(st.eta[jj, h])) and np.all(np.isfinite(st.M[jj, h]))
+    assert np.all(np.isfinite(st.h))
+    st2 = V.update(S, st, G, K[9:9 + S.window], Vv[9:9 + S.window],
+                   np.zeros((S.n_feat_layers, S.hidden)))        # row p leaves the window
+    assert np.all(np.isfinite(st2.Kw))
+    assert np.isnan(st2.eta[j, heads]).all() and np.isnan(st2.M[j, heads]).all()
+
+
+def test_inf_in_a_value_row_leaves_the_normalisers_finite():
+    """eta depends on the keys alone (Eq. 10): an infinite value entry makes
+    the summary values M of the heads reading it non-finite in that one
+    coordinate, while every eta stays finite and equal to the clean run's."""
+    G = Gq()
+    K, Vv = rows(12, 43)
+    clean = ingest(G, K, Vv, [7, 5])
+    Vv[2, 0, 1, 6] = np.inf
+    st = ingest(G, K, Vv, [7, 5])
+    rep = S.n_q_heads // S.n_kv_heads
+    np.testing.assert_array_equal(st.eta, clean.eta)
+    for h in range(S.n_q_heads):
+        hit = h // rep == 1
+        assert (~np.isfinite(st.M[0, h, :, 6])).all() == hit
+        other = np.delete(st.M[0, h], 6, axis=1) if hit else st.M[0, h]
+        assert np.all(np.isfinite(other))
+    np.testing.assert_array_equal(st.M[1], clean.M[1])
