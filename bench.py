@@ -116,6 +116,27 @@ def launch_costs(s, batch):
     return c
 
 
+def algorithmic_step_bytes(s, batch):
+    """Algorithmic HBM bytes of one draft step + sampling: every weight read
+    once (boundary fusion, the D layers' QKV / O / gate-up / down, the
+    vocabulary head), the views the attention reads (window K/V of every
+    layer, the summary values M and queries G), and the fp32 logits written
+    once. 3.603 GB at the Qwen3-8B shape, batch 16 (3.604 GB in round figures)."""
+    el = 2 if s.dtype == "bf16" else 4
+    H, d = s.hidden, s.head_dim
+    drop = getattr(s, "drop_views", 0)
+    pool = 0 if drop & 2 else (getattr(s, "pool_slots", 0) or 0)
+    nw = (0 if drop & 1 else s.window) + 2 * pool
+    nr = 0 if (drop & 2 or pool) else s.summary
+    layer_w = (s.qkv_out * H + H * s.n_q_heads * d + 2 * s.mlp * H + H * s.mlp) * el
+    fc_w = 0 if drop & 4 else H * s.n_feat_layers * H * el
+    weights = s.n_layers * layer_w + fc_w + s.vocab * H * el
+    views = s.n_layers * (batch * 2 * s.n_kv_heads * nw * d * el +
+                          batch * s.n_q_heads * nr * d * 4 + s.n_q_heads * nr * d * el)
+    logits = batch * s.block * s.vocab * 4
+    return weights + views + logits
+
+
 def update_bytes(s, batch, n):
     el = 2 if s.dtype == "bf16" else 4
     rows = batch * n * s.n_layers * s.n_kv_heads * s.head_dim * el * 2     # K/V in
@@ -133,7 +154,7 @@ class Rig:
 
     def __init__(self, torch, ldr, synth, shape, batch, prefix, chunk=4096, reuse_chunk=False,
                  tiled_head=True, markov_rank=0, verify=False, fused_head=False,
-                 keep_logits=True, temperature=1.0):
+                 keep_logits=True, temperature=1.0, loop_steps=0):
         self.torch, self.ldr, self.s, self.batch = torch, ldr, shape, batch
         self.temperature = temperature
         dev = "cuda"
@@ -158,7 +179,12 @@ class Rig:
                 self.views.update(torch.full((batch,), K.shape[1], dtype=torch.int32,
                                              device=dev), K, V, h)
         self.n_new = shape.block + 1
-        self.rows = [synth.decode_rows(shape, batch, self.n_new, st, device=dev) for st in range(4)]
+        # A drafting loop (configuration 3) ingests distinct rows every step and
+        # drafts from the previous step's last sampled token; other workloads
+        # cycle through four decode row sets with fixed anchors.
+        self.loop = loop_steps > 0
+        self.rows = [synth.decode_rows(shape, batch, self.n_new, st, device=dev)
+                     for st in range(loop_steps if self.loop else 4)]
         self.n = torch.full((batch,), self.n_new, dtype=torch.int32, device=dev)
         self.anchor = synth.make_anchors(shape, batch, device=dev)
         self.logits = torch.empty(batch, shape.block, shape.vocab, dtype=torch.float32,
@@ -234,6 +260,18 @@ class Rig:
                             out=self.out, workspace=self.sws)
         if self.verify:
             self.verify_round(i, temperature)
+        elif self.loop:   # the next anchor is this step's sampled y_B
+            B = self.s.block
+            self.anchor.copy_(self.out[0].view(self.batch, B)[:, B - 1])
+
+    def snapshot(self):
+        """Views arena, positions and anchors (restored after warm-up steps of a loop)."""
+        return (self.views.arena.clone(), self.views.pos.clone(), self.anchor.clone())
+
+    def restore(self, snap):
+        self.views.arena.copy_(snap[0])
+        self.views.pos.copy_(snap[1])
+        self.anchor.copy_(snap[2])
 
     def verify_round(self, i, temperature=None):
         """ldr_verify of the step's draft; writes n (the next update's row
@@ -361,11 +399,31 @@ def percentile(xs, q):
 
 # ---- CPU oracle baseline ----------------------------------------------------------------
 
+def host_info():
+    """Host cores and CPU model of the machine the oracle runs on."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count() or 1
+    return {"nproc": usable, "cpu_count": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline(torch, synth, rig, n_seqs):
     """The fp64 oracle on a bounded sample of the same step: views update of 17
     rows + draft forward + sampling of the B positions, for n_seqs sequences
     over views built from a 512-row prefix (the oracle's step cost does not
-    depend on the prefix length once the window is full)."""
+    depend on the prefix length once the window is full: `prefix_1k_vs_32k`
+    times one sequence's step at both lengths). Also times the views update
+    alone and the whole Tiny workload (prefill of 2048 rows + one step)."""
     import numpy as np
     from oracle import draft as OD
     from oracle import sample as OS
@@ -385,19 +443,63 @@ def cpu_baseline(torch, synth, rig, n_seqs):
     for b in range(n_seqs):
         states.append(OV.update(s, OV.empty(s), G64, synth.to_f64(K[b]), synth.to_f64(V[b]),
                                 synth.to_f64(h[b])))
+    upd, fwd = [], []
     t0 = time.perf_counter()
     for b in range(n_seqs):
+        ta = time.perf_counter()
         st = OV.update(s, states[b], G64, synth.to_f64(Kd[b]), synth.to_f64(Vd[b]),
                        synth.to_f64(hd[b]))
+        tb = time.perf_counter()
         z = OD.forward(s, Wt, st, G64, int(anchor[b]))
         OS.sample(z.astype(np.float32), rig.temperature, 0, 5, 0,
                   rows=np.arange(b * s.block, (b + 1) * s.block))
+        upd.append(tb - ta)
+        fwd.append(time.perf_counter() - tb)
     el = time.perf_counter() - t0
+
+    def one_step(st, b=0):
+        t = time.perf_counter()
+        st2 = OV.update(s, st, G64, synth.to_f64(Kd[b]), synth.to_f64(Vd[b]),
+                        synth.to_f64(hd[b]))
+        z = OD.forward(s, Wt, st2, G64, int(anchor[b]))
+        OS.sample(z.astype(np.float32), rig.temperature, 0, 5, 0, rows=np.arange(s.block))
+        return time.perf_counter() - t
+
+    # the step at 1K and 32K rows of prefix: one 1024-row chunk ingested repeatedly
+    Kc, Vc, hc = synth.make_rows(s, 1, 1024, 78) + (synth.make_h(s, 1, 78),)
+    Kc, Vc, hc = synth.to_f64(Kc[0]), synth.to_f64(Vc[0]), synth.to_f64(hc[0])
+    st = OV.empty(s)
+    by_prefix = {}
+    for t in range(1024, 32768 + 1, 1024):
+        st = OV.update(s, st, G64, Kc, Vc, hc)
+        if t in (1024, 32768):
+            by_prefix[str(t)] = statistics.median(one_step(st) for _ in range(3))
     del Wt
+    # the whole Tiny workload: prefill 2048 rows, one update, draft, greedy sample
+    tw = synth.WORKLOADS["tiny-b1-t2048"]
+    ts = tw.shape
+    tiny_w = synth.weights_f64(synth.make_weights(ts, device="cpu"))
+    tiny_G = synth.to_f64(synth.make_G(ts, device="cpu"))
+    t0 = time.perf_counter()
+    tst = OV.empty(ts)
+    for Kp, Vp, hp in synth.prefix_chunks(ts, 1, tw.prefix, 512, device="cpu"):
+        tst = OV.update(ts, tst, tiny_G, synth.to_f64(Kp[0]), synth.to_f64(Vp[0]),
+                        synth.to_f64(hp[0]))
+    t1 = time.perf_counter()
+    Kt, Vt, ht = synth.decode_rows(ts, 1, ts.block + 1, 0)
+    tst = OV.update(ts, tst, tiny_G, synth.to_f64(Kt[0]), synth.to_f64(Vt[0]), synth.to_f64(ht[0]))
+    zt = OD.forward(ts, tiny_w, tst, tiny_G, 1)
+    OS.sample(zt.astype(np.float32), tw.temperature, 0, 5, 0)
+    t2 = time.perf_counter()
     return {"value": n_seqs * s.block / el, "unit": "tokens/s", "cores": cores, "kind": "oracle",
             "sample": f"{n_seqs} sequences of the workload's step: views update (17 rows) + fp64 "
                       f"draft forward + sampling of {s.block} positions over {s.vocab} tokens, "
-                      f"{el:.2f} s (BLAS threads {cores}; elementwise numpy single-threaded)"}
+                      f"{el:.2f} s (BLAS threads {cores}; elementwise numpy single-threaded)",
+            "host": host_info(),
+            "per_sequence_s": {"views_update": statistics.median(upd),
+                               "draft_and_sample": statistics.median(fwd)},
+            "prefix_1k_vs_32k_step_s": by_prefix,
+            "tiny_b1_t2048_s": {"prefill": t1 - t0, "step": t2 - t1}}
 
 
 # ---- HBM traffic from rocprofv3 counters -----------------------------------------------------
@@ -571,6 +673,28 @@ def traffic_for(kind):
     return e.get("hbm_bytes_per_launch") if e else None
 
 
+def gemm_mfma_from_counters(s, batch, kinds):
+    """bf16 flops of all GEMMs of one step over their summed dispatch time,
+    from profiles/mfma.json (rocprofv3 counter pass), or None when it is
+    absent or was taken on other library sources."""
+    try:
+        with open(os.path.join(ROOT, "profiles", "mfma.json")) as f:
+            m = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if m.get("sources_sha256") != source_digest():
+        return None
+    flops = us = 0.0
+    for k, e in m.get("kinds", {}).items():
+        n = sum(1 for x in kinds if x == k)
+        flops += e["bf16_flops_per_launch"] * n
+        us += e["us_per_launch_under_counters"] * n
+    if us <= 0:
+        return None
+    tf = flops / (us * 1e-6) / 1e12
+    return {"tflops": tf, "frac": tf / BF16_PEAK_TFLOPS, "source": "profiles/mfma.json"}
+
+
 # ---- main --------------------------------------------------------------------------------
 
 def main():
@@ -611,40 +735,49 @@ def main():
     s, batch = wl.shape, wl.batch
     if args.drop_views:
         s = s.replace(drop_views=args.drop_views)
+    loop = wl.loop_steps if not (args.verify or args.markov_rank) else 0
+    if loop:
+        args.steps = loop       # the loop's own length: every step is timed
     rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head,
               markov_rank=args.markov_rank, verify=args.verify, fused_head=args.fused_head,
-              keep_logits=not args.no_logits, temperature=args.temperature)
+              keep_logits=not args.no_logits, temperature=args.temperature, loop_steps=loop)
     ev = ldr.HipEvents()
     costs = launch_costs(s, batch)
     # which launch kind dominates the step (events around every launch, outside the timed run)
+    snap = rig.snapshot() if loop else None
     br = kind_breakdown(torch, ldr, rig, ev)
-    gemm_kinds = [k for k in br if k.endswith("gemm") or k == "lm_head"]
     dom = max(br, key=lambda k: br[k])
+    if loop:   # warm-up steps on the same state, then back to the loop's start
+        for i in range(args.warmup):
+            rig.step(i)
+        torch.cuda.synchronize()
+        rig.restore(snap)
+        args_warmup_run = 0
+    else:
+        args_warmup_run = args.warmup
     if rig.fused_head:
         # ldr_draft_step_sample records no per-launch events: the timed run has
         # events at step boundaries only, and the dominant kernel (a draft-layer
         # launch, the same kernel on both paths) is timed over as many steps of
         # the bracketed separate path right after it
-        wall, per_step, _ = time_steps(torch, rig, args.steps, args.warmup, ev=ev)
+        wall, per_step, _ = time_steps(torch, rig, args.steps, args_warmup_run, ev=ev)
         rig.fused_head = False
         _, _, kern = time_steps(torch, rig, args.steps, 0, ev=ev, bracket=dom)
         rig.fused_head = True
     else:
-        wall, per_step, kern = time_steps(torch, rig, args.steps, args.warmup, ev=ev,
+        wall, per_step, kern = time_steps(torch, rig, args.steps, args_warmup_run, ev=ev,
                                           bracket=dom)
     torch.cuda.synchronize()
+    t_final = int(rig.views.pos.min().item())
     ms = wall / args.steps * 1e3
     tokens = batch * s.block * args.steps
     launches_of_dom = sum(1 for k in rig.kinds if k == dom)
     dom_ms = statistics.mean(kern)
     dom_bytes = costs[dom][0]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    # the separate sampler reads the fp32 logits once; the fused head reads none
-    step_bytes = sum(costs[k][0] for k in rig.kinds) + update_bytes(s, batch, s.block + 1) + \
-        (0 if rig.fused_head else batch * s.block * s.vocab * 4)
+    step_bytes = algorithmic_step_bytes(s, batch)
+    upd_bytes = update_bytes(s, batch, s.block + 1)
     step_flops = sum(costs[k][1] for k in rig.kinds)
-    gemm_ms = sum(br[k] for k in gemm_kinds)
-    gemm_flops = sum(costs[k][1] * sum(1 for x in rig.kinds if x == k) for k in gemm_kinds)
     out = {
         "metric": METRIC, "value": tokens / wall, "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
@@ -668,13 +801,18 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic_for(dom),
                      "bytes_per_launch": dom_bytes, "us_per_launch": dom_ms * 1e3,
                      "launches_per_step": launches_of_dom, "launches_timed": len(kern)},
-        "step_roofline": {"algorithmic_bytes": step_bytes, "flops": step_flops,
-                          "hbm_frac": step_bytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                          "gemm_tflops": gemm_flops / (gemm_ms * 1e-3) / 1e12,
-                          "gemm_mfma_frac": gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS},
-        "breakdown_us": {k: v * 1e3 for k, v in sorted(br.items(), key=lambda kv: -kv[1])},
+        "step_roofline": {"algorithmic_bytes": step_bytes, "update_bytes": upd_bytes,
+                          "flops": step_flops,
+                          "hbm_frac": (step_bytes + upd_bytes) / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                          "gemm_mfma": gemm_mfma_from_counters(s, batch, rig.kinds)},
         "state_bytes_per_seq": ldr.state_bytes(s),
     }
+    if loop:
+        out["config"]["loop_steps"] = loop
+        out["config"]["anchor"] = "the previous step's sampled y_B"
+        out["config"]["prefix_after_loop"] = t_final
+        out["us_per_step"]["first"] = per_step[0] * 1e3
+        out["us_per_step"]["last"] = per_step[-1] * 1e3
     out["stream_bw"] = stream_bandwidth(torch)
     if rig.verify:
         out["config"]["rows_per_update"] = "r + 1 from ldr_verify"

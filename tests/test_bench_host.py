@@ -53,6 +53,28 @@ def test_dominant_kernel_bytes():
     assert b == s.vocab * s.hidden * 2 + M * s.hidden * 2 + M * s.vocab * 4
 
 
+def test_step_bytes_are_the_weights_views_and_logits():
+    """Algorithmic bytes of one draft step + sampling at the Qwen3-8B shape,
+    batch 16: weights 3.342 GB (layers 1.929, boundary fusion 0.168, head
+    1.245), views 0.106 GB (window K/V, summary M and G) and the fp32 logits
+    0.156 GB: 3.604 GB, the figure the step roofline divides by."""
+    s, batch = synth.QWEN3_8B, 16
+    H = s.hidden
+    layers = 5 * (6144 * H + H * 4096 + 2 * 12288 * H + H * 12288) * 2
+    assert layers == 1_929_379_840
+    fc = H * 5 * H * 2
+    head = 151936 * H * 2
+    views = 5 * (16 * 2 * 8 * 256 * 128 * 2 + 16 * 32 * 16 * 128 * 4 + 32 * 16 * 128 * 2)
+    logits = 16 * 16 * 151936 * 4
+    got = bench.algorithmic_step_bytes(s, batch)
+    assert got == layers + fc + head + views + logits
+    assert abs(got / 1e9 - 3.604) < 0.002        # 3.603 GB
+    # a dropped boundary has no fusion weight; a dropped window no window rows
+    assert bench.algorithmic_step_bytes(s.replace(drop_views=4), batch) == got - fc
+    assert bench.algorithmic_step_bytes(s.replace(drop_views=1), batch) == \
+        got - 5 * 16 * 2 * 8 * 256 * 128 * 2
+
+
 def _write_csv(path, rows, extra=()):
     cols = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value",
             "Start_Timestamp", "End_Timestamp"] + list(extra)
