@@ -137,3 +137,29 @@ def lazy_weights_f64(w):
     out["lm_head"] = LazyRows(w["lm_head"])
     out["layers"] = LazyLayers(w["layers"])
     return out
+
+
+def residual_decision(d, bonus_tok, rel_err, key_abs=1e-5):
+    """(clean, valid tokens) of a residual draw (Eq. 2) from the oracle's
+    float64 stop row d = {p, q, w, g}, when the kernel's p_v and q_v are each
+    within rel_err (relative) of the oracle's: token v's key log w_v + g_v
+    then lies in [log(w_v - e_v), log(w_v + e_v)] + g_v, e_v = rel_err
+    max(p_v, q_v). Clean: the oracle's token has a lower bound above every
+    other token's upper bound and some w_v exceeds e_v (so the kernel's
+    residual cannot be empty); the kernel must then emit the oracle's token.
+    Otherwise the valid tokens are those whose upper bound reaches the best
+    lower bound, plus the bonus-rule draw when every w_v is within e_v."""
+    p, q, w, g = d["p"], d["q"], d["w"], d["g"]
+    e = rel_err * np.maximum(p, q)
+    with np.errstate(divide="ignore"):
+        lo = np.where(w > e, np.log(np.maximum(w - e, 1e-300)), -np.inf) + g - key_abs
+        hi = np.where(w + e > 0, np.log(w + e), -np.inf) + g + key_abs
+    can_be_empty = not np.any(w > e)
+    best_lo = lo.max()
+    valid = set(np.flatnonzero(hi >= best_lo).tolist()) if np.isfinite(best_lo) else \
+        set(np.flatnonzero(np.isfinite(hi)).tolist())
+    if can_be_empty:
+        valid.add(int(bonus_tok))
+    t = int(np.argmax(lo))
+    clean = (not can_be_empty) and lo[t] > np.max(np.delete(hi, t))
+    return clean, valid

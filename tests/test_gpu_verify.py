@@ -26,6 +26,7 @@ import pytest
 import torch
 
 import synth
+from gpu_common import residual_decision
 from oracle import sample as OS
 
 pytestmark = pytest.mark.gpu
@@ -46,23 +47,7 @@ def _run(ldr, y, z, P, T, seed, step, top_k=0):
 
 
 def _residual_decision(d, bonus_tok):
-    """(clean, valid tokens) of a residual draw from the oracle's float64
-    stop row d = {p, q, w, g}: clean when the GPU must reproduce the oracle's
-    token, else the set of tokens a fp32 evaluation may legitimately emit."""
-    p, q, w, g = d["p"], d["q"], d["w"], d["g"]
-    e = REL_ERR * np.maximum(p, q)
-    with np.errstate(divide="ignore"):
-        lo = np.where(w > e, np.log(np.maximum(w - e, 1e-300)), -np.inf) + g - KEY_ABS
-        hi = np.where(w + e > 0, np.log(w + e), -np.inf) + g + KEY_ABS
-    can_be_empty = not np.any(w > e)
-    best_lo = lo.max()
-    valid = set(np.flatnonzero(hi >= best_lo).tolist()) if np.isfinite(best_lo) else \
-        set(np.flatnonzero(np.isfinite(hi)).tolist())
-    if can_be_empty:
-        valid.add(int(bonus_tok))
-    t = int(np.argmax(lo))
-    clean = (not can_be_empty) and lo[t] > np.max(np.delete(hi, t))
-    return clean, valid
+    return residual_decision(d, bonus_tok, REL_ERR, KEY_ABS)
 
 
 def _compare(acc, tok, n_new, y, z, P, T, seed, step, max_ties=1, top_k=0):
