@@ -79,7 +79,7 @@ Layout make_layout(const Shape& s) {
 
 // Workspace regions of one draft step for `batch` sequences.
 struct WsPlan {
-  size_t part, x, nrm, qkvb, o, act, rope, nrmt, bytes;
+  size_t part, x, nrm, qkvb, o, act, rope, nrmt, nrmf, bytes;
   GemmPlan fc, qkv, wo, gu, down, lm;
 };
 
@@ -106,6 +106,9 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   w.rope = off; off = align_up(off + (size_t)2 * M * (s.d / 2) * 4);
   // final normalised rows in the tiled layout, for a tiled vocabulary head
   w.nrmt = off; off = align_up(off + (s.dtype == LDR_BF16 ? tiled_elems(M, s.hidden) * 2 : 0));
+  // the SwiGLU GEMM's rows in the fragment layout (rows padded to 16)
+  w.nrmf = off;
+  off = align_up(off + (gemm_plan_frag(w.gu) ? (size_t)(M + 15) / 16 * 16 * s.hidden * 2 : 0));
   w.bytes = off;
   return w;
 }
@@ -399,10 +402,14 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         e = launch_gemm(s.dtype, EPI_STORE, ws.wo, g, st);
         break;
       case LDR_LAUNCH_POST_NORM:
-        e = launch_resid_norm(s, M, p, ws.wo.splits, L.post_norm, st);
+        e = gemm_plan_frag(ws.gu)
+                ? launch_resid_norm(s, M, p, ws.wo.splits, L.post_norm, st, base + ws.nrmf,
+                                    NRM_FRAG)
+                : launch_resid_norm(s, M, p, ws.wo.splits, L.post_norm, st);
         break;
       case LDR_LAUNCH_GATE_UP_GEMM:
-        g.A = p.nrm; g.lda = s.hidden; g.W = L.w_gate_up; g.ldw = s.hidden; g.out = p.act;
+        g.A = gemm_plan_frag(ws.gu) ? static_cast<const void*>(base + ws.nrmf) : p.nrm;
+        g.lda = s.hidden; g.W = L.w_gate_up; g.ldw = s.hidden; g.out = p.act;
         g.ldo = s.mlp; g.split_stride = 0; g.M = M; g.N = 2 * s.mlp; g.K = s.hidden;
         g.splits = 1; g.mlp = s.mlp;
         e = launch_gemm(s.dtype, EPI_SWIGLU, ws.gu, g, st);

@@ -145,7 +145,7 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
 struct ResidArgs {
   const float* part; long split_stride; int splits;
   float* x; void* nrm; const void* gain; int hidden; float eps;
-  int tiled;   // nrm in the 256 x 32 tiled layout of ldr_tile_matrix (hidden % 32 == 0)
+  int layout;  // nrm layout: NRM_ROWS, NRM_TILED or NRM_FRAG (hidden % 32 == 0)
 };
 
 template <typename T, int SPLITS>
@@ -172,13 +172,19 @@ __global__ void __launch_bounds__(kThreads) resid_norm_kernel(ResidArgs a) {
   }
   const float inv = rsqrtf(block_sum(ss, red) / H + a.eps);
   T* out = static_cast<T*>(a.nrm);
-  const long rbase = a.tiled ? (m >> 8) * (long)(H >> 5) * 8192 + (m & 255) * 32 : m * H;
+  const long rbase = a.layout == NRM_TILED ? (m >> 8) * (long)(H >> 5) * 8192 + (m & 255) * 32
+                   : a.layout == NRM_FRAG ? (m >> 4) * (long)(H >> 5) * 512 + (m & 15) * 8
+                                          : m * H;
 #pragma unroll
   for (int ch = 0; ch < kChunks; ++ch) {
     const int k = (threadIdx.x + ch * kThreads) * 4;
     if (k < H) {
       *reinterpret_cast<float4*>(x + k) = v[ch];
-      const long o = a.tiled ? rbase + (long)(k >> 5) * 8192 + (k & 31) : rbase + k;
+      // four consecutive k stay inside one 16-byte chunk of either tiled layout
+      const long o = a.layout == NRM_TILED ? rbase + (long)(k >> 5) * 8192 + (k & 31)
+                   : a.layout == NRM_FRAG ? rbase + (long)(k >> 5) * 512 + ((k >> 3) & 3) * 128 +
+                                                (k & 7)
+                                          : rbase + k;
       Vec4<T>::store(out + o, f4scale(v[ch], inv, g[ch]));
     }
   }
@@ -373,11 +379,11 @@ hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int f
 }
 
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
-                             const void* gain, hipStream_t st, void* tiled_out) {
+                             const void* gain, hipStream_t st, void* tiled_out, int layout) {
   ResidArgs a;
   a.part = p.part; a.split_stride = (long)M * s.hidden; a.splits = splits;
   a.x = p.x; a.nrm = tiled_out ? tiled_out : p.nrm; a.gain = gain; a.hidden = s.hidden;
-  a.eps = s.eps; a.tiled = tiled_out != nullptr;
+  a.eps = s.eps; a.layout = tiled_out ? layout : NRM_ROWS;
   return s.dtype == LDR_BF16 ? launch_split<uint16_t, ResidLaunch>(splits, dim3(M), a, st)
                             : launch_split<float, ResidLaunch>(splits, dim3(M), a, st);
 }

@@ -269,6 +269,174 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
   }
 }
 
+template <int N> __device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+__device__ inline void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14)); }
+__device__ inline void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+__device__ inline void group_barrier() {
+  sched_fence();
+  __builtin_amdgcn_s_barrier();
+  sched_fence();
+}
+
+#define LDR_GP(p) ((__attribute__((address_space(1))) void*)(p))
+#define LDR_LP(p) ((__attribute__((address_space(3))) void*)(p))
+
+// ---------------------------------------------------------------------------
+// GEMM with the activation rows in the fragment layout (the SwiGLU GEMM).
+//
+// In the fragment layout of a [M][K] bf16 matrix (rows padded to 16), the
+// 16 x 32 block of rows 16 r .. and columns 32 c .. is 1 KB at element
+// (r * (K / 32) + c) * 512, its 16-byte chunk l holding row 16 r + (l & 15),
+// columns 32 c + (l >> 4) * 8 .. + 8: the A operand of v_mfma_f32_16x16x32_bf16
+// for lane l, so a wave loads an A fragment from global memory with one fully
+// coalesced 16-byte load per lane. The residual norm before this GEMM writes
+// its rows in that layout.
+//
+// Eight waves each own 32 rows (private: their A fragments go straight to
+// registers, RA K steps ahead) and all BN columns; the BN weight rows of a
+// 64-deep K step reach LDS by DMA (global_load_lds, 8 rows of 128 bytes per
+// instruction, 16-byte chunk c of row r at c ^ (r & 7)) in a ring of NB
+// stages issued NB - 1 steps ahead. Against the staged kernel above this
+// removes the activation tiles' LDS stores and reads (32 KB each per step at
+// 256 rows), which bounded it.
+// Ordering: before step kt every wave waits until at most the last RA - 1
+// steps' loads are pending (vmcnt counts its DMA and A loads in issue order)
+// and its own LDS reads are done, then a barrier: stage kt is whole in LDS,
+// and the buffer refilled at this step (read at step kt - 1) has no reader left.
+constexpr int FNB = 6, FRA = 3;   // W stages in LDS, A stages in registers
+
+__device__ inline long frag_elem(long m, int k, int K) {
+  return ((m >> 4) * (K >> 5) + (k >> 5)) * 512 + ((((k >> 3) & 3) << 4) | (m & 15)) * 8 +
+         (k & 7);
+}
+
+template <int N> __device__ inline void wait_vm_lgkm0() {
+  static_assert(N >= 0 && N < 64, "vmcnt");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
+template <int MTW, int NTW, int EPI>
+__global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
+  constexpr int WM = 8, WN = 1, NW = WM * WN, TM = MTW * 16, TN = NTW * 16;
+  constexpr int BM = WM * TM, BN = WN * TN;
+  constexpr int STAGE = BN * 128;             // W bytes per stage (BN rows x 64 k)
+  constexpr int GROUPS = BN / 8;              // DMA instructions per stage (8 rows each)
+  constexpr int GPW = (GROUPS + NW - 1) / NW;
+  constexpr int AV = MTW * 2;                 // A loads per stage per lane
+  constexpr int PER_STEP = GPW + AV;          // VMEM instructions per step and wave
+  static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
+  __shared__ __attribute__((aligned(1024))) uint8_t Wsm[FNB * STAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave, wn = 0;
+  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, z = blockIdx.z;
+  const int kper = a.K / a.splits, kbeg = z * kper, nk = kper / BK;
+  const uint16_t* A = static_cast<const uint16_t*>(a.A);
+  const uint16_t* W = static_cast<const uint16_t*>(a.W);
+  // W DMA: group g covers stage rows g * 8 .. + 8; lane -> row g * 8 + lane / 8,
+  // physical chunk lane % 8 <- logical chunk (lane % 8) ^ (row & 7). Waves past
+  // the group count repeat the last group (the same bytes to the same place).
+  const uint16_t* wsrc[GPW];
+  int wdst[GPW];
+#pragma unroll
+  for (int q = 0; q < GPW; ++q) {
+    const int g = min(wave * GPW + q, GROUPS - 1);
+    const int r = g * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (r & 7);
+    const int gn = min(n0 + r, a.N - 1);
+    const int wrow = EPI == EPI_SWIGLU ? swiglu_row(gn, a.mlp) : gn;
+    wsrc[q] = W + (long)wrow * a.ldw + kbeg + c * 8;
+    wdst[q] = g * 1024;
+  }
+  auto issue_w = [&](int buf, int stage) {
+    const int off = min(stage, nk - 1) * BK;
+    uint8_t* dst = Wsm + buf * STAGE;
+#pragma unroll
+    for (int q = 0; q < GPW; ++q)
+      __builtin_amdgcn_global_load_lds(LDR_GP(wsrc[q] + off), LDR_LP(dst + wdst[q]), 16, 0, 0);
+  };
+  // A fragments of m-tile i and k half kk of a step: one 1 KB block each.
+  // Row blocks past the padded row count repeat the last one (never stored).
+  const int mpad = (a.M + 15) & ~15;
+  const uint16_t* asrc[MTW];
+#pragma unroll
+  for (int i = 0; i < MTW; ++i) {
+    const int rg = min(m0 + wm * TM + i * 16, mpad - 16) >> 4;
+    asrc[i] = A + ((long)rg * (a.K >> 5) + (kbeg >> 5)) * 512 + lane * 8;
+  }
+  u32x4 aq[FRA][MTW][2];
+  auto load_a = [&](u32x4 (&dst)[MTW][2], int stage) {
+    const long off = (long)min(stage, nk - 1) * 1024;
+#pragma unroll
+    for (int i = 0; i < MTW; ++i)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+        dst[i][kk] = *reinterpret_cast<const u32x4*>(asrc[i] + off + kk * 512);
+  };
+  // W fragment offsets in a stage: row wn * TN + j * 16 + lane % 16, logical
+  // chunk kk * 4 + lane / 16
+  int woff[NTW][2];
+#pragma unroll
+  for (int j = 0; j < NTW; ++j)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      const int r = wn * TN + j * 16 + (lane & 15);
+      woff[j][kk] = r * 128 + (((kk * 4 + (lane >> 4)) ^ (r & 7)) * 16);
+    }
+  f32x4 acc[MTW][NTW];
+#pragma unroll
+  for (int i = 0; i < MTW; ++i)
+#pragma unroll
+    for (int j = 0; j < NTW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // step kt in phase p = kt mod FNB: W stage kt in buffer p, A stage kt in ring
+  // slot p mod FRA; refills buffer (p + FNB - 1) mod FNB with stage kt + FNB - 1
+#define LDR_FSTEP(kt, p)                                                                     \
+  {                                                                                          \
+    sched_fence();                                                                           \
+    wait_vm_lgkm0<PER_STEP * (FRA - 1)>();                                                   \
+    __builtin_amdgcn_s_barrier();                                                            \
+    sched_fence();                                                                           \
+    issue_w(((p) + FNB - 1) % FNB, (kt) + FNB - 1);                                          \
+    const uint8_t* cur = Wsm + (p) * STAGE;                                                  \
+    bf16x8 bfr[2][NTW];                                                                      \
+    _Pragma("unroll") for (int kk = 0; kk < 2; ++kk)                                         \
+      _Pragma("unroll") for (int j = 0; j < NTW; ++j)                                        \
+        bfr[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + woff[j][kk])); \
+    _Pragma("unroll") for (int kk = 0; kk < 2; ++kk)                                         \
+      _Pragma("unroll") for (int i = 0; i < MTW; ++i)                                        \
+        _Pragma("unroll") for (int j = 0; j < NTW; ++j) acc[i][j] =                          \
+            __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                         \
+                __builtin_bit_cast(bf16x8, aq[(p) % FRA][i][kk]), bfr[kk][j], acc[i][j], 0, 0, 0); \
+    load_a(aq[(p) % FRA], (kt) + FRA);                                                       \
+    sched_fence();                                                                           \
+  }
+  // prologue: W stages 0 .. FNB - 2 and A stages 0 .. FRA - 1, ordered so that
+  // the last FRA - 1 (W, A) pairs look like steps to the in-order count
+  issue_w(0, 0); issue_w(1, 1); issue_w(2, 2);
+  load_a(aq[0], 0);
+  issue_w(3, 3); load_a(aq[1], 1);
+  issue_w(4, 4); load_a(aq[2], 2);
+  static_assert(FNB == 6 && FRA == 3, "prologue and unrolled loop assume 6 and 3");
+  const int full = nk / FNB * FNB;
+  int kt = 0;
+  for (; kt < full; kt += FNB) {
+    LDR_FSTEP(kt, 0) LDR_FSTEP(kt + 1, 1) LDR_FSTEP(kt + 2, 2)
+    LDR_FSTEP(kt + 3, 3) LDR_FSTEP(kt + 4, 4) LDR_FSTEP(kt + 5, 5)
+  }
+  const int rem = nk - full;   // uniform: every wave takes the same steps
+  if (rem > 0) LDR_FSTEP(kt, 0)
+  if (rem > 1) LDR_FSTEP(kt + 1, 1)
+  if (rem > 2) LDR_FSTEP(kt + 2, 2)
+  if (rem > 3) LDR_FSTEP(kt + 3, 3)
+  if (rem > 4) LDR_FSTEP(kt + 4, 4)
+#undef LDR_FSTEP
+  wait_vm_lgkm0<0>();   // no DMA outlives the workgroup
+  store_tile<MTW, NTW, WM, WN, EPI>(a, n0, m0, z, acc);
+}
+
 // ---------------------------------------------------------------------------
 // GEMM on tiled operands (the vocabulary head).
 //
@@ -300,21 +468,6 @@ constexpr int TR = 256, TK = 32;
 constexpr long TBLK = (long)TR * TK;
 
 __device__ inline int tile_swz(int r) { return (r >> 2) & 3; }
-
-template <int N> __device__ inline void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt");
-  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-__device__ inline void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(15 | (7 << 4) | (3 << 14)); }
-__device__ inline void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
-__device__ inline void group_barrier() {
-  sched_fence();
-  __builtin_amdgcn_s_barrier();
-  sched_fence();
-}
-
-#define LDR_GP(p) ((__attribute__((address_space(1))) void*)(p))
-#define LDR_LP(p) ((__attribute__((address_space(3))) void*)(p))
 
 // Greedy partial of the fused head: the largest logit of a column range and
 // its first token.
@@ -516,7 +669,10 @@ __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, l
 // 2 x 12288 columns at the Qwen3-8B shape make exactly 256 tiles (one per CU);
 // 5: BM 256 with 4 x 2 waves of 64 x 32 (BN 64), in place of cfg 3 when cfg 3
 // would split K eight ways into pieces of at most 512: as fast there (the O
-// projection) with half the split-K partials for the next kernel to read.
+// projection) with half the split-K partials for the next kernel to read;
+// 6, 7: gemm_frag_kernel, BM 256 with 8 waves of 32 x 96 (BN 96) or 32 x 128
+// (BN 128), activation rows in the fragment layout: the SwiGLU GEMM above 64
+// rows in place of cfg 4 or 3.
 template <int EPI>
 hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
   switch (cfg) {
@@ -525,6 +681,8 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
     case 2: hipLaunchKernelGGL((gemm_kernel<4, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 4: hipLaunchKernelGGL((gemm_kernel<2, 6, 8, 1, EPI>), grid, dim3(512), 0, st, a); break;
     case 5: hipLaunchKernelGGL((gemm_kernel<4, 2, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
+    case 6: hipLaunchKernelGGL((gemm_frag_kernel<2, 6, EPI>), grid, dim3(512), 0, st, a); break;
+    case 7: hipLaunchKernelGGL((gemm_frag_kernel<2, 8, EPI>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -556,13 +714,16 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
         if (best == 0.0 || cost < best) { best = cost; p.cfg = c[0]; }
       }
     }
+    // the SwiGLU GEMM above 64 rows reads its rows in the fragment layout
+    if (swiglu && M > 64 && K % BK == 0) p.cfg = p.cfg == 4 ? 6 : p.cfg == 3 ? 7 : p.cfg;
     if (p.cfg == 3 && allow_split && !swiglu) {
       const int t128 = ((N + 127) / 128) * ((M + 255) / 256);
       if (t128 * 8 <= kCUs && t128 * 16 > kCUs && K / 8 <= 512 && K % (4 * 2 * 2 * BK) == 0)
         p.cfg = 5;
     }
     bm = p.cfg >= 3 ? 256 : 16 << p.cfg;
-    bn = p.cfg == 5 ? 64 : p.cfg == 4 ? 96 : (p.cfg == 3 || p.cfg == 0) ? 128 : 256;
+    bn = p.cfg == 5 ? 64 : (p.cfg == 4 || p.cfg == 6) ? 96
+         : (p.cfg == 3 || p.cfg == 0 || p.cfg == 7) ? 128 : 256;
     kstep = 2 * BK;
   }
   p.ntw = 0;

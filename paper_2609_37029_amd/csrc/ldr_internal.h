@@ -154,6 +154,8 @@ struct GemmArgs {
   int mlp;                     // EPI_SWIGLU: N / 2
 };
 struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile configuration
+// The plan's kernel reads its activation rows in the fragment layout (NRM_FRAG).
+inline bool gemm_plan_frag(const GemmPlan& p) { return p.cfg >= 6; }
 // Tile configuration and split-K factor; splits = 1 unless allow_split.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
@@ -215,9 +217,16 @@ bool attention_mfma_supported(int d, int rep, int B, int R, int Wx);
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
                             const ldr_weights* w, const int32_t* anchor, hipStream_t st);
 bool norm_hidden_supported(int hidden);
-// tiled_out: write the normalised rows there in the tiled layout instead of to p.nrm.
+// Layouts of the normalised rows a residual norm writes.
+enum NrmLayout {
+  NRM_ROWS = 0,   // row-major [M][hidden] (p.nrm)
+  NRM_TILED = 1,  // 256-row x 32-column blocks of ldr_tile_matrix (the tiled vocabulary head)
+  NRM_FRAG = 2,   // 16-row x 32-column MFMA fragments, lane order (gemm_frag_kernel)
+};
+// tiled_out: write the normalised rows there in `layout` instead of to p.nrm.
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
-                             const void* gain, hipStream_t st, void* tiled_out = nullptr);
+                             const void* gain, hipStream_t st, void* tiled_out = nullptr,
+                             int layout = NRM_TILED);
 hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const ldr_layer_weights* lw, hipStream_t st);
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
