@@ -51,11 +51,11 @@ def parse():
                          "per-position sampler (0: off)")
     ap.add_argument("--temperature", type=float, default=1.0,
                     help="sampling temperature of the drafted positions (0: greedy argmax)")
-    ap.add_argument("--fused-head", action="store_true",
-                    help="draft and sample through ldr_draft_step_sample (greedy steps take the "
-                         "argmax in the vocabulary head's epilogue)")
+    ap.add_argument("--separate-sampler", action="store_true",
+                    help="draft with ldr_draft_step and sample with ldr_sample (two calls) "
+                         "instead of the one call ldr_draft_step_sample")
     ap.add_argument("--no-logits", action="store_true",
-                    help="with --fused-head: do not write the fp32 logits")
+                    help="greedy steps only: do not write the fp32 logits")
     ap.add_argument("--drop-views", type=int, default=0,
                     help="ablation variant: 1 no window, 2 no summary, 4 no boundary")
     ap.add_argument("--verify", action="store_true",
@@ -739,7 +739,8 @@ def main():
     if loop:
         args.steps = loop       # the loop's own length: every step is timed
     rig = Rig(torch, ldr, synth, s, batch, wl.prefix, tiled_head=not args.row_major_head,
-              markov_rank=args.markov_rank, verify=args.verify, fused_head=args.fused_head,
+              markov_rank=args.markov_rank, verify=args.verify,
+              fused_head=not args.separate_sampler,
               keep_logits=not args.no_logits, temperature=args.temperature, loop_steps=loop)
     ev = ldr.HipEvents()
     costs = launch_costs(s, batch)
@@ -790,9 +791,12 @@ def main():
                    "window": s.window, "summary": s.summary, "draft_layers": s.n_layers,
                    "lm_head_layout": "tiled" if rig.tiled_head else "row-major",
                    "sampler": (f"markov rank {rig.markov_rank}" if rig.markov_rank else
-                               ("fused into the vocabulary head" +
-                                ("" if rig.keep_logits else ", logits not written"))
-                               if rig.fused_head else "per-position"),
+                               ("ldr_draft_step_sample: " +
+                                ("argmax in the vocabulary head's epilogue" +
+                                 ("" if rig.keep_logits else ", logits not written")
+                                 if rig.temperature == 0 else
+                                 "per-position sampler overlapping the head's last round"))
+                               if rig.fused_head else "ldr_draft_step + ldr_sample"),
                    "views": {0: "window + summary + boundary", 1: "no window", 2: "no summary",
                              4: "no boundary"}.get(s.drop_views, f"drop {s.drop_views}")},
         "us_per_step": {"p10": percentile(per_step, .1) * 1e3, "p50": percentile(per_step, .5) * 1e3,
@@ -830,7 +834,7 @@ def sweep(args, torch, ldr, synth):
     for batch in [int(x) for x in args.sweep_batch.split(",")]:
         for prefix in [int(x) for x in args.sweep_prefix.split(",")]:
             rig = Rig(torch, ldr, synth, s, batch, prefix, reuse_chunk=True,
-                      tiled_head=not args.row_major_head)
+                      tiled_head=not args.row_major_head, fused_head=not args.separate_sampler)
             wall, per_step, _ = time_steps(torch, rig, args.steps, args.warmup, ev=ev)
             r = {"batch": batch, "prefix": prefix, "us_p50": percentile(per_step, .5) * 1e3,
                  "us_p10": percentile(per_step, .1) * 1e3,

@@ -490,9 +490,10 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
   const int grp = wave >> 2, wq = wave & 3;
   const int wm = grp, wn = wq;   // output rows wm * 128 .., columns wn * 64 ..
   const int nkb = a.K / TK, kper = nkb / a.splits, kb0 = blockIdx.z * kper;
+  const int ct = blockIdx.x + hs.col_tile0;   // column tile
   const uint16_t* tile =
       grp == 0 ? static_cast<const uint16_t*>(a.A) + (long)blockIdx.y * nkb * TBLK
-               : static_cast<const uint16_t*>(a.W) + (long)blockIdx.x * nkb * TBLK;
+               : static_cast<const uint16_t*>(a.W) + (long)ct * nkb * TBLK;
   // DMA: wave wq of a group moves rows wq * 64 + q * 16 + lane / 4 of its
   // operand (4 lanes per 64-byte row, lane & 3 = destination chunk).
   const uint16_t* src[4];
@@ -573,7 +574,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
 #undef LDR_MEM
   wait_vmcnt<0>();   // no DMA outlives the workgroup
   const int crow = (lane >> 4) * 4, ccol = lane & 15;
-  const int r0 = blockIdx.y * TR + wm * 128, c0 = blockIdx.x * TR + wn * 64;
+  const int r0 = blockIdx.y * TR + wm * 128, c0 = ct * TR + wn * 64;
   if (!SAMPLE || hs.store_logits) {
     float* out = static_cast<float*>(a.out) + (long)blockIdx.z * a.split_stride;
 #pragma unroll
@@ -622,7 +623,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
       HeadPart p = tab[tid][0];
 #pragma unroll
       for (int q = 1; q < 4; ++q) head_combine(p, tab[tid][q]);
-      if (row < a.M) parts[(long)row * hs.nparts + blockIdx.x] = p;
+      if (row < a.M) parts[(long)row * hs.nparts + ct] = p;
     }
   }
 }
@@ -759,13 +760,19 @@ bool gemm_tiled_supported(int M, int N, int K, int splits) {
   return M > 0 && N > 0 && splits > 0 && K % (TK * 4 * splits) == 0;
 }
 
-hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st) {
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st, int tile0, int ntiles) {
   if (!gemm_tiled_supported(a.M, a.N, a.K, a.splits)) return hipErrorInvalidValue;
-  const dim3 grid((a.N + TR - 1) / TR, (a.M + TR - 1) / TR, a.splits);
-  HeadSampleArgs none{};
-  hipLaunchKernelGGL((gemm_tiled_kernel<false>), grid, dim3(512), 0, st, a, none);
+  const int nt = (a.N + TR - 1) / TR;
+  if (ntiles < 0) ntiles = nt - tile0;
+  if (tile0 < 0 || ntiles <= 0 || tile0 + ntiles > nt) return hipErrorInvalidValue;
+  const dim3 grid(ntiles, (a.M + TR - 1) / TR, a.splits);
+  HeadSampleArgs hs{};
+  hs.col_tile0 = tile0;
+  hipLaunchKernelGGL((gemm_tiled_kernel<false>), grid, dim3(512), 0, st, a, hs);
   return hipGetLastError();
 }
+
+int gemm_tiled_width() { return TR; }
 
 size_t head_sample_part_bytes(int rows, int vocab) {
   return (size_t)rows * ((vocab + TR - 1) / TR) * sizeof(HeadPart);

@@ -163,7 +163,9 @@ hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a,
 // its M rows, W over its N rows); fp32 out [splits][M][ldo]. Needs
 // K % (128 * splits) == 0.
 bool gemm_tiled_supported(int M, int N, int K, int splits);
-hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st);
+// Column tiles [tile0, tile0 + ntiles) of the output (ntiles < 0: to the end).
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st, int tile0 = 0, int ntiles = -1);
+int gemm_tiled_width();   // output columns per tile (and rows per row tile)
 // The vocabulary head with greedy sampling (T = 0) fused into its epilogue:
 // per row and column tile the first argmax goes to `parts`, then one merge per
 // row writes the token, lse (its logit) and log q = 0. The logits are written
@@ -172,6 +174,7 @@ struct HeadSampleArgs {
   void* parts;        // head_sample_part_bytes(M, V) bytes
   int nparts;         // partials per row (set by the launcher)
   int store_logits;
+  int col_tile0;      // column tile of the launch's first workgroup column
 };
 size_t head_sample_part_bytes(int rows, int vocab);
 hipError_t launch_gemm_tiled_argmax(const GemmArgs& a, const HeadSampleArgs& hs, int32_t* tokens,
@@ -233,7 +236,20 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
                             int layer, hipStream_t st);
 
 // Sampler (sample.hip)
-int sample_splits(int rows, int vocab);
+// Vocabulary chunks of a row: n_a chunks of chunk_a tokens below `split`, then
+// n_b chunks of chunk_b tokens from it (n_b = 0: split = vocab).
+struct SamplePlan { int chunk_a, n_a, split, chunk_b, n_b; };
+SamplePlan sample_plan(int rows, int vocab);
+int sample_splits(int rows, int vocab);   // chunks per row
+// The full-vocabulary sampler in pieces (top_k = 0): the partial pass over
+// chunks [c0, c1) of every row, and the merge of all chunks; ws as for
+// launch_sample.
+hipError_t launch_sample_partials(const float* logits, int rows, int vocab, float temperature,
+                                  uint64_t seed, uint64_t step, void* ws, int c0, int c1,
+                                  hipStream_t st);
+hipError_t launch_sample_merge(const float* logits, int rows, int vocab, float temperature,
+                               void* ws, int32_t* tokens, float* lse, float* logq,
+                               hipStream_t st);
 size_t sample_part_bytes(int rows, int vocab);
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,

@@ -41,10 +41,12 @@ __device__ inline void combine(Partial& a, const Partial& b) {
 
 struct SampleArgs {
   const float* logits; int rows, vocab, chunk, splits;
+  int n_a, split, chunk_b;   // chunks below `split` are `chunk` tokens, from it `chunk_b`
   float T; uint64_t seed, step;
   Partial* part;
   const TopK* sel;  // top-k support per row, or null for the full vocabulary
   int row_mul, row_add;  // row r of the launch is logits row (and noise row) r * mul + add
+  int chunk0;            // vocabulary chunk of the launch's first workgroup column
   int vec;               // rows start on 16 bytes (V % 4 == 0, aligned logits): 16-byte loads
 };
 
@@ -346,8 +348,9 @@ __global__ void __launch_bounds__(kMkThreads) markov_correct_kernel(
 }
 
 __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) {
-  const int sp = blockIdx.x, r = blockIdx.y;
-  const int v0 = sp * a.chunk, v1 = min(a.vocab, v0 + a.chunk);
+  const int sp = blockIdx.x + a.chunk0, r = blockIdx.y;
+  const int v0 = sp < a.n_a ? sp * a.chunk : a.split + (sp - a.n_a) * a.chunk_b;
+  const int v1 = min(a.vocab, sp < a.n_a ? min(a.split, v0 + a.chunk) : v0 + a.chunk_b);
   const float* z = a.logits + ((long)r * a.row_mul + a.row_add) * a.vocab;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
   if (a.T == 0.f) {
@@ -417,14 +420,45 @@ __global__ void __launch_bounds__(kThreads) gumbel_fill_kernel(uint64_t seed, ui
 
 }  // namespace
 
+SamplePlan sample_plan(int rows, int vocab) {
+  // About 2048 workgroups (8 waves per SIMD; 4096 measured no faster): a
+  // chunk of one sweep times the largest power of two that keeps at least
+  // 2048 / rows chunks per row (from 2048 rows on, one chunk per row).
+  // Up to 256 rows and past 65536 tokens, the tokens from the last multiple
+  // of 65536 covered by whole 65536-token blocks of the vocabulary head's
+  // full rounds (256 column tiles of 256) take one-sweep chunks instead: that
+  // region is sampled after the head's last round (ldr_draft_step_sample), by
+  // many short workgroups; ldr_sample uses the same plan, so both calls give
+  // the same partials and the same results.
+  constexpr int sweep = kThreads * kGroup;
+  SamplePlan p;
+  if (rows >= 2048) {
+    p.chunk_a = (vocab + sweep - 1) / sweep * sweep;
+    p.n_a = 1; p.split = vocab; p.chunk_b = sweep; p.n_b = 0;
+    return p;
+  }
+  const long target = ((long)vocab * rows + 2047) / 2048;
+  int chunk = sweep;
+  while (chunk * 2L <= target && chunk < 32 * sweep) chunk *= 2;
+  p.chunk_a = chunk;
+  p.chunk_b = sweep;
+  const int tiles = (vocab + 255) / 256, full = tiles / 256 * 256;
+  const int split = full * 256;
+  if (rows <= 256 && full > 0 && split < vocab && split % chunk == 0) {
+    p.split = split;
+    p.n_a = split / chunk;
+    p.n_b = (vocab - split + sweep - 1) / sweep;
+  } else {
+    p.split = vocab;
+    p.n_a = (vocab + chunk - 1) / chunk;
+    p.n_b = 0;
+  }
+  return p;
+}
+
 int sample_splits(int rows, int vocab) {
-  // about 2048 workgroups (8 waves per SIMD; 4096 measured no faster), each
-  // chunk a multiple of one sweep
-  int splits = rows >= 2048 ? 1 : 2048 / rows;
-  const int sweep = kThreads * kGroup;
-  const int max_splits = (vocab + sweep - 1) / sweep;
-  if (splits > max_splits) splits = max_splits;
-  return splits < 1 ? 1 : splits;
+  const SamplePlan p = sample_plan(rows, vocab);
+  return p.n_a + p.n_b;
 }
 
 size_t sample_part_bytes(int rows, int vocab) {
@@ -484,13 +518,47 @@ hipError_t launch_sample(const float* logits, int rows, int vocab, float tempera
     if (e != hipSuccess) return e;
     a.sel = sel;
   }
-  a.splits = sample_splits(rows, vocab);
-  const int sweep = kThreads * kGroup;
-  a.chunk = ((vocab + a.splits - 1) / a.splits + sweep - 1) / sweep * sweep;
-  a.splits = (vocab + a.chunk - 1) / a.chunk;
+  const SamplePlan pl = sample_plan(rows, vocab);
+  a.chunk = pl.chunk_a; a.n_a = pl.n_a; a.split = pl.split; a.chunk_b = pl.chunk_b;
+  a.splits = pl.n_a + pl.n_b;
+  a.chunk0 = 0;
   hipLaunchKernelGGL(sample_partial_kernel, dim3(a.splits, rows), dim3(kThreads), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sample_merge_kernel, dim3(rows), dim3(64), 0, st, a, tokens, lse, logq);
+  return hipGetLastError();
+}
+
+namespace {
+SampleArgs full_vocab_args(const float* logits, int rows, int vocab, float temperature,
+                           uint64_t seed, uint64_t step, void* ws) {
+  SampleArgs a;
+  a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
+  a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
+  a.sel = nullptr; a.row_mul = 1; a.row_add = 0;
+  a.vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0;
+  const SamplePlan pl = sample_plan(rows, vocab);
+  a.chunk = pl.chunk_a; a.n_a = pl.n_a; a.split = pl.split; a.chunk_b = pl.chunk_b;
+  a.splits = pl.n_a + pl.n_b;
+  a.chunk0 = 0;
+  return a;
+}
+}  // namespace
+
+hipError_t launch_sample_partials(const float* logits, int rows, int vocab, float temperature,
+                                  uint64_t seed, uint64_t step, void* ws, int c0, int c1,
+                                  hipStream_t st) {
+  SampleArgs a = full_vocab_args(logits, rows, vocab, temperature, seed, step, ws);
+  if (c0 < 0 || c1 > a.splits || c0 >= c1) return hipErrorInvalidValue;
+  a.chunk0 = c0;
+  hipLaunchKernelGGL(sample_partial_kernel, dim3(c1 - c0, rows), dim3(kThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample_merge(const float* logits, int rows, int vocab, float temperature,
+                               void* ws, int32_t* tokens, float* lse, float* logq,
+                               hipStream_t st) {
+  const SampleArgs a = full_vocab_args(logits, rows, vocab, temperature, 0, 0, ws);
   hipLaunchKernelGGL(sample_merge_kernel, dim3(rows), dim3(64), 0, st, a, tokens, lse, logq);
   return hipGetLastError();
 }

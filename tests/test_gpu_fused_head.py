@@ -4,7 +4,11 @@ epilogue: the logits it writes are ldr_draft_step's bit for bit, and its
 tokens, lse and log q are the separate sampler's at T = 0 on those logits
 (the separate sampler is itself compared with the oracle in
 test_gpu_sample.py); without the logits it draws the same tokens. Sampled
-steps run the head and the separate sampler."""
+steps run the head and the sampler's kernels; when the head's column tiles
+take more than one round over the CUs (one row tile), the sampler works on
+the chunks of the finished rounds on a second stream while the head's last
+round runs, and the tokens, lse and log q are the separate sampler's bit for
+bit."""
 import numpy as np
 import pytest
 import torch
@@ -129,3 +133,42 @@ def test_small_steps_take_the_separate_sampler(gpu_lib):
     assert torch.equal(z, z_ref) and torch.equal(tok.view(-1), tok_ref)
     with pytest.raises(RuntimeError):
         gpu_lib.draft_step_sample(p.views, dw, anchor, 1.0, 3, 1, logits=None)
+
+
+MINI_WIDE = MINI_BF16.replace(name="mini-bf16-v70000", vocab=70000)
+
+
+@pytest.mark.parametrize("batch,T", [(5, 1.0), (16, 0.8)])
+def test_sampled_step_overlapping_the_head_matches_the_separate_calls(gpu_lib, batch, T):
+    """Vocabulary 70000: 274 column tiles, so the head's last round (18 tiles)
+    overlaps the sampler's chunks below token 65536 on the second stream
+    (80 rows: 2048-token chunks, 32 of 35 there; 256 rows: 16384-token
+    chunks, 4 of 5). Logits, tokens, lse and log q equal the separate
+    ldr_draft_step + ldr_sample bit for bit, over several calls in a row."""
+    p, dw, anchor = setup(gpu_lib, MINI_WIDE, batch, 120)
+    V = MINI_WIDE.vocab
+    for step in range(3):
+        z_ref = gpu_lib.draft_step(p.views, dw, anchor)
+        tok_ref, lse_ref, logq_ref = gpu_lib.sample(z_ref.view(-1, V), T, 0, 21, step)
+        z, tok, lse, logq = gpu_lib.draft_step_sample(p.views, dw, anchor, T, 21, step)
+        torch.cuda.synchronize()
+        assert torch.equal(z, z_ref)
+        assert torch.equal(tok.view(-1), tok_ref)
+        assert torch.equal(lse.view(-1), lse_ref) and torch.equal(logq.view(-1), logq_ref)
+        assert len(set(tok.view(-1).tolist())) > 1
+
+
+@pytest.mark.slow
+def test_sampled_step_overlapping_the_head_full_size(gpu_lib):
+    """Qwen3-8B shape, batch 16, T = 1: the benchmarked call (594 column tiles,
+    the last 82 overlapping 8 of the 10 sampler chunks), bit for bit against
+    the separate calls."""
+    p, dw, anchor = setup(gpu_lib, synth.QWEN3_8B, 16, 300)
+    V = synth.QWEN3_8B.vocab
+    z_ref = gpu_lib.draft_step(p.views, dw, anchor)
+    ref = gpu_lib.sample(z_ref.view(-1, V), 1.0, 0, 5, 9)
+    z, tok, lse, logq = gpu_lib.draft_step_sample(p.views, dw, anchor, 1.0, 5, 9)
+    torch.cuda.synchronize()
+    assert torch.equal(z, z_ref)
+    for a, b in zip((tok, lse, logq), ref):
+        assert torch.equal(a.view(-1), b)
