@@ -18,6 +18,8 @@ from paper_2609_37029_amd import build as B
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HOST = os.path.join(ROOT, "tests", "host")
 OUT = os.path.join(HOST, "_build")
+CLANG = "/opt/rocm/llvm/bin/clang++"
+ROCM_LIB = "/opt/rocm/lib"
 SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
        "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
 
@@ -48,15 +50,18 @@ def _build():
         return o
     with cf.ThreadPoolExecutor(max_workers=min(8, os.cpu_count() or 1)) as ex:
         objs = list(ex.map(obj, B.SOURCES))
+    # the driver is host code only: plain clang++, linked against the HIP runtime
     drv = os.path.join(OUT, "abi_checks.o")
-    r = subprocess.run([hipcc, "-O1", "-std=c++17", "-fsanitize=address,undefined",
-                        "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g",
-                        "-I", os.path.join(ROOT, "include"), "-c",
+    host_san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+                "-fno-omit-frame-pointer", "-g"]
+    r = subprocess.run([CLANG, "-O1", "-std=c++17"] + host_san +
+                       ["-I", os.path.join(ROOT, "include"), "-c",
                         os.path.join(HOST, "abi_checks.cpp"), "-o", drv],
                        capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-4000:]
-    r = subprocess.run([hipcc, "--offload-arch=gfx950", "-fsanitize=address,undefined",
-                        "-o", exe, drv] + objs, capture_output=True, text=True)
+    r = subprocess.run([CLANG] + host_san + ["-o", exe, drv] + objs +
+                       ["-L", ROCM_LIB, "-lamdhip64", "-Wl,-rpath," + ROCM_LIB],
+                       capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-4000:]
     open(stamp, "w").write(dig)
     return exe
