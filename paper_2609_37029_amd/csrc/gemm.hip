@@ -302,23 +302,27 @@ __device__ inline void group_barrier() {
 // stages issued NB - 1 steps ahead. Against the staged kernel above this
 // removes the activation tiles' LDS stores and reads (32 KB each per step at
 // 256 rows), which bounded it.
-// Ordering: before step kt every wave waits until at most the last RA - 1
-// steps' loads are pending (vmcnt counts its DMA and A loads in issue order)
-// and its own LDS reads are done, then a barrier: stage kt is whole in LDS,
-// and the buffer refilled at this step (read at step kt - 1) has no reader left.
-constexpr int FNB = 6, FRA = 3;   // W stages in LDS, A stages in registers
+// Ordering: every step issues the DMA of W stage kt + FNB - 1, then the A loads
+// of stage kt + FRA (FRA stages of A in registers). Before step kt every wave
+// waits until the later of W stage kt and A stage kt in that order has
+// landed (vmcnt counts its DMA and A loads in issue order) and its own LDS
+// reads are done, then a barrier: stage kt is whole in LDS, and the buffer
+// refilled at this step (read at step kt - 1) has no reader left. Three A
+// stages ahead measured fastest: six (the register limit) and a second
+// register buffer for the weight fragments were both slower.
+constexpr int FNB = 6;   // W stages in LDS (DMA issued FNB - 1 steps ahead)
 
-__device__ inline long frag_elem(long m, int k, int K) {
-  return ((m >> 4) * (K >> 5) + (k >> 5)) * 512 + ((((k >> 3) & 3) << 4) | (m & 15)) * 8 +
-         (k & 7);
-}
+// Activation layout (written by the residual norm): element (m, k) of an
+// M x K matrix sits at ((m >> 4) * (K >> 5) + (k >> 5)) * 512
+// + ((((k >> 3) & 3) << 4) | (m & 15)) * 8 + (k & 7), so each 16 x 32 block is
+// 1 KB in the lane order of the MFMA A operand.
 
 template <int N> __device__ inline void wait_vm_lgkm0() {
   static_assert(N >= 0 && N < 64, "vmcnt");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
-template <int MTW, int NTW, int EPI>
+template <int MTW, int NTW, int EPI, int FRA>
 __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
   constexpr int WM = 8, WN = 1, NW = WM * WN, TM = MTW * 16, TN = NTW * 16;
   constexpr int BM = WM * TM, BN = WN * TN;
@@ -327,6 +331,9 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
   constexpr int GPW = (GROUPS + NW - 1) / NW;
   constexpr int AV = MTW * 2;                 // A loads per stage per lane
   constexpr int PER_STEP = GPW + AV;          // VMEM instructions per step and wave
+  static_assert(FNB % FRA == 0, "the unrolled loop cycles both rings");
+  // loads issued after the later of W(kt) (step kt - FNB + 1) and A(kt) (step kt - FRA)
+  constexpr int WAIT = FNB - 1 >= FRA ? PER_STEP * (FRA - 1) : AV + PER_STEP * (FNB - 2);
   static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
   __shared__ __attribute__((aligned(1024))) uint8_t Wsm[FNB * STAGE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -396,7 +403,7 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
 #define LDR_FSTEP(kt, p)                                                                     \
   {                                                                                          \
     sched_fence();                                                                           \
-    wait_vm_lgkm0<PER_STEP * (FRA - 1)>();                                                   \
+    wait_vm_lgkm0<WAIT>();                                                                   \
     __builtin_amdgcn_s_barrier();                                                            \
     sched_fence();                                                                           \
     issue_w(((p) + FNB - 1) % FNB, (kt) + FNB - 1);                                          \
@@ -413,13 +420,16 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
     load_a(aq[(p) % FRA], (kt) + FRA);                                                       \
     sched_fence();                                                                           \
   }
-  // prologue: W stages 0 .. FNB - 2 and A stages 0 .. FRA - 1, ordered so that
-  // the last FRA - 1 (W, A) pairs look like steps to the in-order count
-  issue_w(0, 0); issue_w(1, 1); issue_w(2, 2);
-  load_a(aq[0], 0);
-  issue_w(3, 3); load_a(aq[1], 1);
-  issue_w(4, 4); load_a(aq[2], 2);
-  static_assert(FNB == 6 && FRA == 3, "prologue and unrolled loop assume 6 and 3");
+  // prologue: W stages 0 .. FNB - 2 and A stages 0 .. FRA - 1 issued as the
+  // virtual steps -max(FNB - 1, FRA) .. -1 would (W, then A), so that the
+  // in-order count of the first steps is that of any other step
+  constexpr int PRO = FNB - 1 > FRA ? FNB - 1 : FRA;
+#pragma unroll
+  for (int v = -PRO; v < 0; ++v) {
+    if (v + FNB - 1 >= 0) issue_w(v + FNB - 1, v + FNB - 1);
+    if (v + FRA >= 0) load_a(aq[v + FRA], v + FRA);
+  }
+  static_assert(FNB == 6, "the unrolled loop has six phases");
   const int full = nk / FNB * FNB;
   int kt = 0;
   for (; kt < full; kt += FNB) {
@@ -682,8 +692,8 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
     case 2: hipLaunchKernelGGL((gemm_kernel<4, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 4: hipLaunchKernelGGL((gemm_kernel<2, 6, 8, 1, EPI>), grid, dim3(512), 0, st, a); break;
     case 5: hipLaunchKernelGGL((gemm_kernel<4, 2, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((gemm_frag_kernel<2, 6, EPI>), grid, dim3(512), 0, st, a); break;
-    case 7: hipLaunchKernelGGL((gemm_frag_kernel<2, 8, EPI>), grid, dim3(512), 0, st, a); break;
+    case 6: hipLaunchKernelGGL((gemm_frag_kernel<2, 6, EPI, 3>), grid, dim3(512), 0, st, a); break;
+    case 7: hipLaunchKernelGGL((gemm_frag_kernel<2, 8, EPI, 3>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
