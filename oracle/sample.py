@@ -1,24 +1,45 @@
 """Oracle for per-position sampling of the factorised proposal (Eq. 8).
 
+This file is test infrastructure: only the tests, the smoke check and the
+benchmark's CPU baseline use it; the library never does.
+
 Each drafted position i of each sequence is one row of base logits z
 (fp32, [V]). For temperature T > 0 the proposal is q_i = softmax(z/T) over a
 support S (all V tokens, or the top_k largest logits, lower index first on
-ties), and the token is drawn by Gumbel-max: y = argmax_{v in S} (z_v/T + g_v)
-with g_v standard Gumbel noise. T = 0 is greedy: y = argmax_v z_v (lowest index
-on ties), q a point mass. The row also yields lse = log sum_{v in S} exp(z_v/T)
-and log q(y) = z_y/T - lse, which the verifier's acceptance test and residual
-(Eq. 1-2) need.
+ties). The paper fixes only q_i; the draw is a two-level Gumbel-max, which is
+an exact sample of q_i:
 
-The argmax is an integer decision taken from fp32 keys, so the keys are
-computed exactly as the GPU kernel does: fl(fl(z_v / T) + g_v), every step an
-IEEE fp32 operation. The noise is fully specified here:
+* the vocabulary is cut into chunks of C = 16 consecutive tokens
+  (chunk c = tokens 16c .. 16c + 15, the last one ragged);
+* each chunk's log-mass L_c = log sum_{v in c, v in S} exp(z_v/T) (-inf for
+  a chunk with no support token);
+* the chunk c* = argmax_c (L_c + h_c), h_c standard Gumbel noise: the maximum
+  of independent Gumbels shifted by L_c picks c with probability
+  exp(L_c) / sum exp(L), i.e. q_i(c);
+* the token y = argmax_{v in c*, v in S} (z_v/T + g_v), g_v Gumbel noise
+  independent of h: y given c* has probability exp(z_y/T - L_c*), so
+  P(y) = q_i(y).
+
+T = 0 is greedy: y = argmax_v z_v (lowest index on ties), q a point mass. The
+row also yields lse = log sum_{v in S} exp(z_v/T) and log q(y) = z_y/T - lse,
+which the verifier's acceptance test and residual (Eq. 1-2) need.
+
+Both argmaxes are integer decisions taken from fp32 keys, so the keys are
+fp32 as the GPU kernel computes them: the token keys fl(fl(z_v / T) + g_v),
+every step an IEEE fp32 operation, and the chunk keys fl(fl32(L_c) + h_c)
+with L_c computed here in float64 and rounded to fp32 (the kernel sums the
+chunk's 16 exponentials in fp32, so its L_c can differ in the last bits: its
+chunk choice can differ from this one only where two chunk keys tie within
+that error). Ties go to the lower index at both levels. The noise is fully
+specified here:
 
 * bits: Philox4x32-10 (Salmon, Moraes, Dror, Shaw, "Parallel random numbers:
   as easy as 1, 2, 3", SC 2011) with key (seed mod 2^32, seed div 2^32) and
   counter (v div 4, row, step mod 2^32, (step div 2^32) mod 2^30 + 2^30 s),
-  s the stream (0 for drafting); token v takes output word v mod 4;
+  s the stream; entry v takes output word v mod 4. Token noise g_v is entry
+  v of stream 0, chunk noise h_c entry c of stream 3;
 * uniform: k = bits >> 9, u = (2k + 1) * 2^-24, exact in fp32, in (0, 1);
-* Gumbel: g = -log(-log(u)) with the fp32 logarithm ``logf`` below, a fixed
+* Gumbel: -log(-log(u)) with the fp32 logarithm ``logf`` below, a fixed
   sequence of IEEE fp32 operations (no fused multiply-add): exponent split,
   mantissa folded into [sqrt(1/2), sqrt(2)], then 2 atanh(f), f = (m-1)/(m+1),
   by its odd power series to the f^11 term.
@@ -132,10 +153,15 @@ def uniform(bits):
     return ((k * TWO + ONE) * np.float32(2.0 ** -24)).astype(np.float32)
 
 
-def gumbel(seed, step, row, v):
-    """g = -log(-log(u)) in fp32 for token(s) v of row `row`."""
-    u = uniform(philox_bits(seed, step, row, v))
+def gumbel(seed, step, row, v, stream=0):
+    """-log(-log(u)) in fp32 for entry (entries) v of row `row` of a stream:
+    stream 0 holds the token noise g_v, stream 3 the chunk noise h_c."""
+    u = uniform(philox_bits(seed, step, row, v, stream))
     return -logf(-logf(u))
+
+
+CHUNK = 16          # tokens per vocabulary chunk of the two-level draw
+CHUNK_STREAM = 3    # noise stream of the chunk keys
 
 
 def support(z, top_k):
@@ -147,31 +173,75 @@ def support(z, top_k):
     return np.sort(np.argsort(-z.astype(np.float64), kind="stable")[:top_k])
 
 
-def sample(logits, temperature, top_k, seed, step, rows=None, chunk=16):
+def chunk_log_mass(zt, inside, chunk=CHUNK):
+    """L_c = log sum over the support tokens of chunk c of exp(zt_v), float64
+    [n][ceil(V / chunk)], -inf for a chunk without support tokens. zt: [n][V]
+    scaled logits, inside: [n][V] support mask."""
+    n, V = zt.shape
+    nch = -(-V // chunk)
+    x = np.full((n, nch * chunk), -np.inf)
+    x[:, :V] = np.where(inside, np.asarray(zt, dtype=np.float64), -np.inf)
+    with np.errstate(divide="ignore"):
+        return scipy.special.logsumexp(x.reshape(n, nch, chunk), axis=2)
+
+
+def chunk_keys(L, seed, step, rows):
+    """fp32 chunk keys fl(fl32(L_c) + h_c) of [n][nch] log-masses for the
+    noise rows `rows`; -inf where L_c = -inf."""
+    n, nch = L.shape
+    h = gumbel(seed, step, np.asarray(rows)[:, None], np.arange(nch)[None, :], CHUNK_STREAM)
+    with np.errstate(invalid="ignore"):
+        return (np.asarray(L, dtype=np.float32) + h).astype(np.float32)
+
+
+def draw_in_chunks(zt, inside, c, seed, step, rows, chunk=CHUNK):
+    """The token of chunk c[i] of each row i: first argmax of the fp32 keys
+    fl(zt_v + g_v) over the chunk's support tokens."""
+    n, V = zt.shape
+    v = np.asarray(c)[:, None] * chunk + np.arange(chunk)[None, :]
+    valid = v < V
+    v = np.minimum(v, V - 1)
+    key = (np.take_along_axis(zt, v, 1) +
+           gumbel(seed, step, np.asarray(rows)[:, None], v)).astype(np.float32)
+    key = np.where(valid & np.take_along_axis(inside, v, 1), key, -np.inf)
+    return v[np.arange(n), np.argmax(key, axis=1)]
+
+
+def sample(logits, temperature, top_k, seed, step, rows=None, chunk=CHUNK, rows_per_pass=16,
+           detail=False):
     """Tokens (int64), lse and log q (float64) for the rows of a [n][V] fp32
-    logits array. `rows` gives each row's index in the noise counter
-    (default 0..n-1). Rows are processed `chunk` at a time."""
+    logits array, drawn by the two-level Gumbel-max over chunks of `chunk`
+    tokens. `rows` gives each row's index in the noise counter (default
+    0..n-1). detail=True appends, for T > 0, the fp32 chunk keys [n][nch]
+    and the chosen chunks [n]."""
     z = np.asarray(logits, dtype=np.float32)
     n, V = z.shape
     rows = np.arange(n) if rows is None else np.asarray(rows)
     if temperature == 0.0:
         y = np.argmax(z, axis=1)                                # first maximum
-        return y.astype(np.int64), z[np.arange(n), y].astype(np.float64), np.zeros(n)
+        out = (y.astype(np.int64), z[np.arange(n), y].astype(np.float64), np.zeros(n))
+        return out + (None, None) if detail else out
     T = np.float32(temperature)
-    ys, lses = [], []
-    for a in range(0, n, chunk):
-        zc = z[a:a + chunk]
+    ys, lses, keys, cs = [], [], [], []
+    for a in range(0, n, rows_per_pass):
+        zc = z[a:a + rows_per_pass]
+        zt = (zc / T).astype(np.float32)                       # IEEE fp32 division
         inside = np.zeros(zc.shape, dtype=bool)
         for i in range(zc.shape[0]):
             inside[i, support(zc[i], top_k)] = True
-        key = zc / T + gumbel(seed, step, rows[a:a + chunk, None], np.arange(V)[None, :])
-        key = np.where(inside, key, -np.inf)                   # fp32 keys, support only
-        ys.append(np.argmax(key, axis=1))                      # first maximum
+        K = chunk_keys(chunk_log_mass(zt, inside, chunk), seed, step, rows[a:a + rows_per_pass])
+        c = np.argmax(K, axis=1)                               # first maximum
+        ys.append(draw_in_chunks(zt, inside, c, seed, step, rows[a:a + rows_per_pass], chunk))
         zs = np.where(inside, zc.astype(np.float64) / float(T), -np.inf)
         lses.append(scipy.special.logsumexp(zs, axis=1))
+        keys.append(K)
+        cs.append(c)
     y = np.concatenate(ys).astype(np.int64)
     lse = np.concatenate(lses)
-    return y, lse, z[np.arange(n), y].astype(np.float64) / float(T) - lse
+    out = (y, lse, z[np.arange(n), y].astype(np.float64) / float(T) - lse)
+    if detail:
+        out = out + (np.concatenate(keys), np.concatenate(cs).astype(np.int64))
+    return out
 
 
 def sample_row(z, temperature, top_k, seed, step, row):
@@ -231,9 +301,10 @@ def sample_markov(z0, anchor, E_c, W_c, temperature, top_k, seed, step):
 #    proposal cannot produce it) and is rejected;
 #  * a residual with no positive entry (p_i = q_i exactly, where a rejection
 #    has probability zero) draws from p_i with the bonus rule instead;
-#  * the bonus token is drawn exactly as the drafting sampler draws, from the
-#    fp32 keys fl(fl(P_v / T) + g_v), first maximum; the correction token is
-#    the first maximum of log w_v + g_v over the tokens with w_v > 0;
+#  * the bonus token is drawn by a one-level Gumbel-max over the whole
+#    vocabulary, from the fp32 keys fl(fl(P_v / T) + g_v), first maximum; the
+#    correction token is the first maximum of log w_v + g_v over the tokens
+#    with w_v > 0;
 #  * T = 0 verifies greedily: y_i is accepted when it is the first argmax of
 #    P_i, and the round emits the first argmax of the row where it stops.
 #

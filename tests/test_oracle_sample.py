@@ -1,7 +1,9 @@
 """Pins of the sampler oracle (Eq. 8): Philox4x32-10 against its published
 known-answer vectors, the fp32 logarithm against numpy's log, Gumbel moments
-(closed forms), Gumbel-max frequencies against softmax(z/T) (chi-square),
-greedy against numpy argmax, top-k support against a sort, lse closed forms."""
+(closed forms), the two-level Gumbel-max against the one-level one in its two
+degenerate cases (one chunk; one token per chunk), its frequencies against
+softmax(z/T) (chi-square), greedy against numpy argmax, top-k support against
+a sort, lse closed forms."""
 import json
 import math
 import os
@@ -81,7 +83,7 @@ def test_noise_streams_differ_by_seed_step_and_row():
 def test_gumbel_max_frequencies_follow_softmax(T, top_k):
     z = np.float32([0.3, -1.2, 1.1, 0.0, 2.0, -0.4])
     n = 30_000
-    y, _, _ = Sm.sample(np.tile(z, (n, 1)), T, top_k, 42, 7, chunk=4096)
+    y, _, _ = Sm.sample(np.tile(z, (n, 1)), T, top_k, 42, 7, rows_per_pass=4096)
     counts = np.bincount(y, minlength=6).astype(np.float64)
     S = Sm.support(z, top_k)
     zs = z[S].astype(np.float64) / T
@@ -100,7 +102,7 @@ def test_logq_is_the_log_probability_of_the_token():
     assert logq == pytest.approx(float(z[y]) / T - lse, rel=1e-12)
     # the empirical frequency of each token matches exp(log q)
     n = 20_000
-    ys, _, lq = Sm.sample(np.tile(z, (n, 1)), 0.8, 0, 3, 4, chunk=4096)
+    ys, _, lq = Sm.sample(np.tile(z, (n, 1)), 0.8, 0, 3, 4, rows_per_pass=4096)
     for v in range(4):
         sel = ys == v
         assert abs(sel.mean() - math.exp(lq[sel][0])) < 0.015
@@ -145,6 +147,93 @@ def test_sampled_token_is_in_the_top_k_support():
     y, _, _ = Sm.sample(z, 1.0, 5, 9, 1)
     for r in range(40):
         assert y[r] in set(Sm.support(z[r], 5).tolist())
+
+
+# ---- the two-level draw --------------------------------------------------------------------
+
+def test_one_chunk_is_the_flat_gumbel_max():
+    """With one chunk over the whole vocabulary the draw is the one-level
+    Gumbel-max: the first argmax of fl(fl(z/T) + g) with the token noise."""
+    rng = np.random.default_rng(11)
+    z = rng.normal(size=(30, 257)).astype(np.float32) * np.float32(2.0)
+    for T in (1.0, 0.6):
+        y, _, _ = Sm.sample(z, T, 0, 5, 8, chunk=257)
+        zt = (z / np.float32(T)).astype(np.float32)
+        for r in range(30):
+            key = (zt[r] + Sm.gumbel(5, 8, r, np.arange(257))).astype(np.float32)
+            assert y[r] == int(np.argmax(key))
+
+
+def test_unit_chunks_draw_from_the_chunk_stream():
+    """With one token per chunk, L_c = z_c/T exactly, so the draw is the
+    one-level Gumbel-max with the chunk noise (stream 3) in place of the
+    token noise."""
+    rng = np.random.default_rng(12)
+    z = rng.normal(size=(30, 100)).astype(np.float32) * np.float32(3.0)
+    for T, k in ((1.0, 0), (0.8, 0), (1.0, 9)):
+        y, _, _ = Sm.sample(z, T, k, 6, 2, chunk=1)
+        zt = (z / np.float32(T)).astype(np.float32)
+        for r in range(30):
+            key = (zt[r] + Sm.gumbel(6, 2, r, np.arange(100), stream=3)).astype(np.float32)
+            S = Sm.support(z[r], k)
+            masked = np.full(100, -np.inf, dtype=np.float32)
+            masked[S] = key[S]
+            assert y[r] == int(np.argmax(masked))
+
+
+def test_chunk_log_mass_brute_force():
+    """L_c against a scalar loop over each chunk's support tokens, with a
+    ragged last chunk and a chunk left empty by the support."""
+    rng = np.random.default_rng(13)
+    zt = rng.normal(size=(3, 37)) * 4.0
+    inside = rng.random((3, 37)) < 0.6
+    inside[1, 16:32] = False
+    L = Sm.chunk_log_mass(zt, inside, 16)
+    assert L.shape == (3, 3)
+    for r in range(3):
+        for c in range(3):
+            terms = [math.exp(zt[r, v]) for v in range(16 * c, min(37, 16 * c + 16)) if inside[r, v]]
+            if terms:
+                assert L[r, c] == pytest.approx(math.log(sum(terms)), rel=1e-13, abs=1e-13)
+            else:
+                assert L[r, c] == -np.inf
+
+
+@pytest.mark.parametrize("T,top_k", [(1.0, 0), (0.7, 0), (1.0, 11)])
+def test_two_level_frequencies_follow_softmax(T, top_k):
+    """Several chunks, the last ragged (V = 40 in chunks of 16), top-k
+    supports that cut chunks: the token frequencies follow softmax(z/T) over
+    the support (chi-square), and every token's log q is its log frequency."""
+    z = np.float32([0.3, -1.2, 1.1, 0.0, 2.0, -0.4, 0.9, 1.4, -2.0, 0.5,
+                    1.0, 1.0, -0.3, 0.2, 1.7, -1.1, 0.8, 0.1, 1.2, -0.6,
+                    0.4, 1.9, -0.9, 0.6, 1.3, -1.5, 0.7, 0.0, 1.6, -0.2,
+                    1.1, 0.3, -0.7, 1.8, 0.2, -1.3, 0.9, 1.5, -0.1, 1.0])
+    n = 60_000
+    y, _, lq = Sm.sample(np.tile(z, (n, 1)), T, top_k, 43, 9, rows_per_pass=4096)
+    S = Sm.support(z, top_k)
+    counts = np.bincount(y, minlength=40).astype(np.float64)
+    assert counts.sum() == counts[S].sum()
+    zs = z[S].astype(np.float64) / float(np.float32(T))
+    p = np.exp(zs - zs.max())
+    p = p / p.sum()
+    assert scipy.stats.chisquare(counts[S], p * n).pvalue > 1e-3
+    for v in S[:5]:
+        sel = y == v
+        assert abs(np.exp(lq[sel][0]) - p[list(S).index(v)]) < 1e-12
+
+
+def test_chunk_choice_and_token_of_the_detail():
+    """The reported chunk keys are fl(fl32(L_c) + h_c), the chosen chunk is
+    their first argmax and the token lies in it."""
+    rng = np.random.default_rng(14)
+    z = rng.normal(size=(8, 100)).astype(np.float32)
+    y, _, _, K, c = Sm.sample(z, 1.0, 0, 3, 1, detail=True)
+    inside = np.ones(z.shape, dtype=bool)
+    L = Sm.chunk_log_mass(z.astype(np.float64), inside)
+    for r in range(8):
+        h = Sm.gumbel(3, 1, r, np.arange(7), stream=3)
+        assert np.array_equal(K[r], (L[r].astype(np.float32) + h).astype(np.float32))
+        assert c[r] == int(np.argmax(K[r])) and y[r] // 16 == c[r]
 
 
 # ---- Markov-corrected sampling (Eq. 7-8) ----------------------------------------------------
