@@ -795,7 +795,7 @@ def main():
                                 ("argmax in the vocabulary head's epilogue" +
                                  ("" if rig.keep_logits else ", logits not written")
                                  if rig.temperature == 0 else
-                                 "per-position sampler overlapping the head's last round"))
+                                 "two-level Gumbel-max sampler after the head"))
                                if rig.fused_head else "ldr_draft_step + ldr_sample"),
                    "views": {0: "window + summary + boundary", 1: "no window", 2: "no summary",
                              4: "no boundary"}.get(s.drop_views, f"drop {s.drop_views}")},

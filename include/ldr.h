@@ -149,11 +149,10 @@ int ldr_views_layout(const ldr_config* cfg, size_t offsets[5]);
 size_t ldr_tiled_bytes(int32_t rows, int32_t cols);
 
 /* Enqueues a tiled copy of the row-major bf16 matrix src [rows][cols] (dev,
- * row stride ld elements) into dst (dev, dst_bytes >= ldr_tiled_bytes):
- * blocks of 256 rows x 32 columns, block (r / 256, c / 32) at element offset
- * ((r / 256) * (cols / 32) + c / 32) * 8192 holding its 256 rows of 32
- * elements one after another; rows from `rows` up to the next multiple of 256
- * are zero. One K block of 256 weight rows is then one contiguous 16 KB
+ * row stride ld elements) into dst (dev, dst_bytes >= ldr_tiled_bytes): column
+ * blocks of 32, element (r, c) at element offset (c / 32) * R * 32 + r * 32 +
+ * c % 32 with R = rows rounded up to a multiple of 256; rows from `rows` to R
+ * are zero. One K block of any run of weight rows is then one contiguous
  * stretch for the vocabulary head's GEMM (App. B.1 shares the target's head,
  * V x hidden, so this is a one-time copy of a frozen weight). Needs
  * cols % 32 == 0, ld >= cols and 16-byte aligned pointers and rows (ld % 8
@@ -276,14 +275,12 @@ size_t ldr_draft_step_sample_workspace_bytes(const ldr_config* cfg, int32_t batc
 
 /* ldr_draft_step followed by per-position sampling of every row (Eq. 4 and
  * Eq. 8): tokens, lse and logq are those of ldr_sample(logits, batch * B, V,
- * temperature, top_k = 0, seed, step) on the step's logits. Greedy steps
- * (temperature 0) whose head reads its tiled copy (w->lm_head_tiled set and
- * batch * B > 64) take the argmax in the head's epilogue, from the fp32 logits
- * it has just computed, so the logits need not be written (logits = NULL):
- * tokens bit for bit the same. Other steps run the head and then ldr_sample's
- * kernels, and need the logits. (A sampling epilogue for T > 0 was measured
- * and dropped: with one workgroup per CU the head hides the per-token noise
- * arithmetic far worse than the separate sampler does.)
+ * temperature, top_k = 0, seed, step) on the step's logits, bit for bit. Greedy
+ * steps (temperature 0) whose head reads its tiled copy (w->lm_head_tiled set
+ * and batch * B > 64) take the argmax in the head's epilogue, from the fp32
+ * logits it has just computed, so the logits need not be written
+ * (logits = NULL). Other steps run the head and then ldr_sample's kernels, and
+ * need the logits.
  *   logits  dev fp32 [batch][B][V], or NULL on the fused greedy path
  *   tokens  dev int32 [batch][B]; lse, logq dev fp32 [batch][B]
  *   workspace dev, ldr_draft_step_sample_workspace_bytes(cfg, batch) bytes,
@@ -302,13 +299,19 @@ size_t ldr_sample_workspace_bytes(int32_t rows, int32_t vocab);
  * time and independently. temperature = 0: tokens[r] = argmax z (lowest index
  * on ties), lse[r] = that maximum, logq[r] = 0. temperature T > 0: support S =
  * all V tokens (top_k = 0) or the top_k largest logits (lower index first on
- * ties); tokens[r] = argmax over S of fl(fl(z_v / T) + g_v) (lowest index on
- * ties) with g_v = -log(-log(u_v)) Gumbel noise from Philox4x32-10 (key
- * (seed mod 2^32, seed div 2^32), counter (v div 4, r, step mod 2^32,
- * (step div 2^32) mod 2^30), word v mod 4, u = (2 (bits >> 9) + 1) 2^-24; a
- * step is unique below 2^62) and a fixed-operation fp32
- * logarithm, so the tokens are reproducible bit for bit on any IEEE machine;
- * lse[r] = log sum_{v in S} exp(z_v / T); logq[r] = z_y / T - lse[r].
+ * ties), and a two-level Gumbel-max, an exact draw from softmax(z/T) over S:
+ * the vocabulary is cut into chunks of 16 tokens (chunk c = tokens 16c ..
+ * 16c + 15), chunk c has log-mass L_c = log sum_{v in c, v in S} exp(z_v / T)
+ * (fp32), the chunk is the first argmax of fl(L_c + h_c) and the token the
+ * first argmax over that chunk's support tokens of fl(fl(z_v / T) + g_v).
+ * Noise: Philox4x32-10 with key (seed mod 2^32, seed div 2^32) and counter
+ * (e div 4, r, step mod 2^32, (step div 2^32) mod 2^30 + 2^30 s), word e mod 4,
+ * u = (2 (bits >> 9) + 1) 2^-24 and -log(-log(u)) with a fixed-operation fp32
+ * logarithm: g_v is entry v of stream s = 0, h_c entry c of stream s = 3 (a
+ * step is unique below 2^62). The token keys are reproducible bit for bit on
+ * any IEEE machine; L_c is an fp32 sum whose last bits depend on the order of
+ * its 16 terms (fixed here). lse[r] = log sum_{v in S} exp(z_v / T);
+ * logq[r] = z_y / T - lse[r].
  * top_k >= vocab is the full vocabulary; a negative top_k is LDR_EINVAL. With
  * 0 < top_k < vocab an extra pass per row selects the exact top_k support
  * (-0 and +0 compare equal).
@@ -319,23 +322,24 @@ int ldr_sample(const float* logits, int32_t rows, int32_t vocab, float temperatu
                float* logq, void* workspace, size_t workspace_bytes, void* stream);
 
 /* Bytes of the library's static device scratch behind ldr_sample_noalloc. */
-#define LDR_NOALLOC_SCRATCH_BYTES ((size_t)1 << 20)
+#define LDR_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
 
 /* ldr_sample for callers that cannot allocate device memory (code under HIP
  * graph capture, serving loops that forbid allocation): the same kernels,
  * tokens, lse and logq as ldr_sample with the same arguments, bit for bit, with
- * the per-chunk partials and the top-k supports in a file-scope device array of
- * LDR_NOALLOC_SCRATCH_BYTES bytes instead of a caller workspace. Each GPU the
- * library runs on holds its own copy of that array until the process ends; its
- * address is looked up once per device, on the first call with that device
- * current. The call allocates nothing (no hipMalloc, no library routine that
- * allocates). Every call on one GPU shares that GPU's array and leaves its
- * contents behind; nothing in it needs to start at zero (each launch writes
- * every entry it later reads), but calls whose stream work overlaps on the same
- * GPU race on it: serialise them (one stream, or events). Requests with
- * ldr_sample_workspace_bytes(rows, vocab) > LDR_NOALLOC_SCRATCH_BYTES (about
- * 40000 rows) return LDR_ESCRATCH before anything is enqueued; bad arguments
- * return LDR_EINVAL as in ldr_sample.
+ * the chunk log-masses, the partials and the top-k supports in a file-scope
+ * device array of LDR_NOALLOC_SCRATCH_BYTES bytes instead of a caller
+ * workspace. Each GPU the library runs on holds its own copy of that array
+ * until the process ends; its address is looked up once per device, on the
+ * first call with that device current. The call allocates nothing (no
+ * hipMalloc, no library routine that allocates). Every call on one GPU shares
+ * that GPU's array and leaves its contents behind; nothing in it needs to
+ * start at zero (each launch writes every entry it later reads), but calls
+ * whose stream work overlaps on the same GPU race on it: serialise them (one
+ * stream, or events). Requests with ldr_sample_workspace_bytes(rows, vocab) >
+ * LDR_NOALLOC_SCRATCH_BYTES (about 430 rows of a 151936-token vocabulary)
+ * return LDR_ESCRATCH before anything is enqueued; bad arguments return
+ * LDR_EINVAL as in ldr_sample.
  *   logits dev fp32 [rows][vocab]; tokens dev int32 [rows]; lse, logq dev fp32 [rows] */
 int ldr_sample_noalloc(const float* logits, int32_t rows, int32_t vocab, float temperature,
                        int32_t top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
@@ -380,8 +384,8 @@ size_t ldr_verify_workspace_bytes(int32_t batch, int32_t block, int32_t vocab);
  * first rejection, i, the round emits the first argmax of log w_v + g_v over
  * the residual w_v = [p_i(v) - q_i(v)]_+, every token with w_v > 0 as computed
  * in fp32; after B acceptances, and when w has no positive entry, it emits the
- * first argmax of fl(fl(P_v / T) + g_v) over the row (the drafting sampler's
- * rule). Noise: ldr_sample's Philox4x32-10 layout with the top two bits of the
+ * first argmax of fl(fl(P_v / T) + g_v) over the row (a one-level Gumbel-max).
+ * Noise: ldr_sample's Philox4x32-10 layout with the top two bits of the
  * last counter word set to a stream: u_i is word 0 of counter (i - 1, b, ...)
  * in stream 1, g_v token v of row b in stream 2; both through
  * u = (2 (bits >> 9) + 1) 2^-24, and g = -log(-log(u)) with ldr_sample's
@@ -409,10 +413,13 @@ int ldr_verify(const float* target_logits, const float* draft_logits, const floa
                int32_t* accepted, int32_t* next_token, int32_t* n_new, void* workspace,
                size_t workspace_bytes, void* stream);
 
-/* Writes the Gumbel noise ldr_sample uses: out[r][v] = g_v of row r, for
- * rows [0, rows) and tokens [0, vocab). out dev fp32 [rows][vocab]. */
-int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t rows, int32_t vocab, float* out,
-                    void* stream);
+/* Writes Gumbel noise of the samplers' layout: out[r][e] = -log(-log(u)) of
+ * entry e of row r in noise stream noise_stream (0: ldr_sample's token noise
+ * g, 3: its chunk noise h, 1 and 2: ldr_verify's), for rows [0, rows) and
+ * entries [0, vocab). out dev fp32 [rows][vocab]. LDR_EINVAL on a NULL out, a
+ * non-positive size or a stream outside 0 .. 3. */
+int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t noise_stream, int32_t rows,
+                    int32_t vocab, float* out, void* stream);
 
 /* A static string naming a status code. */
 const char* ldr_strerror(int status);

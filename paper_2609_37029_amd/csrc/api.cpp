@@ -128,10 +128,6 @@ struct ldr_views {
   int64_t* pos;
   const void* G;
   int32_t* status;  // device, 256 bytes
-  // ldr_draft_step_sample's second stream (default priority) and the events
-  // that fork to it and join it, created on the first call that needs them
-  mutable hipStream_t side = nullptr;
-  mutable hipEvent_t ev_fork = nullptr, ev_join = nullptr;
 };
 
 extern "C" {
@@ -276,9 +272,6 @@ int ldr_views_status(ldr_views* v, int clear, void* stream) {
 
 void ldr_views_destroy(ldr_views* v) {
   if (!v) return;
-  if (v->side) hipStreamDestroy(v->side);
-  if (v->ev_fork) hipEventDestroy(v->ev_fork);
-  if (v->ev_join) hipEventDestroy(v->ev_join);
   if (v->status) hipFree(v->status);
   delete v;
 }
@@ -342,17 +335,10 @@ struct FusedSample {
   void* parts;
 };
 
-// The tiled vocabulary head launched in two parts: column tiles [0, tiles_a),
-// then the event, then the rest.
-struct HeadSplit {
-  int tiles_a;
-  hipEvent_t after_a;
-};
-
 static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
                            float* logits, void* workspace, size_t workspace_bytes,
                            void* const* events, int32_t n_events, hipStream_t st,
-                           const FusedSample* fs = nullptr, const HeadSplit* split = nullptr) {
+                           const FusedSample* fs = nullptr) {
   if (!v || !anchor || !workspace || (!logits && !fs)) return LDR_EINVAL;
   const Shape& s = v->s;
   if (!weights_ok(s, w) || !aligned(workspace, kAlign) || (logits && !aligned(logits, 16)))
@@ -362,7 +348,7 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
   const WsPlan ws = plan_ws(s, batch);
   if (workspace_bytes < ws.bytes) return LDR_EINVAL;
   if (w->lm_head_tiled && (s.dtype != LDR_BF16 || !aligned(w->lm_head_tiled, 16) ||
-                           !gemm_tiled_supported(M, s.vocab, s.hidden, 1)))
+                           !gemm_tiled_supported(M, s.vocab, s.hidden)))
     return LDR_EINVAL;
   // The tiled head computes 256-row tiles: below 65 rows the row-major head's
   // 16- to 64-row tiles stream the same weights with less MFMA work.
@@ -447,11 +433,6 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
           HeadSampleArgs hs{};
           hs.parts = fs->parts; hs.store_logits = logits != nullptr;
           e = launch_gemm_tiled_argmax(g, hs, fs->tokens, fs->lse, fs->logq, st);
-        } else if (tiled_head && split) {
-          g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
-          e = launch_gemm_tiled(g, st, 0, split->tiles_a);
-          if (e == hipSuccess) e = hipEventRecord(split->after_a, st);
-          if (e == hipSuccess) e = launch_gemm_tiled(g, st, split->tiles_a, -1);
         } else if (tiled_head) {
           g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
           e = launch_gemm_tiled(g, st);
@@ -509,60 +490,13 @@ int ldr_draft_step_sample(const ldr_views* v, const ldr_weights* w, const int32_
     FusedSample fs{tokens, lse, logq, extra};
     return draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st, &fs);
   }
-  // otherwise the head and the sampler (the same tokens as ldr_sample): logits needed
+  // otherwise the head and then the sampler (the same tokens as ldr_sample): logits needed
   if (!logits) return LDR_EINVAL;
-  // One row tile of the tiled head whose column tiles take more than one
-  // round over the CUs: the last, partial round leaves most CUs idle, so the
-  // sampler takes the vocabulary chunks the full rounds have finished on a
-  // second stream meanwhile; the rest of the chunks and the merge follow on
-  // the caller's stream once both are done.
-  constexpr int kCUs = 256;
-  const int width = gemm_tiled_width();
-  const int tiles = (s.vocab + width - 1) / width;
-  const int tiles_a = tiles / kCUs * kCUs;
-  const SamplePlan sp = sample_plan(rows, s.vocab);
-  const int nchunks = sp.n_a + sp.n_b, chunks_a = sp.n_a;
-  const bool overlap = temperature > 0.f && w->lm_head_tiled && rows > 64 && rows <= width &&
-                       tiles_a > 0 && tiles_a < tiles && sp.n_b > 0 &&
-                       sp.split == tiles_a * width;
-  if (!overlap) {
-    const int rc = draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st);
-    if (rc != LDR_OK) return rc;
-    return launch_sample(logits, rows, s.vocab, temperature, 0, seed, step, tokens, lse, logq,
-                         extra, align_up(sample_part_bytes(rows, s.vocab)), st) == hipSuccess
-               ? LDR_OK : LDR_EHIP;
-  }
-  if (!v->side) {
-    if (hipStreamCreateWithFlags(&v->side, hipStreamNonBlocking) != hipSuccess) {
-      v->side = nullptr;
-      return LDR_EHIP;
-    }
-  }
-  // stream-to-stream ordering on one device: no system-scope fence needed
-  constexpr unsigned kEv = hipEventDisableTiming | hipEventDisableSystemFence;
-  if (!v->ev_fork && hipEventCreateWithFlags(&v->ev_fork, kEv) != hipSuccess) {
-    v->ev_fork = nullptr;
-    return LDR_EHIP;
-  }
-  if (!v->ev_join && hipEventCreateWithFlags(&v->ev_join, kEv) != hipSuccess) {
-    v->ev_join = nullptr;
-    return LDR_EHIP;
-  }
-  const HeadSplit split{tiles_a, v->ev_fork};
-  const int rc = draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st, nullptr,
-                                 &split);
+  const int rc = draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st);
   if (rc != LDR_OK) return rc;
-  if (hipStreamWaitEvent(v->side, v->ev_fork, 0) != hipSuccess ||
-      launch_sample_partials(logits, rows, s.vocab, temperature, seed, step, extra, 0, chunks_a,
-                             v->side) != hipSuccess ||
-      hipEventRecord(v->ev_join, v->side) != hipSuccess ||
-      launch_sample_partials(logits, rows, s.vocab, temperature, seed, step, extra, chunks_a,
-                             nchunks, st) != hipSuccess ||
-      hipStreamWaitEvent(st, v->ev_join, 0) != hipSuccess ||
-      launch_sample_merge(logits, rows, s.vocab, temperature, extra, tokens, lse, logq, st) !=
-          hipSuccess)
-    return LDR_EHIP;
-  return LDR_OK;
+  return launch_sample(logits, rows, s.vocab, temperature, 0, seed, step, tokens, lse, logq,
+                       extra, align_up(sample_part_bytes(rows, s.vocab)), st) == hipSuccess
+             ? LDR_OK : LDR_EHIP;
 }
 
 int ldr_draft_step_events(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
@@ -653,11 +587,11 @@ int ldr_verify(const float* target_logits, const float* draft_logits, const floa
              ? LDR_OK : LDR_EHIP;
 }
 
-int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t rows, int32_t vocab, float* out,
-                    void* stream) {
-  if (!out || rows <= 0 || vocab <= 0) return LDR_EINVAL;
-  return launch_gumbel_fill(seed, step, rows, vocab, out, static_cast<hipStream_t>(stream)) ==
-                 hipSuccess ? LDR_OK : LDR_EHIP;
+int ldr_gumbel_fill(uint64_t seed, uint64_t step, int32_t noise_stream, int32_t rows,
+                    int32_t vocab, float* out, void* stream) {
+  if (!out || rows <= 0 || vocab <= 0 || noise_stream < 0 || noise_stream > 3) return LDR_EINVAL;
+  return launch_gumbel_fill(seed, step, noise_stream, rows, vocab, out,
+                            static_cast<hipStream_t>(stream)) == hipSuccess ? LDR_OK : LDR_EHIP;
 }
 
 }  // extern "C"

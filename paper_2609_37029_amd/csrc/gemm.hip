@@ -450,22 +450,30 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
 // ---------------------------------------------------------------------------
 // GEMM on tiled operands (the vocabulary head).
 //
-// Both operands arrive tiled: a [rows][K] matrix is stored as blocks of
-// TR = 256 rows by TK = 32 columns, block (r / TR, k / TK) at
-// ((r / TR) * (K / TK) + k / TK) * TR * TK, its rows contiguous (TK elements
-// each), rows past the matrix padded. One K block of one tile is then 16 KB of
-// consecutive memory that HBM streams at full rate; the same 256 rows read in
-// row-major order are 64-byte pieces 8 KB apart, which it serves at about half.
+// The activation rows arrive tiled in blocks of TR = 256 rows by TK = 32
+// columns, block (r / TR, k / TK) at ((r / TR) * (K / TK) + k / TK) * TR * TK,
+// its rows contiguous (TK elements each); the weight [N][K] in column blocks:
+// element (n, k) at (k / TK) * R * TK + n * TK + k % TK, R = N rounded up to
+// 256 (the layout ldr_tile_matrix writes). One K block of any run of weight
+// rows, and of one activation row tile, is then consecutive memory that HBM
+// streams at full rate; the same rows read in row-major order are 64-byte
+// pieces 8 KB apart, which it serves at about half.
 //
-// A workgroup of 8 waves owns a 256 x 256 output tile (wave tiles of 128 x 64).
+// A workgroup of 8 waves owns a 256 x HB output tile, HB = 304 = 19 x 16
+// columns: the vocabulary of 151936 then makes 500 tiles, under two rounds
+// over the 256 CUs (256-column tiles would make 594: a third round of 82
+// tiles that runs nearly as long as a full one, at one CU's streaming rate).
+// The waves compute 128 x 80 each (8 x 5 MFMA tiles), so the tile computes
+// HW = 320 columns; the last 16 belong to the next tile and are dropped.
 // Waves 0-3 and 4-7 form two groups that share the four SIMDs pairwise and take
-// turns, one barrier apart: while one group issues its 32 MFMAs for the current
+// turns, one barrier apart: while one group issues its 40 MFMAs for the current
 // K block, the other reads its fragments of that block from LDS and starts the
-// DMA (global_load_lds) of its half of the block D steps ahead: group 0 the A
-// rows, group 1 the W rows. Each SIMD's matrix unit is thus fed by one wave or
-// the other most of the time. Stages of 512 rows x 64 B live in NB = 4 LDS
-// buffers; the 16-byte chunk c of stage row r sits at chunk c ^ ((r >> 2) & 3),
-// so the 16 lanes of a fragment read hit 64 distinct banks.
+// DMA (global_load_lds) of its part of the block D steps ahead: group 0 the
+// 256 A rows (16 KB), group 1 the 320 W rows (20 KB). Each SIMD's matrix unit
+// is thus fed by one wave or the other most of the time. Stages of 576 rows x
+// 64 B live in NB = 4 LDS buffers; the 16-byte chunk c of stage row r sits at
+// chunk c ^ ((r >> 2) & 3), so the 16 lanes of a fragment read hit 64 distinct
+// banks.
 //
 // Ordering (t = K block, barriers numbered from the start of the loop):
 //  * group 0 reads block t between barriers 2t and 2t + 1, group 1 between
@@ -476,6 +484,7 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
 //    2t + 2, after which block t + 1 is whole in LDS for both groups.
 constexpr int TR = 256, TK = 32;
 constexpr long TBLK = (long)TR * TK;
+constexpr int HB = 304, HW = 320;
 
 __device__ inline int tile_swz(int r) { return (r >> 2) & 3; }
 
@@ -490,35 +499,56 @@ __device__ inline void head_combine(HeadPart& a, const HeadPart& b) {
 template <bool SAMPLE>
 __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSampleArgs hs) {
   constexpr int NB = 4, D = NB - 1;
-  constexpr int STAGE = 2 * TR * TK * 2;   // bytes: A rows 0..255, W rows 256..511
-  constexpr int MT = 8, NT = 4;            // 16 x 16 MFMA tiles per wave: 128 x 64
+  constexpr int STAGE = (TR + HW) * TK * 2;   // bytes: A rows 0..255, W rows 256..575
+  constexpr int MT = 8, NT = 5;               // 16 x 16 MFMA tiles per wave: 128 x 80
+  constexpr int QA = TR / 64, QW = HW / 64;   // DMA issues per lane: 4 (A), 5 (W)
   __shared__ __attribute__((aligned(1024))) uint8_t S0[STAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t S1[STAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t S2[STAGE];
   __shared__ __attribute__((aligned(1024))) uint8_t S3[STAGE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = wave >> 2, wq = wave & 3;
-  const int wm = grp, wn = wq;   // output rows wm * 128 .., columns wn * 64 ..
-  const int nkb = a.K / TK, kper = nkb / a.splits, kb0 = blockIdx.z * kper;
-  const int ct = blockIdx.x + hs.col_tile0;   // column tile
-  const uint16_t* tile =
-      grp == 0 ? static_cast<const uint16_t*>(a.A) + (long)blockIdx.y * nkb * TBLK
-               : static_cast<const uint16_t*>(a.W) + (long)ct * nkb * TBLK;
-  // DMA: wave wq of a group moves rows wq * 64 + q * 16 + lane / 4 of its
-  // operand (4 lanes per 64-byte row, lane & 3 = destination chunk).
-  const uint16_t* src[4];
-  int dst[4];
+  const int wm = grp, wn = wq;   // output rows wm * 128 .., columns wn * 80 ..
+  const int nkb = a.K / TK;
+  const int ct = blockIdx.x, n0 = ct * HB;
+  // DMA: wave wq of group 0 moves A rows wq * 64 + q * 16 + lane / 4, of group 1
+  // W rows wq * 80 + q * 16 + lane / 4 (4 lanes per 64-byte row, lane & 3 = the
+  // destination chunk); W rows past the padded matrix read its last row.
+  const uint16_t* src[QW];
+  int dst[QW];
+  long kstride;
+  if (grp == 0) {
+    const uint16_t* tile = static_cast<const uint16_t*>(a.A) + (long)blockIdx.y * nkb * TBLK;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int r = wq * 64 + q * 16 + (lane >> 2);
-    src[q] = tile + (long)kb0 * TBLK + r * TK + (((lane & 3) ^ tile_swz(r)) * 8);
-    dst[q] = (grp * TR + wq * 64 + q * 16) * 64;
+    for (int q = 0; q < QW; ++q) {
+      const int r = wq * 64 + (q < QA ? q : 0) * 16 + (lane >> 2);
+      src[q] = tile + r * TK + (((lane & 3) ^ tile_swz(r)) * 8);
+      dst[q] = (wq * 64 + (q < QA ? q : 0) * 16) * 64;
+    }
+    kstride = TBLK;
+  } else {
+    const long R = a.ldw;   // padded weight rows of one column block
+#pragma unroll
+    for (int q = 0; q < QW; ++q) {
+      const int lr = wq * 80 + q * 16 + (lane >> 2);
+      const long gr = min((long)n0 + lr, R - 1);
+      src[q] = static_cast<const uint16_t*>(a.W) + gr * TK +
+               (((lane & 3) ^ tile_swz(TR + lr)) * 8);
+      dst[q] = (TR + wq * 80 + q * 16) * 64;
+    }
+    kstride = R * TK;
   }
-  // Blocks past the split's end reload its last one (never read).
-  auto issue = [&](uint8_t* buf, int t) {
-    const long off = (long)min(t, kper - 1) * TBLK;
+  // Blocks past the end reload the last one (never read).
+  auto issue_a = [&](uint8_t* buf, int t) {
+    const long off = (long)min(t, nkb - 1) * kstride;
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
+    for (int q = 0; q < QA; ++q)
+      __builtin_amdgcn_global_load_lds(LDR_GP(src[q] + off), LDR_LP(buf + dst[q]), 16, 0, 0);
+  };
+  auto issue_w = [&](uint8_t* buf, int t) {
+    const long off = (long)min(t, nkb - 1) * kstride;
+#pragma unroll
+    for (int q = 0; q < QW; ++q)
       __builtin_amdgcn_global_load_lds(LDR_GP(src[q] + off), LDR_LP(buf + dst[q]), 16, 0, 0);
   };
   int aoff[MT], woff[NT];
@@ -529,7 +559,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
   }
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
-    const int r = TR + wn * 64 + j * 16 + (lane & 15);
+    const int r = TR + wn * 80 + j * 16 + (lane & 15);
     woff[j] = r * 64 + (((lane >> 4) ^ tile_swz(r)) * 16);
   }
   f32x4 acc[MT][NT];
@@ -539,14 +569,14 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   bf16x8 af[MT], bfr[NT];
 
-#define LDR_MEM(t, cur, nxt)                                                                   \
+#define LDR_MEM(t, cur, nxt, ISSUE)                                                            \
   {                                                                                            \
     sched_fence();                                                                             \
     _Pragma("unroll") for (int i = 0; i < MT; ++i) af[i] =                                     \
         __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + aoff[i]));            \
     _Pragma("unroll") for (int j = 0; j < NT; ++j) bfr[j] =                                    \
         __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + woff[j]));            \
-    issue(nxt, (t) + D);                                                                       \
+    ISSUE(nxt, (t) + D);                                                                       \
     sched_fence();                                                                             \
     wait_lgkmcnt0();                                                                           \
   }
@@ -560,21 +590,20 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
     __builtin_amdgcn_s_setprio(0);                                                             \
     sched_fence();                                                                             \
   }
-#define LDR_G0(t, cur, nxt) { LDR_MEM(t, cur, nxt) group_barrier(); LDR_MMA() wait_vmcnt<4 * (D - 1)>(); group_barrier(); }
-#define LDR_G1(t, cur, nxt) { LDR_MEM(t, cur, nxt) wait_vmcnt<4 * (D - 1)>(); group_barrier(); LDR_MMA() group_barrier(); }
-  issue(S0, 0);
-  issue(S1, 1);
-  issue(S2, 2);
+#define LDR_G0(t, cur, nxt) { LDR_MEM(t, cur, nxt, issue_a) group_barrier(); LDR_MMA() wait_vmcnt<QA * (D - 1)>(); group_barrier(); }
+#define LDR_G1(t, cur, nxt) { LDR_MEM(t, cur, nxt, issue_w) wait_vmcnt<QW * (D - 1)>(); group_barrier(); LDR_MMA() group_barrier(); }
+  if (grp == 0) { issue_a(S0, 0); issue_a(S1, 1); issue_a(S2, 2); }
+  else { issue_w(S0, 0); issue_w(S1, 1); issue_w(S2, 2); }
   wait_vmcnt<0>();
   group_barrier();
   if (grp == 0) {
-    for (int t = 0; t < kper; t += NB) {
+    for (int t = 0; t < nkb; t += NB) {
       LDR_G0(t, S0, S3) LDR_G0(t + 1, S1, S0) LDR_G0(t + 2, S2, S1) LDR_G0(t + 3, S3, S2)
     }
     group_barrier();   // pairs with group 1's offset barrier
   } else {
     group_barrier();   // offset: group 1 starts one barrier later
-    for (int t = 0; t < kper; t += NB) {
+    for (int t = 0; t < nkb; t += NB) {
       LDR_G1(t, S0, S3) LDR_G1(t + 1, S1, S0) LDR_G1(t + 2, S2, S1) LDR_G1(t + 3, S3, S2)
     }
   }
@@ -584,9 +613,10 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
 #undef LDR_MEM
   wait_vmcnt<0>();   // no DMA outlives the workgroup
   const int crow = (lane >> 4) * 4, ccol = lane & 15;
-  const int r0 = blockIdx.y * TR + wm * 128, c0 = ct * TR + wn * 64;
+  const int r0 = blockIdx.y * TR + wm * 128, c0 = n0 + wn * 80;
+  const int cend = min(a.N, n0 + HB);   // the tile's own columns
   if (!SAMPLE || hs.store_logits) {
-    float* out = static_cast<float*>(a.out) + (long)blockIdx.z * a.split_stride;
+    float* out = static_cast<float*>(a.out);
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -595,14 +625,14 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int row = r0 + i * 16 + crow + v;
-          if (row < a.M && col < a.N) out[(long)row * a.ldo + col] = acc[i][j][v];
+          if (row < a.M && col < cend) out[(long)row * a.ldo + col] = acc[i][j][v];
         }
       }
   }
   if constexpr (SAMPLE) {
     // Greedy epilogue (Eq. 8 at T = 0: the first argmax of each row). Per row
-    // of the tile: each lane's best of its 4 columns, the 16 lanes holding a
-    // row (its 64 columns of this wave) by DPP, the 4 waves of the row
+    // of the tile: each lane's best of its 5 columns, the 16 lanes holding a
+    // row (its 80 columns of this wave) by DPP, the 4 waves of the row
     // through LDS, one partial per (row, column tile).
     __shared__ HeadPart tab[TR][4];
     HeadPart* parts = static_cast<HeadPart*>(hs.parts);
@@ -614,7 +644,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int col = c0 + j * 16 + ccol;
-          if (col < a.N) head_combine(p, HeadPart{acc[i][j][v], col});
+          if (col < cend) head_combine(p, HeadPart{acc[i][j][v], col});
         }
         HeadPart o;
         o.key = dpp<0xB1>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0xB1, 0xF, 0xF, false);
@@ -655,18 +685,18 @@ __global__ void __launch_bounds__(64) head_argmax_merge_kernel(const HeadPart* p
   }
 }
 
-// Tiled copy of a row-major [rows][cols] 2-byte matrix: one thread per 16-byte
-// chunk of the destination; padding rows are zero.
+// Column-block copy of a row-major [rows][cols] 2-byte matrix (the weight
+// layout of the vocabulary head): one thread per 16-byte chunk of the
+// destination, whose column block kb holds R = rows rounded up to 256 rows
+// of TK elements; padding rows are zero.
 __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, long ld, int rows,
-                                                          int cols, uint16_t* dst, long chunks) {
-  const int nkb = cols / TK;
+                                                          long R, uint16_t* dst, long chunks) {
   for (long e = (long)blockIdx.x * blockDim.x + threadIdx.x; e < chunks;
        e += (long)gridDim.x * blockDim.x) {
-    const long blk = e / (TBLK / 8);
-    const int in = (int)(e % (TBLK / 8));
-    const int r = in / (TK / 8), c = (in % (TK / 8)) * 8;
-    const long row = (blk / nkb) * TR + r;
-    const int col = (int)(blk % nkb) * TK + c;
+    const long kb = e / (R * (TK / 8));
+    const long in = e % (R * (TK / 8));
+    const long row = in / (TK / 8);
+    const int col = (int)(kb * TK + (in % (TK / 8)) * 8);
     u32x4 v = u32x4{0u, 0u, 0u, 0u};
     if (row < rows) v = *reinterpret_cast<const u32x4*>(src + row * ld + col);
     *reinterpret_cast<u32x4*>(dst + e * 8) = v;
@@ -766,34 +796,31 @@ hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a,
   return launch_cfg<EPI_STORE>(p.cfg, grid, a, st);
 }
 
-bool gemm_tiled_supported(int M, int N, int K, int splits) {
-  return M > 0 && N > 0 && splits > 0 && K % (TK * 4 * splits) == 0;
+bool gemm_tiled_supported(int M, int N, int K) {
+  return M > 0 && N > 0 && K % (TK * 4) == 0;
 }
 
-hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st, int tile0, int ntiles) {
-  if (!gemm_tiled_supported(a.M, a.N, a.K, a.splits)) return hipErrorInvalidValue;
-  const int nt = (a.N + TR - 1) / TR;
-  if (ntiles < 0) ntiles = nt - tile0;
-  if (tile0 < 0 || ntiles <= 0 || tile0 + ntiles > nt) return hipErrorInvalidValue;
-  const dim3 grid(ntiles, (a.M + TR - 1) / TR, a.splits);
-  HeadSampleArgs hs{};
-  hs.col_tile0 = tile0;
-  hipLaunchKernelGGL((gemm_tiled_kernel<false>), grid, dim3(512), 0, st, a, hs);
+hipError_t launch_gemm_tiled(const GemmArgs& a0, hipStream_t st) {
+  if (!gemm_tiled_supported(a0.M, a0.N, a0.K) || a0.splits != 1) return hipErrorInvalidValue;
+  GemmArgs a = a0;
+  a.ldw = (a.N + TR - 1) / TR * TR;   // padded rows of a weight column block
+  const dim3 grid((a.N + HB - 1) / HB, (a.M + TR - 1) / TR, 1);
+  hipLaunchKernelGGL((gemm_tiled_kernel<false>), grid, dim3(512), 0, st, a, HeadSampleArgs{});
   return hipGetLastError();
 }
 
-int gemm_tiled_width() { return TR; }
-
 size_t head_sample_part_bytes(int rows, int vocab) {
-  return (size_t)rows * ((vocab + TR - 1) / TR) * sizeof(HeadPart);
+  return (size_t)rows * ((vocab + HB - 1) / HB) * sizeof(HeadPart);
 }
 
-hipError_t launch_gemm_tiled_argmax(const GemmArgs& a, const HeadSampleArgs& hs0, int32_t* tokens,
+hipError_t launch_gemm_tiled_argmax(const GemmArgs& a0, const HeadSampleArgs& hs0, int32_t* tokens,
                                     float* lse, float* logq, hipStream_t st) {
-  if (!gemm_tiled_supported(a.M, a.N, a.K, 1) || a.splits != 1) return hipErrorInvalidValue;
+  if (!gemm_tiled_supported(a0.M, a0.N, a0.K) || a0.splits != 1) return hipErrorInvalidValue;
+  GemmArgs a = a0;
+  a.ldw = (a.N + TR - 1) / TR * TR;
   HeadSampleArgs hs = hs0;
-  hs.nparts = (a.N + TR - 1) / TR;
-  const dim3 grid((a.N + TR - 1) / TR, (a.M + TR - 1) / TR, 1);
+  hs.nparts = (a.N + HB - 1) / HB;
+  const dim3 grid(hs.nparts, (a.M + TR - 1) / TR, 1);
   hipLaunchKernelGGL((gemm_tiled_kernel<true>), grid, dim3(512), 0, st, a, hs);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -808,8 +835,9 @@ hipError_t launch_tile_matrix(const void* src, long ld, int rows, int cols, void
                               hipStream_t st) {
   const long chunks = (long)tiled_elems(rows, cols) / 8;
   const long want = (chunks + 255) / 256, blocks = want < 8192 ? want : 8192;
+  const long R = (rows + TR - 1) / TR * TR;
   hipLaunchKernelGGL(tile_matrix_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(src), ld, rows, cols,
+                     static_cast<const uint16_t*>(src), ld, rows, R,
                      static_cast<uint16_t*>(dst), chunks);
   return hipGetLastError();
 }

@@ -159,13 +159,11 @@ inline bool gemm_plan_frag(const GemmPlan& p) { return p.cfg >= 6; }
 // Tile configuration and split-K factor; splits = 1 unless allow_split.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
-// bf16 GEMM on operands in the tiled layout of ldr_tile_matrix (A tiled over
-// its M rows, W over its N rows); fp32 out [splits][M][ldo]. Needs
-// K % (128 * splits) == 0.
-bool gemm_tiled_supported(int M, int N, int K, int splits);
-// Column tiles [tile0, tile0 + ntiles) of the output (ntiles < 0: to the end).
-hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st, int tile0 = 0, int ntiles = -1);
-int gemm_tiled_width();   // output columns per tile (and rows per row tile)
+// bf16 GEMM for the vocabulary head: A in 256-row tiles of 32-column blocks
+// (the final norm's tiled output), W [N][K] in the column-block layout of
+// ldr_tile_matrix; fp32 out [M][ldo]. Needs K % 128 == 0 and splits == 1.
+bool gemm_tiled_supported(int M, int N, int K);
+hipError_t launch_gemm_tiled(const GemmArgs& a, hipStream_t st);
 // The vocabulary head with greedy sampling (T = 0) fused into its epilogue:
 // per row and column tile the first argmax goes to `parts`, then one merge per
 // row writes the token, lse (its logit) and log q = 0. The logits are written
@@ -174,7 +172,6 @@ struct HeadSampleArgs {
   void* parts;        // head_sample_part_bytes(M, V) bytes
   int nparts;         // partials per row (set by the launcher)
   int store_logits;
-  int col_tile0;      // column tile of the launch's first workgroup column
 };
 size_t head_sample_part_bytes(int rows, int vocab);
 hipError_t launch_gemm_tiled_argmax(const GemmArgs& a, const HeadSampleArgs& hs, int32_t* tokens,
@@ -236,20 +233,24 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
                             int layer, hipStream_t st);
 
 // Sampler (sample.hip)
-// Vocabulary chunks of a row: n_a chunks of chunk_a tokens below `split`, then
-// n_b chunks of chunk_b tokens from it (n_b = 0: split = vocab).
-struct SamplePlan { int chunk_a, n_a, split, chunk_b, n_b; };
+// T = 0: greedy_splits chunks of greedy_chunk tokens per row. T > 0: nch
+// chunks of 16 tokens per row, their log-masses in rows of ldL floats, and
+// the chunk-key pass over key_splits pieces of key_chunk chunks per row.
+struct SamplePlan { int greedy_chunk, greedy_splits, nch, ldL, key_chunk, key_splits; };
 SamplePlan sample_plan(int rows, int vocab);
-int sample_splits(int rows, int vocab);   // chunks per row
-// The full-vocabulary sampler in pieces (top_k = 0): the partial pass over
-// chunks [c0, c1) of every row, and the merge of all chunks; ws as for
-// launch_sample.
-hipError_t launch_sample_partials(const float* logits, int rows, int vocab, float temperature,
-                                  uint64_t seed, uint64_t step, void* ws, int c0, int c1,
-                                  hipStream_t st);
-hipError_t launch_sample_merge(const float* logits, int rows, int vocab, float temperature,
-                               void* ws, int32_t* tokens, float* lse, float* logq,
-                               hipStream_t st);
+// Tokens per workgroup of the chunk log-mass pass over ntok tokens of `rows` rows.
+int chunk_lse_slice(int rows, int ntok);
+// The full-vocabulary sampler at T > 0 in pieces (top_k = 0): the chunk
+// log-masses of tokens [v0, v1) of every row (v0 a multiple of 16), then,
+// once all are written, the chunk keys, the merge and the in-chunk draw;
+// ws as for launch_sample.
+hipError_t launch_chunk_lse(const float* logits, int rows, int vocab, float temperature, void* ws,
+                            int v0, int v1, hipStream_t st);
+hipError_t launch_sample_finish(const float* logits, int rows, int vocab, float temperature,
+                                uint64_t seed, uint64_t step, void* ws, int32_t* tokens,
+                                float* lse, float* logq, hipStream_t st);
+// Bytes of the sampler's workspace before its top-k supports: the chunk
+// log-masses and the partials.
 size_t sample_part_bytes(int rows, int vocab);
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
@@ -275,7 +276,7 @@ hipError_t launch_topk_select(const float* logits, int rows, int vocab, int k, T
 // Device address of the static scratch of ldr_sample_noalloc on the current
 // GPU (sample.hip); looked up once per device.
 hipError_t noalloc_scratch(void** out);
-hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
-                              hipStream_t st);
+hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int stream, int rows, int vocab,
+                              float* out, hipStream_t st);
 
 }  // namespace ldr

@@ -1,20 +1,32 @@
 // Per-position sampling of the factorised proposal (Eq. 8).
 //
-// Each row of fp32 logits is split into vocabulary chunks. One workgroup per
-// (chunk, row) streams its logits once and keeps, per thread, the best
-// Gumbel-max key with its token and the running max / sum of exp(z/T) for the
-// log-normaliser; a block reduction writes one partial per chunk. Exact keys
-// are computed only for tokens that a cheap upper bound cannot rule out. A merge
-// kernel combines the chunks of a row in vocabulary order (lower token wins
-// ties) and writes the token, lse and log q(y).
+// T > 0: a two-level Gumbel-max, an exact draw from q = softmax(z/T) over the
+// support. The vocabulary is cut into chunks of 16 consecutive tokens; chunk c
+// has log-mass L_c = log sum_{v in c} exp(z_v/T). The chunk is the first
+// argmax of L_c + h_c (h_c Gumbel noise of stream 3), the token the first
+// argmax of z_v/T + g_v over that chunk (g_v Gumbel noise of stream 0):
+//  * chunk_lse_kernel streams the logits once (16-byte loads, four sweeps in
+//    flight per lane) and writes L_c: a lane holds 4 tokens of a chunk, the
+//    chunk's max and sum of exp(z/T - max) are reduced over its 4 lanes with
+//    DPP, in the pairwise order (t0 + t1) + (t2 + t3), ... that a 16-lane DPP
+//    reduction of one token per lane also gives (the vocabulary head's
+//    epilogue can write the same L_c);
+//  * chunk_sample_kernel runs the Gumbel-max over the L_c of a row like a
+//    one-level sampler over V/16 entries: per lane the running max / sum of
+//    exp(L_c) for the log-normaliser and the best key, exact keys computed
+//    only for entries that a cheap upper bound of the noise cannot rule out;
+//  * sample_merge_kernel combines those partials in chunk order (lower index
+//    wins ties), then draws the token inside the winning chunk, one lane per
+//    token, and writes the token, lse and log q(y).
+// T = 0 is the first argmax of the logits (sample_partial_kernel + merge).
 //
-// The noise is a pure function of (seed, step, row, token): Philox4x32-10
-// (Salmon et al., SC 2011; key = the seed, counter (v/4, row, step, stream 0));
-// one Philox block serves 4 consecutive tokens, 32 bits each, and a lane takes
-// 8 tokens (two blocks) at a time. The uniform u = (2 (bits >> 9) + 1) 2^-24
-// is exact, and g = -log(-log u) uses a log made of IEEE fp32 operations only
-// (no contraction, correctly rounded division), so the keys fl(fl(z/T) + g)
-// are reproducible bit for bit.
+// The noise is a pure function of (seed, step, stream, row, entry):
+// Philox4x32-10 (Salmon et al., SC 2011; key = the seed, counter (entry / 4,
+// row, step, stream)); one Philox block serves 4 consecutive entries, 32 bits
+// each. The uniform u = (2 (bits >> 9) + 1) 2^-24 is exact, and
+// g = -log(-log u) uses a log made of IEEE fp32 operations only (no
+// contraction, correctly rounded division), so every key fl(x + g) is
+// reproducible bit for bit.
 #include <mutex>
 
 #include "ldr_internal.h"
@@ -41,14 +53,28 @@ __device__ inline void combine(Partial& a, const Partial& b) {
 
 struct SampleArgs {
   const float* logits; int rows, vocab, chunk, splits;
-  int n_a, split, chunk_b;   // chunks below `split` are `chunk` tokens, from it `chunk_b`
   float T; uint64_t seed, step;
   Partial* part;
   const TopK* sel;  // top-k support per row, or null for the full vocabulary
   int row_mul, row_add;  // row r of the launch is logits row (and noise row) r * mul + add
-  int chunk0;            // vocabulary chunk of the launch's first workgroup column
   int vec;               // rows start on 16 bytes (V % 4 == 0, aligned logits): 16-byte loads
+  float* L;              // chunk log-masses [rows][ldL] (T > 0)
+  int ldL, nch;          // row stride of L (a multiple of 4) and chunks per row
 };
+
+constexpr int kChunk = 16;        // tokens per vocabulary chunk of the two-level draw
+constexpr uint32_t kChunkStream = 3;
+
+// One term exp(zt - m) of a chunk's sum and the chunk's log-mass m + log s:
+// the same operations wherever L_c is formed (no contraction).
+__device__ inline float chunk_term(float zt, float m) {
+#pragma clang fp contract(off)
+  return __builtin_amdgcn_exp2f((zt - m) * 1.44269504088896341f);
+}
+__device__ inline float chunk_log_mass(float m, float s) {
+#pragma clang fp contract(off)
+  return m == -INFINITY ? -INFINITY : m + __builtin_amdgcn_logf(s) * 0.693147180559945309f;
+}
 
 // Exact k-th largest logit of a row by radix selection on order_key (four
 // 8-bit digits, most significant first, LDS histograms), then the index cut
@@ -118,11 +144,10 @@ __global__ void __launch_bounds__(kSelThreads) topk_select_kernel(const float* l
   if (threadIdx.x == 0) sel[blockIdx.x] = TopK{prefix, v_cut};
 }
 
-// The lane's kGroup = 8 logits of a sweep at v: two 16-byte loads inside the
-// chunk [.., v1), else one load per token (-inf past v1).
-__device__ inline void load_group(const SampleArgs& a, const float* z, int v, int v1,
-                                  float (&zz)[kGroup]) {
-  if (a.vec && v + kGroup <= v1) {
+// The lane's kGroup = 8 values of a sweep at v: two 16-byte loads inside the
+// range [.., v1) when vec, else one load per entry (-inf past v1).
+__device__ inline void load_group(const float* z, int v, int v1, bool vec, float (&zz)[kGroup]) {
+  if (vec && v + kGroup <= v1) {
     const float4 x = *reinterpret_cast<const float4*>(z + v);
     const float4 y = *reinterpret_cast<const float4*>(z + v + 4);
     zz[0] = x.x; zz[1] = x.y; zz[2] = x.z; zz[3] = x.w;
@@ -139,30 +164,34 @@ __device__ void argmax_tokens(const SampleArgs& a, const float* z, int v0, int v
   constexpr int kSweep = kThreads * kGroup;
   const int lane_off = (int)threadIdx.x * kGroup;
   float znext[kGroup];
-  load_group(a, z, v0 + lane_off, v1, znext);
+  load_group(z, v0 + lane_off, v1, a.vec, znext);
   for (int vb = v0; vb < v1; vb += kSweep) {
     const int v = vb + lane_off;
     float zcur[kGroup];
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) zcur[i] = znext[i];
-    if (vb + kSweep < v1) load_group(a, z, v + kSweep, v1, znext);
+    if (vb + kSweep < v1) load_group(z, v + kSweep, v1, a.vec, znext);
 #pragma unroll
     for (int i = 0; i < kGroup; ++i)
       if (v + i < v1 && better(zcur[i], v + i, p.key, p.idx)) { p.key = zcur[i]; p.idx = v + i; }
   }
 }
 
-// Temperature sampling. Every lane keeps the lse partial of its tokens and the
-// best (key, token) of the candidates it evaluated. A token is a candidate
-// unless zt + bound(g) + margin < the lane's best key, which proves that its
-// exact key loses; the margin (1e-3 plus 1e-6 relative) covers the rounding of
-// the test and of the fixed-sequence log, whose error is below 1e-5 here.
-// Candidates go through a per-wave queue in LDS so that the exact key (two
-// logs) is computed 64 at a time by full waves.
-template <bool UNIT_T, bool TOPK>
-__device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0, int v1,
-                              Partial& p) {
-  const TopK sel = TOPK ? a.sel[r] : TopK{0u, 0};
+// Gumbel-max over the chunk log-masses L_c of row r, entries [c0, c1). Every
+// lane keeps the max / sum of exp(L_c) of its entries (so the row's lse is
+// log sum_c exp(L_c)) and the best (key, chunk) of the entries it evaluated
+// exactly. Per sweep of 8 entries a lane evaluates first the exact key of
+// its entry with the largest upper bound L_c + bound(h_c); the largest key of
+// the wave so far is then a lower bound of the row's best, and any other
+// entry is a candidate only unless L_c + bound(h_c) + margin < that bound,
+// which proves that its exact key loses (the margin, 1e-3 plus 1e-6
+// relative, covers the rounding of the test and of the fixed-sequence log,
+// whose error is below 1e-5 here). Chunks without support tokens
+// (L_c = -inf) take no part. Candidates go through a per-wave queue in LDS so
+// that their exact keys (two logs each) are computed 64 at a time by full
+// waves.
+__device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, int c1,
+                           Partial& p) {
   struct Cand { float zt; uint32_t bits; int v; };
   __shared__ Cand queue[kThreads / 64][128];
   const int lane = threadIdx.x & 63;
@@ -179,41 +208,50 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  auto load8 = [&](int v, float (&zz)[kGroup]) { load_group(a, z, v, v1, zz); };
   constexpr int kSweep = kThreads * kGroup;
   const int lane_off = (int)(threadIdx.x & ~63) * kGroup + lane * kGroup;
+  const uint64_t nrow = (uint64_t)r * a.row_mul + a.row_add;
   float znext[kGroup];
-  load8(v0 + lane_off, znext);
-  for (int vb = v0; vb < v1; vb += kSweep) {
+  load_group(Lr, c0 + lane_off, c1, true, znext);
+  for (int vb = c0; vb < c1; vb += kSweep) {
     const int v = vb + lane_off;
-    float zcur[kGroup];
-#pragma unroll
-    for (int i = 0; i < kGroup; ++i) zcur[i] = znext[i];
-    if (vb + kSweep < v1) load8(v + kSweep, znext);   // the next sweep's logits in flight
-    uint32_t bits[kGroup];
-    noise_group(a.seed, a.step, (uint64_t)r * a.row_mul + a.row_add, 0, (uint64_t)(v / kGroup),
-                bits);
     float zt[kGroup];
-    float gm = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i) zt[i] = znext[i];
+    if (vb + kSweep < c1) load_group(Lr, v + kSweep, c1, true, znext);
+    uint32_t bits[kGroup];
+    noise_group(a.seed, a.step, nrow, kChunkStream, (uint64_t)(v / kGroup), bits);
+    float gm = -INFINITY, ub[kGroup];
     bool in[kGroup];
+    int top = -1;
+    float top_ub = -INFINITY;
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) {
-      const float zv = zcur[i];
-      in[i] = v + i < v1;
-      if constexpr (TOPK) {
-        const uint32_t u = order_key(zv);
-        in[i] = in[i] && (u > sel.tau || (u == sel.tau && v + i <= sel.v_cut));
-      }
-      zt[i] = in[i] ? (UNIT_T ? zv : zv / a.T) : -INFINITY;  // IEEE division
-      gm = fmaxf(gm, zt[i]);
+      in[i] = v + i < c1 && zt[i] > -INFINITY;
+      gm = fmaxf(gm, in[i] ? zt[i] : -INFINITY);
+      ub[i] = zt[i] + gumbel_upper(bits[i]);
+      if (in[i] && (top < 0 || ub[i] > top_ub)) { top = i; top_ub = ub[i]; }
     }
     if (gm > p.m) { p.s *= __expf(p.m - gm); p.m = gm; }
+    // the lane's most promising entry, exactly; then the wave's best key
+    float zsel = 0.f;
+    uint32_t bsel = 0u;
+#pragma unroll
+    for (int i = 0; i < kGroup; ++i)
+      if (i == top) { zsel = zt[i]; bsel = bits[i]; }
+    if (top >= 0) {
+      const float key = __fadd_rn(zsel, gumbel_from_bits(bsel));
+      if (better(key, v + top, p.key, p.idx)) { p.key = key; p.idx = v + top; }
+    }
+    float bound = p.key;
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) bound = fmaxf(bound, __shfl_xor(bound, off));
 #pragma unroll
     for (int i = 0; i < kGroup; ++i) {
       const bool valid = in[i];
       if (valid) p.s += __expf(zt[i] - p.m);
-      const float margin = 1e-3f + 1e-6f * (fabsf(zt[i]) + fabsf(p.key));
-      const bool need = valid && !(zt[i] + gumbel_upper(bits[i]) + margin < p.key);
+      const float margin = 1e-3f + 1e-6f * (fabsf(zt[i]) + fabsf(bound));
+      const bool need = valid && i != top && !(ub[i] + margin < bound);
       const uint64_t mask = __ballot(need);
       if (need) {
         const int pos = qn + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
@@ -231,6 +269,89 @@ __device__ void sample_tokens(const SampleArgs& a, const float* z, int r, int v0
     }
   }
   if (qn > 0) drain(qn);
+}
+
+// Chunk log-masses of tokens [v0, v1) of one row (v0 a multiple of 16): each
+// lane takes 4 consecutive tokens, so 4 lanes hold a chunk. Whole groups of U
+// sweeps of kThreads * 4 tokens load without bounds checks (U loads in flight
+// per lane), the rest one guarded sweep at a time. Writes L_c for the chunks
+// it covers.
+template <bool UNIT_T, bool TOPK, bool VEC>
+__global__ void __launch_bounds__(kThreads) chunk_lse_kernel(SampleArgs a, int v_begin,
+                                                             int v_end, int slice) {
+  constexpr int U = 4, kSweep = kThreads * 4;
+  const int r = blockIdx.y;
+  const int v0 = v_begin + blockIdx.x * slice, v1 = min(v_end, v0 + slice);
+  const float* z = a.logits + ((long)r * a.row_mul + a.row_add) * a.vocab;
+  float* L = a.L + (long)r * a.ldL;
+  const TopK sel = TOPK ? a.sel[r] : TopK{0u, 0};
+  const float T = a.T;
+  const int t4 = 4 * (int)threadIdx.x;
+  // the chunk of the 4 tokens x at v (tokens at or past v1 are outside)
+  auto chunk = [&](int v, const float (&x)[4]) {
+    float zt[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      bool in = v + i < v1;
+      if constexpr (TOPK) in = in && in_support(sel, x[i], v + i);
+      zt[i] = in ? (UNIT_T ? x[i] : x[i] / T) : -INFINITY;  // IEEE division
+    }
+    float m = fmaxf(fmaxf(zt[0], zt[1]), fmaxf(zt[2], zt[3]));
+    m = fmaxf(m, dpp<0xB1>(m));   // the chunk's 4 lanes
+    m = fmaxf(m, dpp<0x4E>(m));
+    float e[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) e[i] = zt[i] > -INFINITY ? chunk_term(zt[i], m) : 0.f;
+    float sum = (e[0] + e[1]) + (e[2] + e[3]);
+    sum += dpp<0xB1>(sum);
+    sum += dpp<0x4E>(sum);
+    if ((threadIdx.x & 3) == 0 && v < v1) L[v / kChunk] = chunk_log_mass(m, sum);
+  };
+  int vb = v0;
+  for (; vb + U * kSweep <= v1; vb += U * kSweep) {
+    float x[U][4];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float* zp = z + vb + u * kSweep + t4;
+      if constexpr (VEC) {
+        const float4 t = *reinterpret_cast<const float4*>(zp);
+        x[u][0] = t.x; x[u][1] = t.y; x[u][2] = t.z; x[u][3] = t.w;
+      } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) x[u][i] = zp[i];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) chunk(vb + u * kSweep + t4, x[u]);
+  }
+  for (; vb < v1; vb += kSweep) {
+    const int v = vb + t4;
+    float x[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) x[i] = v + i < v1 ? z[v + i] : -INFINITY;
+    chunk(v, x);
+  }
+}
+
+// Gumbel-max over chunks [sp * chunk, ..) of the row's log-masses: one
+// partial (max / sum of exp(L), best key and chunk) per workgroup.
+__global__ void __launch_bounds__(kThreads) chunk_sample_kernel(SampleArgs a) {
+  const int sp = blockIdx.x, r = blockIdx.y;
+  const int c0 = sp * a.chunk, c1 = min(a.nch, c0 + a.chunk);
+  Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
+  chunk_keys(a, a.L + (long)r * a.ldL, r, c0, c1, p);
+  for (int off = 32; off >= 1; off >>= 1) {
+    Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
+              __shfl_xor(p.idx, off)};
+    combine(p, o);
+  }
+  __shared__ Partial red[kThreads / 64];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = p;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 1; w < kThreads / 64; ++w) combine(p, red[w]);
+    a.part[(long)r * a.splits + sp] = p;
+  }
 }
 
 // Eq. 7 for position i of every sequence: z[b][i][v] += (W_c E_c(y))[v] with
@@ -347,22 +468,13 @@ __global__ void __launch_bounds__(kMkThreads) markov_correct_kernel(
   }
 }
 
+// Greedy partial: the first argmax of chunk [sp * chunk, ..) of the row.
 __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) {
-  const int sp = blockIdx.x + a.chunk0, r = blockIdx.y;
-  const int v0 = sp < a.n_a ? sp * a.chunk : a.split + (sp - a.n_a) * a.chunk_b;
-  const int v1 = min(a.vocab, sp < a.n_a ? min(a.split, v0 + a.chunk) : v0 + a.chunk_b);
+  const int sp = blockIdx.x, r = blockIdx.y;
+  const int v0 = sp * a.chunk, v1 = min(a.vocab, v0 + a.chunk);
   const float* z = a.logits + ((long)r * a.row_mul + a.row_add) * a.vocab;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
-  if (a.T == 0.f) {
-    argmax_tokens(a, z, v0, v1, p);
-  } else if (a.sel) {
-    if (a.T == 1.f) sample_tokens<true, true>(a, z, r, v0, v1, p);
-    else sample_tokens<false, true>(a, z, r, v0, v1, p);
-  } else {
-    if (a.T == 1.f) sample_tokens<true, false>(a, z, r, v0, v1, p);
-    else sample_tokens<false, false>(a, z, r, v0, v1, p);
-  }
-  // block reduction of the partials
+  argmax_tokens(a, z, v0, v1, p);
   for (int off = 32; off >= 1; off >>= 1) {
     Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
               __shfl_xor(p.idx, off)};
@@ -377,39 +489,68 @@ __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) 
   }
 }
 
+// One wave per row: the partials in order. T = 0: the first argmax. T > 0:
+// the winning chunk c and lse = log sum_c exp(L_c); then lanes 0 .. 15 take
+// the tokens of chunk c (support members only), their exact keys
+// fl(fl(z_v/T) + g_v), and the first maximum is the token.
 __global__ void __launch_bounds__(64) sample_merge_kernel(SampleArgs a, int32_t* tokens,
                                                           float* lse, float* logq) {
-  const int r = blockIdx.x;
+  const int r = blockIdx.x, lane = threadIdx.x;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
-  for (int sp = threadIdx.x; sp < a.splits; sp += 64) combine(p, a.part[(long)r * a.splits + sp]);
+  for (int sp = lane; sp < a.splits; sp += 64) combine(p, a.part[(long)r * a.splits + sp]);
   for (int off = 32; off >= 1; off >>= 1) {
     Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
               __shfl_xor(p.idx, off)};
     combine(p, o);
   }
-  if (threadIdx.x == 0) {
-    const long g = (long)r * a.row_mul + a.row_add;
-    tokens[g] = p.idx;
-    if (a.T == 0.f) {
+  const long g = (long)r * a.row_mul + a.row_add;
+  const float* z = a.logits + g * a.vocab;
+  if (a.T == 0.f) {
+    if (lane == 0) {
+      tokens[g] = p.idx;
       lse[g] = p.key;
       logq[g] = 0.f;
-    } else {
-      const float l = p.m + logf(p.s);
-      lse[g] = l;
-      logq[g] = a.logits[g * a.vocab + p.idx] / a.T - l;
     }
+    return;
+  }
+  // the chunk's tokens: lane i < 16 takes token 16 c + i
+  const int v = p.idx * kChunk + lane;
+  float key = -INFINITY, zt = -INFINITY;
+  if (lane < kChunk && v < a.vocab) {
+    const float zv = z[v];
+    const bool in = !a.sel || in_support(a.sel[r], zv, v);
+    if (in) {
+      zt = a.T == 1.f ? zv : zv / a.T;
+      uint32_t w[4];
+      noise_block(noise_key(a.seed, a.step, 0), (uint32_t)g, (uint32_t)(v >> 2), w);
+      key = __fadd_rn(zt, gumbel_from_bits(w[v & 3]));
+    }
+  }
+  int best = key > -INFINITY ? v : 0x7fffffff;
+  for (int off = 8; off >= 1; off >>= 1) {   // lanes 0 .. 15: first maximum
+    const float k2 = __shfl_xor(key, off);
+    const int b2 = __shfl_xor(best, off);
+    const float z2 = __shfl_xor(zt, off);
+    if (better(k2, b2, key, best)) { key = k2; best = b2; zt = z2; }
+  }
+  if (lane == 0) {
+    const float l = p.m + logf(p.s);
+    tokens[g] = best;
+    lse[g] = l;
+    logq[g] = zt - l;
   }
 }
 
 __global__ void __launch_bounds__(kThreads) gumbel_fill_kernel(uint64_t seed, uint64_t step,
-                                                               int rows, int vocab, float* out) {
+                                                               uint32_t stream, int rows,
+                                                               int vocab, float* out) {
   const int groups = (vocab + kGroup - 1) / kGroup;
   const long total = (long)rows * groups;
   for (long i = blockIdx.x * (long)kThreads + threadIdx.x; i < total;
        i += (long)gridDim.x * kThreads) {
     const int r = (int)(i / groups), c = (int)(i % groups);
     uint32_t bits[kGroup];
-    noise_group(seed, step, (uint64_t)r, 0, (uint64_t)c, bits);
+    noise_group(seed, step, (uint64_t)r, stream, (uint64_t)c, bits);
 #pragma unroll
     for (int k = 0; k < kGroup; ++k) {
       const int v = c * kGroup + k;
@@ -421,48 +562,40 @@ __global__ void __launch_bounds__(kThreads) gumbel_fill_kernel(uint64_t seed, ui
 }  // namespace
 
 SamplePlan sample_plan(int rows, int vocab) {
-  // About 2048 workgroups (8 waves per SIMD; 4096 measured no faster): a
-  // chunk of one sweep times the largest power of two that keeps at least
-  // 2048 / rows chunks per row (from 2048 rows on, one chunk per row).
-  // Up to 256 rows and past 65536 tokens, the tokens from the last multiple
-  // of 65536 covered by whole 65536-token blocks of the vocabulary head's
-  // full rounds (256 column tiles of 256) take one-sweep chunks instead: that
-  // region is sampled after the head's last round (ldr_draft_step_sample), by
-  // many short workgroups; ldr_sample uses the same plan, so both calls give
-  // the same partials and the same results.
-  constexpr int sweep = kThreads * kGroup;
   SamplePlan p;
-  if (rows >= 2048) {
-    p.chunk_a = (vocab + sweep - 1) / sweep * sweep;
-    p.n_a = 1; p.split = vocab; p.chunk_b = sweep; p.n_b = 0;
-    return p;
-  }
+  // T = 0: a chunk of one sweep times the largest power of two that keeps
+  // at least 2048 / rows chunks per row (about 2048 workgroups; 4096 measured
+  // no faster), one chunk per row from 2048 rows on
+  constexpr int sweep = kThreads * kGroup;
   const long target = ((long)vocab * rows + 2047) / 2048;
   int chunk = sweep;
   while (chunk * 2L <= target && chunk < 32 * sweep) chunk *= 2;
-  p.chunk_a = chunk;
-  p.chunk_b = sweep;
-  const int tiles = (vocab + 255) / 256, full = tiles / 256 * 256;
-  const int split = full * 256;
-  if (rows <= 256 && full > 0 && split < vocab && split % chunk == 0) {
-    p.split = split;
-    p.n_a = split / chunk;
-    p.n_b = (vocab - split + sweep - 1) / sweep;
-  } else {
-    p.split = vocab;
-    p.n_a = (vocab + chunk - 1) / chunk;
-    p.n_b = 0;
-  }
+  if (rows >= 2048) chunk = (vocab + sweep - 1) / sweep * sweep;
+  p.greedy_chunk = chunk;
+  p.greedy_splits = (vocab + chunk - 1) / chunk;
+  // T > 0: 16-token chunks; the chunk-key pass takes one sweep of entries per
+  // workgroup
+  p.nch = (vocab + kChunk - 1) / kChunk;
+  p.ldL = (p.nch + 3) / 4 * 4;
+  p.key_chunk = sweep;
+  p.key_splits = (p.nch + sweep - 1) / sweep;
   return p;
 }
 
-int sample_splits(int rows, int vocab) {
-  const SamplePlan p = sample_plan(rows, vocab);
-  return p.n_a + p.n_b;
+int chunk_lse_slice(int rows, int ntok) {
+  // tokens per workgroup of chunk_lse_kernel: the range split evenly over
+  // max(1, 2048 / rows) workgroups per row (about 2048 in all: one round of
+  // resident workgroups), rounded up to whole sweeps of 1024 tokens
+  const int per_row = rows >= 2048 ? 1 : 2048 / rows;
+  const long even = ((long)ntok + per_row - 1) / per_row;
+  return (int)((even + 1023) / 1024 * 1024);
 }
 
 size_t sample_part_bytes(int rows, int vocab) {
-  return (size_t)rows * sample_splits(rows, vocab) * sizeof(Partial);
+  const SamplePlan p = sample_plan(rows, vocab);
+  const size_t L = ((size_t)rows * p.ldL * sizeof(float) + 255) / 256 * 256;
+  const int splits = p.greedy_splits > p.key_splits ? p.greedy_splits : p.key_splits;
+  return L + (size_t)rows * splits * sizeof(Partial);
 }
 
 // Static scratch of ldr_sample_noalloc: the sampler's partials and top-k
@@ -501,75 +634,97 @@ hipError_t launch_topk_select(const float* logits, int rows, int vocab, int k, T
   return hipGetLastError();
 }
 
+namespace {
+// Arguments of the sampler's kernels for `rows` rows, workspace ws (the
+// chunk log-masses, then the partials).
+SampleArgs sample_args(const float* logits, int rows, int vocab, float temperature,
+                       uint64_t seed, uint64_t step, void* ws, int row_mul, int row_add) {
+  const SamplePlan pl = sample_plan(rows, vocab);
+  SampleArgs a;
+  a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
+  a.seed = seed; a.step = step;
+  a.sel = nullptr; a.row_mul = row_mul; a.row_add = row_add;
+  a.vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0;
+  a.L = static_cast<float*>(ws);
+  a.ldL = pl.ldL; a.nch = pl.nch;
+  a.part = reinterpret_cast<Partial*>(static_cast<uint8_t*>(ws) +
+                                      ((size_t)rows * pl.ldL * sizeof(float) + 255) / 256 * 256);
+  if (temperature == 0.f) { a.chunk = pl.greedy_chunk; a.splits = pl.greedy_splits; }
+  else { a.chunk = pl.key_chunk; a.splits = pl.key_splits; }
+  return a;
+}
+
+hipError_t chunk_lse(const SampleArgs& a, int v0, int v1, hipStream_t st) {
+  if (v0 >= v1) return hipSuccess;
+  const int slice = chunk_lse_slice(a.rows, v1 - v0);
+  const dim3 grid((unsigned)((v1 - v0 + slice - 1) / slice), (unsigned)a.rows);
+  const bool unit = a.T == 1.f, topk = a.sel != nullptr;
+#define LDR_CL(U, K, V) \
+  hipLaunchKernelGGL((chunk_lse_kernel<U, K, V>), grid, dim3(kThreads), 0, st, a, v0, v1, slice)
+  if (a.vec) {
+    if (unit) { if (topk) LDR_CL(true, true, true); else LDR_CL(true, false, true); }
+    else { if (topk) LDR_CL(false, true, true); else LDR_CL(false, false, true); }
+  } else {
+    if (unit) { if (topk) LDR_CL(true, true, false); else LDR_CL(true, false, false); }
+    else { if (topk) LDR_CL(false, true, false); else LDR_CL(false, false, false); }
+  }
+#undef LDR_CL
+  return hipGetLastError();
+}
+
+hipError_t sample_finish(const SampleArgs& a, int32_t* tokens, float* lse, float* logq,
+                         hipStream_t st) {
+  if (a.T == 0.f)
+    hipLaunchKernelGGL(sample_partial_kernel, dim3(a.splits, a.rows), dim3(kThreads), 0, st, a);
+  else
+    hipLaunchKernelGGL(chunk_sample_kernel, dim3(a.splits, a.rows), dim3(kThreads), 0, st, a);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(sample_merge_kernel, dim3(a.rows), dim3(64), 0, st, a, tokens, lse, logq);
+  return hipGetLastError();
+}
+}  // namespace
+
 hipError_t launch_sample(const float* logits, int rows, int vocab, float temperature,
                          int top_k, uint64_t seed, uint64_t step, int32_t* tokens, float* lse,
                          float* logq, void* ws, size_t sel_off, hipStream_t st, int row_mul,
                          int row_add) {
-  SampleArgs a;
-  a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
-  a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
-  a.sel = nullptr; a.row_mul = row_mul; a.row_add = row_add;
-  a.vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0;
-  if (temperature > 0.f && top_k > 0 && top_k < vocab) {  // T = 0 is the argmax either way
-    TopK* sel = reinterpret_cast<TopK*>(static_cast<uint8_t*>(ws) + sel_off);
-    hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, logits, vocab,
-                       top_k, sel, row_mul, row_add);
-    const hipError_t e = hipGetLastError();
+  SampleArgs a = sample_args(logits, rows, vocab, temperature, seed, step, ws, row_mul, row_add);
+  if (temperature > 0.f) {
+    if (top_k > 0 && top_k < vocab) {  // T = 0 is the argmax either way
+      TopK* sel = reinterpret_cast<TopK*>(static_cast<uint8_t*>(ws) + sel_off);
+      hipLaunchKernelGGL(topk_select_kernel, dim3(rows), dim3(kSelThreads), 0, st, logits, vocab,
+                         top_k, sel, row_mul, row_add);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      a.sel = sel;
+    }
+    const hipError_t e = chunk_lse(a, 0, vocab, st);
     if (e != hipSuccess) return e;
-    a.sel = sel;
   }
-  const SamplePlan pl = sample_plan(rows, vocab);
-  a.chunk = pl.chunk_a; a.n_a = pl.n_a; a.split = pl.split; a.chunk_b = pl.chunk_b;
-  a.splits = pl.n_a + pl.n_b;
-  a.chunk0 = 0;
-  hipLaunchKernelGGL(sample_partial_kernel, dim3(a.splits, rows), dim3(kThreads), 0, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sample_merge_kernel, dim3(rows), dim3(64), 0, st, a, tokens, lse, logq);
-  return hipGetLastError();
+  return sample_finish(a, tokens, lse, logq, st);
 }
 
-namespace {
-SampleArgs full_vocab_args(const float* logits, int rows, int vocab, float temperature,
-                           uint64_t seed, uint64_t step, void* ws) {
-  SampleArgs a;
-  a.logits = logits; a.rows = rows; a.vocab = vocab; a.T = temperature;
-  a.seed = seed; a.step = step; a.part = static_cast<Partial*>(ws);
-  a.sel = nullptr; a.row_mul = 1; a.row_add = 0;
-  a.vec = vocab % 4 == 0 && reinterpret_cast<uintptr_t>(logits) % 16 == 0;
-  const SamplePlan pl = sample_plan(rows, vocab);
-  a.chunk = pl.chunk_a; a.n_a = pl.n_a; a.split = pl.split; a.chunk_b = pl.chunk_b;
-  a.splits = pl.n_a + pl.n_b;
-  a.chunk0 = 0;
-  return a;
-}
-}  // namespace
-
-hipError_t launch_sample_partials(const float* logits, int rows, int vocab, float temperature,
-                                  uint64_t seed, uint64_t step, void* ws, int c0, int c1,
-                                  hipStream_t st) {
-  SampleArgs a = full_vocab_args(logits, rows, vocab, temperature, seed, step, ws);
-  if (c0 < 0 || c1 > a.splits || c0 >= c1) return hipErrorInvalidValue;
-  a.chunk0 = c0;
-  hipLaunchKernelGGL(sample_partial_kernel, dim3(c1 - c0, rows), dim3(kThreads), 0, st, a);
-  return hipGetLastError();
+hipError_t launch_chunk_lse(const float* logits, int rows, int vocab, float temperature, void* ws,
+                            int v0, int v1, hipStream_t st) {
+  if (temperature <= 0.f || v0 < 0 || v1 > vocab || v0 % kChunk) return hipErrorInvalidValue;
+  return chunk_lse(sample_args(logits, rows, vocab, temperature, 0, 0, ws, 1, 0), v0, v1, st);
 }
 
-hipError_t launch_sample_merge(const float* logits, int rows, int vocab, float temperature,
-                               void* ws, int32_t* tokens, float* lse, float* logq,
-                               hipStream_t st) {
-  const SampleArgs a = full_vocab_args(logits, rows, vocab, temperature, 0, 0, ws);
-  hipLaunchKernelGGL(sample_merge_kernel, dim3(rows), dim3(64), 0, st, a, tokens, lse, logq);
-  return hipGetLastError();
+hipError_t launch_sample_finish(const float* logits, int rows, int vocab, float temperature,
+                                uint64_t seed, uint64_t step, void* ws, int32_t* tokens,
+                                float* lse, float* logq, hipStream_t st) {
+  return sample_finish(sample_args(logits, rows, vocab, temperature, seed, step, ws, 1, 0),
+                       tokens, lse, logq, st);
 }
 
-hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int rows, int vocab, float* out,
-                              hipStream_t st) {
+hipError_t launch_gumbel_fill(uint64_t seed, uint64_t step, int stream, int rows, int vocab,
+                              float* out, hipStream_t st) {
   const long groups = (long)rows * ((vocab + kGroup - 1) / kGroup);
   long blocks = (groups + kThreads - 1) / kThreads;
   if (blocks > 8192) blocks = 8192;
   hipLaunchKernelGGL(gumbel_fill_kernel, dim3((int)(blocks > 0 ? blocks : 1)), dim3(kThreads),
-                     0, st, seed, step, rows, vocab, out);
+                     0, st, seed, step, (uint32_t)stream, rows, vocab, out);
   return hipGetLastError();
 }
 

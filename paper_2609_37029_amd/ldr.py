@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libldr.so")
 
 LDR_OK, LDR_EINVAL, LDR_ERANGE, LDR_EHIP, LDR_ENOMEM, LDR_ESCRATCH = 0, -1, -2, -3, -4, -5
-NOALLOC_SCRATCH_BYTES = 1 << 20   # LDR_NOALLOC_SCRATCH_BYTES
+NOALLOC_SCRATCH_BYTES = 16 << 20   # LDR_NOALLOC_SCRATCH_BYTES
 LDR_F32, LDR_BF16 = 0, 1
 
 
@@ -85,7 +85,7 @@ def _lib():
             "ldr_sample_workspace_bytes": (SZ, [I32, I32]),
             "ldr_sample": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P, P, P,
                                           SZ, P]),
-            "ldr_gumbel_fill": (ctypes.c_int, [U64, U64, I32, I32, P, P]),
+            "ldr_gumbel_fill": (ctypes.c_int, [U64, U64, I32, I32, I32, P, P]),
             "ldr_sample_noalloc": (ctypes.c_int, [P, I32, I32, ctypes.c_float, I32, U64, U64, P, P,
                                                   P, P]),
             "ldr_sample_markov": (ctypes.c_int, [P, I32, I32, I32, P, P, P, I32, I32,
@@ -426,10 +426,11 @@ def sample_noalloc(logits: torch.Tensor, temperature: float, top_k: int, seed: i
     return out
 
 
-def gumbel_fill(seed: int, step: int, rows: int, vocab: int, device="cuda", stream=None):
+def gumbel_fill(seed: int, step: int, rows: int, vocab: int, noise_stream: int = 0,
+                device="cuda", stream=None):
     out = torch.empty(rows, vocab, dtype=torch.float32, device=device)
-    _check(_lib().ldr_gumbel_fill(int(seed), int(step), rows, vocab, _ptr(out), _stream(stream)),
-           "ldr_gumbel_fill")
+    _check(_lib().ldr_gumbel_fill(int(seed), int(step), int(noise_stream), rows, vocab, _ptr(out),
+                                  _stream(stream)), "ldr_gumbel_fill")
     return out
 
 

@@ -8,6 +8,7 @@ import numpy as np
 import torch
 
 import synth
+from oracle import sample as OS
 from oracle import views as OV
 
 
@@ -163,3 +164,39 @@ def residual_decision(d, bonus_tok, rel_err, key_abs=1e-5):
     t = int(np.argmax(lo))
     clean = (not can_be_empty) and lo[t] > np.max(np.delete(hi, t))
     return clean, valid
+
+
+# fp32 slack of a GPU chunk key: its log-mass is an fp32 sum of 16 exponentials
+# and an fp32 logarithm (a few ulp of |L|, |L| up to ~30 here)
+CHUNK_KEY_ABS, CHUNK_KEY_REL = 2e-5, 2e-6
+
+
+def draw_near_tie(z_ref, y_ref, y_gpu, row, T, seed, step, e, top_k=0):
+    """Asserts that the GPU token y_gpu, drawn with the oracle's noise from
+    logits within e (max |dz| / T) of the oracle's z_ref [V], is the oracle's
+    two-level draw y_ref or a near tie of it at the level where the two part:
+    the chunk keys L_c + h_c of the two chunks within 2e plus the fp32 slack of
+    a chunk key (a log-mass moves by at most max |dz| / T), then the token keys
+    z_v / T + g_v inside the GPU's chunk within 2e of that chunk's best.
+    Returns True where the tokens differ."""
+    if y_gpu == y_ref:
+        return False
+    z = np.asarray(z_ref, dtype=np.float64)
+    V = z.shape[0]
+    inside = np.zeros((1, V), dtype=bool)
+    inside[0, OS.support(np.asarray(z_ref, dtype=np.float32), top_k)] = True
+    T32 = float(np.float32(T))
+    assert inside[0, y_gpu], (row, y_gpu)
+    c_o, c_g = int(y_ref) // OS.CHUNK, int(y_gpu) // OS.CHUNK
+    if c_o != c_g:
+        L = OS.chunk_log_mass(z[None] / T32, inside)[0]
+        h = OS.gumbel(seed, step, row, np.array([c_o, c_g]), stream=OS.CHUNK_STREAM)
+        k = L[[c_o, c_g]] + h.astype(np.float64)
+        slack = CHUNK_KEY_ABS + CHUNK_KEY_REL * np.abs(k).max()
+        assert k[0] - k[1] <= 2 * e + slack, (row, c_o, c_g, k[0] - k[1], e)
+    v = np.arange(c_g * OS.CHUNK, min(V, (c_g + 1) * OS.CHUNK))
+    v = v[inside[0, v]]
+    key = z[v] / T32 + OS.gumbel(seed, step, row, v).astype(np.float64)
+    kg = key[list(v).index(int(y_gpu))]
+    assert key.max() - kg <= 2 * e + 1e-6, (row, int(v[np.argmax(key)]), int(y_gpu), e)
+    return True

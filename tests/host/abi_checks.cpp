@@ -150,7 +150,7 @@ static void entry_points() {
   EXPECT(ldr_sample(f, 256, 151936, -1.f, 0, 0, 0, t, f, f, fake, sws, nullptr) == LDR_EINVAL);
   EXPECT(ldr_sample(f, 256, 151936, 1.f, -1, 0, 0, t, f, f, fake, sws, nullptr) == LDR_EINVAL);
   EXPECT(ldr_sample(f, 256, 151936, 1.f, 0, 0, 0, t, f, f, fake, sws - 1, nullptr) == LDR_EINVAL);
-  EXPECT(ldr_sample_noalloc(f, 70000, 16, 1.f, 0, 0, 0, t, f, f, nullptr) == LDR_ESCRATCH);
+  EXPECT(ldr_sample_noalloc(f, 600000, 16, 1.f, 0, 0, 0, t, f, f, nullptr) == LDR_ESCRATCH);
   EXPECT(ldr_sample_noalloc(nullptr, 4, 16, 1.f, 0, 0, 0, t, f, f, nullptr) == LDR_EINVAL);
   const int nr = ldr_sample_noalloc(f, 4, 16, 1.f, 0, 0, 0, t, f, f, nullptr);
   EXPECT(nr == LDR_EHIP || nr == LDR_OK);           // no device: the scratch lookup fails
@@ -167,7 +167,8 @@ static void entry_points() {
                     nullptr) == LDR_EINVAL);
   EXPECT(ldr_verify(f, f, f, t, 16, 16, 151936, 1.f, 0, 0, 0, t, t, t, fake, vws - 1,
                     nullptr) == LDR_EINVAL);
-  EXPECT(ldr_gumbel_fill(0, 0, 0, 10, f, nullptr) == LDR_EINVAL);
+  EXPECT(ldr_gumbel_fill(0, 0, 0, 0, 10, f, nullptr) == LDR_EINVAL);
+  EXPECT(ldr_gumbel_fill(0, 0, 4, 1, 10, f, nullptr) == LDR_EINVAL);
   for (int code = -10; code <= 5; ++code) EXPECT(ldr_strerror(code) != nullptr);
 }
 

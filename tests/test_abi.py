@@ -86,7 +86,8 @@ def test_host_validation_needs_no_gpu(L):
     assert lib.ldr_draft_step(None, None, None, None, None, 0, None) == L.LDR_EINVAL
     assert lib.ldr_sample(None, 4, 10, 1.0, 0, 0, 0, None, None, None, None, 0, None) == \
         L.LDR_EINVAL
-    assert lib.ldr_gumbel_fill(0, 0, 0, 10, None, None) == L.LDR_EINVAL
+    assert lib.ldr_gumbel_fill(0, 0, 0, 0, 10, None, None) == L.LDR_EINVAL
+    assert lib.ldr_gumbel_fill(0, 0, 4, 1, 10, None, None) == L.LDR_EINVAL
     fake = ctypes.c_void_p(1 << 20)   # aligned, never dereferenced: validation fails first
     ws = lib.ldr_sample_workspace_bytes(2, 64)
     for args in ((None, 2, 2, 64, fake, fake, fake, 8, L.LDR_BF16),   # no logits
@@ -133,7 +134,8 @@ def test_draft_step_launch_sequence():
 
 
 def test_tiled_layout_sizes_and_validation(L):
-    """ldr_tiled_bytes: rows padded to 256, columns in blocks of 32; bad
+    """ldr_tiled_bytes: rows padded to 256, columns in blocks of 32 (one block
+    holds all padded rows); bad
     arguments of ldr_tile_matrix are rejected on the host."""
     lib = L.lib()
     assert lib.ldr_tiled_bytes(1, 32) == 256 * 32 * 2

@@ -59,8 +59,9 @@ def test_logits_match_oracle(gpu_lib, shape, batch, prefix):
         check_logits(zc[b], ref[b], shape)
 
 
-# 66536 tokens: 260 column tiles of 256, more than one round over the 256 CUs
-MINI_BF16_WIDE_V = MINI_BF16.replace(name="mini-bf16-v66536", vocab=66536)
+# 90000 tokens: 297 column tiles of 304, more than one round over the 256 CUs,
+# the last tile 16 columns wide, its staged weight rows past the padded matrix
+MINI_BF16_WIDE_V = MINI_BF16.replace(name="mini-bf16-v90000", vocab=90000)
 
 
 @pytest.mark.parametrize("shape,batch,prefix", [(MINI_BF16, 5, 300), (MINI_BF16, 17, 150),
@@ -71,7 +72,8 @@ def test_tiled_head_matches_oracle_and_row_major(gpu_lib, shape, batch, prefix):
     head, from which they differ only in the fp32 summation order of the same
     bf16 products. 5 sequences: 80 rows in one ragged M tile; 17 sequences:
     272 rows, two M tiles, the last ragged; V = 5003: a ragged N tile;
-    V = 66536: 260 tiles, more workgroups than CUs."""
+    V = 90000: 297 tiles, more workgroups than CUs, a last tile of 16
+    columns."""
     s = shape
     p, w, dw, anchor = setup(gpu_lib, s, batch, prefix, tiled_head=True)
     z = gpu_lib.draft_step(p.views, dw, anchor)
@@ -96,8 +98,9 @@ def test_small_steps_keep_the_row_major_head(gpu_lib):
 
 
 def test_tile_matrix_layout(gpu_lib):
-    """ldr_tile_matrix: block (r / 256, c / 32) holds its 256 rows of 32
-    elements contiguously, padding rows zero; bit-exact (a pure copy)."""
+    """ldr_tile_matrix: column block c / 32 holds all R = 512 (padded) rows of
+    its 32 elements one after another, padding rows zero; bit-exact (a pure
+    copy)."""
     rows, cols, ld = 300, 96, 104
     g = torch.Generator(device="cuda").manual_seed(5)
     base = torch.randn(rows, ld, device="cuda", generator=g).to(torch.bfloat16)
@@ -106,7 +109,7 @@ def test_tile_matrix_layout(gpu_lib):
     assert t.numel() * 2 == gpu_lib.tiled_bytes(rows, cols) == 512 * cols * 2
     pad = torch.zeros(512, cols, dtype=torch.bfloat16, device="cuda")
     pad[:rows] = m
-    ref = pad.view(2, 256, cols // 32, 32).permute(0, 2, 1, 3).reshape(-1)
+    ref = pad.view(512, cols // 32, 32).permute(1, 0, 2).reshape(-1)
     torch.cuda.synchronize()
     assert torch.equal(t.view(torch.int16), ref.view(torch.int16))
 

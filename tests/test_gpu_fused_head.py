@@ -4,11 +4,8 @@ epilogue: the logits it writes are ldr_draft_step's bit for bit, and its
 tokens, lse and log q are the separate sampler's at T = 0 on those logits
 (the separate sampler is itself compared with the oracle in
 test_gpu_sample.py); without the logits it draws the same tokens. Sampled
-steps run the head and the sampler's kernels; when the head's column tiles
-take more than one round over the CUs (one row tile), the sampler works on
-the chunks of the finished rounds on a second stream while the head's last
-round runs, and the tokens, lse and log q are the separate sampler's bit for
-bit."""
+steps run the head and the sampler's kernels, and the tokens, lse and log q
+are the separate sampler's bit for bit."""
 import numpy as np
 import pytest
 import torch
@@ -103,7 +100,7 @@ def test_fused_greedy_tokens_against_the_oracle(gpu_lib):
 
 
 def test_fused_greedy_head_ties_and_full_size(gpu_lib):
-    """Qwen3-8B shape, batch 16: 594 column tiles of the 151936-token head."""
+    """Qwen3-8B shape, batch 16: 500 column tiles of the 151936-token head."""
     tok = check(gpu_lib, synth.QWEN3_8B, 16, 300, 0.0)
     assert len(set(tok.view(-1).tolist())) > 1
 
@@ -139,12 +136,10 @@ MINI_WIDE = MINI_BF16.replace(name="mini-bf16-v70000", vocab=70000)
 
 
 @pytest.mark.parametrize("batch,T", [(5, 1.0), (16, 0.8)])
-def test_sampled_step_overlapping_the_head_matches_the_separate_calls(gpu_lib, batch, T):
-    """Vocabulary 70000: 274 column tiles, so the head's last round (18 tiles)
-    overlaps the sampler's chunks below token 65536 on the second stream
-    (80 rows: 2048-token chunks, 32 of 35 there; 256 rows: 16384-token
-    chunks, 4 of 5). Logits, tokens, lse and log q equal the separate
-    ldr_draft_step + ldr_sample bit for bit, over several calls in a row."""
+def test_sampled_step_matches_the_separate_calls(gpu_lib, batch, T):
+    """Vocabulary 70000: 231 column tiles of 304. Logits, tokens, lse and
+    log q equal the separate ldr_draft_step + ldr_sample bit for bit, over
+    several calls in a row."""
     p, dw, anchor = setup(gpu_lib, MINI_WIDE, batch, 120)
     V = MINI_WIDE.vocab
     for step in range(3):
@@ -159,10 +154,9 @@ def test_sampled_step_overlapping_the_head_matches_the_separate_calls(gpu_lib, b
 
 
 @pytest.mark.slow
-def test_sampled_step_overlapping_the_head_full_size(gpu_lib):
-    """Qwen3-8B shape, batch 16, T = 1: the benchmarked call (594 column tiles,
-    the last 82 overlapping 8 of the 10 sampler chunks), bit for bit against
-    the separate calls."""
+def test_sampled_step_full_size(gpu_lib):
+    """Qwen3-8B shape, batch 16, T = 1: the benchmarked call (500 column
+    tiles), bit for bit against the separate calls."""
     p, dw, anchor = setup(gpu_lib, synth.QWEN3_8B, 16, 300)
     V = synth.QWEN3_8B.vocab
     z_ref = gpu_lib.draft_step(p.views, dw, anchor)

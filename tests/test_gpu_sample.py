@@ -1,21 +1,36 @@
-"""GPU parity of per-position sampling (Eq. 8): the Gumbel noise bit for bit,
-tokens exactly, lse and log q within fp32 tolerance, against the oracle fed
-the same fp32 logits buffer."""
+"""GPU parity of per-position sampling (Eq. 8): the Gumbel noise of both
+levels bit for bit; tokens equal to the oracle's two-level draw from the same
+fp32 logits buffer, except where two chunk keys tie within the fp32 error of
+the kernel's chunk log-masses (then the GPU's chunk must be such a near tie
+and its token that chunk's exact draw; at most one such row per call); lse
+and log q within fp32 tolerance."""
 import numpy as np
 import pytest
 import torch
 
+from gpu_common import draw_near_tie
 from oracle import sample as OS
 
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("rows,vocab", [(3, 151936), (37, 1001), (5, 7)])
-def test_gumbel_noise_is_bit_exact(gpu_lib, rows, vocab):
-    g = gpu_lib.gumbel_fill(1234, 9, rows, vocab).cpu().numpy()
-    ref = OS.gumbel(1234, 9, np.arange(rows)[:, None], np.arange(vocab)[None, :])
+@pytest.mark.parametrize("rows,vocab,stream", [(3, 151936, 0), (37, 1001, 0), (5, 7, 0),
+                                               (16, 9496, 3), (3, 257, 3), (2, 100, 1)])
+def test_gumbel_noise_is_bit_exact(gpu_lib, rows, vocab, stream):
+    g = gpu_lib.gumbel_fill(1234, 9, rows, vocab, noise_stream=stream).cpu().numpy()
+    ref = OS.gumbel(1234, 9, np.arange(rows)[:, None], np.arange(vocab)[None, :], stream)
     assert g.dtype == np.float32
     assert np.array_equal(g.view(np.uint32), ref.view(np.uint32))
+
+
+def _tokens_match(tok, y, z, T, k, seed, step, rows=None):
+    """The GPU tokens against the oracle's draw from the same logits: equal, or
+    (at most one row) a near tie of the chunk keys within fp32 error."""
+    tok = np.asarray(tok).astype(np.int64)
+    rows = np.arange(len(y)) if rows is None else rows
+    ties = sum(draw_near_tie(z[i], int(y[i]), int(tok[i]), int(rows[i]), T, seed, step, 0.0, k)
+               for i in range(len(y)) if tok[i] != y[i])
+    assert ties <= 1, ties
 
 
 def _logits(rows, vocab, seed, scale=1.3):
@@ -30,8 +45,9 @@ def test_tokens_exact_given_the_same_logits(gpu_lib, rows, vocab, T):
     z = _logits(rows, vocab, rows * 7 + vocab)
     tok, lse, logq = gpu_lib.sample(z, T, 0, seed=77, step=5)
     torch.cuda.synchronize()
-    y, l, lq = OS.sample(z.cpu().numpy(), T, 0, 77, 5)
-    assert np.array_equal(tok.cpu().numpy().astype(np.int64), y)
+    zc = z.cpu().numpy()
+    y, l, lq = OS.sample(zc, T, 0, 77, 5)
+    _tokens_match(tok.cpu().numpy(), y, zc, T, 0, 77, 5)
     np.testing.assert_allclose(lse.cpu().numpy(), l, rtol=2e-6, atol=2e-5)
     np.testing.assert_allclose(logq.cpu().numpy(), lq, rtol=1e-5, atol=2e-4)
 
@@ -64,8 +80,9 @@ def test_steps_and_seeds_change_the_draw(gpu_lib):
 def _check_sample(gpu_lib, z, T, k, seed, step):
     tok, lse, logq = gpu_lib.sample(z, T, k, seed=seed, step=step)
     torch.cuda.synchronize()
-    y, l, lq = OS.sample(z.cpu().numpy(), T, k, seed, step)
-    assert np.array_equal(tok.cpu().numpy().astype(np.int64), y)
+    zc = z.cpu().numpy()
+    y, l, lq = OS.sample(zc, T, k, seed, step)
+    _tokens_match(tok.cpu().numpy(), y, zc, T, k, seed, step)
     np.testing.assert_allclose(lse.cpu().numpy(), l, rtol=2e-6, atol=2e-5)
     np.testing.assert_allclose(logq.cpu().numpy(), lq, rtol=1e-5, atol=2e-4)
     return tok.cpu().numpy()
@@ -129,7 +146,9 @@ def _markov_case(batch, B, vocab, rank, dtype, seed, scale=0.4):
 def test_markov_matches_oracle(gpu_lib, batch, B, vocab, rank, dtype, T, k):
     """Corrected logits bit for bit, tokens exactly, lse and log q within fp32
     tolerance, against the oracle's sequential sampling from the same base
-    logits, anchors and correction weights."""
+    logits, anchors and correction weights (a chunk-key near tie would change
+    every later position of its sequence; the chance at these sizes is about
+    1e-3 per run)."""
     z0, a, E, W = _markov_case(batch, B, vocab, rank, dtype, batch * 31 + vocab + rank)
     z0_host = z0.cpu().numpy()
     z = z0.clone()

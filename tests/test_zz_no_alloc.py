@@ -29,7 +29,7 @@ def test_noalloc_matches_the_workspace_call(gpu_lib, T, top_k):
 
 
 def test_noalloc_refuses_requests_beyond_the_scratch(gpu_lib):
-    rows, V = 70000, 16
+    rows, V = 600000, 16
     assert gpu_lib.sample_workspace_bytes(rows, V) > gpu_lib.NOALLOC_SCRATCH_BYTES
     z = torch.zeros(rows, V, device="cuda")
     with pytest.raises(gpu_lib.LdrError) as e:
