@@ -87,8 +87,8 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   WsPlan w;
   const int M = batch * s.B;
   w.fc = plan_gemm(s.dtype, batch, s.hidden, s.Lb * s.hidden, true);
-  w.qkv = plan_gemm(s.dtype, M, s.qkv_out, s.hidden, true);
-  w.wo = plan_gemm(s.dtype, M, s.hidden, s.hq * s.d, true);
+  w.qkv = plan_gemm(s.dtype, M, s.qkv_out, s.hidden, true, false, true);
+  w.wo = plan_gemm(s.dtype, M, s.hidden, s.hq * s.d, true, false, true);
   w.gu = plan_gemm(s.dtype, M, 2 * s.mlp, s.hidden, false, true);   // SwiGLU epilogue: no split
   w.down = plan_gemm(s.dtype, M, s.hidden, s.mlp, true);
   w.lm = plan_gemm(s.dtype, M, s.vocab, s.hidden, false);     // writes the logits directly
@@ -101,14 +101,17 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   w.x = off; off = align_up(off + (size_t)M * s.hidden * 4);
   w.nrm = off; off = align_up(off + (size_t)M * s.hidden * s.el);
   w.qkvb = off; off = align_up(off + (size_t)M * s.qkv_out * s.el);
-  w.o = off; off = align_up(off + (size_t)M * s.hq * s.d * s.el);
+  // attention output rows padded to 16 for the fragment layout
+  const size_t Mp = (size_t)(M + 15) / 16 * 16;
+  w.o = off; off = align_up(off + Mp * s.hq * s.d * s.el);
   w.act = off; off = align_up(off + (size_t)M * s.mlp * s.el);
   w.rope = off; off = align_up(off + (size_t)2 * M * (s.d / 2) * 4);
   // final normalised rows in the tiled layout, for a tiled vocabulary head
   w.nrmt = off; off = align_up(off + (s.dtype == LDR_BF16 ? tiled_elems(M, s.hidden) * 2 : 0));
-  // the SwiGLU GEMM's rows in the fragment layout (rows padded to 16)
+  // the QKV and SwiGLU GEMMs' rows in the fragment layout (rows padded to 16)
   w.nrmf = off;
-  off = align_up(off + (gemm_plan_frag(w.gu) ? (size_t)(M + 15) / 16 * 16 * s.hidden * 2 : 0));
+  off = align_up(off + (gemm_plan_frag(w.gu) || gemm_plan_frag(w.qkv)
+                            ? (size_t)(M + 15) / 16 * 16 * s.hidden * 2 : 0));
   w.bytes = off;
   return w;
 }
@@ -381,10 +384,12 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         e = launch_gemm(s.dtype, EPI_STORE, ws.fc, g, st);
         break;
       case LDR_LAUNCH_SLOT_INIT:
-        e = launch_slot_init(s, batch, p, ws.fc.splits, w, anchor, st);
+        e = launch_slot_init(s, batch, p, ws.fc.splits, w, anchor, st,
+                             gemm_plan_frag(ws.qkv) ? base + ws.nrmf : nullptr);
         break;
       case LDR_LAUNCH_QKV_GEMM:
-        g.A = p.nrm; g.lda = s.hidden; g.W = L.wqkv; g.ldw = s.hidden; g.out = p.part;
+        g.A = gemm_plan_frag(ws.qkv) ? static_cast<const void*>(base + ws.nrmf) : p.nrm;
+        g.lda = s.hidden; g.W = L.wqkv; g.ldw = s.hidden; g.out = p.part;
         g.ldo = s.qkv_out; g.split_stride = (long)M * s.qkv_out; g.M = M; g.N = s.qkv_out;
         g.K = s.hidden; g.splits = ws.qkv.splits;
         e = launch_gemm(s.dtype, EPI_STORE, ws.qkv, g, st);
@@ -393,7 +398,7 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         e = launch_qkv_finish(s, M, p, ws.qkv.splits, &L, st);
         break;
       case LDR_LAUNCH_ATTENTION:
-        e = launch_attention(s, v->L, batch, p, j, st);
+        e = launch_attention(s, v->L, batch, p, j, st, gemm_plan_frag(ws.wo));
         break;
       case LDR_LAUNCH_O_GEMM:
         g.A = p.o; g.lda = (long)s.hq * s.d; g.W = L.wo; g.ldw = (long)s.hq * s.d;
@@ -421,9 +426,14 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         e = launch_gemm(s.dtype, EPI_STORE, ws.down, g, st);
         break;
       case LDR_LAUNCH_NEXT_NORM:
-        e = launch_resid_norm(s, M, p, ws.down.splits,
-                              j + 1 < s.D ? w->layers[j + 1].in_norm : w->final_norm, st,
-                              j + 1 == s.D && tiled_head ? base + ws.nrmt : nullptr);
+        if (j + 1 < s.D)   // the next layer's QKV input
+          e = gemm_plan_frag(ws.qkv)
+                  ? launch_resid_norm(s, M, p, ws.down.splits, w->layers[j + 1].in_norm, st,
+                                      base + ws.nrmf, NRM_FRAG)
+                  : launch_resid_norm(s, M, p, ws.down.splits, w->layers[j + 1].in_norm, st);
+        else               // the vocabulary head's input
+          e = launch_resid_norm(s, M, p, ws.down.splits, w->final_norm, st,
+                                tiled_head ? base + ws.nrmt : nullptr);
         break;
       case LDR_LAUNCH_LM_HEAD:
         g.lda = s.hidden; g.ldw = s.hidden; g.out = logits; g.ldo = s.vocab;

@@ -437,12 +437,18 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
       for (int c = 0; c < CPL / 2; ++c)
         pk[c] = (uint32_t)f32_to_bf16(acc[2 * c] * inv) |
                 ((uint32_t)f32_to_bf16(acc[2 * c + 1] * inv) << 16);
-      uint32_t* dst = reinterpret_cast<uint32_t*>(static_cast<uint16_t*>(a.o) +
-                                                  ((long)b * B + q) * ((long)a.hq * D) +
-                                                  (long)h * D + c0);
+      const long m = (long)b * B + q, K = (long)a.hq * D;
+      uint16_t* o = static_cast<uint16_t*>(a.o);
 #pragma unroll
-      for (int c = 0; c < CPL / 2; c += 2)
-        *reinterpret_cast<uint2*>(dst + c) = make_uint2(pk[c], pk[c + 1]);
+      for (int c = 0; c < CPL / 2; c += 2) {
+        // 4 columns k .. k + 3 (k a multiple of 4): 8 bytes of one row, inside
+        // one 16-byte chunk of the fragment layout
+        const long k = (long)h * D + c0 + 2 * c;
+        const long off = a.o_frag ? ((m >> 4) * (K >> 5) + (k >> 5)) * 512 +
+                                        ((k >> 3) & 3) * 128 + (m & 15) * 8 + (k & 7)
+                                  : m * K + k;
+        *reinterpret_cast<uint2*>(o + off) = make_uint2(pk[c], pk[c + 1]);
+      }
     }
   }
 }

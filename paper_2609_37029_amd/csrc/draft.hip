@@ -40,6 +40,7 @@ struct SlotArgs {
   const void* embed; const void* mask_emb; const void* pos_emb; const void* fc_norm;
   const void* in_norm0; const int32_t* anchor; const int64_t* pos;
   float* x; void* nrm; float* rope; int32_t* status;
+  int frag;   // nrm in the fragment layout (else row-major)
   int hidden, B, d, M, vocab;
   float eps; double base;
 };
@@ -129,7 +130,13 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
 #pragma unroll
   for (int ch = 0; ch < kChunks; ++ch) {
     const int k = (threadIdx.x + ch * kThreads) * 4;
-    if (k < H) Vec4<T>::store(static_cast<T*>(a.nrm) + m * H + k, f4scale(c[ch], inv, gin[ch]));
+    if (k < H) {
+      // four consecutive k stay inside one 16-byte chunk of the fragment layout
+      const long o = a.frag ? ((m >> 4) * (long)(H >> 5) + (k >> 5)) * 512 +
+                                  ((k >> 3) & 3) * 128 + (m & 15) * 8 + (k & 7)
+                            : m * H + k;
+      Vec4<T>::store(static_cast<T*>(a.nrm) + o, f4scale(c[ch], inv, gin[ch]));
+    }
   }
   // rotary table row of this slot, absolute position t + i
   const int half = a.d / 2;
@@ -365,13 +372,15 @@ hipError_t launch_split(int splits, dim3 grid, const Args& a, hipStream_t st) {
 bool norm_hidden_supported(int hidden) { return hidden % 4 == 0 && hidden <= kMaxHidden; }
 
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
-                            const ldr_weights* w, const int32_t* anchor, hipStream_t st) {
+                            const ldr_weights* w, const int32_t* anchor, hipStream_t st,
+                            void* frag_out) {
   SlotArgs a;
   a.part = p.part; a.split_stride = (long)batch * s.hidden; a.splits = fc_splits;
   a.use_c = s.keep_bnd;
   a.embed = w->embed; a.mask_emb = w->mask_emb; a.pos_emb = w->pos_emb; a.fc_norm = w->fc_norm;
   a.in_norm0 = w->layers[0].in_norm; a.anchor = anchor; a.pos = p.pos;
-  a.x = p.x; a.nrm = p.nrm; a.rope = p.rope; a.status = p.status;
+  a.x = p.x; a.nrm = frag_out ? frag_out : p.nrm; a.rope = p.rope; a.status = p.status;
+  a.frag = frag_out != nullptr;
   a.hidden = s.hidden; a.B = s.B; a.d = s.d; a.M = batch * s.B; a.vocab = s.vocab;
   a.eps = s.eps; a.base = s.rope_base;
   return s.dtype == LDR_BF16 ? launch_split<uint16_t, SlotLaunch>(fc_splits, dim3(s.B, batch), a, st)
@@ -402,7 +411,7 @@ hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int spli
 }
 
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
-                            int layer, hipStream_t st) {
+                            int layer, hipStream_t st, bool o_frag) {
   AttnArgs a;
   a.qkv = p.qkv;
   a.arena = p.arena; a.stride = L.stride; a.kw = L.kw; a.vw = L.vw; a.m_off = L.m;
@@ -412,6 +421,7 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
   a.R = s.R; a.rep = s.rep; a.qkv_out = s.qkv_out;
   a.use_summary = s.learned;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
+  a.o_frag = o_frag && s.dtype == LDR_BF16;
   const size_t shm = (size_t)(3 * s.B * s.d + s.B * (s.B + s.Wx + s.R)) * sizeof(float);
   if (s.dtype == LDR_BF16) return launch_attention_mfma(a, s.hkv, batch, st);
   const dim3 grid(s.hq, batch);

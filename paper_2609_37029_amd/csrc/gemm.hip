@@ -711,9 +711,10 @@ __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, l
 // 5: BM 256 with 4 x 2 waves of 64 x 32 (BN 64), in place of cfg 3 when cfg 3
 // would split K eight ways into pieces of at most 512: as fast there (the O
 // projection) with half the split-K partials for the next kernel to read;
-// 6, 7: gemm_frag_kernel, BM 256 with 8 waves of 32 x 96 (BN 96) or 32 x 128
-// (BN 128), activation rows in the fragment layout: the SwiGLU GEMM above 64
-// rows in place of cfg 4 or 3.
+// 6, 7, 8: gemm_frag_kernel, BM 256 with 8 waves of 32 x 96 (BN 96), 32 x 128
+// (BN 128) or 32 x 64 (BN 64), activation rows in the fragment layout: the
+// GEMMs above 64 rows whose input is written in that layout (the SwiGLU GEMM in
+// place of cfg 4 or 3; the QKV and O projections).
 template <int EPI>
 hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
   switch (cfg) {
@@ -724,6 +725,7 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
     case 5: hipLaunchKernelGGL((gemm_kernel<4, 2, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
     case 6: hipLaunchKernelGGL((gemm_frag_kernel<2, 6, EPI, 3>), grid, dim3(512), 0, st, a); break;
     case 7: hipLaunchKernelGGL((gemm_frag_kernel<2, 8, EPI, 3>), grid, dim3(512), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((gemm_frag_kernel<2, 4, EPI, 3>), grid, dim3(512), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -734,9 +736,44 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
 // bf16: the smallest BM of {16, 32, 64, 256} that covers M (several M tiles
 // past 256); the SwiGLU GEMM at BM 256 uses the 96-column tile. Split-K (1, 2, 4 or 8) only where allowed, to about one workgroup
 // per CU, keeping an even number of at least 4 K steps per split.
-GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu) {
+GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu, bool frag) {
   GemmPlan p;
   constexpr int kCUs = 256;
+  if (frag && !swiglu && dtype == LDR_BF16 && M > 64 && K % BK == 0) {
+    // Activation rows in the fragment layout: 256 x BN tiles of 128, 96 or 64
+    // columns and a K split of 1 .. 8 that keeps the workgroups within one
+    // round over the CUs (no split where the tiles alone take more). Taken in
+    // order: the plan whose workgroups fill the most of their last round; then
+    // one whose K range is at most 2048 (longer ranges measured slower, each
+    // workgroup re-reading more activation rows); then the fewest splits (the
+    // fp32 partial tiles are written in a burst at the end and read back by
+    // the next kernel); then the fewest bytes per workgroup.
+    const int cands[3][2] = {{7, 128}, {6, 96}, {8, 64}};
+    double best_u = -1.0, best_v = 0.0;
+    bool best_short = false;
+    for (const auto& c : cands) {
+      const long tiles = (long)((N + c[1] - 1) / c[1]) * ((M + 255) / 256);
+      for (int sp = 1; sp <= (allow_split ? 8 : 1); sp *= 2) {
+        if (K % (sp * BK) != 0 || K / sp < 2 * BK) break;
+        const long wg = tiles * sp;
+        if (sp > 1 && wg > kCUs) break;
+        const double u = (double)wg / (double)(((wg + kCUs - 1) / kCUs) * kCUs);
+        const bool shrt = K / sp <= 2048;
+        const double vol = (256.0 + c[1]) * (K / sp) * 2.0;
+        bool take;
+        if (u > best_u + 1e-9) take = true;
+        else if (u < best_u - 1e-9) take = false;
+        else if (shrt != best_short) take = shrt;
+        else if (sp != p.splits) take = sp < p.splits;
+        else take = vol < best_v;
+        if (take) {
+          best_u = u; best_v = vol; best_short = shrt; p.cfg = c[0]; p.splits = sp;
+          p.grid_x = (N + c[1] - 1) / c[1]; p.grid_y = (M + 255) / 256;
+        }
+      }
+    }
+    if (best_u > 0.0) { p.ntw = 0; return p; }
+  }
   int bm, bn, kstep;
   if (dtype == LDR_F32) {
     p.cfg = -1; bm = 32; bn = 64; kstep = 16;

@@ -156,8 +156,10 @@ struct GemmArgs {
 struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile configuration
 // The plan's kernel reads its activation rows in the fragment layout (NRM_FRAG).
 inline bool gemm_plan_frag(const GemmPlan& p) { return p.cfg >= 6; }
-// Tile configuration and split-K factor; splits = 1 unless allow_split.
-GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false);
+// Tile configuration and split-K factor; splits = 1 unless allow_split. frag:
+// the caller can give the activation rows in the fragment layout.
+GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false,
+                   bool frag = false);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
 // bf16 GEMM for the vocabulary head: A in 256-row tiles of 32-column blocks
 // (the final norm's tiled output), W [N][K] in the column-block layout of
@@ -209,18 +211,22 @@ struct AttnArgs {
   int P, S0, S1;     // mean-pooled summary (P = 0: none)
   int use_summary;   // the learned summary is kept
   float inv_sqrt_d;
+  int o_frag;        // o in the fragment layout of [M][hq d] (bf16 kernel), else row-major
 };
 // bf16 MFMA kernel (attn.hip): one workgroup per (kv group, sequence).
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st);
 bool attention_mfma_supported(int d, int rep, int B, int R, int Wx);
 
+// frag_out: write layer 0's normalised rows there in the fragment layout
+// instead of to p.nrm.
 hipError_t launch_slot_init(const Shape& s, int batch, const DraftPtrs& p, int fc_splits,
-                            const ldr_weights* w, const int32_t* anchor, hipStream_t st);
+                            const ldr_weights* w, const int32_t* anchor, hipStream_t st,
+                            void* frag_out = nullptr);
 bool norm_hidden_supported(int hidden);
 // Layouts of the normalised rows a residual norm writes.
 enum NrmLayout {
   NRM_ROWS = 0,   // row-major [M][hidden] (p.nrm)
-  NRM_TILED = 1,  // 256-row x 32-column blocks of ldr_tile_matrix (the tiled vocabulary head)
+  NRM_TILED = 1,  // 256-row x 32-column blocks (the tiled vocabulary head's activation rows)
   NRM_FRAG = 2,   // 16-row x 32-column MFMA fragments, lane order (gemm_frag_kernel)
 };
 // tiled_out: write the normalised rows there in `layout` instead of to p.nrm.
@@ -229,8 +235,9 @@ hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int spli
                              int layout = NRM_TILED);
 hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const ldr_layer_weights* lw, hipStream_t st);
+// o_frag: the output in the fragment layout (bf16 only).
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
-                            int layer, hipStream_t st);
+                            int layer, hipStream_t st, bool o_frag = false);
 
 // Sampler (sample.hip)
 // T = 0: greedy_splits chunks of greedy_chunk tokens per row. T > 0: nch
