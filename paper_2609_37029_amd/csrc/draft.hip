@@ -22,7 +22,8 @@ __device__ inline float wave_max(float v) {
   for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
   return v;
 }
-// Sum over the block (kThreads threads); every thread gets the result.
+// Sum over the block (NT threads); every thread gets the result.
+template <int NT = kThreads>
 __device__ inline float block_sum(float v, float* red) {
   v = wave_sum(v);
   const int w = threadIdx.x >> 6, l = threadIdx.x & 63;
@@ -30,7 +31,7 @@ __device__ inline float block_sum(float v, float* red) {
   if (l == 0) red[w] = v;
   __syncthreads();
   float s = 0.f;
-  for (int i = 0; i < kThreads / 64; ++i) s += red[i];
+  for (int i = 0; i < NT / 64; ++i) s += red[i];
   return s;
 }
 
@@ -155,18 +156,23 @@ struct ResidArgs {
   int layout;  // nrm layout: NRM_ROWS, NRM_TILED or NRM_FRAG (hidden % 32 == 0)
 };
 
+// One workgroup of kNormThreads threads per row: with 1024 threads a row of
+// up to 4096 elements is one float4 per thread, and every CU keeps 16 waves
+// of loads in flight.
+constexpr int kNormThreads = 1024, kNormChunks = kMaxHidden / (kNormThreads * 4);
+
 template <typename T, int SPLITS>
-__global__ void __launch_bounds__(kThreads) resid_norm_kernel(ResidArgs a) {
-  __shared__ float red[kThreads / 64];
+__global__ void __launch_bounds__(kNormThreads) resid_norm_kernel(ResidArgs a) {
+  __shared__ float red[kNormThreads / 64];
   const long m = blockIdx.x;
   const int H = a.hidden;
   float* x = a.x + m * H;
   const float* part = a.part + m * H;
-  float4 v[kChunks], g[kChunks];
+  float4 v[kNormChunks], g[kNormChunks];
   float ss = 0.f;
 #pragma unroll
-  for (int ch = 0; ch < kChunks; ++ch) {
-    const int k = (threadIdx.x + ch * kThreads) * 4;
+  for (int ch = 0; ch < kNormChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kNormThreads) * 4;
     if (k < H) {
       float4 u = *reinterpret_cast<const float4*>(x + k);
 #pragma unroll
@@ -177,14 +183,14 @@ __global__ void __launch_bounds__(kThreads) resid_norm_kernel(ResidArgs a) {
       ss += f4dot(u);
     }
   }
-  const float inv = rsqrtf(block_sum(ss, red) / H + a.eps);
+  const float inv = rsqrtf(block_sum<kNormThreads>(ss, red) / H + a.eps);
   T* out = static_cast<T*>(a.nrm);
   const long rbase = a.layout == NRM_TILED ? (m >> 8) * (long)(H >> 5) * 8192 + (m & 255) * 32
                    : a.layout == NRM_FRAG ? (m >> 4) * (long)(H >> 5) * 512 + (m & 15) * 8
                                           : m * H;
 #pragma unroll
-  for (int ch = 0; ch < kChunks; ++ch) {
-    const int k = (threadIdx.x + ch * kThreads) * 4;
+  for (int ch = 0; ch < kNormChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kNormThreads) * 4;
     if (k < H) {
       *reinterpret_cast<float4*>(x + k) = v[ch];
       // four consecutive k stay inside one 16-byte chunk of either tiled layout
@@ -351,7 +357,7 @@ struct QkvLaunch {
 struct ResidLaunch {
   template <typename T, int S>
   static void go(dim3 grid, const ResidArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL((resid_norm_kernel<T, S>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((resid_norm_kernel<T, S>), grid, dim3(kNormThreads), 0, st, a);
   }
 };
 // Dispatch on the split-K factor (1, 2, 4 or 8).
