@@ -241,15 +241,14 @@ hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const Dr
 
 // Sampler (sample.hip)
 // T = 0: greedy_splits chunks of greedy_chunk tokens per row. T > 0: nch
-// chunks of 16 tokens per row, their log-masses in rows of ldL floats, and
-// the chunk-key pass over key_splits pieces of key_chunk chunks per row.
-struct SamplePlan { int greedy_chunk, greedy_splits, nch, ldL, key_chunk, key_splits; };
+// chunks of 16 tokens per row, their log-masses in rows of ldL floats.
+struct SamplePlan { int greedy_chunk, greedy_splits, nch, ldL; };
 SamplePlan sample_plan(int rows, int vocab);
 // Tokens per workgroup of the chunk log-mass pass over ntok tokens of `rows` rows.
 int chunk_lse_slice(int rows, int ntok);
 // The full-vocabulary sampler at T > 0 in pieces (top_k = 0): the chunk
 // log-masses of tokens [v0, v1) of every row (v0 a multiple of 16), then,
-// once all are written, the chunk keys, the merge and the in-chunk draw;
+// once all are written, the chunk keys and the in-chunk draw;
 // ws as for launch_sample.
 hipError_t launch_chunk_lse(const float* logits, int rows, int vocab, float temperature, void* ws,
                             int v0, int v1, hipStream_t st);

@@ -11,12 +11,12 @@
 //    DPP, in the pairwise order (t0 + t1) + (t2 + t3), ... that a 16-lane DPP
 //    reduction of one token per lane also gives (the vocabulary head's
 //    epilogue can write the same L_c);
-//  * chunk_sample_kernel runs the Gumbel-max over the L_c of a row like a
-//    one-level sampler over V/16 entries: per lane the running max / sum of
-//    exp(L_c) for the log-normaliser and the best key, exact keys computed
-//    only for entries that a cheap upper bound of the noise cannot rule out;
-//  * sample_merge_kernel combines those partials in chunk order (lower index
-//    wins ties), then draws the token inside the winning chunk, one lane per
+//  * chunk_draw_kernel, one workgroup per row, runs the Gumbel-max over the
+//    row's L_c like a one-level sampler over V/16 entries: per lane the
+//    running max / sum of exp(L_c) for the log-normaliser and the best key,
+//    exact keys computed only for entries that a cheap upper bound of the
+//    noise cannot rule out; it combines the lanes' results (lower index wins
+//    ties), then draws the token inside the winning chunk, one lane per
 //    token, and writes the token, lse and log q(y).
 // T = 0 is the first argmax of the logits (sample_partial_kernel + merge).
 //
@@ -190,10 +190,11 @@ __device__ void argmax_tokens(const SampleArgs& a, const float* z, int v0, int v
 // (L_c = -inf) take no part. Candidates go through a per-wave queue in LDS so
 // that their exact keys (two logs each) are computed 64 at a time by full
 // waves.
+template <int NT>
 __device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, int c1,
                            Partial& p) {
   struct Cand { float zt; uint32_t bits; int v; };
-  __shared__ Cand queue[kThreads / 64][128];
+  __shared__ Cand queue[NT / 64][128];
   const int lane = threadIdx.x & 63;
   Cand* q = queue[threadIdx.x >> 6];
   int qn = 0;  // wave-uniform queue length
@@ -208,7 +209,7 @@ __device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, 
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  constexpr int kSweep = kThreads * kGroup;
+  constexpr int kSweep = NT * kGroup;
   const int lane_off = (int)(threadIdx.x & ~63) * kGroup + lane * kGroup;
   const uint64_t nrow = (uint64_t)r * a.row_mul + a.row_add;
   float znext[kGroup];
@@ -333,24 +334,56 @@ __global__ void __launch_bounds__(kThreads) chunk_lse_kernel(SampleArgs a, int v
   }
 }
 
-// Gumbel-max over chunks [sp * chunk, ..) of the row's log-masses: one
-// partial (max / sum of exp(L), best key and chunk) per workgroup.
-__global__ void __launch_bounds__(kThreads) chunk_sample_kernel(SampleArgs a) {
-  const int sp = blockIdx.x, r = blockIdx.y;
-  const int c0 = sp * a.chunk, c1 = min(a.nch, c0 + a.chunk);
+// The chunk keys and the in-chunk draw of one row (T > 0), one workgroup of
+// kDrawThreads threads per row: the Gumbel-max over all its chunk log-masses
+// (each lane a sweep or two of 8 entries), the lanes' partials combined (max /
+// sum of exp(L) for lse, best key and chunk), then lanes 0 .. 15 of the first
+// wave take the 16 tokens of the winning chunk c (support members only), their
+// exact keys fl(fl(z_v/T) + g_v), and the first maximum is the token.
+constexpr int kDrawThreads = 1024;
+__global__ void __launch_bounds__(kDrawThreads) chunk_draw_kernel(SampleArgs a, int32_t* tokens,
+                                                                  float* lse, float* logq) {
+  const int r = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
-  chunk_keys(a, a.L + (long)r * a.ldL, r, c0, c1, p);
+  chunk_keys<kDrawThreads>(a, a.L + (long)r * a.ldL, r, 0, a.nch, p);
   for (int off = 32; off >= 1; off >>= 1) {
     Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
               __shfl_xor(p.idx, off)};
     combine(p, o);
   }
-  __shared__ Partial red[kThreads / 64];
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = p;
+  __shared__ Partial red[kDrawThreads / 64];
+  if (lane == 0) red[wave] = p;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    for (int w = 1; w < kThreads / 64; ++w) combine(p, red[w]);
-    a.part[(long)r * a.splits + sp] = p;
+  if (wave != 0) return;
+  p = red[0];
+  for (int w = 1; w < kDrawThreads / 64; ++w) combine(p, red[w]);
+  const long g = (long)r * a.row_mul + a.row_add;
+  const float* z = a.logits + g * a.vocab;
+  // the chunk's tokens: lane i < 16 takes token 16 c + i (no chunk: none)
+  const int v = p.idx < a.nch ? p.idx * kChunk + lane : a.vocab;
+  float key = -INFINITY, zt = -INFINITY;
+  if (lane < kChunk && v < a.vocab) {
+    const float zv = z[v];
+    const bool in = !a.sel || in_support(a.sel[r], zv, v);
+    if (in) {
+      zt = a.T == 1.f ? zv : zv / a.T;
+      uint32_t w[4];
+      noise_block(noise_key(a.seed, a.step, 0), (uint32_t)g, (uint32_t)(v >> 2), w);
+      key = __fadd_rn(zt, gumbel_from_bits(w[v & 3]));
+    }
+  }
+  int best = key > -INFINITY ? v : 0x7fffffff;
+  for (int off = 8; off >= 1; off >>= 1) {   // lanes 0 .. 15: first maximum
+    const float k2 = __shfl_xor(key, off);
+    const int b2 = __shfl_xor(best, off);
+    const float z2 = __shfl_xor(zt, off);
+    if (better(k2, b2, key, best)) { key = k2; best = b2; zt = z2; }
+  }
+  if (lane == 0) {
+    const float l = p.m + logf(p.s);
+    tokens[g] = best;
+    lse[g] = l;
+    logq[g] = zt - l;
   }
 }
 
@@ -489,10 +522,8 @@ __global__ void __launch_bounds__(kThreads) sample_partial_kernel(SampleArgs a) 
   }
 }
 
-// One wave per row: the partials in order. T = 0: the first argmax. T > 0:
-// the winning chunk c and lse = log sum_c exp(L_c); then lanes 0 .. 15 take
-// the tokens of chunk c (support members only), their exact keys
-// fl(fl(z_v/T) + g_v), and the first maximum is the token.
+// One wave per row (T = 0): the greedy partials in order, the first argmax,
+// its logit as lse and log q = 0.
 __global__ void __launch_bounds__(64) sample_merge_kernel(SampleArgs a, int32_t* tokens,
                                                           float* lse, float* logq) {
   const int r = blockIdx.x, lane = threadIdx.x;
@@ -503,41 +534,11 @@ __global__ void __launch_bounds__(64) sample_merge_kernel(SampleArgs a, int32_t*
               __shfl_xor(p.idx, off)};
     combine(p, o);
   }
-  const long g = (long)r * a.row_mul + a.row_add;
-  const float* z = a.logits + g * a.vocab;
-  if (a.T == 0.f) {
-    if (lane == 0) {
-      tokens[g] = p.idx;
-      lse[g] = p.key;
-      logq[g] = 0.f;
-    }
-    return;
-  }
-  // the chunk's tokens: lane i < 16 takes token 16 c + i
-  const int v = p.idx * kChunk + lane;
-  float key = -INFINITY, zt = -INFINITY;
-  if (lane < kChunk && v < a.vocab) {
-    const float zv = z[v];
-    const bool in = !a.sel || in_support(a.sel[r], zv, v);
-    if (in) {
-      zt = a.T == 1.f ? zv : zv / a.T;
-      uint32_t w[4];
-      noise_block(noise_key(a.seed, a.step, 0), (uint32_t)g, (uint32_t)(v >> 2), w);
-      key = __fadd_rn(zt, gumbel_from_bits(w[v & 3]));
-    }
-  }
-  int best = key > -INFINITY ? v : 0x7fffffff;
-  for (int off = 8; off >= 1; off >>= 1) {   // lanes 0 .. 15: first maximum
-    const float k2 = __shfl_xor(key, off);
-    const int b2 = __shfl_xor(best, off);
-    const float z2 = __shfl_xor(zt, off);
-    if (better(k2, b2, key, best)) { key = k2; best = b2; zt = z2; }
-  }
   if (lane == 0) {
-    const float l = p.m + logf(p.s);
-    tokens[g] = best;
-    lse[g] = l;
-    logq[g] = zt - l;
+    const long g = (long)r * a.row_mul + a.row_add;
+    tokens[g] = p.idx;
+    lse[g] = p.key;
+    logq[g] = 0.f;
   }
 }
 
@@ -573,12 +574,9 @@ SamplePlan sample_plan(int rows, int vocab) {
   if (rows >= 2048) chunk = (vocab + sweep - 1) / sweep * sweep;
   p.greedy_chunk = chunk;
   p.greedy_splits = (vocab + chunk - 1) / chunk;
-  // T > 0: 16-token chunks; the chunk-key pass takes one sweep of entries per
-  // workgroup
+  // T > 0: 16-token chunks, their log-masses in rows padded to 4 floats
   p.nch = (vocab + kChunk - 1) / kChunk;
   p.ldL = (p.nch + 3) / 4 * 4;
-  p.key_chunk = sweep;
-  p.key_splits = (p.nch + sweep - 1) / sweep;
   return p;
 }
 
@@ -594,8 +592,7 @@ int chunk_lse_slice(int rows, int ntok) {
 size_t sample_part_bytes(int rows, int vocab) {
   const SamplePlan p = sample_plan(rows, vocab);
   const size_t L = ((size_t)rows * p.ldL * sizeof(float) + 255) / 256 * 256;
-  const int splits = p.greedy_splits > p.key_splits ? p.greedy_splits : p.key_splits;
-  return L + (size_t)rows * splits * sizeof(Partial);
+  return L + (size_t)rows * p.greedy_splits * sizeof(Partial);
 }
 
 // Static scratch of ldr_sample_noalloc: the sampler's partials and top-k
@@ -649,8 +646,7 @@ SampleArgs sample_args(const float* logits, int rows, int vocab, float temperatu
   a.ldL = pl.ldL; a.nch = pl.nch;
   a.part = reinterpret_cast<Partial*>(static_cast<uint8_t*>(ws) +
                                       ((size_t)rows * pl.ldL * sizeof(float) + 255) / 256 * 256);
-  if (temperature == 0.f) { a.chunk = pl.greedy_chunk; a.splits = pl.greedy_splits; }
-  else { a.chunk = pl.key_chunk; a.splits = pl.key_splits; }
+  a.chunk = pl.greedy_chunk; a.splits = pl.greedy_splits;
   return a;
 }
 
@@ -674,10 +670,12 @@ hipError_t chunk_lse(const SampleArgs& a, int v0, int v1, hipStream_t st) {
 
 hipError_t sample_finish(const SampleArgs& a, int32_t* tokens, float* lse, float* logq,
                          hipStream_t st) {
-  if (a.T == 0.f)
-    hipLaunchKernelGGL(sample_partial_kernel, dim3(a.splits, a.rows), dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL(chunk_sample_kernel, dim3(a.splits, a.rows), dim3(kThreads), 0, st, a);
+  if (a.T > 0.f) {
+    hipLaunchKernelGGL(chunk_draw_kernel, dim3(a.rows), dim3(kDrawThreads), 0, st, a, tokens,
+                       lse, logq);
+    return hipGetLastError();
+  }
+  hipLaunchKernelGGL(sample_partial_kernel, dim3(a.splits, a.rows), dim3(kThreads), 0, st, a);
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(sample_merge_kernel, dim3(a.rows), dim3(64), 0, st, a, tokens, lse, logq);
