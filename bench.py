@@ -762,14 +762,15 @@ def main():
         # launch, the same kernel on both paths) is timed over as many steps of
         # the bracketed separate path right after it
         wall, per_step, _ = time_steps(torch, rig, args.steps, args_warmup_run, ev=ev)
+        t_final = int(rig.views.pos.min().item())   # the timed steps' prefix, before the bracketed run
         rig.fused_head = False
         _, _, kern = time_steps(torch, rig, args.steps, 0, ev=ev, bracket=dom)
         rig.fused_head = True
     else:
         wall, per_step, kern = time_steps(torch, rig, args.steps, args_warmup_run, ev=ev,
                                           bracket=dom)
+        t_final = int(rig.views.pos.min().item())
     torch.cuda.synchronize()
-    t_final = int(rig.views.pos.min().item())
     ms = wall / args.steps * 1e3
     tokens = batch * s.block * args.steps
     launches_of_dom = sum(1 for k in rig.kinds if k == dom)
