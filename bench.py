@@ -106,7 +106,10 @@ def launch_costs(s, batch):
     nr = 0 if (drop & 2 or pool) else s.summary
     win = batch * 2 * s.n_kv_heads * nw * s.head_dim * el
     summ = s.n_q_heads * nr * s.head_dim * el + batch * s.n_q_heads * nr * s.head_dim * 4
-    qkv = M * s.qkv_out * el + M * s.n_q_heads * s.head_dim * el
+    # bf16: the kernel also finishes q / k / v (fp32 projection rows in, the
+    # rotary table and gains), and no q / k / v rows go through memory
+    qkv = (M * s.qkv_out * 4 + M * s.head_dim * 4 + 2 * s.head_dim * el if el == 2
+           else M * s.qkv_out * el) + M * s.n_q_heads * s.head_dim * el
     nk = s.block + nw + nr
     c["attention"] = (win + summ + qkv, 4 * M * s.n_q_heads * nk * s.head_dim)
     norm = M * H * 4 * 2 + M * H * el
@@ -351,15 +354,18 @@ def time_steps(torch, rig, steps, warmup, ev=None, bracket=None):
 
 
 def kind_breakdown(torch, ldr, rig, ev, reps=5):
-    """Milliseconds per step of each launch kind (events around every launch)."""
+    """Milliseconds per step of each launch kind (events around every launch),
+    after one untimed step (a kernel's first launch also loads its code)."""
     n = len(rig.kinds)
     tot = {}
-    for r in range(reps):
+    for r in range(-1, reps):
         evs = [ev.create() for _ in range(n + 1)]
         K, V, h = rig.rows[r % 4]
         rig.views.update(rig.n, K, V, h)
         ldr.draft_step_events(rig.views, rig.dw, rig.anchor, rig.logits, rig.ws, evs)
         torch.cuda.synchronize()
+        if r < 0:
+            continue
         for li, k in enumerate(rig.kinds):
             tot[k] = tot.get(k, 0.0) + ev.elapsed_ms(evs[li], evs[li + 1])
     return {k: v / reps for k, v in tot.items()}

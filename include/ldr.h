@@ -247,14 +247,16 @@ enum ldr_launch_kind {
   LDR_LAUNCH_FC_GEMM = 0,      /* boundary fusion W_fc (split-K partials)          */
   LDR_LAUNCH_SLOT_INIT = 1,    /* c_t norm, slot inputs, first pre-norm, RoPE table */
   LDR_LAUNCH_QKV_GEMM = 2,     /* per layer: QKV projection                         */
-  LDR_LAUNCH_ATTENTION = 3,    /* per layer: block-view attention (Eq. 6)           */
+  LDR_LAUNCH_ATTENTION = 3,    /* per layer: block-view attention (Eq. 6); bf16: it
+                                  also finishes q, k, v from the QKV partials       */
   LDR_LAUNCH_O_GEMM = 4,       /* per layer: output projection                      */
   LDR_LAUNCH_POST_NORM = 5,    /* per layer: residual add + pre-MLP RMSNorm         */
   LDR_LAUNCH_GATE_UP_GEMM = 6, /* per layer: gate/up projection + SwiGLU            */
   LDR_LAUNCH_DOWN_GEMM = 7,    /* per layer: down projection                        */
   LDR_LAUNCH_NEXT_NORM = 8,    /* per layer: residual add + next (or final) RMSNorm */
   LDR_LAUNCH_LM_HEAD = 9,      /* vocabulary head, fp32 logits                      */
-  LDR_LAUNCH_QKV_FINISH = 10   /* per layer: QKV split-K sum, q/k RMSNorm, RoPE     */
+  LDR_LAUNCH_QKV_FINISH = 10   /* per layer (fp32 models): QKV split-K sum, q/k
+                                  RMSNorm, RoPE                                     */
 };
 
 /* Number of kernel launches of ldr_draft_step for this configuration

@@ -87,10 +87,14 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   WsPlan w;
   const int M = batch * s.B;
   w.fc = plan_gemm(s.dtype, batch, s.hidden, s.Lb * s.hidden, true);
-  w.qkv = plan_gemm(s.dtype, M, s.qkv_out, s.hidden, true, false, true);
+  // at most 4 QKV splits in bf16: the attention kernel holds them all in registers
+  w.qkv = plan_gemm(s.dtype, M, s.qkv_out, s.hidden, true, false, true,
+                    s.dtype == LDR_BF16 ? 4 : 8);
   w.wo = plan_gemm(s.dtype, M, s.hidden, s.hq * s.d, true, false, true);
   w.gu = plan_gemm(s.dtype, M, 2 * s.mlp, s.hidden, false, true);   // SwiGLU epilogue: no split
-  w.down = plan_gemm(s.dtype, M, s.hidden, s.mlp, true);
+  // the down projection reads the SwiGLU rows in the fragment layout when the
+  // SwiGLU GEMM (itself on the fragment layout) can write them so
+  w.down = plan_gemm(s.dtype, M, s.hidden, s.mlp, true, false, gemm_plan_frag(w.gu));
   w.lm = plan_gemm(s.dtype, M, s.vocab, s.hidden, false);     // writes the logits directly
   size_t part = (size_t)w.fc.splits * batch * s.hidden;
   part = part > (size_t)w.qkv.splits * M * s.qkv_out ? part : (size_t)w.qkv.splits * M * s.qkv_out;
@@ -100,11 +104,12 @@ static WsPlan plan_ws(const Shape& s, int batch) {
   w.part = off; off = align_up(off + part * 4);
   w.x = off; off = align_up(off + (size_t)M * s.hidden * 4);
   w.nrm = off; off = align_up(off + (size_t)M * s.hidden * s.el);
-  w.qkvb = off; off = align_up(off + (size_t)M * s.qkv_out * s.el);
-  // attention output rows padded to 16 for the fragment layout
+  // finished q / k / v rows (fp32 models; the bf16 attention finishes its own)
+  w.qkvb = off; off = align_up(off + (s.dtype == LDR_BF16 ? 0 : (size_t)M * s.qkv_out * s.el));
+  // attention output and SwiGLU rows padded to 16 for the fragment layout
   const size_t Mp = (size_t)(M + 15) / 16 * 16;
   w.o = off; off = align_up(off + Mp * s.hq * s.d * s.el);
-  w.act = off; off = align_up(off + (size_t)M * s.mlp * s.el);
+  w.act = off; off = align_up(off + Mp * s.mlp * s.el);
   w.rope = off; off = align_up(off + (size_t)2 * M * (s.d / 2) * 4);
   // final normalised rows in the tiled layout, for a tiled vocabulary head
   w.nrmt = off; off = align_up(off + (s.dtype == LDR_BF16 ? tiled_elems(M, s.hidden) * 2 : 0));
@@ -307,12 +312,13 @@ static int draft_sequence(const Shape& s, int D, Emit&& emit) {
   int rc = s.keep_bnd ? emit(LDR_LAUNCH_FC_GEMM, 0) : (int)LDR_OK;   // no boundary: c = 0
   if (rc == LDR_OK) rc = emit(LDR_LAUNCH_SLOT_INIT, 0);
   for (int j = 0; j < D && rc == LDR_OK; ++j) {
+    // bf16: the attention kernel finishes q, k and v itself
     const int kinds[] = {LDR_LAUNCH_QKV_GEMM, LDR_LAUNCH_QKV_FINISH, LDR_LAUNCH_ATTENTION,
                          LDR_LAUNCH_O_GEMM,
                          LDR_LAUNCH_POST_NORM, LDR_LAUNCH_GATE_UP_GEMM, LDR_LAUNCH_DOWN_GEMM,
                          LDR_LAUNCH_NEXT_NORM};
     for (int k : kinds)
-      if (rc == LDR_OK) rc = emit(k, j);
+      if (rc == LDR_OK && !(k == LDR_LAUNCH_QKV_FINISH && s.dtype == LDR_BF16)) rc = emit(k, j);
   }
   if (rc == LDR_OK) rc = emit(LDR_LAUNCH_LM_HEAD, 0);
   return rc;
@@ -398,7 +404,7 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         e = launch_qkv_finish(s, M, p, ws.qkv.splits, &L, st);
         break;
       case LDR_LAUNCH_ATTENTION:
-        e = launch_attention(s, v->L, batch, p, j, st, gemm_plan_frag(ws.wo));
+        e = launch_attention(s, v->L, batch, p, j, &L, ws.qkv.splits, st, gemm_plan_frag(ws.wo));
         break;
       case LDR_LAUNCH_O_GEMM:
         g.A = p.o; g.lda = (long)s.hq * s.d; g.W = L.wo; g.ldw = (long)s.hq * s.d;
@@ -416,7 +422,7 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
         g.A = gemm_plan_frag(ws.gu) ? static_cast<const void*>(base + ws.nrmf) : p.nrm;
         g.lda = s.hidden; g.W = L.w_gate_up; g.ldw = s.hidden; g.out = p.act;
         g.ldo = s.mlp; g.split_stride = 0; g.M = M; g.N = 2 * s.mlp; g.K = s.hidden;
-        g.splits = 1; g.mlp = s.mlp;
+        g.splits = 1; g.mlp = s.mlp; g.out_frag = gemm_plan_frag(ws.down);
         e = launch_gemm(s.dtype, EPI_SWIGLU, ws.gu, g, st);
         break;
       case LDR_LAUNCH_DOWN_GEMM:

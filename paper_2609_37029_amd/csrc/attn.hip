@@ -2,8 +2,8 @@
 //
 // One workgroup per (kv group g, sequence b, HPW query heads of the group),
 // NSEG waves per head, each taking one segment of the key sources under its
-// own online softmax: segment 0 the block's own k / v (B rows, normalised and
-// rotated by the QKV finishing kernel) and the first window chunks, the last
+// own online softmax: segment 0 the block's own k / v (B rows) and the first
+// window chunks, the last
 // segment the last window chunks of layer j and the head's R summary entries
 // (keys G[j,h], values M[j,h] rounded to bf16). Window chunks of 32 keys are
 // staged through LDS once for all heads of the workgroup (K rows and the
@@ -15,6 +15,11 @@
 // S = Q K^T and O += P V run on v_mfma_f32_16x16x32_bf16 (16 query rows per
 // wave = the B <= 16 slots); P goes through a per-wave LDS tile to change
 // from the C layout to the A layout.
+// The block's q, k and v are finished in the prologue from the QKV
+// projection's fp32 split-K partials: the split sum, the per-head RMSNorm of
+// q and k with their gains, and rotate-half RoPE (Sec. 2.4), rounded to bf16
+// into LDS. The k / v of a group are finished by each workgroup that reads
+// them (rep / HPW of them).
 #include "ldr_internal.h"
 
 namespace ldr {
@@ -50,7 +55,7 @@ __device__ inline void wave_lds_sync() {
 // summary, block rows, then WD window chunks per segment. Each later wait then
 // covers only what the next stage needs. WIN: the views have window or pooled
 // rows. PREFETCHED: no segment has more chunks than the WD the prologue loads.
-template <int D, int HPW, int NSEG, int WD, bool WIN, bool PREFETCHED>
+template <int D, int HPW, int NSEG, int WD, bool WIN, bool PREFETCHED, int SPLITS>
 __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArgs a) {
   constexpr int NT = 64 * HPW * NSEG, ST = 64 * HPW;  // threads, threads per segment
   constexpr int LDQ = D + 8;   // bf16 row of the Q / K tiles (conflict-free 16-row reads)
@@ -93,8 +98,8 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
   // the position first: its wait then leaves every later load in flight
   const long t = a.pos[b];
   // ---- summary keys G and values M of the workgroup's heads (rows past R: 0).
-  // Without the summary the loads read the first 16 bytes of the q / k / v
-  // rows instead (unused), so that every path issues the same loads.
+  // Without the summary the loads read the first 16 bytes of the projection
+  // partials instead (unused), so that every path issues the same loads.
   constexpr int SG = HPW * RMAX * D / 8;      // 16-byte pieces of G (bf16)
   constexpr int SM = HPW * RMAX * D / 4;      // 16-byte pieces of M (fp32)
   constexpr int GL = (SG + NT - 1) / NT, ML = (SM + NT - 1) / NT;
@@ -103,9 +108,9 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
   {
     const size_t hrow = (size_t)(a.layer * a.hq + h0) * a.R;  // first row of the workgroup
     const uint16_t* Gg = use_sum ? static_cast<const uint16_t*>(a.G) + hrow * D
-                                 : static_cast<const uint16_t*>(a.qkv);
+                                 : reinterpret_cast<const uint16_t*>(a.part);
     const float* Mg = use_sum ? reinterpret_cast<const float*>(seq + a.m_off) + hrow * D
-                              : static_cast<const float*>(a.qkv);
+                              : a.part;
 #pragma unroll
     for (int i = 0; i < GL; ++i) {
       const int idx = min(threadIdx.x + i * NT, SG - 1);
@@ -122,20 +127,47 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
     }
   }
 
-  // ---- block rows: q of the workgroup's heads, k and v of the group (already
-  // normalised and rotated); rows past the B slots of the 16-row tile are 0
-  constexpr int QP = HPW * QR * D / 8, KP = QR * D / 8;  // 16-byte pieces
-  constexpr int NP = QP + 2 * KP, PP = (NP + NT - 1) / NT;
-  const uint16_t* qkv = static_cast<const uint16_t*>(a.qkv) + (size_t)b * B * a.qkv_out;
-  u32x4 pre[PP];
+  // ---- block rows, finished here from the QKV projection's fp32 split-K
+  // partials: q of the workgroup's heads, k and v of the group, for rows
+  // min(i, B - 1) of the 16-row tile. A piece is elements e .. e + 7 and
+  // e + D/2 .. e + D/2 + 7 (e = 8 x piece) of one (row, head slot) unit, so
+  // that it holds whole rotary pairs (rotate-half RoPE); the PPU pieces of a
+  // unit sit on consecutive lanes. Units: q heads (slot < HPW), k, v.
+  constexpr int HALF = D / 2, PPU = D / 16, NU = (HPW + 2) * QR, NPC = NU * PPU;
+  constexpr int FI = (NPC + NT - 1) / NT;     // pieces per thread
+  static_assert(64 % PPU == 0, "a unit's pieces in one wave");
+  float4 fp[FI][SPLITS][4];                   // partials: e .. + 3, + 4 .. + 7, e + D/2 ..
+  u32x4 gq[FI][2];                            // q or k gains of the piece (bf16)
+  float4 rc[FI][4];                           // cos, sin of the piece's row (e .. + 7)
+  auto piece = [&](int f, int& unit_slot, int& row, int& pc) {
+    const int idx = min((int)threadIdx.x + f * NT, NPC - 1);
+    const int u = idx / PPU;
+    pc = idx % PPU; unit_slot = u / QR; row = u % QR;
+  };
 #pragma unroll
-  for (int i = 0; i < PP; ++i) {
-    const int idx = min(threadIdx.x + i * NT, NP - 1);
-    const int j = idx < QP ? idx % (QR * D / 8) : (idx - QP) % KP;
-    const int row = min(j / (D / 8), B - 1), c8 = (j % (D / 8)) * 8;
-    const int col = idx < QP ? (h0 + idx / (QR * D / 8)) * D + c8
-                  : idx < QP + KP ? (a.hq + g) * D + c8 : (a.hq + a.hkv + g) * D + c8;
-    pre[i] = *reinterpret_cast<const u32x4*>(qkv + (size_t)row * a.qkv_out + col);
+  for (int f = 0; f < FI; ++f) {
+    int us, row, pc;
+    piece(f, us, row, pc);
+    const int hs = us < HPW ? h0 + us : us == HPW ? a.hq + g : a.hq + a.hkv + g;
+    const long m = (long)b * B + min(row, B - 1);
+    const float* src = a.part + m * a.qkv_out + (long)hs * D + pc * 8;
+#pragma unroll
+    for (int sp = 0; sp < SPLITS; ++sp) {
+      const float* ps = src + sp * a.split_stride;
+      fp[f][sp][0] = *reinterpret_cast<const float4*>(ps);
+      fp[f][sp][1] = *reinterpret_cast<const float4*>(ps + 4);
+      fp[f][sp][2] = *reinterpret_cast<const float4*>(ps + HALF);
+      fp[f][sp][3] = *reinterpret_cast<const float4*>(ps + HALF + 4);
+    }
+    const uint16_t* gain = static_cast<const uint16_t*>(us < HPW ? a.q_norm : a.k_norm) + pc * 8;
+    gq[f][0] = *reinterpret_cast<const u32x4*>(gain);
+    gq[f][1] = *reinterpret_cast<const u32x4*>(gain + HALF);
+    const float* cs = a.rope + m * HALF + pc * 8;
+    const float* sn = cs + (long)a.rows * HALF;
+    rc[f][0] = *reinterpret_cast<const float4*>(cs);
+    rc[f][1] = *reinterpret_cast<const float4*>(cs + 4);
+    rc[f][2] = *reinterpret_cast<const float4*>(sn);
+    rc[f][3] = *reinterpret_cast<const float4*>(sn + 4);
   }
 
   // ---- window chunks: ring slot p holds the segment's chunk cbeg + p (the
@@ -157,24 +189,61 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
     for (int p = 0; p < WD; ++p) { LDR_FETCH(p, min(cbeg + p, cend - 1)) }
   }
 
-  // ---- Q, the block tile and the summary tiles into LDS
-  const int valid_r = B;
+  // ---- Q, the block tile and the summary tiles into LDS. Finishing a piece:
+  // the split sum (in split order), then for q and k the per-head RMSNorm
+  // (sum of squares over the unit's lanes) with its gain and the rotation of
+  // each pair (e, e + D/2) by the row's angle; rows past B are 0.
 #pragma unroll
-  for (int i = 0; i < PP; ++i) {
-    const int idx = threadIdx.x + i * NT;
-    if (idx >= NP) break;
-    const int j = idx < QP ? idx % (QR * D / 8) : (idx - QP) % KP;
-    const int row = j / (D / 8), c8 = (j % (D / 8)) * 8;
-    const u32x4 v = row < valid_r ? pre[i] : u32x4{0u, 0u, 0u, 0u};
-    if (idx < QP) {
-      *reinterpret_cast<u32x4*>(&Lds[OQ + (idx / (QR * D / 8)) * QR * LDQ + row * LDQ + c8]) = v;
-    } else if (idx < QP + KP) {
-      *reinterpret_cast<u32x4*>(&Blk[row * LDQ + c8]) = v;
-    } else {
+  for (int f = 0; f < FI; ++f) {
+    int us, row, pc;
+    piece(f, us, row, pc);
+    float x1[8], x2[8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Blk[KTILE + (c8 + 2 * e) * LDV + row] = (uint16_t)(v[e] & 0xffffu);
-        Blk[KTILE + (c8 + 2 * e + 1) * LDV + row] = (uint16_t)(v[e] >> 16);
+    for (int j = 0; j < 8; ++j) {
+      x1[j] = 0.f; x2[j] = 0.f;
+#pragma unroll
+      for (int sp = 0; sp < SPLITS; ++sp) {
+        x1[j] += fp[f][sp][j >> 2][j & 3];
+        x2[j] += fp[f][sp][2 + (j >> 2)][j & 3];
+      }
+    }
+    float ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) ss += x1[j] * x1[j] + x2[j] * x2[j];
+    ss += dpp<0xB1>(ss);                       // the unit's PPU lanes (4 or 8)
+    ss += dpp<0x4E>(ss);
+    if constexpr (PPU == 8) ss += dpp<0x141>(ss);
+    if (us <= HPW) {                           // q or k
+      const float inv = rsqrtf(ss / D + a.eps);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t w1 = gq[f][0][j >> 1], w2 = gq[f][1][j >> 1];
+        const float g1 = bf16_to_f32((uint16_t)(j & 1 ? w1 >> 16 : w1 & 0xffffu));
+        const float g2 = bf16_to_f32((uint16_t)(j & 1 ? w2 >> 16 : w2 & 0xffffu));
+        const float z1 = x1[j] * inv * g1, z2 = x2[j] * inv * g2;
+        const float c = rc[f][j >> 2][j & 3], sn = rc[f][2 + (j >> 2)][j & 3];
+        x1[j] = z1 * c - z2 * sn;
+        x2[j] = z1 * sn + z2 * c;
+      }
+    }
+    if ((int)threadIdx.x + f * NT >= NPC) continue;
+    const bool live = row < B;
+    uint32_t h1[4], h2[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      h1[j] = live ? (uint32_t)f32_to_bf16(x1[2 * j]) | ((uint32_t)f32_to_bf16(x1[2 * j + 1]) << 16) : 0u;
+      h2[j] = live ? (uint32_t)f32_to_bf16(x2[2 * j]) | ((uint32_t)f32_to_bf16(x2[2 * j + 1]) << 16) : 0u;
+    }
+    const int c8 = pc * 8;
+    if (us < HPW || us == HPW) {
+      uint16_t* dst = us < HPW ? &Lds[OQ + us * QR * LDQ + row * LDQ] : &Blk[row * LDQ];
+      *reinterpret_cast<u32x4*>(dst + c8) = u32x4{h1[0], h1[1], h1[2], h1[3]};
+      *reinterpret_cast<u32x4*>(dst + HALF + c8) = u32x4{h2[0], h2[1], h2[2], h2[3]};
+    } else {                                   // v, transposed: V^T[e][row]
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        Blk[KTILE + (c8 + j) * LDV + row] = (uint16_t)(h1[j >> 1] >> (16 * (j & 1)));
+        Blk[KTILE + (HALF + c8 + j) * LDV + row] = (uint16_t)(h2[j >> 1] >> (16 * (j & 1)));
       }
     }
   }
@@ -453,19 +522,28 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
   }
 }
 
-template <int D, int HPW, int NSEG, int WD>
+template <int D, int HPW, int NSEG, int WD, int SPLITS>
 void launch_cfg(const AttnArgs& a, dim3 grid, hipStream_t st) {
   const int nwf = a.Wx / KC;
   const bool pre = (nwf + NSEG - 1) / NSEG <= WD;   // every segment's chunks fit in the ring
   if (a.Wx == 0)
-    hipLaunchKernelGGL((attention_mfma_kernel<D, HPW, NSEG, WD, false, true>), grid,
+    hipLaunchKernelGGL((attention_mfma_kernel<D, HPW, NSEG, WD, false, true, SPLITS>), grid,
                        dim3(64 * HPW * NSEG), 0, st, a);
   else if (pre)
-    hipLaunchKernelGGL((attention_mfma_kernel<D, HPW, NSEG, WD, true, true>), grid,
+    hipLaunchKernelGGL((attention_mfma_kernel<D, HPW, NSEG, WD, true, true, SPLITS>), grid,
                        dim3(64 * HPW * NSEG), 0, st, a);
   else
-    hipLaunchKernelGGL((attention_mfma_kernel<D, HPW, NSEG, WD, true, false>), grid,
+    hipLaunchKernelGGL((attention_mfma_kernel<D, HPW, NSEG, WD, true, false, SPLITS>), grid,
                        dim3(64 * HPW * NSEG), 0, st, a);
+}
+
+template <int D, int HPW, int NSEG, int WD>
+void launch_splits(const AttnArgs& a, dim3 grid, hipStream_t st) {
+  switch (a.splits) {
+    case 1: launch_cfg<D, HPW, NSEG, WD, 1>(a, grid, st); break;
+    case 2: launch_cfg<D, HPW, NSEG, WD, 2>(a, grid, st); break;
+    default: launch_cfg<D, HPW, NSEG, WD, 4>(a, grid, st); break;
+  }
 }
 
 template <int D>
@@ -476,15 +554,15 @@ hipError_t launch_d(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
   // two segments per head.
   const int nwf = a.Wx / KC;
   if (nwf >= 8 && a.rep % 2 == 0) {
-    launch_cfg<D, 2, 4, 2>(a, dim3(hkv * (a.rep / 2), batch), st);
+    launch_splits<D, 2, 4, 2>(a, dim3(hkv * (a.rep / 2), batch), st);
     return hipGetLastError();
   }
   const int hpw = a.rep < 4 ? a.rep : 4;
   const dim3 grid(hkv * (a.rep / hpw), batch);
   switch (hpw) {
-    case 1: launch_cfg<D, 1, 2, 4>(a, grid, st); break;
-    case 2: launch_cfg<D, 2, 2, 4>(a, grid, st); break;
-    default: launch_cfg<D, 4, 2, 4>(a, grid, st); break;
+    case 1: launch_splits<D, 1, 2, 4>(a, grid, st); break;
+    case 2: launch_splits<D, 2, 2, 4>(a, grid, st); break;
+    default: launch_splits<D, 4, 2, 4>(a, grid, st); break;
   }
   return hipGetLastError();
 }
@@ -498,6 +576,7 @@ bool attention_mfma_supported(int d, int rep, int B, int R, int W) {   // W: reg
 
 hipError_t launch_attention_mfma(const AttnArgs& a, int hkv, int batch, hipStream_t st) {
   if (!attention_mfma_supported(a.d, a.rep, a.B, a.R, a.W)) return hipErrorInvalidValue;
+  if (a.splits != 1 && a.splits != 2 && a.splits != 4) return hipErrorInvalidValue;
   return a.d == 128 ? launch_d<128>(a, hkv, batch, st) : launch_d<64>(a, hkv, batch, st);
 }
 

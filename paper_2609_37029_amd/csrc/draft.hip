@@ -417,9 +417,13 @@ hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int spli
 }
 
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
-                            int layer, hipStream_t st, bool o_frag) {
+                            int layer, const ldr_layer_weights* lw, int qkv_splits,
+                            hipStream_t st, bool o_frag) {
   AttnArgs a;
   a.qkv = p.qkv;
+  a.part = p.part; a.split_stride = (long)batch * s.B * s.qkv_out; a.splits = qkv_splits;
+  a.rows = batch * s.B; a.q_norm = lw->q_norm; a.k_norm = lw->k_norm; a.rope = p.rope;
+  a.eps = s.eps;
   a.arena = p.arena; a.stride = L.stride; a.kw = L.kw; a.vw = L.vw; a.m_off = L.m;
   a.pos = p.pos; a.G = p.G;
   a.o = p.o; a.layer = layer; a.hq = s.hq; a.hkv = s.hkv; a.d = s.d; a.B = s.B; a.W = s.Wr;

@@ -24,6 +24,9 @@
 // and writes silu(gate) * up in the activation dtype.
 #include "ldr_internal.h"
 
+#include <type_traits>
+#include <utility>
+
 namespace ldr {
 namespace {
 
@@ -162,7 +165,8 @@ __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int 
 }
 
 // Stores one tile's accumulators: EPI_STORE / EPI_LOGITS fp32 (split z at
-// z * split_stride), EPI_SWIGLU silu(gate) * up in the activation dtype.
+// z * split_stride), EPI_SWIGLU silu(gate) * up in the activation dtype,
+// row-major or in the fragment layout of [M][mlp] (a.out_frag).
 template <int MTW, int NTW, int WM, int WN, int EPI>
 __device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, int z,
                                            const f32x4 (&acc)[MTW][NTW]) {
@@ -194,11 +198,30 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, in
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const int row = m0 + wm * TM + i * 16 + crow + v;
+          const long off = a.out_frag ? ((long)(row >> 4) * (a.mlp >> 5) + (col >> 5)) * 512 +
+                                            ((((col >> 3) & 3) << 4) | (row & 15)) * 8 + (col & 7)
+                                      : (long)row * a.ldo + col;
           if (row < a.M && col < a.mlp)
-            out[(long)row * a.ldo + col] = f32_to_bf16(silu(acc[i][j][v]) * acc[i][j + 1][v]);
+            out[off] = f32_to_bf16(silu(acc[i][j][v]) * acc[i][j + 1][v]);
         }
     }
   }
+}
+
+// The tile (x, y) and K split z of this workgroup. Workgroups go to the 8
+// XCDs in turn by linear id (id mod 8), and each XCD has its own L2: the
+// linear ids are renumbered so that XCD c takes the c-th eighth of the tiles
+// in (z, y, x) order. A K split's activation columns are then read into one
+// or two XCDs' L2 instead of all eight.
+__device__ __forceinline__ void xcd_tile(int& x, int& y, int& z) {
+  const int gx = gridDim.x, gy = gridDim.y;
+  const int total = gx * gy * gridDim.z;
+  const int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
+  const int q = total >> 3, r = total & 7, c = lin & 7, slot = lin >> 3;
+  const int l = c < r ? c * (q + 1) + slot : r * (q + 1) + (c - r) * q + slot;
+  x = l % gx;
+  y = (l / gx) % gy;
+  z = l / (gx * gy);
 }
 
 template <int MTW, int NTW, int WM, int WN, int EPI>
@@ -207,7 +230,9 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
   static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LDK];
   __shared__ __attribute__((aligned(16))) uint16_t Ws[2][BN * LDK];
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, z = blockIdx.z;
+  int bx, by, z;
+  xcd_tile(bx, by, z);
+  const int n0 = bx * BN, m0 = by * BM;
   const int kper = a.K / a.splits, kbeg = z * kper, nk = kper / BK;
   f32x4 acc[MTW][NTW];
   tile_mma<MTW, NTW, WM, WN, EPI == EPI_SWIGLU>(a, n0, m0, kbeg, nk, As, Ws, acc);
@@ -285,85 +310,106 @@ __device__ inline void group_barrier() {
 #define LDR_LP(p) ((__attribute__((address_space(3))) void*)(p))
 
 // ---------------------------------------------------------------------------
-// GEMM with the activation rows in the fragment layout (the SwiGLU GEMM).
+// GEMM with the activation rows in the fragment layout.
 //
 // In the fragment layout of a [M][K] bf16 matrix (rows padded to 16), the
 // 16 x 32 block of rows 16 r .. and columns 32 c .. is 1 KB at element
 // (r * (K / 32) + c) * 512, its 16-byte chunk l holding row 16 r + (l & 15),
 // columns 32 c + (l >> 4) * 8 .. + 8: the A operand of v_mfma_f32_16x16x32_bf16
 // for lane l, so a wave loads an A fragment from global memory with one fully
-// coalesced 16-byte load per lane. The residual norm before this GEMM writes
-// its rows in that layout.
+// coalesced 16-byte load per lane. That is, element (m, k) sits at
+// ((m >> 4) * (K >> 5) + (k >> 5)) * 512 + ((((k >> 3) & 3) << 4) | (m & 15)) * 8
+// + (k & 7). The residual norms, the attention output and the SwiGLU GEMM write
+// their rows in that layout for the GEMM that reads them.
 //
-// Eight waves each own 32 rows (private: their A fragments go straight to
-// registers, RA K steps ahead) and all BN columns; the BN weight rows of a
-// 64-deep K step reach LDS by DMA (global_load_lds, 8 rows of 128 bytes per
-// instruction, 16-byte chunk c of row r at c ^ (r & 7)) in a ring of NB
-// stages issued NB - 1 steps ahead. Against the staged kernel above this
-// removes the activation tiles' LDS stores and reads (32 KB each per step at
-// 256 rows), which bounded it.
-// Ordering: every step issues the DMA of W stage kt + FNB - 1, then the A loads
-// of stage kt + FRA (FRA stages of A in registers). Before step kt every wave
-// waits until the later of W stage kt and A stage kt in that order has
-// landed (vmcnt counts its DMA and A loads in issue order) and its own LDS
-// reads are done, then a barrier: stage kt is whole in LDS, and the buffer
-// refilled at this step (read at step kt - 1) has no reader left. Three A
-// stages ahead measured fastest: six (the register limit) and a second
-// register buffer for the weight fragments were both slower.
-constexpr int FNB = 6;   // W stages in LDS (DMA issued FNB - 1 steps ahead)
-
-// Activation layout (written by the residual norm): element (m, k) of an
-// M x K matrix sits at ((m >> 4) * (K >> 5) + (k >> 5)) * 512
-// + ((((k >> 3) & 3) << 4) | (m & 15)) * 8 + (k & 7), so each 16 x 32 block is
-// 1 KB in the lane order of the MFMA A operand.
+// A workgroup owns all 256 rows x BN columns of the output and a 1/splits
+// share of K, in steps of 64. Eight compute waves own 32 rows each: their A
+// fragments go straight to registers, FRA steps ahead (private, so no LDS),
+// and they read all BN weight rows of a step from LDS. NL loader waves only
+// stage the weights by DMA (global_load_lds, 8 rows of 128 bytes per
+// instruction, 16-byte chunk c of row r at c ^ (r & 7)) into a ring of NB
+// stages, NB - 1 steps ahead. A wave that issued the weight DMA itself
+// between its MFMAs ran them at about half their rate; with the DMA in waves
+// of its own the compute waves keep most of it.
+// Ordering: at step kt every wave waits for its own share of what the step
+// needs (a loader: its DMA of stage kt, with the NB - 2 later stages still in
+// flight; a compute wave: its A loads of stage kt and its LDS reads of step
+// kt - 1), then the step's barrier. After it the loaders refill the buffer of
+// stage kt - 1, whose readers are past the barrier, with stage kt + NB - 1,
+// and the compute waves read stage kt. Both roles meet the same nk barriers.
+template <class F, int... P>
+__device__ __forceinline__ void for_phases(F&& f, std::integer_sequence<int, P...>) {
+  (f(std::integral_constant<int, P>{}), ...);
+}
 
 template <int N> __device__ inline void wait_vm_lgkm0() {
   static_assert(N >= 0 && N < 64, "vmcnt");
   __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
 }
 
-template <int MTW, int NTW, int EPI, int FRA>
-__global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
-  constexpr int WM = 8, WN = 1, NW = WM * WN, TM = MTW * 16, TN = NTW * 16;
+constexpr int kFragWaves = 8;    // compute waves of the fragment-layout GEMM
+constexpr int kFragLoaders = 4;  // its loader waves
+constexpr int kFragThreads = 64 * (kFragWaves + kFragLoaders);
+
+template <int MTW, int NTW, int EPI, int FRA, int NL, int NB>
+__global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(GemmArgs a) {
+  constexpr int NW = kFragWaves, WM = NW, WN = 1, TM = MTW * 16, TN = NTW * 16;
   constexpr int BM = WM * TM, BN = WN * TN;
   constexpr int STAGE = BN * 128;             // W bytes per stage (BN rows x 64 k)
   constexpr int GROUPS = BN / 8;              // DMA instructions per stage (8 rows each)
-  constexpr int GPW = (GROUPS + NW - 1) / NW;
-  constexpr int AV = MTW * 2;                 // A loads per stage per lane
-  constexpr int PER_STEP = GPW + AV;          // VMEM instructions per step and wave
-  static_assert(FNB % FRA == 0, "the unrolled loop cycles both rings");
-  // loads issued after the later of W(kt) (step kt - FNB + 1) and A(kt) (step kt - FRA)
-  constexpr int WAIT = FNB - 1 >= FRA ? PER_STEP * (FRA - 1) : AV + PER_STEP * (FNB - 2);
+  static_assert(GROUPS % NL == 0, "loaders share the stage evenly");
+  constexpr int GPL = GROUPS / NL;            // DMA instructions per loader and stage
+  constexpr int AV = MTW * 2;                 // A loads per stage per compute lane
+  constexpr int WAIT_W = GPL * (NB - 2);
+  constexpr int WAIT_A = AV * (FRA - 1);
+  static_assert(WAIT_W < 64 && WAIT_A < 64, "vmcnt range");
+  static_assert(NB % FRA == 0, "the unrolled loop cycles both rings");
   static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
-  __shared__ __attribute__((aligned(1024))) uint8_t Wsm[FNB * STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t Wsm[NB * STAGE];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave, wn = 0;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM, z = blockIdx.z;
+  int bx, by, z;
+  xcd_tile(bx, by, z);
+  const int n0 = bx * BN, m0 = by * BM;
   const int kper = a.K / a.splits, kbeg = z * kper, nk = kper / BK;
-  const uint16_t* A = static_cast<const uint16_t*>(a.A);
-  const uint16_t* W = static_cast<const uint16_t*>(a.W);
-  // W DMA: group g covers stage rows g * 8 .. + 8; lane -> row g * 8 + lane / 8,
-  // physical chunk lane % 8 <- logical chunk (lane % 8) ^ (row & 7). Waves past
-  // the group count repeat the last group (the same bytes to the same place).
-  const uint16_t* wsrc[GPW];
-  int wdst[GPW];
+  if (wave >= NW) {
+    // loader l: groups l * GPL .. + GPL of every stage; lane -> row g * 8 +
+    // lane / 8, physical chunk lane % 8 <- logical chunk (lane % 8) ^ (row & 7);
+    // weight rows past N repeat the last one (their columns are not stored)
+    const int l = wave - NW;
+    const uint16_t* W = static_cast<const uint16_t*>(a.W);
+    const uint16_t* wsrc[GPL];
+    int wdst[GPL];
 #pragma unroll
-  for (int q = 0; q < GPW; ++q) {
-    const int g = min(wave * GPW + q, GROUPS - 1);
-    const int r = g * 8 + (lane >> 3);
-    const int c = (lane & 7) ^ (r & 7);
-    const int gn = min(n0 + r, a.N - 1);
-    const int wrow = EPI == EPI_SWIGLU ? swiglu_row(gn, a.mlp) : gn;
-    wsrc[q] = W + (long)wrow * a.ldw + kbeg + c * 8;
-    wdst[q] = g * 1024;
+    for (int q = 0; q < GPL; ++q) {
+      const int g = l * GPL + q;
+      const int r = g * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ (r & 7);
+      const int gn = min(n0 + r, a.N - 1);
+      const int wrow = EPI == EPI_SWIGLU ? swiglu_row(gn, a.mlp) : gn;
+      wsrc[q] = W + (long)wrow * a.ldw + kbeg + c * 8;
+      wdst[q] = g * 1024;
+    }
+    auto issue_w = [&](int buf, int stage) {   // stages past the end reload the last one
+      const int off = min(stage, nk - 1) * BK;
+      uint8_t* dst = Wsm + buf * STAGE;
+#pragma unroll
+      for (int q = 0; q < GPL; ++q)
+        __builtin_amdgcn_global_load_lds(LDR_GP(wsrc[q] + off), LDR_LP(dst + wdst[q]), 16, 0, 0);
+    };
+#pragma unroll
+    for (int st = 0; st < NB - 1; ++st) issue_w(st, st);
+    int buf = NB - 1;
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_vmcnt<WAIT_W>();
+      group_barrier();
+      issue_w(buf, kt + NB - 1);
+      buf = buf == NB - 1 ? 0 : buf + 1;
+    }
+    wait_vmcnt<0>();   // no DMA outlives the workgroup
+    return;
   }
-  auto issue_w = [&](int buf, int stage) {
-    const int off = min(stage, nk - 1) * BK;
-    uint8_t* dst = Wsm + buf * STAGE;
-#pragma unroll
-    for (int q = 0; q < GPW; ++q)
-      __builtin_amdgcn_global_load_lds(LDR_GP(wsrc[q] + off), LDR_LP(dst + wdst[q]), 16, 0, 0);
-  };
+  const int wm = wave;
+  const uint16_t* A = static_cast<const uint16_t*>(a.A);
   // A fragments of m-tile i and k half kk of a step: one 1 KB block each.
   // Row blocks past the padded row count repeat the last one (never stored).
   const int mpad = (a.M + 15) & ~15;
@@ -374,7 +420,7 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
     asrc[i] = A + ((long)rg * (a.K >> 5) + (kbeg >> 5)) * 512 + lane * 8;
   }
   u32x4 aq[FRA][MTW][2];
-  auto load_a = [&](u32x4 (&dst)[MTW][2], int stage) {
+  auto load_a = [&](u32x4 (&dst)[MTW][2], int stage) {   // past the end: the last stage again
     const long off = (long)min(stage, nk - 1) * 1024;
 #pragma unroll
     for (int i = 0; i < MTW; ++i)
@@ -382,14 +428,14 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
       for (int kk = 0; kk < 2; ++kk)
         dst[i][kk] = *reinterpret_cast<const u32x4*>(asrc[i] + off + kk * 512);
   };
-  // W fragment offsets in a stage: row wn * TN + j * 16 + lane % 16, logical
-  // chunk kk * 4 + lane / 16
+  // W fragment offsets in a stage: row j * 16 + lane % 16, logical chunk
+  // kk * 4 + lane / 16
   int woff[NTW][2];
 #pragma unroll
   for (int j = 0; j < NTW; ++j)
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      const int r = wn * TN + j * 16 + (lane & 15);
+      const int r = j * 16 + (lane & 15);
       woff[j][kk] = r * 128 + (((kk * 4 + (lane >> 4)) ^ (r & 7)) * 16);
     }
   f32x4 acc[MTW][NTW];
@@ -397,53 +443,43 @@ __global__ void __launch_bounds__(512, 1) gemm_frag_kernel(GemmArgs a) {
   for (int i = 0; i < MTW; ++i)
 #pragma unroll
     for (int j = 0; j < NTW; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // step kt in phase p = kt mod FNB: W stage kt in buffer p, A stage kt in ring
-  // slot p mod FRA; refills buffer (p + FNB - 1) mod FNB with stage kt + FNB - 1
-#define LDR_FSTEP(kt, p)                                                                     \
-  {                                                                                          \
-    sched_fence();                                                                           \
-    wait_vm_lgkm0<WAIT>();                                                                   \
-    __builtin_amdgcn_s_barrier();                                                            \
-    sched_fence();                                                                           \
-    issue_w(((p) + FNB - 1) % FNB, (kt) + FNB - 1);                                          \
-    const uint8_t* cur = Wsm + (p) * STAGE;                                                  \
-    bf16x8 bfr[2][NTW];                                                                      \
-    _Pragma("unroll") for (int kk = 0; kk < 2; ++kk)                                         \
-      _Pragma("unroll") for (int j = 0; j < NTW; ++j)                                        \
-        bfr[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + woff[j][kk])); \
-    _Pragma("unroll") for (int kk = 0; kk < 2; ++kk)                                         \
-      _Pragma("unroll") for (int i = 0; i < MTW; ++i)                                        \
-        _Pragma("unroll") for (int j = 0; j < NTW; ++j) acc[i][j] =                          \
-            __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                         \
-                __builtin_bit_cast(bf16x8, aq[(p) % FRA][i][kk]), bfr[kk][j], acc[i][j], 0, 0, 0); \
-    load_a(aq[(p) % FRA], (kt) + FRA);                                                       \
-    sched_fence();                                                                           \
-  }
-  // prologue: W stages 0 .. FNB - 2 and A stages 0 .. FRA - 1 issued as the
-  // virtual steps -max(FNB - 1, FRA) .. -1 would (W, then A), so that the
-  // in-order count of the first steps is that of any other step
-  constexpr int PRO = FNB - 1 > FRA ? FNB - 1 : FRA;
 #pragma unroll
-  for (int v = -PRO; v < 0; ++v) {
-    if (v + FNB - 1 >= 0) issue_w(v + FNB - 1, v + FNB - 1);
-    if (v + FRA >= 0) load_a(aq[v + FRA], v + FRA);
-  }
-  static_assert(FNB == 6, "the unrolled loop has six phases");
-  const int full = nk / FNB * FNB;
+  for (int st = 0; st < FRA; ++st) load_a(aq[st], st);
+  // step kt in phase p = kt mod NB: W stage kt in buffer p, A stage kt in
+  // register slot p mod FRA, refilled with stage kt + FRA after the MFMAs
+  auto step = [&](int kt, auto pc) {
+    constexpr int p = decltype(pc)::value;
+    sched_fence();
+    wait_vm_lgkm0<WAIT_A>();
+    __builtin_amdgcn_s_barrier();
+    sched_fence();
+    const uint8_t* cur = Wsm + p * STAGE;
+    bf16x8 bfr[2][NTW];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int j = 0; j < NTW; ++j)
+        bfr[kk][j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(cur + woff[j][kk]));
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int i = 0; i < MTW; ++i)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              __builtin_bit_cast(bf16x8, aq[p % FRA][i][kk]), bfr[kk][j], acc[i][j], 0, 0, 0);
+    load_a(aq[p % FRA], kt + FRA);
+    sched_fence();
+  };
+  const int full = nk / NB * NB;
   int kt = 0;
-  for (; kt < full; kt += FNB) {
-    LDR_FSTEP(kt, 0) LDR_FSTEP(kt + 1, 1) LDR_FSTEP(kt + 2, 2)
-    LDR_FSTEP(kt + 3, 3) LDR_FSTEP(kt + 4, 4) LDR_FSTEP(kt + 5, 5)
-  }
+  for (; kt < full; kt += NB)
+    for_phases([&](auto pc) { step(kt + decltype(pc)::value, pc); },
+               std::make_integer_sequence<int, NB>{});
   const int rem = nk - full;   // uniform: every wave takes the same steps
-  if (rem > 0) LDR_FSTEP(kt, 0)
-  if (rem > 1) LDR_FSTEP(kt + 1, 1)
-  if (rem > 2) LDR_FSTEP(kt + 2, 2)
-  if (rem > 3) LDR_FSTEP(kt + 3, 3)
-  if (rem > 4) LDR_FSTEP(kt + 4, 4)
-#undef LDR_FSTEP
-  wait_vm_lgkm0<0>();   // no DMA outlives the workgroup
+  for_phases([&](auto pc) { if (decltype(pc)::value < rem) step(kt + decltype(pc)::value, pc); },
+             std::make_integer_sequence<int, NB - 1>{});
+  wait_vm_lgkm0<0>();
   store_tile<MTW, NTW, WM, WN, EPI>(a, n0, m0, z, acc);
 }
 
@@ -711,10 +747,11 @@ __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, l
 // 5: BM 256 with 4 x 2 waves of 64 x 32 (BN 64), in place of cfg 3 when cfg 3
 // would split K eight ways into pieces of at most 512: as fast there (the O
 // projection) with half the split-K partials for the next kernel to read;
-// 6, 7, 8: gemm_frag_kernel, BM 256 with 8 waves of 32 x 96 (BN 96), 32 x 128
-// (BN 128) or 32 x 64 (BN 64), activation rows in the fragment layout: the
-// GEMMs above 64 rows whose input is written in that layout (the SwiGLU GEMM in
-// place of cfg 4 or 3; the QKV and O projections).
+// 6, 7, 8: gemm_frag_kernel, BM 256 with 8 compute waves of 32 x 96 (BN 96),
+// 32 x 128 (BN 128) or 32 x 64 (BN 64) and 4 loader waves, activation rows in
+// the fragment layout: the GEMMs above 64 rows whose input is written in that
+// layout (the SwiGLU GEMM in place of cfg 4 or 3; the QKV, O and down
+// projections).
 template <int EPI>
 hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
   switch (cfg) {
@@ -723,9 +760,18 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
     case 2: hipLaunchKernelGGL((gemm_kernel<4, 2, 1, 8, EPI>), grid, dim3(512), 0, st, a); break;
     case 4: hipLaunchKernelGGL((gemm_kernel<2, 6, 8, 1, EPI>), grid, dim3(512), 0, st, a); break;
     case 5: hipLaunchKernelGGL((gemm_kernel<4, 2, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
-    case 6: hipLaunchKernelGGL((gemm_frag_kernel<2, 6, EPI, 3>), grid, dim3(512), 0, st, a); break;
-    case 7: hipLaunchKernelGGL((gemm_frag_kernel<2, 8, EPI, 3>), grid, dim3(512), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((gemm_frag_kernel<2, 4, EPI, 3>), grid, dim3(512), 0, st, a); break;
+    case 6:
+      hipLaunchKernelGGL((gemm_frag_kernel<2, 6, EPI, 2, kFragLoaders, 6>), grid,
+                         dim3(kFragThreads), 0, st, a);
+      break;
+    case 7:
+      hipLaunchKernelGGL((gemm_frag_kernel<2, 8, EPI, 2, kFragLoaders, 6>), grid,
+                         dim3(kFragThreads), 0, st, a);
+      break;
+    case 8:
+      hipLaunchKernelGGL((gemm_frag_kernel<2, 4, EPI, 2, kFragLoaders, 6>), grid,
+                         dim3(kFragThreads), 0, st, a);
+      break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -736,7 +782,8 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
 // bf16: the smallest BM of {16, 32, 64, 256} that covers M (several M tiles
 // past 256); the SwiGLU GEMM at BM 256 uses the 96-column tile. Split-K (1, 2, 4 or 8) only where allowed, to about one workgroup
 // per CU, keeping an even number of at least 4 K steps per split.
-GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu, bool frag) {
+GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu, bool frag,
+                   int max_splits) {
   GemmPlan p;
   constexpr int kCUs = 256;
   if (frag && !swiglu && dtype == LDR_BF16 && M > 64 && K % BK == 0) {
@@ -753,7 +800,7 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
     bool best_short = false;
     for (const auto& c : cands) {
       const long tiles = (long)((N + c[1] - 1) / c[1]) * ((M + 255) / 256);
-      for (int sp = 1; sp <= (allow_split ? 8 : 1); sp *= 2) {
+      for (int sp = 1; sp <= (allow_split ? max_splits : 1); sp *= 2) {
         if (K % (sp * BK) != 0 || K / sp < 2 * BK) break;
         const long wg = tiles * sp;
         if (sp > 1 && wg > kCUs) break;
@@ -810,7 +857,8 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
   int s = 1;
   if (allow_split) {
     const int tiles = p.grid_x * p.grid_y;
-    while (s < 8 && tiles * s * 2 <= kCUs && K % (2 * s * kstep) == 0 && K / (2 * s) >= 2 * kstep)
+    while (s < max_splits && tiles * s * 2 <= kCUs && K % (2 * s * kstep) == 0 &&
+           K / (2 * s) >= 2 * kstep)
       s *= 2;
   }
   p.splits = s;

@@ -152,14 +152,16 @@ struct GemmArgs {
   long split_stride;           // EPI_STORE: elements between split partials
   int M, N, K, splits;
   int mlp;                     // EPI_SWIGLU: N / 2
+  int out_frag = 0;            // EPI_SWIGLU: output [M][mlp] in the fragment layout
 };
 struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile configuration
 // The plan's kernel reads its activation rows in the fragment layout (NRM_FRAG).
 inline bool gemm_plan_frag(const GemmPlan& p) { return p.cfg >= 6; }
-// Tile configuration and split-K factor; splits = 1 unless allow_split. frag:
-// the caller can give the activation rows in the fragment layout.
+// Tile configuration and split-K factor; splits = 1 unless allow_split, at
+// most max_splits (a power of two). frag: the caller can give the activation
+// rows in the fragment layout.
 GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu = false,
-                   bool frag = false);
+                   bool frag = false, int max_splits = 8);
 hipError_t launch_gemm(int dtype, int epi, const GemmPlan& p, const GemmArgs& a, hipStream_t st);
 // bf16 GEMM for the vocabulary head: A in 256-row tiles of 32-column blocks
 // (the final norm's tiled output), W [N][K] in the column-block layout of
@@ -202,6 +204,12 @@ constexpr int kFlagAnchor = 2;  // a draft step saw an anchor outside [0, V)
 // Attention over [block; window; summary] of one layer (Eq. 6).
 struct AttnArgs {
   const void* qkv;   // block q, k, v rows (dtype) [M][qkv_out], normalised and rotated
+                     // (vector kernel)
+  // bf16 kernel: the QKV projection's fp32 split-K partials [splits][rows][qkv_out]
+  // and what finishing them takes (q / k RMSNorm gains, the RoPE table
+  // cos / sin [rows][d/2] x 2, eps)
+  const float* part; long split_stride; int splits, rows;
+  const void* q_norm; const void* k_norm; const float* rope; float eps;
   const uint8_t* arena; size_t stride; size_t kw, vw, m_off;
   const int64_t* pos; const void* G;
   void* o;
@@ -236,8 +244,11 @@ hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int spli
 hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const ldr_layer_weights* lw, hipStream_t st);
 // o_frag: the output in the fragment layout (bf16 only).
+// bf16: the kernel also finishes q, k and v from the QKV partials (qkv_splits
+// of them, 1, 2 or 4; lw's q / k gains); the vector kernel reads p.qkv.
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,
-                            int layer, hipStream_t st, bool o_frag = false);
+                            int layer, const ldr_layer_weights* lw, int qkv_splits,
+                            hipStream_t st, bool o_frag = false);
 
 // Sampler (sample.hip)
 // T = 0: greedy_splits chunks of greedy_chunk tokens per row. T > 0: nch

@@ -123,13 +123,15 @@ def test_host_validation_needs_no_gpu(L):
 
 
 def test_draft_step_launch_sequence():
-    # fc + slot init, then per layer QKV, finishing, attention, O, post norm,
+    # fc + slot init, then per layer QKV, finishing (fp32 models; the bf16
+    # attention kernel finishes q, k, v itself), attention, O, post norm,
     # gate/up, down, next norm, then the LM head
     from paper_2609_37029_amd import ldr
     for shape in (synth.TINY, synth.QWEN3_8B):
         kinds = ldr.draft_launches(shape)
-        layer = ["qkv_gemm", "qkv_finish", "attention", "o_gemm", "post_norm", "gate_up_gemm",
-                 "down_gemm", "next_norm"]
+        finish = ["qkv_finish"] if shape.dtype == "f32" else []
+        layer = ["qkv_gemm"] + finish + ["attention", "o_gemm", "post_norm", "gate_up_gemm",
+                                          "down_gemm", "next_norm"]
         assert kinds == ["fc_gemm", "slot_init"] + layer * shape.n_layers + ["lm_head"]
 
 
