@@ -70,6 +70,12 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
   // it. P tiles apart.
   constexpr int OQ = 0, OB = OQ + HPW * QR * LDQ, OG = OB + SEGT, OM = OG + HPW * RMAX * LDQ;
   constexpr int OT = OM + HPW * VTILE, AREA = OT + NSEG * SEGT;
+  // The summary values M are fp32: M^T goes to the MFMA as bf16 M_hi plus
+  // bf16 M_lo = M - M_hi (rows of LDL keys, the R <= 16 entries), so the P.M
+  // product keeps M to about 2^-17 relative. The low halves overlay the
+  // segments' chunk tiles, which are first staged after the summary item.
+  constexpr int LDL = RMAX + 8, OL = OT;
+  static_assert(HPW * D * LDL <= NSEG * SEGT, "M_lo fits in the chunk tiles");
   constexpr int MERGE = NSEG * HPW * QR * (D + 2) * 2;
   __shared__ __attribute__((aligned(16))) uint16_t Lds[AREA > MERGE ? AREA : MERGE];
   __shared__ __attribute__((aligned(16))) uint16_t Pt[HPW * NSEG][QR * LDV];
@@ -262,7 +268,7 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
     }
   }
 #pragma unroll
-  for (int i = 0; i < ML; ++i) {  // M^T in bf16: Mt[head][e][r]
+  for (int i = 0; i < ML; ++i) {  // M^T as bf16 high and low parts: Mt[head][e][r]
     const int idx = threadIdx.x + i * NT;
     if (idx < SM) {
       const int hq_ = idx / (RMAX * D / 4), r = idx % RMAX, col = ((idx / RMAX) % (D / 4)) * 4;
@@ -271,8 +277,12 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
       // keeps the conversion here: moved up to the loads, it would wait for them there
       asm volatile("" : "+v"(m4[0]), "+v"(m4[1]), "+v"(m4[2]), "+v"(m4[3]));
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        Lds[OM + hq_ * VTILE + (col + k) * LDV + r] = ok ? f32_to_bf16(__uint_as_float(m4[k])) : 0;
+      for (int k = 0; k < 4; ++k) {
+        const float m = __uint_as_float(m4[k]);
+        const uint16_t hi = f32_to_bf16(m);
+        Lds[OM + hq_ * VTILE + (col + k) * LDV + r] = ok ? hi : 0;
+        Lds[OL + hq_ * D * LDL + (col + k) * LDL + r] = ok ? f32_to_bf16(m - bf16_to_f32(hi)) : 0;
+      }
     }
   }
   for (int idx = threadIdx.x; idx < HPW * D * (KC - RMAX) / 8; idx += NT) {  // keys 16..31
@@ -365,7 +375,8 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
       }
   };
   // O += P V for the probabilities of a score tile, through the wave's P tile
-  auto pv = [&](f32x4 (&sc)[2], const uint16_t* vbuf) {
+  // (vlo: the low parts of the first 16 keys' values, rows of LDL)
+  auto pv = [&](f32x4 (&sc)[2], const uint16_t* vbuf, const uint16_t* vlo = nullptr) {
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
@@ -377,6 +388,14 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
     for (int n = 0; n < NDT; ++n)
       o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
           pf, frag(&vbuf[(n * 16 + (lane & 15)) * LDV + (lane >> 4) * 8]), o[n], 0, 0, 0);
+    if (vlo) {
+      const bool low_keys = (lane >> 4) < 2;   // keys 0 .. 15; keys 16 .. 31 carry 0
+#pragma unroll
+      for (int n = 0; n < NDT; ++n) {
+        const bf16x8 lf = frag(&vlo[(n * 16 + (lane & 15)) * LDL + (low_keys ? (lane >> 4) * 8 : 0)]);
+        o[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pf, low_keys ? lf : bf16x8{}, o[n], 0, 0, 0);
+      }
+    }
     wave_lds_sync();
   };
   // scores of one 32-key tile (keys kbuf, values vbuf), softmax, O += P V
@@ -406,8 +425,9 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
           qf[kk], frag(&Lds[OG + hh * RMAX * LDQ + (lane & 15) * LDQ + kk * 32 + (lane >> 4) * 8]),
           sc[0], 0, 0, 0);
     absorb(sc, a.R);
-    pv(sc, Lds + OM + hh * VTILE);
+    pv(sc, Lds + OM + hh * VTILE, Lds + OL + hh * D * LDL);
   }
+  lds_barrier();   // every wave is past the summary item: the chunk tiles are free
 
   // ---- the segments walk their window chunks in step: stage, barrier,
   // compute, barrier
