@@ -73,17 +73,21 @@ __device__ inline float4 f4scale(float4 a, float s, float4 g) {
   return make_float4(a.x * s * g.x, a.y * s * g.y, a.z * s * g.z, a.w * s * g.w);
 }
 
-// Rows of `hidden` <= kMaxHidden elements: each thread owns float4 chunk
-// c of (threadIdx + c * kThreads) for c < kChunks. The loops over chunks and
+// The row kernels below (slot init, residual norm) take one workgroup of
+// kNormThreads threads per row of `hidden` <= kMaxHidden elements: each
+// thread owns float4 chunk c of (threadIdx + c * kNormThreads) for
+// c < kNormChunks, so a row of up to 4096 elements is one float4 per thread,
+// and every CU keeps 16 waves of loads in flight. The loops over chunks and
 // splits have compile-time bounds, so every load is issued before the first
 // reduction instead of one memory round trip per loop iteration.
-constexpr int kChunks = 8, kMaxHidden = kThreads * 4 * kChunks;
+constexpr int kMaxHidden = 8192;
+constexpr int kNormThreads = 1024, kNormChunks = kMaxHidden / (kNormThreads * 4);
 
 // One workgroup per (slot i, sequence b); every workgroup of a sequence
 // reduces the boundary-fusion partials itself (from L2).
 template <typename T, int SPLITS>
-__global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
-  __shared__ float red[kThreads / 64];
+__global__ void __launch_bounds__(kNormThreads) slot_init_kernel(SlotArgs a) {
+  __shared__ float red[kNormThreads / 64];
   const int H = a.hidden;
   const int i = blockIdx.x, b = blockIdx.y;
   const long m = (long)b * a.B + i;
@@ -95,11 +99,11 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
   const T* e = i == 0 ? static_cast<const T*>(a.embed) + (long)anchor * H
                       : static_cast<const T*>(a.mask_emb);
   const T* p = static_cast<const T*>(a.pos_emb) + (long)i * H;
-  float4 c[kChunks], ep[kChunks], gfc[kChunks], gin[kChunks];
+  float4 c[kNormChunks], ep[kNormChunks], gfc[kNormChunks], gin[kNormChunks];
   float ss = 0.f;
 #pragma unroll
-  for (int ch = 0; ch < kChunks; ++ch) {
-    const int k = (threadIdx.x + ch * kThreads) * 4;
+  for (int ch = 0; ch < kNormChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kNormThreads) * 4;
     if (k < H) {
       float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
       gfc[ch] = v;
@@ -116,21 +120,21 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
       ss += f4dot(v);
     }
   }
-  const float inv_c = rsqrtf(block_sum(ss, red) / H + a.eps);
+  const float inv_c = rsqrtf(block_sum<kNormThreads>(ss, red) / H + a.eps);
   float sx = 0.f;
 #pragma unroll
-  for (int ch = 0; ch < kChunks; ++ch) {
-    const int k = (threadIdx.x + ch * kThreads) * 4;
+  for (int ch = 0; ch < kNormChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kNormThreads) * 4;
     if (k < H) {
       c[ch] = f4add(ep[ch], f4scale(c[ch], inv_c, gfc[ch]));
       *reinterpret_cast<float4*>(a.x + m * H + k) = c[ch];
       sx += f4dot(c[ch]);
     }
   }
-  const float inv = rsqrtf(block_sum(sx, red) / H + a.eps);
+  const float inv = rsqrtf(block_sum<kNormThreads>(sx, red) / H + a.eps);
 #pragma unroll
-  for (int ch = 0; ch < kChunks; ++ch) {
-    const int k = (threadIdx.x + ch * kThreads) * 4;
+  for (int ch = 0; ch < kNormChunks; ++ch) {
+    const int k = (threadIdx.x + ch * kNormThreads) * 4;
     if (k < H) {
       // four consecutive k stay inside one 16-byte chunk of the fragment layout
       const long o = a.frag ? ((m >> 4) * (long)(H >> 5) + (k >> 5)) * 512 +
@@ -142,7 +146,7 @@ __global__ void __launch_bounds__(kThreads) slot_init_kernel(SlotArgs a) {
   // rotary table row of this slot, absolute position t + i
   const int half = a.d / 2;
   const long t = a.pos[b];
-  for (int e2 = threadIdx.x; e2 < half; e2 += kThreads) {
+  for (int e2 = threadIdx.x; e2 < half; e2 += kNormThreads) {
     const double inv_freq = pow(a.base, -2.0 * e2 / a.d);
     const double ang = (double)(t + i) * inv_freq;
     a.rope[m * half + e2] = (float)cos(ang);
@@ -155,11 +159,6 @@ struct ResidArgs {
   float* x; void* nrm; const void* gain; int hidden; float eps;
   int layout;  // nrm layout: NRM_ROWS, NRM_TILED or NRM_FRAG (hidden % 32 == 0)
 };
-
-// One workgroup of kNormThreads threads per row: with 1024 threads a row of
-// up to 4096 elements is one float4 per thread, and every CU keeps 16 waves
-// of loads in flight.
-constexpr int kNormThreads = 1024, kNormChunks = kMaxHidden / (kNormThreads * 4);
 
 template <typename T, int SPLITS>
 __global__ void __launch_bounds__(kNormThreads) resid_norm_kernel(ResidArgs a) {
@@ -345,7 +344,7 @@ __global__ void __launch_bounds__(kThreads) attention_valu_kernel(AttnArgs a) {
 struct SlotLaunch {
   template <typename T, int S>
   static void go(dim3 grid, const SlotArgs& a, hipStream_t st) {
-    hipLaunchKernelGGL((slot_init_kernel<T, S>), grid, dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((slot_init_kernel<T, S>), grid, dim3(kNormThreads), 0, st, a);
   }
 };
 struct QkvLaunch {
