@@ -175,6 +175,10 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
     rc[f][2] = *reinterpret_cast<const float4*>(sn);
     rc[f][3] = *reinterpret_cast<const float4*>(sn + 4);
   }
+  // the window loads stay behind these in issue order, so that finishing the
+  // block rows waits for its own loads only (the scheduler does not move
+  // loads across this point)
+  __builtin_amdgcn_sched_barrier(0);
 
   // ---- window chunks: ring slot p holds the segment's chunk cbeg + p (the
   // last one repeated for a segment with fewer chunks)
@@ -315,7 +319,7 @@ __global__ void __launch_bounds__(64 * HPW * NSEG) attention_mfma_kernel(AttnArg
   int steps = 0;   // the same on every thread: every wave meets every barrier
 #pragma unroll
   for (int sg = 0; sg < NSEG; ++sg) steps = max(steps, seg_items(sg));
-  __syncthreads();
+  lds_barrier();   // the staged tiles are whole; the window loads stay in flight
 
   bf16x8 qf[KS];
 #pragma unroll
