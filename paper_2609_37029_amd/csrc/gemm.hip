@@ -500,12 +500,13 @@ __global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(Ge
 // over the 256 CUs (256-column tiles would make 594: a third round of 82
 // tiles that runs nearly as long as a full one, at one CU's streaming rate).
 // The waves compute 128 x 80 each (8 x 5 MFMA tiles), so the tile computes
-// HW = 320 columns; the last 16 belong to the next tile and are dropped.
+// HW = 320 columns; the last 16 belong to the next tile: their weight rows
+// are not staged and their columns are dropped.
 // Waves 0-3 and 4-7 form two groups that share the four SIMDs pairwise and take
 // turns, one barrier apart: while one group issues its 40 MFMAs for the current
 // K block, the other reads its fragments of that block from LDS and starts the
 // DMA (global_load_lds) of its part of the block D steps ahead: group 0 the
-// 256 A rows (16 KB), group 1 the 320 W rows (20 KB). Each SIMD's matrix unit
+// 256 A rows (16 KB), group 1 the 304 W rows (19 KB). Each SIMD's matrix unit
 // is thus fed by one wave or the other most of the time. Stages of 576 rows x
 // 64 B live in NB = 4 LDS buffers; the 16-byte chunk c of stage row r sits at
 // chunk c ^ ((r >> 2) & 3), so the 16 lanes of a fragment read hit 64 distinct
@@ -523,6 +524,8 @@ constexpr long TBLK = (long)TR * TK;
 constexpr int HB = 304, HW = 320;
 
 __device__ inline int tile_swz(int r) { return (r >> 2) & 3; }
+// The 16 rows of wave wq's DMA issue q past the tile's HB columns.
+__device__ inline bool lr_overlap(int wq, int q) { return wq * 80 + q * 16 >= HB; }
 
 // Greedy partial of the fused head: the largest logit of a column range and
 // its first token.
@@ -563,10 +566,15 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
     }
     kstride = TBLK;
   } else {
+    // The last 16 of the 320 rows belong to the next tile; their output
+    // columns are dropped. Their DMA (wave 3, q = 4) re-reads the 16 rows
+    // before them, which the same wave has just requested (a cache hit, with
+    // the same chunk swizzle), instead of fetching 16 more rows from memory:
+    // every wave still issues QW DMAs per block.
     const long R = a.ldw;   // padded weight rows of one column block
 #pragma unroll
     for (int q = 0; q < QW; ++q) {
-      const int lr = wq * 80 + q * 16 + (lane >> 2);
+      const int lr = wq * 80 + q * 16 + (lane >> 2) - (lr_overlap(wq, q) ? 16 : 0);
       const long gr = min((long)n0 + lr, R - 1);
       src[q] = static_cast<const uint16_t*>(a.W) + gr * TK +
                (((lane & 3) ^ tile_swz(TR + lr)) * 8);
