@@ -8,9 +8,8 @@
 //  * chunk_lse_kernel streams the logits once (16-byte loads, four sweeps in
 //    flight per lane) and writes L_c: a lane holds 4 tokens of a chunk, the
 //    chunk's max and sum of exp(z/T - max) are reduced over its 4 lanes with
-//    DPP, in the pairwise order (t0 + t1) + (t2 + t3), ... that a 16-lane DPP
-//    reduction of one token per lane also gives (the vocabulary head's
-//    epilogue can write the same L_c);
+//    DPP, in the balanced pairwise order (t0 + t1) + (t2 + t3), ... over the
+//    chunk's tokens;
 //  * chunk_draw_kernel, one workgroup per row, runs the Gumbel-max over the
 //    row's L_c like a one-level sampler over V/16 entries: per lane the
 //    running max / sum of exp(L_c) for the log-normaliser and the best key,
