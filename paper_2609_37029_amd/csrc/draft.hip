@@ -211,7 +211,8 @@ struct QkvArgs {
   float eps;
 };
 
-// Block q, k and v rows (Eq. 6 inputs): sum of the split-K partials, then for
+// Block q, k and v rows (Eq. 6 inputs) for fp32 models (the bf16 attention
+// kernel does this in its prologue): sum of the split-K partials, then for
 // q and k heads the per-head RMSNorm and the rotate-half RoPE at position
 // t + i (table of slot_init). One wave per (row m, head slot hs), where slots
 // [0, hq) are query heads, [hq, hq + hkv) key heads and the rest value heads;
@@ -411,8 +412,8 @@ hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int spli
   a.qkv_out = s.qkv_out; a.eps = s.eps;
   const int waves = kThreads / 64;
   const dim3 grid((unsigned)(((long)M * a.nh + waves - 1) / waves));
-  return s.dtype == LDR_BF16 ? launch_split<uint16_t, QkvLaunch>(splits, grid, a, st)
-                            : launch_split<float, QkvLaunch>(splits, grid, a, st);
+  if (s.dtype == LDR_BF16) return hipErrorInvalidValue;   // the bf16 attention finishes q/k/v
+  return launch_split<float, QkvLaunch>(splits, grid, a, st);
 }
 
 hipError_t launch_attention(const Shape& s, const Layout& L, int batch, const DraftPtrs& p,

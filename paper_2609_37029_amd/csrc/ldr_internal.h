@@ -241,6 +241,7 @@ enum NrmLayout {
 hipError_t launch_resid_norm(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const void* gain, hipStream_t st, void* tiled_out = nullptr,
                              int layout = NRM_TILED);
+// fp32 models only (the bf16 attention kernel finishes q, k, v itself).
 hipError_t launch_qkv_finish(const Shape& s, int M, const DraftPtrs& p, int splits,
                              const ldr_layer_weights* lw, hipStream_t st);
 // o_frag: the output in the fragment layout (bf16 only).
