@@ -44,7 +44,6 @@ constexpr int LDK = BK;       // LDS row (elements): 128 B, 16-byte chunks swizz
 // (two rows of 8 chunks) and of fragment reads (16 rows, one chunk) hit 64
 // distinct banks.
 __device__ inline int lds_chunk(int r, int c) { return c ^ ((r >> 1) & 7); }
-constexpr int WPF = 4;        // weight steps in flight
 
 // Interleaved N index of the SwiGLU GEMM -> row of w_gate_up.
 __device__ inline int swiglu_row(int c, int mlp) {
@@ -56,8 +55,9 @@ __device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
 
 // acc = A[m0 .., kbeg .. kbeg + nk BK) . W[n0 .., same]^T for one BM x BN tile
 // (SWI: W rows in the interleaved gate/up order), through the LDS buffers
-// As / Ws of the calling kernel. nk even (two steps per loop pass).
-template <int MTW, int NTW, int WM, int WN, bool SWI>
+// As / Ws of the calling kernel, WPF weight steps in flight in registers.
+// nk even (two steps per loop pass).
+template <int MTW, int NTW, int WM, int WN, bool SWI, int WPF>
 __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int kbeg, int nk,
                                          uint16_t (&As)[2][WM * MTW * 16 * LDK],
                                          uint16_t (&Ws)[2][WN * NTW * 16 * LDK],
@@ -224,7 +224,9 @@ __device__ __forceinline__ void xcd_tile(int& x, int& y, int& z) {
   z = l / (gx * gy);
 }
 
-template <int MTW, int NTW, int WM, int WN, int EPI>
+// WPF: weight steps in flight (8 measured no faster for the 16-row tiles,
+// which only stream weights).
+template <int MTW, int NTW, int WM, int WN, int EPI, int WPF = 4>
 __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
   constexpr int BM = WM * MTW * 16, BN = WN * NTW * 16;
   static_assert(EPI != EPI_SWIGLU || NTW % 2 == 0, "swiglu pairs");
@@ -235,7 +237,7 @@ __global__ void __launch_bounds__(WM * WN * 64, 1) gemm_kernel(GemmArgs a) {
   const int n0 = bx * BN, m0 = by * BM;
   const int kper = a.K / a.splits, kbeg = z * kper, nk = kper / BK;
   f32x4 acc[MTW][NTW];
-  tile_mma<MTW, NTW, WM, WN, EPI == EPI_SWIGLU>(a, n0, m0, kbeg, nk, As, Ws, acc);
+  tile_mma<MTW, NTW, WM, WN, EPI == EPI_SWIGLU, WPF>(a, n0, m0, kbeg, nk, As, Ws, acc);
   store_tile<MTW, NTW, WM, WN, EPI>(a, n0, m0, z, acc);
 }
 
@@ -755,6 +757,8 @@ __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, l
 // 5: BM 256 with 4 x 2 waves of 64 x 32 (BN 64), in place of cfg 3 when cfg 3
 // would split K eight ways into pieces of at most 512: as fast there (the O
 // projection) with half the split-K partials for the next kernel to read;
+// 9: BM 16 with 3 waves along N (BN 96), in place of cfg 0 where 96-column
+// tiles fill the CUs better;
 // 6, 7, 8: gemm_frag_kernel, BM 256 with 8 compute waves of 32 x 96 (BN 96),
 // 32 x 128 (BN 128) or 32 x 64 (BN 64) and 4 loader waves, activation rows in
 // the fragment layout: the GEMMs above 64 rows whose input is written in that
@@ -780,6 +784,7 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
       hipLaunchKernelGGL((gemm_frag_kernel<2, 4, EPI, 2, kFragLoaders, 6>), grid,
                          dim3(kFragThreads), 0, st, a);
       break;
+    case 9: hipLaunchKernelGGL((gemm_kernel<1, 2, 1, 3, EPI>), grid, dim3(192), 0, st, a); break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -859,17 +864,34 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
          : (p.cfg == 3 || p.cfg == 0 || p.cfg == 7) ? 128 : 256;
     kstep = 2 * BK;
   }
+  // split-K factor for `tiles` tiles: up to about one workgroup per CU, an
+  // even number of at least 2 K steps per split
+  auto split_for = [&](long tiles) {
+    int s = 1;
+    if (allow_split)
+      while (s < max_splits && tiles * s * 2 <= kCUs && K % (2 * s * kstep) == 0 &&
+             K / (2 * s) >= 2 * kstep)
+        s *= 2;
+    return s;
+  };
+  if (p.cfg == 0) {
+    // 16-row tiles of 128 columns (4 waves) or 96 columns (cfg 9, 3 waves):
+    // the width whose workgroups fill more of their last round over the CUs
+    // (128 on a tie). At batch 1 the SwiGLU GEMM's 24576 columns make 192
+    // tiles of 128 but 256 of 96 (47.6 and 47.7 us: these tiles stream their
+    // weights at the chip's rate either way), and the QKV projection 48 x 4
+    // against 64 x 4 (14.6 -> 13.2 us).
+    auto fill = [&](int w) {
+      const long tiles = (long)((N + w - 1) / w) * ((M + 15) / 16);
+      const long wg = tiles * split_for(tiles);
+      return (double)wg / (double)(((wg + kCUs - 1) / kCUs) * kCUs);
+    };
+    if (fill(96) > fill(128) + 1e-9) { p.cfg = 9; bn = 96; }
+  }
   p.ntw = 0;
   p.grid_x = (N + bn - 1) / bn;
   p.grid_y = (M + bm - 1) / bm;
-  int s = 1;
-  if (allow_split) {
-    const int tiles = p.grid_x * p.grid_y;
-    while (s < max_splits && tiles * s * 2 <= kCUs && K % (2 * s * kstep) == 0 &&
-           K / (2 * s) >= 2 * kstep)
-      s *= 2;
-  }
-  p.splits = s;
+  p.splits = split_for((long)p.grid_x * p.grid_y);
   return p;
 }
 

@@ -156,7 +156,7 @@ struct GemmArgs {
 };
 struct GemmPlan { int cfg, ntw, splits; int grid_x, grid_y; };  // cfg: tile configuration
 // The plan's kernel reads its activation rows in the fragment layout (NRM_FRAG).
-inline bool gemm_plan_frag(const GemmPlan& p) { return p.cfg >= 6; }
+inline bool gemm_plan_frag(const GemmPlan& p) { return p.cfg >= 6 && p.cfg <= 8; }
 // Tile configuration and split-K factor; splits = 1 unless allow_split, at
 // most max_splits (a power of two). frag: the caller can give the activation
 // rows in the fragment layout.
