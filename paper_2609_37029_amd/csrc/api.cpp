@@ -135,7 +135,8 @@ struct ldr_views {
   uint8_t* arena;
   int64_t* pos;
   const void* G;
-  int32_t* status;  // device, 256 bytes
+  int32_t* status;  // device, 256 bytes: the sticky flags, and at word
+                    // kCommitCounter the update's commit counter
 };
 
 extern "C" {
@@ -206,13 +207,16 @@ static int views_update_impl(ldr_views* v, const int32_t* n_new, int32_t max_new
   if (max_new > 0 && (!K_new || !V_new || !aligned(K_new, 16) || !aligned(V_new, 16)))
     return LDR_EINVAL;
   if (v->s.keep_bnd && (!h_new || !aligned(h_new, 16))) return LDR_EINVAL;
+  // the last launch that reads t commits from its last workgroup
+  int32_t* done = v->status + kCommitCounter;
   if (max_new > 0) {
     if (launch_views_update(v->s, v->L, v->batch, v->arena, v->pos, v->G, n_new, max_new, K_new,
-                            V_new, h_new, st) != hipSuccess)
+                            V_new, h_new, st, v->status, v->s.P ? nullptr : done) != hipSuccess)
       return LDR_EHIP;
     if (v->s.P && launch_views_pool(v->s, v->L, v->batch, v->arena, v->pos, n_new, max_new,
-                                    K_new, V_new, st) != hipSuccess)
+                                    K_new, V_new, st, v->status, done) != hipSuccess)
       return LDR_EHIP;
+    return LDR_OK;
   }
   if (launch_views_commit(v->batch, v->pos, n_new, max_new, v->status, st) != hipSuccess)
     return LDR_EHIP;

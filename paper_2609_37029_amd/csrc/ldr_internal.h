@@ -127,14 +127,21 @@ __device__ inline bool in_support(const TopK& t, float z, int v) {
 // Views (views.hip)
 hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* arena,
                               int64_t* pos, hipStream_t st);
+// done: a device counter (0 between launches) when this launch commits
+// (advances pos, or flags a bad count in status) from its last workgroup;
+// null when a later launch reads pos and commits instead.
 hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void* arena,
-                               const int64_t* pos, const void* G, const int32_t* n_new,
+                               int64_t* pos, const void* G, const int32_t* n_new,
                                int max_new, const void* K_new, const void* V_new,
-                               const void* h_new, hipStream_t st);
-// Mean-pooled summary banks (views.hip); runs before the commit.
+                               const void* h_new, hipStream_t st, int32_t* status,
+                               int32_t* done);
+// Mean-pooled summary banks (views.hip); runs after the update, before the
+// commit (done as above).
 hipError_t launch_views_pool(const Shape& s, const Layout& L, int batch, void* arena,
-                             const int64_t* pos, const int32_t* n_new, int max_new,
-                             const void* K_new, const void* V_new, hipStream_t st);
+                             int64_t* pos, const int32_t* n_new, int max_new,
+                             const void* K_new, const void* V_new, hipStream_t st,
+                             int32_t* status, int32_t* done);
+// Without new rows (no update launch): the commit alone.
 hipError_t launch_views_commit(int batch, int64_t* pos, const int32_t* n_new, int max_new,
                                int32_t* status, hipStream_t st);
 
@@ -201,6 +208,9 @@ struct DraftPtrs {
 // Bits of the sticky device status word.
 constexpr int kFlagRange = 1;   // an update saw a row count outside [0, max_new]
 constexpr int kFlagAnchor = 2;  // a draft step saw an anchor outside [0, V)
+// Word of the views' 256-byte status block (its own 64-byte line) that counts
+// the workgroups of an update launch done (0 between launches).
+constexpr int kCommitCounter = 16;
 // Attention over [block; window; summary] of one layer (Eq. 6).
 struct AttnArgs {
   const void* qkv;   // block q, k, v rows (dtype) [M][qkv_out], normalised and rotated

@@ -9,9 +9,12 @@
 //    statistics of the new set N (Eq. 10) by a tiled online log-sum-exp over
 //    the rows, then the two-way merge with the stored (eta, m) (Eq. 11);
 //  * a slice of the boundary-state copy.
-// A one-thread-per-sequence commit kernel then advances t (or raises the
-// sticky range flag); it runs after the update kernel on the same stream, so
-// every workgroup read the old t.
+// The commit then advances t (or raises the sticky range flag): the last
+// workgroup of the last kernel that reads t does it, once every other
+// workgroup of that launch has counted itself done on a device counter (each
+// counts after its own reads of t), so every workgroup reads the old t and
+// no separate launch is needed; without new rows a one-thread-per-sequence
+// commit kernel does it.
 #include "ldr_internal.h"
 
 namespace ldr {
@@ -36,6 +39,30 @@ views_reset_kernel(uint8_t* arena, size_t stride, size_t eta_off, size_t eta_byt
     for (int b = threadIdx.x; b < batch; b += kThreads) pos[b] = 0;
 }
 
+// The commit by the last workgroup of a launch (done == null: not this launch).
+struct CommitTail {
+  int32_t* done;      // device counter, 0 between launches
+  int total;          // workgroups of the launch
+  int64_t* pos; const int32_t* n_new; int max_new, batch; int32_t* status;
+};
+
+__device__ void commit_tail(const CommitTail& c) {
+  if (!c.done) return;
+  __shared__ int last;
+  __syncthreads();   // every thread of the workgroup is past its reads of t
+  if (threadIdx.x == 0) last = atomicAdd(c.done, 1) == c.total - 1;
+  __syncthreads();
+  if (!last) return;
+  for (int b = (int)threadIdx.x; b < c.batch; b += (int)blockDim.x) {
+    const int n = c.n_new[b];
+    if (n < 0 || n > c.max_new)
+      atomicOr(c.status, kFlagRange);
+    else
+      c.pos[b] += n;
+  }
+  if (threadIdx.x == 0) atomicExch(c.done, 0);   // ready for the next launch
+}
+
 struct UpdateArgs {
   uint8_t* arena; size_t stride; size_t kw, vw, m, eta, h;
   const int64_t* pos; const void* G; const int32_t* n_new; int max_new;
@@ -44,6 +71,7 @@ struct UpdateArgs {
   int keep_win, keep_sum, keep_bnd;         // views kept (ablation variants drop some)
   int Wx;                                   // rows per (layer, group) region (window first)
   float inv_sqrt_d;
+  CommitTail ct;
 };
 
 // Sum over aligned groups of tpq lanes (tpq a power of two): DPP lane swaps
@@ -80,7 +108,7 @@ __device__ inline void boundary_slice(const UpdateArgs& a, uint8_t* seq, int j, 
 // DPT: dims of the head each thread owns; TPQ = d / DPT threads share one
 // summary query, Q = rep * R queries per workgroup, Q * TPQ = kThreads.
 template <typename T, int DPT>
-__global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
+__device__ __forceinline__ void views_update_body(const UpdateArgs& a) {
   const int g = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
   const int n = a.n_new[b];
   if (n <= 0 || n > a.max_new) return;  // empty set: identity; bad count: commit flags it
@@ -232,6 +260,12 @@ __global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
   if (part == 0) *etaq = eta;
 }
 
+template <typename T, int DPT>
+__global__ void __launch_bounds__(kThreads) views_update_kernel(UpdateArgs a) {
+  views_update_body<T, DPT>(a);
+  commit_tail(a.ct);
+}
+
 // bf16 path on the matrix cores (v_mfma_f32_16x16x32_bf16). One wave per 16
 // summary queries of the group (NW = rep * R / 16 waves); per tile of up to 32
 // new rows, K rows (row-major) and V^T go to LDS as bf16, then
@@ -256,8 +290,7 @@ __device__ inline void wave_lds_fence() {
 }
 
 template <int DH, int NW>
-__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3)))
-views_update_mfma_kernel(UpdateArgs a) {
+__device__ __forceinline__ void views_update_mfma_body(const UpdateArgs& a) {
   constexpr int KT = 32, KS = DH / 32, NT = DH / 16, NTH = NW * 64;
   constexpr int KLD = DH + 8, VLD = KT + 8;   // padded LDS rows (elements)
   __shared__ __attribute__((aligned(16))) uint16_t Kt[KT * KLD];
@@ -402,6 +435,13 @@ views_update_mfma_kernel(UpdateArgs a) {
   }
 }
 
+template <int DH, int NW>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(3)))
+views_update_mfma_kernel(UpdateArgs a) {
+  views_update_mfma_body<DH, NW>(a);
+  commit_tail(a.ct);
+}
+
 // Mean-pooled summary (the views as the configurations word them): for each
 // of two strides S, slot c mod P of the bank holds the mean K and V row of
 // chunk c = rows [cS, (c+1)S). One workgroup per (kv group, layer, sequence);
@@ -416,10 +456,11 @@ struct PoolArgs {
   const int64_t* pos; const int32_t* n_new; int max_new;
   const void* K_new; const void* V_new;
   int D, hkv, d, Wr, Wx, P, S0, S1;
+  CommitTail ct;
 };
 
 template <typename T>
-__global__ void __launch_bounds__(256) views_pool_kernel(PoolArgs a) {
+__device__ __forceinline__ void views_pool_body(const PoolArgs& a) {
   const int g = blockIdx.x, j = blockIdx.y, b = blockIdx.z;
   const int n = a.n_new[b];
   if (n <= 0 || n > a.max_new) return;   // empty set: identity; bad count: commit flags it
@@ -452,6 +493,12 @@ __global__ void __launch_bounds__(256) views_pool_kernel(PoolArgs a) {
   }
   ps[e] = sk;   // the last chunk's sums (used next time only if it is still open)
   ps[d + e] = sv;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) views_pool_kernel(PoolArgs a) {
+  views_pool_body<T>(a);
+  commit_tail(a.ct);
 }
 
 __global__ void views_commit_kernel(int batch, int64_t* pos, const int32_t* n_new,
@@ -503,9 +550,10 @@ hipError_t launch_views_reset(const Shape& s, const Layout& L, int batch, void* 
 }
 
 hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void* arena,
-                               const int64_t* pos, const void* G, const int32_t* n_new,
+                               int64_t* pos, const void* G, const int32_t* n_new,
                                int max_new, const void* K_new, const void* V_new,
-                               const void* h_new, hipStream_t st) {
+                               const void* h_new, hipStream_t st, int32_t* status,
+                               int32_t* done) {
   UpdateArgs a;
   a.arena = static_cast<uint8_t*>(arena); a.stride = L.stride;
   a.kw = L.kw; a.vw = L.vw; a.m = L.m; a.eta = L.eta; a.h = L.h;
@@ -517,6 +565,8 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
   a.Wx = s.Wx;
   a.inv_sqrt_d = 1.0f / sqrtf((float)s.d);
   const dim3 grid(s.hkv, s.D, batch);
+  a.ct = CommitTail{done, (int)(grid.x * grid.y * grid.z), pos, n_new,
+                    max_new, batch, status};
   const int q = s.rep * s.R;
   if (s.dtype == LDR_BF16 && (s.d == 64 || s.d == 128) && q % 16 == 0) {
     const int nw = q / 16;
@@ -534,14 +584,17 @@ hipError_t launch_views_update(const Shape& s, const Layout& L, int batch, void*
 }
 
 hipError_t launch_views_pool(const Shape& s, const Layout& L, int batch, void* arena,
-                             const int64_t* pos, const int32_t* n_new, int max_new,
-                             const void* K_new, const void* V_new, hipStream_t st) {
+                             int64_t* pos, const int32_t* n_new, int max_new,
+                             const void* K_new, const void* V_new, hipStream_t st,
+                             int32_t* status, int32_t* done) {
   PoolArgs a;
   a.arena = static_cast<uint8_t*>(arena); a.stride = L.stride; a.kw = L.kw; a.vw = L.vw;
   a.ps = L.ps; a.pos = pos; a.n_new = n_new; a.max_new = max_new; a.K_new = K_new;
   a.V_new = V_new; a.D = s.D; a.hkv = s.hkv; a.d = s.d; a.Wr = s.Wr; a.Wx = s.Wx; a.P = s.P;
   a.S0 = s.S0; a.S1 = s.S1;
   const dim3 grid(s.hkv, s.D, batch), block(2 * s.d);   // d <= 128
+  a.ct = CommitTail{done, (int)(grid.x * grid.y * grid.z), pos, n_new,
+                    max_new, batch, status};
   if (s.dtype == LDR_BF16)
     hipLaunchKernelGGL(views_pool_kernel<uint16_t>, grid, block, 0, st, a);
   else
