@@ -550,6 +550,23 @@ def counters_run(args, torch, ldr, synth):
                       "sources_sha256": source_digest()}), flush=True)
 
 
+def step_starts(names, n_kinds):
+    """(i, j) for every draft step in a dispatch sequence: the views update of
+    the step starts at i (its kernels, up to the commit, end before j) and its
+    n_kinds draft launches start at j with the boundary-fusion GEMM (the
+    prefill's updates are followed by further updates instead)."""
+    out = []
+    for i, name in enumerate(names):
+        if "views_update" not in name:
+            continue
+        j = i + 1
+        while j < len(names) and ("views_pool" in names[j] or "views_commit" in names[j]):
+            j += 1
+        if j + n_kinds <= len(names) and "gemm" in names[j]:
+            out.append((i, j))
+    return out
+
+
 def traffic_from_csv(fetch_csv, write_csv, workload):
     """Per-launch FETCH_SIZE / WRITE_SIZE (KiB) of every launch kind of the draft
     step, the views update and the sampler, each scaled by what the counter
@@ -579,20 +596,18 @@ def traffic_from_csv(fetch_csv, write_csv, workload):
         kib = statistics.median(calib)
         factor = COPY_BYTES / 1024 / kib
         per = {}
-        for i, (_, name, _) in enumerate(rows):
-            if "views_commit_kernel" not in name or i + len(kinds) + 2 >= len(rows):
+        for i, j in step_starts([r[1] for r in rows], len(kinds)):
+            if j + len(kinds) + 2 > len(rows):
                 continue
-            seq = rows[i + 1:i + 1 + len(kinds)]
-            if "gemm" not in seq[0][1]:
-                continue          # an update of the prefill, not of a step
-            per.setdefault("views_update", []).append(rows[i - 1][2] + rows[i][2])
+            seq = rows[j:j + len(kinds)]
+            per.setdefault("views_update", []).append(sum(r[2] for r in rows[i:j]))
             out.setdefault("symbols", {})["views_update"] = " + ".join(
-                kernel_symbol(r[1]) for r in rows[i - 1:i + 1])
+                kernel_symbol(r[1]) for r in rows[i:j])
             for k, (_, kname, v) in zip(kinds, seq):
                 e = per.setdefault(k, [])
                 e.append(v)
                 out.setdefault("symbols", {})[k] = kernel_symbol(kname)
-            tail = rows[i + 1 + len(kinds):i + 3 + len(kinds)]
+            tail = rows[j + len(kinds):j + 2 + len(kinds)]
             per.setdefault("sample", []).append(sum(v for _, _, v in tail))
             out.setdefault("symbols", {})["sample"] = " + ".join(kernel_symbol(r[1]) for r in tail)
         out.setdefault("calibration", {})[counter] = {"kib_read_by_counter": kib,
@@ -641,12 +656,8 @@ def mfma_from_csv(path, workload):
     rows = [disp[k] for k in sorted(disp)]
     simds, xcds, ghz = 256 * 4, 8, 2.4
     per = {}
-    for i, r in enumerate(rows):
-        if "views_commit_kernel" not in r["name"] or i + len(kinds) >= len(rows):
-            continue
-        seq = rows[i + 1:i + 1 + len(kinds)]
-        if "gemm" not in seq[0]["name"]:
-            continue              # an update of the prefill, not of a step
+    for _, j in step_starts([r["name"] for r in rows], len(kinds)):
+        seq = rows[j:j + len(kinds)]
         for k, d in zip(kinds, seq):
             if k.endswith("gemm") or k == "lm_head":
                 per.setdefault(k, []).append(d)
