@@ -191,3 +191,18 @@ def test_percentile():
     assert bench.percentile(xs, 0.5) == 3.0
     assert bench.percentile(xs, 0.0) == 1.0 and bench.percentile(xs, 1.0) == 5.0
     assert bench.percentile([], 0.5) is None
+
+
+def test_step_starts_finds_each_draft_step_by_its_views_update():
+    """The counter parsers find a step by its views update launch (with the
+    pooling kernel, or the commit kernel of an update without rows, before the
+    draft launches), skipping the prefill's updates, which are followed by
+    further updates rather than the boundary-fusion GEMM."""
+    names = ["neg", "views_update_mfma_kernel", "views_update_mfma_kernel",       # prefill
+             "views_update_mfma_kernel", "gemm_kernel", "slot", "attn", "lse", "draw",
+             "views_update_kernel", "views_pool_kernel", "gemm_kernel", "slot", "attn",
+             "lse", "draw",
+             "views_commit_kernel", "views_update_mfma_kernel", "views_commit_kernel",
+             "gemm_kernel", "slot", "attn"]
+    assert bench.step_starts(names, 3) == [(3, 4), (9, 11), (17, 19)]
+    assert bench.step_starts(names[:5], 3) == []      # too few launches after it
