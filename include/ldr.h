@@ -181,8 +181,8 @@ int ldr_config_check(const ldr_config* cfg);
  *   K_prefix, V_prefix  dev [batch][max_prefix][D][Hkv][d] dtype
  *   h_boundary dev [batch][L_b][hidden] dtype: boundary states after it (may be
  *              NULL with LDR_DROP_BOUNDARY)
- * The handle also owns a 256-byte device status word, freed by
- * ldr_views_destroy. */
+ * The handle also owns a 256-byte device status block (the sticky flags and
+ * the update's commit counter), freed by ldr_views_destroy. */
 int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* arena,
                    int64_t* pos, const void* G, const int32_t* n_prefix, int32_t max_prefix,
                    const void* K_prefix, const void* V_prefix, const void* h_boundary,
@@ -206,7 +206,9 @@ int ldr_views_init(ldr_views** out, const ldr_config* cfg, int32_t batch, void* 
  * A view the configuration drops (drop_views) is left out of this list.
  * n = 0 leaves that sequence's views and t bit-identical (App. A.2). A count
  * outside [0, max_new] leaves the sequence unchanged and sets the sticky
- * LDR_ERANGE flag.
+ * LDR_ERANGE flag. Calls on one handle must be ordered (one stream, or
+ * streams joined by events): t is advanced by the last workgroup of the
+ * update, counted in the handle's status block.
  *   n_new       dev int32 [batch]
  *   K_new, V_new dev [batch][max_new][D][Hkv][d] dtype (row r of sequence b at
  *               [b][r]; rows r >= n_new[b] are ignored)
