@@ -211,16 +211,17 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, in
 // The tile (x, y) and K split z of this workgroup. Workgroups go to the 8
 // XCDs in turn by linear id (id mod 8), and each XCD has its own L2: the
 // linear ids are renumbered so that XCD c takes the c-th eighth of the tiles
-// in (z, y, x) order. A K split's activation columns are then read into one
-// or two XCDs' L2 instead of all eight.
+// in (z, x, y) order. A K split's activation columns are then read into one
+// or two XCDs' L2 instead of all eight, and the row tiles of one column tile
+// (M above one tile) share their weight columns in one L2.
 __device__ __forceinline__ void xcd_tile(int& x, int& y, int& z) {
   const int gx = gridDim.x, gy = gridDim.y;
   const int total = gx * gy * gridDim.z;
   const int lin = blockIdx.x + gx * (blockIdx.y + gy * blockIdx.z);
   const int q = total >> 3, r = total & 7, c = lin & 7, slot = lin >> 3;
   const int l = c < r ? c * (q + 1) + slot : r * (q + 1) + (c - r) * q + slot;
-  x = l % gx;
-  y = (l / gx) % gy;
+  y = l % gy;
+  x = (l / gy) % gx;
   z = l / (gx * gy);
 }
 
