@@ -552,7 +552,10 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
   const int grp = wave >> 2, wq = wave & 3;
   const int wm = grp, wn = wq;   // output rows wm * 128 .., columns wn * 80 ..
   const int nkb = a.K / TK;
-  const int ct = blockIdx.x, n0 = ct * HB;
+  int ct, rt, z_;
+  xcd_tile(ct, rt, z_);   // column tile, row tile: the row tiles of a column tile share its
+                          // weight columns in one L2
+  const int n0 = ct * HB;
   // DMA: wave wq of group 0 moves A rows wq * 64 + q * 16 + lane / 4, of group 1
   // W rows wq * 80 + q * 16 + lane / 4 (4 lanes per 64-byte row, lane & 3 = the
   // destination chunk); W rows past the padded matrix read its last row.
@@ -560,7 +563,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
   int dst[QW];
   long kstride;
   if (grp == 0) {
-    const uint16_t* tile = static_cast<const uint16_t*>(a.A) + (long)blockIdx.y * nkb * TBLK;
+    const uint16_t* tile = static_cast<const uint16_t*>(a.A) + (long)rt * nkb * TBLK;
 #pragma unroll
     for (int q = 0; q < QW; ++q) {
       const int r = wq * 64 + (q < QA ? q : 0) * 16 + (lane >> 2);
@@ -660,7 +663,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
 #undef LDR_MEM
   wait_vmcnt<0>();   // no DMA outlives the workgroup
   const int crow = (lane >> 4) * 4, ccol = lane & 15;
-  const int r0 = blockIdx.y * TR + wm * 128, c0 = n0 + wn * 80;
+  const int r0 = rt * TR + wm * 128, c0 = n0 + wn * 80;
   const int cend = min(a.N, n0 + HB);   // the tile's own columns
   if (!SAMPLE || hs.store_logits) {
     float* out = static_cast<float*>(a.out);
@@ -706,7 +709,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
       }
     __syncthreads();
     if (tid < TR) {
-      const int row = blockIdx.y * TR + tid;
+      const int row = rt * TR + tid;
       HeadPart p = tab[tid][0];
 #pragma unroll
       for (int q = 1; q < 4; ++q) head_combine(p, tab[tid][q]);
