@@ -45,6 +45,7 @@ MINI_BF16_MLP32B = MINI_BF16.replace(name="mini-bf16-mlp25600", mlp=25600)
 @pytest.mark.parametrize("shape,batch,prefix", [
     (synth.TINY, 1, 2048),     # the fp32 parity configuration
     (synth.TINY, 3, 40),       # partial window (t < W)
+    (MINI_BF16, 1, 300),       # bf16, 16 rows: the 16-row GEMM tiles (128 and 96 columns)
     (MINI_BF16, 3, 300),       # bf16, GQA, ragged vocab, 48 rows
     (MINI_BF16, 17, 150),      # bf16, 272 rows: two M tiles, the last ragged
     (MINI_BF16_MLP32B, 16, 100),
