@@ -597,7 +597,7 @@ def traffic_from_csv(fetch_csv, write_csv, workload):
         factor = COPY_BYTES / 1024 / kib
         per = {}
         for i, j in step_starts([r[1] for r in rows], len(kinds)):
-            if j + len(kinds) + 2 > len(rows):
+            if j + len(kinds) + 1 > len(rows):   # the step's sampler was not recorded
                 continue
             seq = rows[j:j + len(kinds)]
             per.setdefault("views_update", []).append(sum(r[2] for r in rows[i:j]))
@@ -607,7 +607,13 @@ def traffic_from_csv(fetch_csv, write_csv, workload):
                 e = per.setdefault(k, [])
                 e.append(v)
                 out.setdefault("symbols", {})[k] = kernel_symbol(kname)
-            tail = rows[j + len(kinds):j + 2 + len(kinds)]
+            # the sampler's kernels after the head (the chunk draw alone when
+            # the head forms the chunk log-masses), up to the next views update
+            tail = []
+            for r in rows[j + len(kinds):j + 2 + len(kinds)]:
+                if "views_" in r[1]:
+                    break
+                tail.append(r)
             per.setdefault("sample", []).append(sum(v for _, _, v in tail))
             out.setdefault("symbols", {})["sample"] = " + ".join(kernel_symbol(r[1]) for r in tail)
         out.setdefault("calibration", {})[counter] = {"kib_read_by_counter": kib,
@@ -813,7 +819,8 @@ def main():
                                 ("argmax in the vocabulary head's epilogue" +
                                  ("" if rig.keep_logits else ", logits not written")
                                  if rig.temperature == 0 else
-                                 "two-level Gumbel-max sampler after the head"))
+                                 "chunk log-masses in the vocabulary head's epilogue, "
+                                 "then the chunk draw"))
                                if rig.fused_head else "ldr_draft_step + ldr_sample"),
                    "views": {0: "window + summary + boundary", 1: "no window", 2: "no summary",
                              4: "no boundary"}.get(s.drop_views, f"drop {s.drop_views}")},

@@ -283,8 +283,11 @@ size_t ldr_draft_step_sample_workspace_bytes(const ldr_config* cfg, int32_t batc
  * steps (temperature 0) whose head reads its tiled copy (w->lm_head_tiled set
  * and batch * B > 64) take the argmax in the head's epilogue, from the fp32
  * logits it has just computed, so the logits need not be written
- * (logits = NULL). Other steps run the head and then ldr_sample's kernels, and
- * need the logits.
+ * (logits = NULL). Sampled steps on the tiled head form the two-level draw's
+ * 16-token chunk log-masses in the head's epilogue, with the bits ldr_sample's
+ * pass over the written logits gives them, then run ldr_sample's chunk draw;
+ * other steps run the head and then ldr_sample's kernels. Both need the
+ * logits.
  *   logits  dev fp32 [batch][B][V], or NULL on the fused greedy path
  *   tokens  dev int32 [batch][B]; lse, logq dev fp32 [batch][B]
  *   workspace dev, ldr_draft_step_sample_workspace_bytes(cfg, batch) bytes,

@@ -341,11 +341,14 @@ extern "C" int32_t ldr_draft_step_launches(const ldr_config* cfg, int32_t* kinds
   return n;
 }
 
-// Greedy sampling fused into the vocabulary head (tiled head only): outputs
-// and the partials' workspace; logits may then be NULL (not written).
+// Sampling fused into the vocabulary head (tiled head only). T = 0: the
+// outputs and the argmax partials' workspace; logits may then be NULL (not
+// written). T > 0: the chunk log-masses go to the sampler's workspace `parts`
+// (rows of ldL floats) beside the logits, for the chunk draw that follows.
 struct FusedSample {
   int32_t* tokens; float* lse; float* logq;
   void* parts;
+  float T; int ldL;
 };
 
 static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32_t* anchor,
@@ -448,7 +451,12 @@ static int draft_step_impl(const ldr_views* v, const ldr_weights* w, const int32
       case LDR_LAUNCH_LM_HEAD:
         g.lda = s.hidden; g.ldw = s.hidden; g.out = logits; g.ldo = s.vocab;
         g.split_stride = 0; g.M = M; g.N = s.vocab; g.K = s.hidden; g.splits = 1;
-        if (tiled_head && fs) {
+        if (tiled_head && fs && fs->T > 0.f) {
+          g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
+          HeadSampleArgs hs{};
+          hs.L = static_cast<float*>(fs->parts); hs.ldL = fs->ldL; hs.T = fs->T;
+          e = launch_gemm_tiled_chunks(g, hs, st);
+        } else if (tiled_head && fs) {
           g.A = base + ws.nrmt; g.W = w->lm_head_tiled;
           HeadSampleArgs hs{};
           hs.parts = fs->parts; hs.store_logits = logits != nullptr;
@@ -507,11 +515,21 @@ int ldr_draft_step_sample(const ldr_views* v, const ldr_weights* w, const int32_
   // greedy steps fuse the argmax into the head, which needs its tiled copy
   // and runs above 64 rows
   if (temperature == 0.f && w->lm_head_tiled && rows > 64) {
-    FusedSample fs{tokens, lse, logq, extra};
+    FusedSample fs{tokens, lse, logq, extra, 0.f, 0};
     return draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st, &fs);
   }
-  // otherwise the head and then the sampler (the same tokens as ldr_sample): logits needed
+  // otherwise the sampler needs the logits (the same tokens as ldr_sample)
   if (!logits) return LDR_EINVAL;
+  // T > 0 on the tiled head: the chunk log-masses in its epilogue, then the
+  // sampler's chunk draw
+  if (w->lm_head_tiled && rows > 64) {
+    FusedSample fs{tokens, lse, logq, extra, temperature, sample_plan(rows, s.vocab).ldL};
+    const int rc = draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st, &fs);
+    if (rc != LDR_OK) return rc;
+    return launch_sample_finish(logits, rows, s.vocab, temperature, seed, step, extra, tokens,
+                                lse, logq, st) == hipSuccess
+               ? LDR_OK : LDR_EHIP;
+  }
   const int rc = draft_step_impl(v, w, anchor, logits, workspace, draft, nullptr, 0, st);
   if (rc != LDR_OK) return rc;
   return launch_sample(logits, rows, s.vocab, temperature, 0, seed, step, tokens, lse, logq,

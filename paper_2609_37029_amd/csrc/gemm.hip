@@ -538,7 +538,12 @@ __device__ inline void head_combine(HeadPart& a, const HeadPart& b) {
   if (b.key > a.key || (b.key == a.key && b.idx < a.idx)) a = b;
 }
 
-template <bool SAMPLE>
+// Epilogues of the vocabulary head: logits only; the greedy partials (logits
+// optional); the logits and the chunk log-masses at T > 0 (T = 1 without the
+// division).
+constexpr int kHeadLogits = 0, kHeadArgmax = 1, kHeadChunks = 2, kHeadChunksUnitT = 3;
+
+template <int HS>
 __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSampleArgs hs) {
   constexpr int NB = 4, D = NB - 1;
   constexpr int STAGE = (TR + HW) * TK * 2;   // bytes: A rows 0..255, W rows 256..575
@@ -636,7 +641,7 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
     __builtin_amdgcn_s_setprio(1);                                                             \
     _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
       _Pragma("unroll") for (int j = 0; j < NT; ++j) acc[i][j] =                               \
-          __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);          \
+          __builtin_amdgcn_mfma_f32_16x16x32_bf16(bfr[j], af[i], acc[i][j], 0, 0, 0);          \
     __builtin_amdgcn_s_setprio(0);                                                             \
     sched_fence();                                                                             \
   }
@@ -662,51 +667,124 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
 #undef LDR_MMA
 #undef LDR_MEM
   wait_vmcnt<0>();   // no DMA outlives the workgroup
-  const int crow = (lane >> 4) * 4, ccol = lane & 15;
+  // The MFMAs take the weight fragments as their first operand, so each
+  // 16 x 16 accumulator tile is (token, row): lane l holds 4 consecutive
+  // tokens g * 4 .. + 3 (g = l / 16) of row l % 16, one float4 of logits, and
+  // the 4 lanes g = 0 .. 3 of a row hold one 16-token chunk.
+  const int g = lane >> 4, rl = lane & 15;
   const int r0 = rt * TR + wm * 128, c0 = n0 + wn * 80;
   const int cend = min(a.N, n0 + HB);   // the tile's own columns
-  if (!SAMPLE || hs.store_logits) {
+  // Most waves hold no token past the vocabulary and write rows that start
+  // on 16 bytes: their epilogues skip the per-token tests (wave-uniform).
+  const bool full = c0 + NT * 16 <= a.N && (a.ldo & 3) == 0;
+  if (HS != kHeadArgmax || hs.store_logits) {
     float* out = static_cast<float*>(a.out);
+    auto store = [&](auto full_t) {
+      constexpr bool FULL = decltype(full_t)::value;
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+      for (int i = 0; i < MT; ++i) {
+        const int row = r0 + i * 16 + rl;
+        if (row >= a.M) continue;
 #pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        const int col = c0 + j * 16 + ccol;
+        for (int j = 0; j < NT; ++j) {
+          const int col = c0 + j * 16 + g * 4;
+          float* o = out + (long)row * a.ldo + col;
+          if (FULL) {
+            if (c0 + j * 16 < cend) *reinterpret_cast<f32x4*>(o) = acc[i][j];
+          } else {
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = r0 + i * 16 + crow + v;
-          if (row < a.M && col < cend) out[(long)row * a.ldo + col] = acc[i][j][v];
+            for (int v = 0; v < 4; ++v)
+              if (col + v < cend) o[v] = acc[i][j][v];
+          }
         }
       }
+    };
+    if (full) store(std::true_type{});
+    else store(std::false_type{});
   }
-  if constexpr (SAMPLE) {
+  // Lane exchanges across the row groups: xor 16 (a swizzle inside each half
+  // wave) and xor 32 (a permute).
+  auto x16 = [](float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x),
+                                                                 0x401F));
+  };
+  const int perm32 = (lane ^ 32) << 2;
+  auto x32 = [perm32](float x) {
+    return __builtin_bit_cast(float,
+                              __builtin_amdgcn_ds_bpermute(perm32, __builtin_bit_cast(int, x)));
+  };
+  if constexpr (HS == kHeadChunks || HS == kHeadChunksUnitT) {
+    // Chunk log-masses (the first level of the two-level draw of Eq. 8 at
+    // T > 0): each lane's max and sum of exp(z/T - max) over its 4 tokens,
+    // (t0 + t1) + (t2 + t3), then over the chunk's 4 lanes (xor 16, then
+    // xor 32) -- the order and operations of the log-mass pass over stored
+    // logits, so L_c has the same bits. Tokens past the vocabulary count as
+    // -inf; chunks past the tile's own columns belong to the next tile and
+    // are not written. Lane group g keeps chunk g (group 0 also chunk 4).
+    const float T = hs.T;
+    auto chunks = [&](auto full_t) {
+      constexpr bool FULL = decltype(full_t)::value;
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        float keep = 0.f, keep4 = 0.f;
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          const int col = c0 + j * 16 + g * 4;
+          float zt[4], e[4];
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            zt[v] = FULL || col + v < a.N
+                        ? (HS == kHeadChunksUnitT ? acc[i][j][v] : acc[i][j][v] / T)
+                        : -INFINITY;
+          float m = fmaxf(fmaxf(zt[0], zt[1]), fmaxf(zt[2], zt[3]));
+          m = fmaxf(m, x16(m));
+          m = fmaxf(m, x32(m));
+#pragma unroll
+          for (int v = 0; v < 4; ++v) e[v] = zt[v] > -INFINITY ? chunk_term(zt[v], m) : 0.f;
+          float sum = (e[0] + e[1]) + (e[2] + e[3]);
+          sum += x16(sum);
+          sum += x32(sum);
+          const float L = chunk_log_mass(m, sum);
+          if (j == 4) keep4 = L;
+          else keep = g == j ? L : keep;
+        }
+        const int row = r0 + i * 16 + rl;
+        if (row < a.M) {
+          float* Lr = hs.L + (long)row * hs.ldL + c0 / 16;
+          if (c0 + g * 16 < cend) Lr[g] = keep;
+          if (NT > 4 && g == 0 && c0 + 64 < cend) Lr[4] = keep4;
+        }
+      }
+    };
+    if (full) chunks(std::true_type{});
+    else chunks(std::false_type{});
+  }
+  if constexpr (HS == kHeadArgmax) {
     // Greedy epilogue (Eq. 8 at T = 0: the first argmax of each row). Per row
-    // of the tile: each lane's best of its 5 columns, the 16 lanes holding a
-    // row (its 80 columns of this wave) by DPP, the 4 waves of the row
+    // of the tile: each lane's best of its 20 tokens, the 4 lanes of the row
+    // (its 80 columns of this wave) by lane exchanges, the 4 waves of the row
     // through LDS, one partial per (row, column tile).
     __shared__ HeadPart tab[TR][4];
     HeadPart* parts = static_cast<HeadPart*>(hs.parts);
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
+    for (int i = 0; i < MT; ++i) {
+      HeadPart p{-INFINITY, 0x7fffffff};
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        HeadPart p{-INFINITY, 0x7fffffff};
+      for (int j = 0; j < NT; ++j)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          const int col = c0 + j * 16 + ccol;
+        for (int v = 0; v < 4; ++v) {
+          const int col = c0 + j * 16 + g * 4 + v;
           if (col < cend) head_combine(p, HeadPart{acc[i][j][v], col});
         }
-        HeadPart o;
-        o.key = dpp<0xB1>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0xB1, 0xF, 0xF, false);
-        head_combine(p, o);
-        o.key = dpp<0x4E>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0x4E, 0xF, 0xF, false);
-        head_combine(p, o);
-        o.key = dpp<0x141>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0x141, 0xF, 0xF, false);
-        head_combine(p, o);
-        o.key = dpp<0x140>(p.key); o.idx = __builtin_amdgcn_mov_dpp(p.idx, 0x140, 0xF, 0xF, false);
-        head_combine(p, o);
-        if (ccol == 0) tab[wm * 128 + i * 16 + crow + v][wn] = p;
-      }
+      HeadPart o;
+      o.key = x16(p.key);
+      o.idx = __builtin_amdgcn_ds_swizzle(p.idx, 0x401F);
+      head_combine(p, o);
+      o.key = x32(p.key);
+      o.idx = __builtin_amdgcn_ds_bpermute(perm32, p.idx);
+      head_combine(p, o);
+      if (g == 0) tab[wm * 128 + i * 16 + rl][wn] = p;
+    }
     __syncthreads();
     if (tid < TR) {
       const int row = rt * TR + tid;
@@ -924,7 +1002,8 @@ hipError_t launch_gemm_tiled(const GemmArgs& a0, hipStream_t st) {
   GemmArgs a = a0;
   a.ldw = (a.N + TR - 1) / TR * TR;   // padded rows of a weight column block
   const dim3 grid((a.N + HB - 1) / HB, (a.M + TR - 1) / TR, 1);
-  hipLaunchKernelGGL((gemm_tiled_kernel<false>), grid, dim3(512), 0, st, a, HeadSampleArgs{});
+  hipLaunchKernelGGL((gemm_tiled_kernel<kHeadLogits>), grid, dim3(512), 0, st, a,
+                     HeadSampleArgs{});
   return hipGetLastError();
 }
 
@@ -940,11 +1019,28 @@ hipError_t launch_gemm_tiled_argmax(const GemmArgs& a0, const HeadSampleArgs& hs
   HeadSampleArgs hs = hs0;
   hs.nparts = (a.N + HB - 1) / HB;
   const dim3 grid(hs.nparts, (a.M + TR - 1) / TR, 1);
-  hipLaunchKernelGGL((gemm_tiled_kernel<true>), grid, dim3(512), 0, st, a, hs);
+  hipLaunchKernelGGL((gemm_tiled_kernel<kHeadArgmax>), grid, dim3(512), 0, st, a, hs);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(head_argmax_merge_kernel, dim3(a.M), dim3(64), 0, st,
                      static_cast<const HeadPart*>(hs.parts), hs.nparts, tokens, lse, logq);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tiled_chunks(const GemmArgs& a0, const HeadSampleArgs& hs0,
+                                    hipStream_t st) {
+  if (!gemm_tiled_supported(a0.M, a0.N, a0.K) || a0.splits != 1 || !a0.out || !hs0.L ||
+      !(hs0.T > 0.f) || hs0.ldL < (a0.N + 15) / 16)
+    return hipErrorInvalidValue;
+  GemmArgs a = a0;
+  a.ldw = (a.N + TR - 1) / TR * TR;
+  HeadSampleArgs hs = hs0;
+  hs.store_logits = 1;
+  const dim3 grid((a.N + HB - 1) / HB, (a.M + TR - 1) / TR, 1);
+  if (hs.T == 1.f)
+    hipLaunchKernelGGL((gemm_tiled_kernel<kHeadChunksUnitT>), grid, dim3(512), 0, st, a, hs);
+  else
+    hipLaunchKernelGGL((gemm_tiled_kernel<kHeadChunks>), grid, dim3(512), 0, st, a, hs);
   return hipGetLastError();
 }
 

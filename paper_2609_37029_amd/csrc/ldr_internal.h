@@ -73,6 +73,25 @@ __device__ inline float max16(float v) {
   return v;
 }
 
+// Chunk log-mass of the two-level draw at T > 0 (Eq. 8): one term
+// exp(zt - m) of a chunk's sum, and the chunk's log-mass m + log s. The same
+// operations (no contraction) wherever L_c is formed, so the log-mass pass over
+// stored logits and the vocabulary head's epilogue give the same bits when
+// they also sum the 16 terms in the same balanced pairwise order.
+#if defined(__HIP_DEVICE_COMPILE__)
+__device__ inline float chunk_term(float zt, float m) {
+#pragma clang fp contract(off)
+  return __builtin_amdgcn_exp2f((zt - m) * 1.44269504088896341f);
+}
+__device__ inline float chunk_log_mass(float m, float s) {
+#pragma clang fp contract(off)
+  return m == -INFINITY ? -INFINITY : m + __builtin_amdgcn_logf(s) * 0.693147180559945309f;
+}
+#else
+__device__ float chunk_term(float zt, float m);   // device code only
+__device__ float chunk_log_mass(float m, float s);
+#endif
+
 // Round to nearest even (the device uses the gfx950 conversion instruction).
 __host__ __device__ inline uint16_t f32_to_bf16(float f) {
 #if defined(__HIP_DEVICE_COMPILE__)
@@ -183,10 +202,19 @@ struct HeadSampleArgs {
   void* parts;        // head_sample_part_bytes(M, V) bytes
   int nparts;         // partials per row (set by the launcher)
   int store_logits;
+  float* L;           // T > 0: chunk log-masses [M][ldL] (the sampler's layout)
+  int ldL;
+  float T;
 };
 size_t head_sample_part_bytes(int rows, int vocab);
 hipError_t launch_gemm_tiled_argmax(const GemmArgs& a, const HeadSampleArgs& hs, int32_t* tokens,
                                     float* lse, float* logq, hipStream_t st);
+// The vocabulary head at T > 0 with the first level of the two-level draw in
+// its epilogue: it writes the logits and every 16-token chunk's log-mass
+// L_c = log sum exp(z / T) to hs.L, bit for bit what the sampler's log-mass
+// pass forms from the written logits; the chunk draw then follows as in the
+// sampler.
+hipError_t launch_gemm_tiled_chunks(const GemmArgs& a, const HeadSampleArgs& hs, hipStream_t st);
 // Elements of a [rows][cols] matrix in the tiled layout (rows padded to 256).
 size_t tiled_elems(long rows, long cols);
 hipError_t launch_tile_matrix(const void* src, long ld, int rows, int cols, void* dst,

@@ -64,17 +64,6 @@ struct SampleArgs {
 constexpr int kChunk = 16;        // tokens per vocabulary chunk of the two-level draw
 constexpr uint32_t kChunkStream = 3;
 
-// One term exp(zt - m) of a chunk's sum and the chunk's log-mass m + log s:
-// the same operations wherever L_c is formed (no contraction).
-__device__ inline float chunk_term(float zt, float m) {
-#pragma clang fp contract(off)
-  return __builtin_amdgcn_exp2f((zt - m) * 1.44269504088896341f);
-}
-__device__ inline float chunk_log_mass(float m, float s) {
-#pragma clang fp contract(off)
-  return m == -INFINITY ? -INFINITY : m + __builtin_amdgcn_logf(s) * 0.693147180559945309f;
-}
-
 // Exact k-th largest logit of a row by radix selection on order_key (four
 // 8-bit digits, most significant first, LDS histograms), then the index cut
 // among the tokens equal to it. One workgroup per row.

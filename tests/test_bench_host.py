@@ -85,9 +85,10 @@ def _write_csv(path, rows, extra=()):
             w.writerow(r)
 
 
-def _dispatches(kinds, value_of, counter, t0=0, ns=1000):
+def _dispatches(kinds, value_of, counter, t0=0, ns=1000, n_sample=2):
     """Rows of one counter: three calibration copies, a prefill update, then
-    two steps (views update + commit, every draft launch, two sampler kernels)."""
+    two steps (views update + commit, every draft launch, n_sample sampler
+    kernels)."""
     rows, did, t = [], 0, t0
 
     def add(name, v):
@@ -109,16 +110,18 @@ def _dispatches(kinds, value_of, counter, t0=0, ns=1000):
             add(f"void ldr::(anonymous namespace)::{k}_gemm_like_kernel(x)"
                 if k.endswith("gemm") or k == "lm_head"
                 else f"ldr::(anonymous namespace)::{k}_kernel(x)", value_of(k))
-        add("ldr::(anonymous namespace)::sample_partial_kernel(x)", value_of("sample"))
-        add("ldr::(anonymous namespace)::sample_merge_kernel(x)", value_of("sample"))
+        for q in range(n_sample):
+            add(f"ldr::(anonymous namespace)::sample_{q}_kernel(x)", value_of("sample"))
     return rows
 
 
-def test_traffic_scaled_by_the_calibration_copy(tmp_path):
+@pytest.mark.parametrize("n_sample", [2, 1])
+def test_traffic_scaled_by_the_calibration_copy(tmp_path, n_sample):
     """FETCH_SIZE reading half of the 1 GiB copy (factor 2) and WRITE_SIZE all
     of it (factor 1): every kind's KiB per launch times 1024 times its
-    counter's factor; the views update is update + commit, the sampler its two
-    kernels."""
+    counter's factor; the views update is update + commit, the sampler its
+    kernels after the head (two, or the chunk draw alone when the head forms
+    the chunk log-masses), never the next step's update."""
     wl = "qwen3-8b-b16-t32768"
     kinds = kinds_of(synth.WORKLOADS[wl].shape)
     copy_kib = bench.COPY_BYTES / 1024
@@ -129,8 +132,8 @@ def test_traffic_scaled_by_the_calibration_copy(tmp_path):
 
     def write(k):
         return {"neg": copy_kib, "update": 7.0, "commit": 1.0, "sample": 0.5}.get(k, 10.0)
-    _write_csv(tmp_path / "f.csv", _dispatches(kinds, fetch, "FETCH_SIZE"))
-    _write_csv(tmp_path / "w.csv", _dispatches(kinds, write, "WRITE_SIZE"))
+    _write_csv(tmp_path / "f.csv", _dispatches(kinds, fetch, "FETCH_SIZE", n_sample=n_sample))
+    _write_csv(tmp_path / "w.csv", _dispatches(kinds, write, "WRITE_SIZE", n_sample=n_sample))
     t = bench.traffic_from_csv(str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), wl)
     assert t["calibration"]["FETCH_SIZE"]["factor"] == pytest.approx(2.0)
     assert t["calibration"]["WRITE_SIZE"]["factor"] == pytest.approx(1.0)
@@ -141,7 +144,7 @@ def test_traffic_scaled_by_the_calibration_copy(tmp_path):
     u = t["kinds"]["views_update"]
     assert u["hbm_bytes_per_launch"] == pytest.approx((30 + 2) * 1024 * 2 + (7 + 1) * 1024)
     assert t["kinds"]["sample"]["hbm_bytes_per_launch"] == pytest.approx(
-        10 * 1024 * 2 + 1 * 1024)
+        n_sample * (5 * 1024 * 2 + 0.5 * 1024))
     assert t["sources_sha256"] == bench.source_digest()
 
 

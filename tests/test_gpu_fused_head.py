@@ -4,8 +4,10 @@ epilogue: the logits it writes are ldr_draft_step's bit for bit, and its
 tokens, lse and log q are the separate sampler's at T = 0 on those logits
 (the separate sampler is itself compared with the oracle in
 test_gpu_sample.py); without the logits it draws the same tokens. Sampled
-steps run the head and the sampler's kernels, and the tokens, lse and log q
-are the separate sampler's bit for bit."""
+steps form the 16-token chunk log-masses in the head's epilogue and then run
+the sampler's chunk draw: logits, tokens, lse and log q are the separate
+calls' bit for bit (lse sums every chunk's log-mass, so it is equal only if
+each of them is)."""
 import numpy as np
 import pytest
 import torch
@@ -133,6 +135,17 @@ def test_small_steps_take_the_separate_sampler(gpu_lib):
 
 
 MINI_WIDE = MINI_BF16.replace(name="mini-bf16-v70000", vocab=70000)
+MINI_WIDE_RAGGED = MINI_BF16.replace(name="mini-bf16-v70020", vocab=70020)
+
+
+@pytest.mark.parametrize("T", [1.0, 0.9, 0.0])
+def test_last_tile_ends_inside_a_wave_and_a_chunk(gpu_lib, T):
+    """Vocabulary 70020 (a multiple of 4, so the logits rows start on 16
+    bytes): the last column tile holds 100 tokens, so its second wave's 80
+    columns end inside a 16-token chunk (tokens 96 .. 99 of the tile, the rest
+    past the vocabulary), and its last two waves hold no token at all."""
+    tok = check(gpu_lib, MINI_WIDE_RAGGED, 9, 120, T)
+    assert len(set(tok.view(-1).tolist())) > 1
 
 
 @pytest.mark.parametrize("batch,T", [(5, 1.0), (16, 0.8)])
