@@ -52,6 +52,27 @@ __device__ inline int swiglu_row(int c, int mlp) {
 }
 
 __device__ inline float silu(float x) { return x / (1.f + expf(-x)); }
+// silu of the bf16 GEMMs, whose result is rounded to bf16: the hardware
+// exp2 and reciprocal (about 1 ulp each in fp32) instead of expf and an IEEE
+// division, a few VALU operations in place of some thirty.
+__device__ inline float silu_bf16(float x) {
+  return x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(x * -1.44269504088896341f));
+}
+
+// One 16 x 16 x 32 MFMA of an activation fragment and a weight fragment.
+// TRANS (the SwiGLU GEMMs) takes the weight fragment first, so the
+// accumulator tile is transposed: lane l holds columns 4 (l / 16) .. + 3 of
+// row l % 16, 4 consecutive outputs of one row. Otherwise lane l holds rows
+// 4 (l / 16) .. + 3 of column l % 16. The products and sums are the same
+// either way. (The SwiGLU epilogue writes 4 consecutive bf16 at a time; the
+// fp32 split-K stores of 4 consecutive columns per lane measured 1 us slower
+// for the QKV projection, whose rows lie 24 KB apart, and no faster for the
+// others.)
+template <bool TRANS>
+__device__ __forceinline__ void mma_tile(const bf16x8& a, const bf16x8& w, f32x4& acc) {
+  acc = TRANS ? __builtin_amdgcn_mfma_f32_16x16x32_bf16(w, a, acc, 0, 0, 0)
+              : __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, w, acc, 0, 0, 0);
+}
 
 // acc = A[m0 .., kbeg .. kbeg + nk BK) . W[n0 .., same]^T for one BM x BN tile
 // (SWI: W rows in the interleaved gate/up order), through the LDS buffers
@@ -124,8 +145,8 @@ __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int 
       _Pragma("unroll") for (int i = 0; i < MTW; ++i) {                               \
         const bf16x8 av = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>( \
             &As[buf][ard[i] + lds_chunk(lane & 15, kk * 4 + (lane >> 4)) * 8]));         \
-        _Pragma("unroll") for (int j = 0; j < NTW; ++j) acc[i][j] =                   \
-            __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bfr[j], acc[i][j], 0, 0, 0);  \
+        _Pragma("unroll") for (int j = 0; j < NTW; ++j)                               \
+            mma_tile<SWI>(av, bfr[j], acc[i][j]);                                     \
       }                                                                               \
     }                                                                                 \
     _Pragma("unroll") for (int i = 0; i < AL; ++i) LDR_STORE(As[(buf) ^ 1], adst[i], cur[i]); \
@@ -166,16 +187,20 @@ __device__ __forceinline__ void tile_mma(const GemmArgs& a, int n0, int m0, int 
 
 // Stores one tile's accumulators: EPI_STORE / EPI_LOGITS fp32 (split z at
 // z * split_stride), EPI_SWIGLU silu(gate) * up in the activation dtype,
-// row-major or in the fragment layout of [M][mlp] (a.out_frag).
+// row-major or in the fragment layout of [M][mlp] (a.out_frag). The fp32
+// tiles are in the MFMA's own layout (lane l: rows 4 (l / 16) .. + 3 of column
+// l % 16); the SwiGLU tiles are transposed (mma_tile), so a lane writes 4
+// consecutive bf16 of one row (8 bytes in either layout). SwiGLU waves whose
+// tile lies inside the matrix skip the per-element tests (a wave-uniform
+// branch).
 template <int MTW, int NTW, int WM, int WN, int EPI>
 __device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, int z,
                                            const f32x4 (&acc)[MTW][NTW]) {
   constexpr int TM = MTW * 16, TN = NTW * 16;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  // C layout of a 16x16 tile: lane holds rows (lane/16)*4 + v, column lane%16.
-  const int crow = (lane >> 4) * 4, ccol = lane & 15;
   if constexpr (EPI == EPI_STORE || EPI == EPI_LOGITS) {
+    const int crow = (lane >> 4) * 4, ccol = lane & 15;
     float* out = static_cast<float*>(a.out) + (long)z * a.split_stride;
 #pragma unroll
     for (int i = 0; i < MTW; ++i)
@@ -189,22 +214,43 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, in
         }
       }
   } else {
+    const int r0 = m0 + wm * TM + (lane & 15), c4 = (lane >> 4) * 4;
     uint16_t* out = static_cast<uint16_t*>(a.out);
+    // n-tiles j (gate) and j + 1 (up) hold the same 16 output columns
+    const int ob = (n0 + wn * TN) / 2 + c4;
+    const bool full = m0 + wm * TM + TM <= a.M && (n0 + wn * TN + TN) / 2 <= a.mlp &&
+                      (a.out_frag || ((a.ldo & 3) == 0 &&
+                                      (reinterpret_cast<uintptr_t>(a.out) & 7) == 0));
+    auto put = [&](auto full_t) {
+      constexpr bool FULL = decltype(full_t)::value;
 #pragma unroll
-    for (int j = 0; j < NTW; j += 2) {   // n-tiles j (gate) and j + 1 (up) of 16 output columns
-      const int col = (n0 + wn * TN + j * 16) / 2 + ccol;
+      for (int j = 0; j < NTW; j += 2) {
+        const int col = ob + j * 8;
 #pragma unroll
-      for (int i = 0; i < MTW; ++i)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = m0 + wm * TM + i * 16 + crow + v;
+        for (int i = 0; i < MTW; ++i) {
+          const int row = r0 + i * 16;
+          if (!FULL && (row >= a.M || col >= a.mlp)) continue;
+          // col % 8 is 0 or 4: the 4 elements stay inside one 8-element run
+          // of the fragment layout
           const long off = a.out_frag ? ((long)(row >> 4) * (a.mlp >> 5) + (col >> 5)) * 512 +
                                             ((((col >> 3) & 3) << 4) | (row & 15)) * 8 + (col & 7)
                                       : (long)row * a.ldo + col;
-          if (row < a.M && col < a.mlp)
-            out[off] = f32_to_bf16(silu(acc[i][j][v]) * acc[i][j + 1][v]);
+          uint16_t h[4];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) h[v] = f32_to_bf16(silu_bf16(acc[i][j][v]) * acc[i][j + 1][v]);
+          if (FULL) {
+            *reinterpret_cast<uint2*>(out + off) =
+                uint2{(uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16)};
+          } else {
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+              if (col + v < a.mlp) out[off + v] = h[v];
+          }
         }
-    }
+      }
+    };
+    if (full) put(std::true_type{});
+    else put(std::false_type{});
   }
 }
 
@@ -469,8 +515,8 @@ __global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(Ge
       for (int i = 0; i < MTW; ++i)
 #pragma unroll
         for (int j = 0; j < NTW; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              __builtin_bit_cast(bf16x8, aq[p % FRA][i][kk]), bfr[kk][j], acc[i][j], 0, 0, 0);
+          mma_tile<EPI == EPI_SWIGLU>(__builtin_bit_cast(bf16x8, aq[p % FRA][i][kk]), bfr[kk][j],
+                                      acc[i][j]);
     load_a(aq[p % FRA], kt + FRA);
     sched_fence();
   };
