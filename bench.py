@@ -542,7 +542,8 @@ def counters_run(args, torch, ldr, synth):
     torch.cuda.synchronize()
     del src, dst
     wl = synth.WORKLOADS[args.workload]
-    rig = Rig(torch, ldr, synth, wl.shape, wl.batch, wl.prefix)
+    # the benchmarked call: ldr_draft_step_sample
+    rig = Rig(torch, ldr, synth, wl.shape, wl.batch, wl.prefix, fused_head=True)
     for i in range(4):
         rig.step(i)
     torch.cuda.synchronize()

@@ -84,12 +84,16 @@ __device__ inline float gumbel_from_bits(uint32_t bits) {
   return -fixed_logf(-fixed_logf(uniform_from_bits(bits)));
 }
 
-// The noise words of tokens [8 g, 8 g + 8) of `row` in stream `stream`.
+// The noise words of tokens [G g, G g + G) of `row` in stream `stream` (G a
+// multiple of 4: Philox blocks G / 4 g .. + G / 4, one word per token).
+template <int G>
 __device__ inline void noise_group(uint64_t seed, uint64_t step, uint64_t row, uint32_t stream,
-                                   uint64_t g, uint32_t out[kGroup]) {
+                                   uint64_t g, uint32_t (&out)[G]) {
+  static_assert(G % 4 == 0, "whole Philox blocks");
   const NoiseKey k = noise_key(seed, step, stream);
-  noise_block(k, (uint32_t)row, (uint32_t)(2 * g), out);
-  noise_block(k, (uint32_t)row, (uint32_t)(2 * g + 1), out + 4);
+#pragma unroll
+  for (int b = 0; b < G / 4; ++b)
+    noise_block(k, (uint32_t)row, (uint32_t)((G / 4) * g + b), out + 4 * b);
 }
 
 // Upper bound of the Gumbel noise g = -log(-log u) of 23-bit uniform index k,

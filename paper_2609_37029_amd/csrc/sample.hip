@@ -132,17 +132,19 @@ __global__ void __launch_bounds__(kSelThreads) topk_select_kernel(const float* l
   if (threadIdx.x == 0) sel[blockIdx.x] = TopK{prefix, v_cut};
 }
 
-// The lane's kGroup = 8 values of a sweep at v: two 16-byte loads inside the
-// range [.., v1) when vec, else one load per entry (-inf past v1).
-__device__ inline void load_group(const float* z, int v, int v1, bool vec, float (&zz)[kGroup]) {
-  if (vec && v + kGroup <= v1) {
-    const float4 x = *reinterpret_cast<const float4*>(z + v);
-    const float4 y = *reinterpret_cast<const float4*>(z + v + 4);
-    zz[0] = x.x; zz[1] = x.y; zz[2] = x.z; zz[3] = x.w;
-    zz[4] = y.x; zz[5] = y.y; zz[6] = y.z; zz[7] = y.w;
+// The lane's G values of a sweep at v (G a multiple of 4): 16-byte loads
+// inside the range [.., v1) when vec, else one load per entry (-inf past v1).
+template <int G>
+__device__ inline void load_group(const float* z, int v, int v1, bool vec, float (&zz)[G]) {
+  if (vec && v + G <= v1) {
+#pragma unroll
+    for (int b = 0; b < G / 4; ++b) {
+      const float4 x = *reinterpret_cast<const float4*>(z + v + 4 * b);
+      zz[4 * b] = x.x; zz[4 * b + 1] = x.y; zz[4 * b + 2] = x.z; zz[4 * b + 3] = x.w;
+    }
   } else {
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) zz[i] = v + i < v1 ? z[v + i] : -INFINITY;
+    for (int i = 0; i < G; ++i) zz[i] = v + i < v1 ? z[v + i] : -INFINITY;
   }
 }
 
@@ -177,8 +179,10 @@ __device__ void argmax_tokens(const SampleArgs& a, const float* z, int v0, int v
 // whose error is below 1e-5 here). Chunks without support tokens
 // (L_c = -inf) take no part. Candidates go through a per-wave queue in LDS so
 // that their exact keys (two logs each) are computed 64 at a time by full
-// waves.
-template <int NT>
+// waves. G entries per lane and sweep (a multiple of 4, the noise words of
+// G / 4 Philox blocks): with 12, one sweep of 1024 lanes covers 12288 chunks,
+// a 196K-token vocabulary.
+template <int NT, int G = kGroup>
 __device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, int c1,
                            Partial& p) {
   struct Cand { float zt; uint32_t bits; int v; };
@@ -197,25 +201,25 @@ __device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, 
     __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
-  constexpr int kSweep = NT * kGroup;
-  const int lane_off = (int)(threadIdx.x & ~63) * kGroup + lane * kGroup;
+  constexpr int kSweep = NT * G;
+  const int lane_off = (int)threadIdx.x * G;
   const uint64_t nrow = (uint64_t)r * a.row_mul + a.row_add;
-  float znext[kGroup];
+  float znext[G];
   load_group(Lr, c0 + lane_off, c1, true, znext);
   for (int vb = c0; vb < c1; vb += kSweep) {
     const int v = vb + lane_off;
-    float zt[kGroup];
+    float zt[G];
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) zt[i] = znext[i];
+    for (int i = 0; i < G; ++i) zt[i] = znext[i];
     if (vb + kSweep < c1) load_group(Lr, v + kSweep, c1, true, znext);
-    uint32_t bits[kGroup];
-    noise_group(a.seed, a.step, nrow, kChunkStream, (uint64_t)(v / kGroup), bits);
-    float gm = -INFINITY, ub[kGroup];
-    bool in[kGroup];
+    uint32_t bits[G];
+    noise_group(a.seed, a.step, nrow, kChunkStream, (uint64_t)(v / G), bits);
+    float gm = -INFINITY, ub[G];
+    bool in[G];
     int top = -1;
     float top_ub = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
+    for (int i = 0; i < G; ++i) {
       in[i] = v + i < c1 && zt[i] > -INFINITY;
       gm = fmaxf(gm, in[i] ? zt[i] : -INFINITY);
       ub[i] = zt[i] + gumbel_upper(bits[i]);
@@ -226,7 +230,7 @@ __device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, 
     float zsel = 0.f;
     uint32_t bsel = 0u;
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i)
+    for (int i = 0; i < G; ++i)
       if (i == top) { zsel = zt[i]; bsel = bits[i]; }
     if (top >= 0) {
       const float key = __fadd_rn(zsel, gumbel_from_bits(bsel));
@@ -236,7 +240,7 @@ __device__ void chunk_keys(const SampleArgs& a, const float* Lr, int r, int c0, 
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) bound = fmaxf(bound, __shfl_xor(bound, off));
 #pragma unroll
-    for (int i = 0; i < kGroup; ++i) {
+    for (int i = 0; i < G; ++i) {
       const bool valid = in[i];
       if (valid) p.s += __expf(zt[i] - p.m);
       const float margin = 1e-3f + 1e-6f * (fabsf(zt[i]) + fabsf(bound));
@@ -333,7 +337,7 @@ __global__ void __launch_bounds__(kDrawThreads) chunk_draw_kernel(SampleArgs a, 
                                                                   float* lse, float* logq) {
   const int r = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   Partial p{-INFINITY, 0.f, -INFINITY, 0x7fffffff};
-  chunk_keys<kDrawThreads>(a, a.L + (long)r * a.ldL, r, 0, a.nch, p);
+  chunk_keys<kDrawThreads, 12>(a, a.L + (long)r * a.ldL, r, 0, a.nch, p);
   for (int off = 32; off >= 1; off >>= 1) {
     Partial o{__shfl_xor(p.m, off), __shfl_xor(p.s, off), __shfl_xor(p.key, off),
               __shfl_xor(p.idx, off)};
