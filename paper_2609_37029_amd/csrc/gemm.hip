@@ -731,10 +731,11 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
       for (int i = 0; i < MT; ++i) {
         const int row = r0 + i * 16 + rl;
         if (row >= a.M) continue;
+        float* orow = out + (long)row * a.ldo + c0 + g * 4;
 #pragma unroll
         for (int j = 0; j < NT; ++j) {
           const int col = c0 + j * 16 + g * 4;
-          float* o = out + (long)row * a.ldo + col;
+          float* o = orow + j * 16;
           if (FULL) {
             if (c0 + j * 16 < cend) *reinterpret_cast<f32x4*>(o) = acc[i][j];
           } else {
@@ -770,35 +771,75 @@ __global__ void __launch_bounds__(512, 1) gemm_tiled_kernel(GemmArgs a, HeadSamp
     const float T = hs.T;
     auto chunks = [&](auto full_t) {
       constexpr bool FULL = decltype(full_t)::value;
+      // IP row blocks of NT chunks side by side, one phase at a time, so that
+      // each lane exchange waits once for all of them
+      constexpr int IP = 2;
 #pragma unroll
-      for (int i = 0; i < MT; ++i) {
-        float keep = 0.f, keep4 = 0.f;
+      for (int i0 = 0; i0 < MT; i0 += IP) {
+        float zt[IP][NT][4], m[IP][NT], sum[IP][NT], o16[IP][NT], o32[IP][NT];
 #pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          const int col = c0 + j * 16 + g * 4;
-          float zt[4], e[4];
+        for (int ii = 0; ii < IP; ++ii)
 #pragma unroll
-          for (int v = 0; v < 4; ++v)
-            zt[v] = FULL || col + v < a.N
-                        ? (HS == kHeadChunksUnitT ? acc[i][j][v] : acc[i][j][v] / T)
-                        : -INFINITY;
-          float m = fmaxf(fmaxf(zt[0], zt[1]), fmaxf(zt[2], zt[3]));
-          m = fmaxf(m, x16(m));
-          m = fmaxf(m, x32(m));
+          for (int j = 0; j < NT; ++j) {
+            const int col = c0 + j * 16 + g * 4;
 #pragma unroll
-          for (int v = 0; v < 4; ++v) e[v] = zt[v] > -INFINITY ? chunk_term(zt[v], m) : 0.f;
-          float sum = (e[0] + e[1]) + (e[2] + e[3]);
-          sum += x16(sum);
-          sum += x32(sum);
-          const float L = chunk_log_mass(m, sum);
-          if (j == 4) keep4 = L;
-          else keep = g == j ? L : keep;
-        }
-        const int row = r0 + i * 16 + rl;
-        if (row < a.M) {
-          float* Lr = hs.L + (long)row * hs.ldL + c0 / 16;
-          if (c0 + g * 16 < cend) Lr[g] = keep;
-          if (NT > 4 && g == 0 && c0 + 64 < cend) Lr[4] = keep4;
+            for (int v = 0; v < 4; ++v) {
+              const float x = acc[i0 + ii][j][v];
+              zt[ii][j][v] = FULL || col + v < a.N ? (HS == kHeadChunksUnitT ? x : x / T)
+                                                   : -INFINITY;
+            }
+            m[ii][j] = fmaxf(fmaxf(zt[ii][j][0], zt[ii][j][1]), fmaxf(zt[ii][j][2], zt[ii][j][3]));
+          }
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) o16[ii][j] = x16(m[ii][j]);
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) m[ii][j] = fmaxf(m[ii][j], o16[ii][j]);
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) o32[ii][j] = x32(m[ii][j]);
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) {
+            m[ii][j] = fmaxf(m[ii][j], o32[ii][j]);
+            float e[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) e[v] = chunk_term(zt[ii][j][v], m[ii][j]);
+            sum[ii][j] = (e[0] + e[1]) + (e[2] + e[3]);
+          }
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) o16[ii][j] = x16(sum[ii][j]);
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) sum[ii][j] += o16[ii][j];
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii)
+#pragma unroll
+          for (int j = 0; j < NT; ++j) o32[ii][j] = x32(sum[ii][j]);
+#pragma unroll
+        for (int ii = 0; ii < IP; ++ii) {
+          float keep = 0.f, keep4 = 0.f;
+#pragma unroll
+          for (int j = 0; j < NT; ++j) {
+            sum[ii][j] += o32[ii][j];
+            const float L = chunk_log_mass(m[ii][j], sum[ii][j]);
+            if (j == 4) keep4 = L;
+            else keep = g == j ? L : keep;
+          }
+          const int row = r0 + (i0 + ii) * 16 + rl;
+          if (row < a.M) {
+            float* Lr = hs.L + (long)row * hs.ldL + c0 / 16;
+            if (c0 + g * 16 < cend) Lr[g] = keep;
+            if (NT > 4 && g == 0 && c0 + 64 < cend) Lr[4] = keep4;
+          }
         }
       }
     };

@@ -77,7 +77,10 @@ __device__ inline float max16(float v) {
 // exp(zt - m) of a chunk's sum, and the chunk's log-mass m + log s. The same
 // operations (no contraction) wherever L_c is formed, so the log-mass pass over
 // stored logits and the vocabulary head's epilogue give the same bits when
-// they also sum the 16 terms in the same balanced pairwise order.
+// they also sum the 16 terms in the same balanced pairwise order. A token
+// outside the support (zt = -inf) adds exp2(-inf) = 0; a chunk without one
+// has m = -inf and L_c = -inf; a NaN logit makes its chunk's L_c NaN, which the
+// chunk draw leaves out like -inf.
 #if defined(__HIP_DEVICE_COMPILE__)
 __device__ inline float chunk_term(float zt, float m) {
 #pragma clang fp contract(off)

@@ -294,7 +294,7 @@ __global__ void __launch_bounds__(kThreads) chunk_lse_kernel(SampleArgs a, int v
     m = fmaxf(m, dpp<0x4E>(m));
     float e[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) e[i] = zt[i] > -INFINITY ? chunk_term(zt[i], m) : 0.f;
+    for (int i = 0; i < 4; ++i) e[i] = chunk_term(zt[i], m);
     float sum = (e[0] + e[1]) + (e[2] + e[3]);
     sum += dpp<0xB1>(sum);
     sum += dpp<0x4E>(sum);
