@@ -201,18 +201,28 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, int n0, int m0, in
   const int wm = wave / WN, wn = wave % WN;
   if constexpr (EPI == EPI_STORE || EPI == EPI_LOGITS) {
     const int crow = (lane >> 4) * 4, ccol = lane & 15;
-    float* out = static_cast<float*>(a.out) + (long)z * a.split_stride;
+    const int rb = m0 + wm * TM + crow, cb = n0 + wn * TN + ccol;
+    float* out = static_cast<float*>(a.out) + (long)z * a.split_stride + (long)rb * a.ldo + cb;
+    if (m0 + wm * TM + TM <= a.M && n0 + wn * TN + TN <= a.N) {
+      // the wave's tile lies inside the matrix: no per-element tests
 #pragma unroll
-    for (int i = 0; i < MTW; ++i)
-#pragma unroll
-      for (int j = 0; j < NTW; ++j) {
-        const int col = n0 + wn * TN + j * 16 + ccol;
+      for (int i = 0; i < MTW; ++i)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-          const int row = m0 + wm * TM + i * 16 + crow + v;
-          if (row < a.M && col < a.N) out[(long)row * a.ldo + col] = acc[i][j][v];
+          float* o = out + (long)(i * 16 + v) * a.ldo;
+#pragma unroll
+          for (int j = 0; j < NTW; ++j) o[j * 16] = acc[i][j][v];
         }
-      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < MTW; ++i)
+#pragma unroll
+        for (int j = 0; j < NTW; ++j)
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            if (rb + i * 16 + v < a.M && cb + j * 16 < a.N)
+              out[(long)(i * 16 + v) * a.ldo + j * 16] = acc[i][j][v];
+    }
   } else {
     const int r0 = m0 + wm * TM + (lane & 15), c4 = (lane >> 4) * 4;
     uint16_t* out = static_cast<uint16_t*>(a.out);
