@@ -166,6 +166,29 @@ def test_sampled_step_matches_the_separate_calls(gpu_lib, batch, T):
         assert len(set(tok.view(-1).tolist())) > 1
 
 
+def test_nan_logit_in_the_fused_head(gpu_lib):
+    """A NaN row of the vocabulary head (token 117, chunk 7) gives every row a
+    NaN logit: the head's chunk log-mass of that chunk is NaN like the
+    log-mass pass's, so the sampled step still equals the separate calls bit
+    for bit (logits compared as bits) and never draws from that chunk."""
+    p, dw, anchor = setup(gpu_lib, MINI_WIDE, 5, 120)
+    w = dict(dw.w)
+    head = w["lm_head"].clone()
+    head[117] = float("nan")
+    w["lm_head"] = head
+    dn = gpu_lib.DraftWeights(w, tiled_head=True)
+    V = MINI_WIDE.vocab
+    z_ref = gpu_lib.draft_step(p.views, dn, anchor)
+    ref = gpu_lib.sample(z_ref.view(-1, V), 1.0, 0, 21, 1)
+    z, tok, lse, logq = gpu_lib.draft_step_sample(p.views, dn, anchor, 1.0, 21, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(z.view(torch.int32), z_ref.view(torch.int32))
+    assert torch.isnan(z[..., 117]).all()
+    for a, b in zip((tok, lse, logq), ref):
+        assert torch.equal(a.view(-1), b)
+    assert not torch.any((tok >= 112) & (tok < 128))
+
+
 @pytest.mark.slow
 def test_sampled_step_full_size(gpu_lib):
     """Qwen3-8B shape, batch 16, T = 1: the benchmarked call (500 column

@@ -119,6 +119,32 @@ def test_top_k_at_least_vocab_is_the_full_support(gpu_lib):
         assert torch.equal(x[0], y[0]) and torch.equal(x[1], y[1])
 
 
+@pytest.mark.parametrize("T", [1.0, 0.6])
+def test_nan_logit_leaves_its_chunk_out(gpu_lib, T):
+    """A NaN logit makes its 16-token chunk's log-mass NaN, which the chunk
+    draw leaves out as it does a chunk of -inf logits: tokens, lse and log q
+    equal those of the same rows with that chunk at -inf, bit for bit, and no
+    token comes from it (NaN logits are outside the sampler's contract; this
+    pins what the kernels do with them)."""
+    rows, V, c = 12, 5003, 7
+    g = torch.Generator(device="cuda").manual_seed(3)
+    z = torch.randn(rows, V, device="cuda", generator=g) * 3
+    z[:, c * 16:(c + 1) * 16] += 6.0          # a chunk that would often win
+    zn = z.clone()
+    zn[:, c * 16 + 5] = float("nan")
+    zi = z.clone()
+    zi[:, c * 16:(c + 1) * 16] = float("-inf")
+    a = gpu_lib.sample(zn, T, 0, 11, 2)
+    b = gpu_lib.sample(zi, T, 0, 11, 2)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+    tok = a[0]
+    assert not torch.any((tok >= c * 16) & (tok < (c + 1) * 16))
+    ref = gpu_lib.sample(z, T, 0, 11, 2)[0]    # without the NaN the chunk is drawn
+    assert torch.any((ref >= c * 16) & (ref < (c + 1) * 16))
+
+
 def test_negative_top_k_is_rejected(gpu_lib):
     z = _logits(2, 100, 1)
     with pytest.raises(gpu_lib.LdrError):
