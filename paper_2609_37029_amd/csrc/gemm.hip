@@ -384,7 +384,11 @@ __device__ inline void group_barrier() {
 // A workgroup owns all 256 rows x BN columns of the output and a 1/splits
 // share of K, in steps of 64. Eight compute waves own 32 rows each: their A
 // fragments go straight to registers, FRA steps ahead (private, so no LDS),
-// and they read all BN weight rows of a step from LDS. NL loader waves only
+// and they read all BN weight rows of a step from LDS. The same pipeline
+// with one compute wave of 16 rows reading row-major activations (ROWA) takes
+// the GEMMs of at most 16 rows in place of the staged kernel: those only
+// stream their weights, and the DMA streams them faster (the boundary fusion
+// at batch 16 35.8 -> 33.5 us; the batch-1 SwiGLU GEMM 53.4 -> 49.8 us). NL loader waves only
 // stage the weights by DMA (global_load_lds, 8 rows of 128 bytes per
 // instruction, 16-byte chunk c of row r at c ^ (r & 7)) into a ring of NB
 // stages, NB - 1 steps ahead. A wave that issued the weight DMA itself
@@ -409,10 +413,13 @@ template <int N> __device__ inline void wait_vm_lgkm0() {
 constexpr int kFragWaves = 8;    // compute waves of the fragment-layout GEMM
 constexpr int kFragLoaders = 4;  // its loader waves
 constexpr int kFragThreads = 64 * (kFragWaves + kFragLoaders);
+constexpr int kRowsThreads = 64 * (1 + kFragLoaders);   // the 16-row variant
 
-template <int MTW, int NTW, int EPI, int FRA, int NL, int NB>
-__global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(GemmArgs a) {
-  constexpr int NW = kFragWaves, WM = NW, WN = 1, TM = MTW * 16, TN = NTW * 16;
+// NW compute waves of MTW 16-row tiles each; ROWA: activations row-major
+// (row stride lda) instead of the fragment layout.
+template <int MTW, int NTW, int EPI, int FRA, int NL, int NB, int NW, bool ROWA>
+__device__ __forceinline__ void frag_gemm(const GemmArgs& a) {
+  constexpr int WM = NW, WN = 1, TM = MTW * 16, TN = NTW * 16;
   constexpr int BM = WM * TM, BN = WN * TN;
   constexpr int STAGE = BN * 128;             // W bytes per stage (BN rows x 64 k)
   constexpr int GROUPS = BN / 8;              // DMA instructions per stage (8 rows each)
@@ -469,23 +476,35 @@ __global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(Ge
   }
   const int wm = wave;
   const uint16_t* A = static_cast<const uint16_t*>(a.A);
-  // A fragments of m-tile i and k half kk of a step: one 1 KB block each.
-  // Row blocks past the padded row count repeat the last one (never stored).
-  const int mpad = (a.M + 15) & ~15;
+  // A fragments of m-tile i and k half kk of a step: in the fragment layout
+  // one 1 KB block each (row blocks past the padded row count repeat the
+  // last one); row-major, lane l reads row l % 16 (rows past M repeat the
+  // last one), 8 columns from (l / 16) * 8. Those rows are never stored.
   const uint16_t* asrc[MTW];
+  if constexpr (ROWA) {
 #pragma unroll
-  for (int i = 0; i < MTW; ++i) {
-    const int rg = min(m0 + wm * TM + i * 16, mpad - 16) >> 4;
-    asrc[i] = A + ((long)rg * (a.K >> 5) + (kbeg >> 5)) * 512 + lane * 8;
+    for (int i = 0; i < MTW; ++i) {
+      const int r = min(m0 + wm * TM + i * 16 + (lane & 15), a.M - 1);
+      asrc[i] = A + (long)r * a.lda + kbeg + (lane >> 4) * 8;
+    }
+  } else {
+    const int mpad = (a.M + 15) & ~15;
+#pragma unroll
+    for (int i = 0; i < MTW; ++i) {
+      const int rg = min(m0 + wm * TM + i * 16, mpad - 16) >> 4;
+      asrc[i] = A + ((long)rg * (a.K >> 5) + (kbeg >> 5)) * 512 + lane * 8;
+    }
   }
+  constexpr int KKA = ROWA ? 32 : 512;       // elements between the two k halves
+  constexpr long STA = ROWA ? BK : 1024;     // elements between steps
   u32x4 aq[FRA][MTW][2];
   auto load_a = [&](u32x4 (&dst)[MTW][2], int stage) {   // past the end: the last stage again
-    const long off = (long)min(stage, nk - 1) * 1024;
+    const long off = (long)min(stage, nk - 1) * STA;
 #pragma unroll
     for (int i = 0; i < MTW; ++i)
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
-        dst[i][kk] = *reinterpret_cast<const u32x4*>(asrc[i] + off + kk * 512);
+        dst[i][kk] = *reinterpret_cast<const u32x4*>(asrc[i] + off + kk * KKA);
   };
   // W fragment offsets in a stage: row j * 16 + lane % 16, logical chunk
   // kk * 4 + lane / 16
@@ -540,6 +559,17 @@ __global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(Ge
              std::make_integer_sequence<int, NB - 1>{});
   wait_vm_lgkm0<0>();
   store_tile<MTW, NTW, WM, WN, EPI>(a, n0, m0, z, acc);
+}
+
+template <int MTW, int NTW, int EPI, int FRA, int NL, int NB>
+__global__ void __launch_bounds__(64 * (kFragWaves + NL), 1) gemm_frag_kernel(GemmArgs a) {
+  frag_gemm<MTW, NTW, EPI, FRA, NL, NB, kFragWaves, false>(a);
+}
+
+// M <= 16, row-major activations: one compute wave and the loader waves.
+template <int NTW, int EPI>
+__global__ void __launch_bounds__(kRowsThreads, 1) gemm_rows16_kernel(GemmArgs a) {
+  frag_gemm<1, NTW, EPI, 2, kFragLoaders, 6, 1, true>(a);
 }
 
 // ---------------------------------------------------------------------------
@@ -938,6 +968,9 @@ __global__ void __launch_bounds__(256) tile_matrix_kernel(const uint16_t* src, l
 // projection) with half the split-K partials for the next kernel to read;
 // 9: BM 16 with 3 waves along N (BN 96), in place of cfg 0 where 96-column
 // tiles fill the CUs better;
+// 10, 11: gemm_rows16_kernel, cfg 0 and 9 (BM 16, BN 128 or 96) with the
+// weights streamed by loader waves, where each split's K range is a multiple
+// of 64;
 // 6, 7, 8: gemm_frag_kernel, BM 256 with 8 compute waves of 32 x 96 (BN 96),
 // 32 x 128 (BN 128) or 32 x 64 (BN 64) and 4 loader waves, activation rows in
 // the fragment layout: the GEMMs above 64 rows whose input is written in that
@@ -964,6 +997,12 @@ hipError_t launch_cfg(int cfg, dim3 grid, const GemmArgs& a, hipStream_t st) {
                          dim3(kFragThreads), 0, st, a);
       break;
     case 9: hipLaunchKernelGGL((gemm_kernel<1, 2, 1, 3, EPI>), grid, dim3(192), 0, st, a); break;
+    case 10:
+      hipLaunchKernelGGL((gemm_rows16_kernel<8, EPI>), grid, dim3(kRowsThreads), 0, st, a);
+      break;
+    case 11:
+      hipLaunchKernelGGL((gemm_rows16_kernel<6, EPI>), grid, dim3(kRowsThreads), 0, st, a);
+      break;
     default: hipLaunchKernelGGL((gemm_kernel<4, 4, 4, 2, EPI>), grid, dim3(512), 0, st, a); break;
   }
   return hipGetLastError();
@@ -1071,6 +1110,8 @@ GemmPlan plan_gemm(int dtype, int M, int N, int K, bool allow_split, bool swiglu
   p.grid_x = (N + bn - 1) / bn;
   p.grid_y = (M + bm - 1) / bm;
   p.splits = split_for((long)p.grid_x * p.grid_y);
+  // 16-row tiles stream their weights through the loader waves' DMA
+  if ((p.cfg == 0 || p.cfg == 9) && (K / p.splits) % BK == 0) p.cfg = p.cfg == 0 ? 10 : 11;
   return p;
 }
 
