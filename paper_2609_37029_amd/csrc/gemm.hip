@@ -21,7 +21,9 @@
 // Epilogues: EPI_STORE writes fp32 (split-K partials); EPI_LOGITS writes the
 // fp32 logits; EPI_SWIGLU reads the gate and up rows of w_gate_up interleaved
 // in 16-row blocks (each wave's n-tile pairs are matching gate / up columns)
-// and writes silu(gate) * up in the activation dtype.
+// and writes silu(gate) * up in the activation dtype. The vocabulary head's
+// epilogue can also take each row's first argmax (greedy sampling) or form
+// the 16-token chunk log-masses of the two-level draw (Eq. 8).
 #include "ldr_internal.h"
 
 #include <type_traits>

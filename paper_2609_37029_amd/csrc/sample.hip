@@ -170,7 +170,7 @@ __device__ void argmax_tokens(const SampleArgs& a, const float* z, int v0, int v
 // Gumbel-max over the chunk log-masses L_c of row r, entries [c0, c1). Every
 // lane keeps the max / sum of exp(L_c) of its entries (so the row's lse is
 // log sum_c exp(L_c)) and the best (key, chunk) of the entries it evaluated
-// exactly. Per sweep of 8 entries a lane evaluates first the exact key of
+// exactly. Per sweep of G entries a lane evaluates first the exact key of
 // its entry with the largest upper bound L_c + bound(h_c); the largest key of
 // the wave so far is then a lower bound of the row's best, and any other
 // entry is a candidate only unless L_c + bound(h_c) + margin < that bound,
